@@ -1,0 +1,515 @@
+"""Pins for the CPU oracle: each test ties one oracle function to something
+other than the oracle itself (a library routine, a closed form, brute force on
+tiny inputs, a hand-worked example, or an independent textbook algorithm).
+
+Paper passages: squared L2 (Sec 2.1), rank domain (Sec 4), segment tree and
+HotspotLocalization (Sec 4, Alg 3, Eq. endcondition), entry points and
+FROGSearch (Alg 2), ENIdentification (Alg 4), KANNSearch (Alg 1), RFANNS
+(Def. 2), fusion distance (Eq. fusion-distance), boundary effect (Eq.
+naive_attr_dist), construction (Sec 6).
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------------ P1 distance
+
+def test_dist_matches_numpy_fp64():
+    rng = np.random.default_rng(1)
+    for d in (1, 3, 32, 96, 128, 960):
+        a = rng.standard_normal(d).astype(np.float32)
+        b = rng.standard_normal(d).astype(np.float32)
+        ref = np.float32(((a.astype(np.float64) - b.astype(np.float64)) ** 2).sum())
+        got = oracle.dist(a, b)
+        # fp64 sums of the same terms in two orders agree to ~1e-16 relative;
+        # after the single rounding to fp32 they are equal or 1 ulp apart.
+        assert abs(float(got) - float(ref)) <= float(np.spacing(ref))
+
+
+def test_dist_exact_small_integers():
+    # integer-valued inputs: every term and the sum are exact
+    a = np.array([1, 2, 3, 4], np.float32)
+    b = np.array([4, 0, 3, -1], np.float32)
+    assert oracle.dist(a, b) == np.float32(9 + 4 + 0 + 25)
+    assert oracle.dist(a, a) == 0.0
+
+
+def test_splitmix64_published_values():
+    # SplitMix64 stream from state 0: the first outputs of the published
+    # generator (state += golden gamma, then the finaliser).
+    # x_1 = mix(0x9E3779B97F4A7C15), x_2 = mix(2*gamma), ...
+    expected = [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+    gamma = 0x9E3779B97F4A7C15
+    for i, e in enumerate(expected):
+        # fo_splitmix64(x) adds one gamma itself, so feed the state before it
+        assert oracle.splitmix64((i * gamma) & 0xFFFFFFFFFFFFFFFF) == e
+
+
+# ------------------------------------------------------------------ P3 ranks
+
+def test_rank_bounds_match_searchsorted():
+    rng = np.random.default_rng(2)
+    a = np.sort(rng.integers(0, 50, 200).astype(np.float64))  # many duplicates
+    for _ in range(500):
+        lo, hi = rng.uniform(-5, 55, 2)
+        l, r = oracle.rank_bounds(a, lo, hi)
+        assert l == np.searchsorted(a, lo, "left")
+        assert r == np.searchsorted(a, hi, "right") - 1
+    # exact-value endpoints include all duplicates
+    l, r = oracle.rank_bounds(a, 10.0, 10.0)
+    assert (a[l:r + 1] == 10.0).all() and (a == 10.0).sum() == r - l + 1
+
+
+def test_rank_bounds_degenerate():
+    a = np.arange(10, dtype=np.float64)
+    assert oracle.rank_bounds(a, 5, 3)[0] > oracle.rank_bounds(a, 5, 3)[1]   # lo > hi
+    l, r = oracle.rank_bounds(a, np.nan, 3)
+    assert l > r
+    l, r = oracle.rank_bounds(a, 1, np.nan)
+    assert l > r
+    assert oracle.rank_bounds(a, -np.inf, np.inf) == (0, 9)
+    assert oracle.rank_bounds(a, 100, 200)[0] == 10
+
+
+def test_rank_order_is_stable_attribute_sort():
+    import ctypes as C
+    lib = oracle._load()
+    rng = np.random.default_rng(3)
+    attr = rng.integers(0, 20, 300).astype(np.float64)
+    perm = np.empty(300, np.int32)
+    srt = np.empty(300, np.float64)
+    assert lib.fo_rank_order(oracle._p(attr), 300, oracle._p(perm), oracle._p(srt)) == 0
+    assert (perm == np.argsort(attr, kind="stable")).all()
+    assert (srt == np.sort(attr)).all()
+    attr[7] = np.nan
+    assert lib.fo_rank_order(oracle._p(attr), 300, oracle._p(perm), oracle._p(srt)) == -1
+
+
+# ------------------------------------------------------------------ P5 geometry
+
+def _layers(n, H):
+    """Segments per layer by explicit recursive halving (independent of the
+    oracle's per-rank descent)."""
+    out = [[(0, n - 1)]]
+    for _ in range(H - 1):
+        nxt = []
+        for (L, R) in out[-1]:
+            mid = L + (R - L) // 2
+            nxt.append((L, mid))
+            nxt.append((mid + 1, R))
+        out.append(nxt)
+    return out
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 7, 16, 17, 100, 10_000, 1_000_000])
+def test_num_layers_closed_form(n):
+    import math
+    for n_inv in (0, 6, 7):
+        full = (math.ceil(math.log2(n)) if n > 1 else 0) + 1
+        assert oracle.num_layers(n, n_inv) == max(1, full - n_inv)
+    # the configurations used by the benchmarks
+    assert oracle.num_layers(10_000, 7) == 8
+    assert oracle.num_layers(1_000_000, 7) == 14
+    assert oracle.num_layers(1_000_000, 6) == 15
+    assert oracle.num_layers(10_000_000, 7) == 18
+
+
+@pytest.mark.parametrize("n,H", [(16, 4), (17, 5), (100, 6), (1000, 8)])
+def test_segments_partition_each_layer(n, H):
+    layers = _layers(n, H)
+    for h, segs in enumerate(layers):
+        covered = np.zeros(n, int)
+        for (L, R) in segs:
+            if L <= R:
+                covered[L:R + 1] += 1
+        assert (covered == 1).all()          # every rank in exactly one segment
+        for p in range(n):
+            s, e = oracle.segment(n, h, p)
+            assert (s, e) in segs and s <= p <= e
+
+
+# ------------------------------------------------------------------ P4 hotspot
+
+def _hotspot_bruteforce(l, r, H, n):
+    layers = _layers(n, H)
+
+    def seg_of(h, p):
+        for (L, R) in layers[h]:
+            if L <= p <= R:
+                return L, R
+        raise AssertionError
+
+    Ls = max(h for h in range(H) if seg_of(h, l) == seg_of(h, r))
+    Le = Ls
+    for h in range(Ls + 1, H):
+        _, el = seg_of(h, l)
+        sr, _ = seg_of(h, r)
+        # overlap with the two boundary segments vs 2^-h (r - l), exactly
+        if ((el + 1 - l) + (r - sr)) * 2 ** h >= (r - l):
+            Le = h
+        else:
+            break
+    return Ls, Le
+
+
+def test_hotspot_hand_examples():
+    rows = [list(map(int, ln.split())) for ln in open(os.path.join(GOLDEN, "hotspot_n16.txt"))
+            if ln.strip() and not ln.startswith("#")]
+    assert len(rows) >= 6
+    for n, H, l, r, Ls, Le in rows:
+        assert oracle.hotspot(l, r, H, n) == (Ls, Le), (l, r)
+
+
+@pytest.mark.parametrize("n,H", [(16, 4), (37, 5), (100, 6), (1000, 8)])
+def test_hotspot_bruteforce(n, H):
+    rng = np.random.default_rng(n)
+    pairs = [(l, r) for l in range(n) for r in range(l, n)] if n <= 40 else \
+        [tuple(sorted(rng.integers(0, n, 2))) for _ in range(400)]
+    for l, r in pairs:
+        assert oracle.hotspot(l, r, H, n) == _hotspot_bruteforce(l, r, H, n), (l, r)
+
+
+# ------------------------------------------------------------------ entry points
+
+def test_entry_points_all_when_small():
+    assert list(oracle.entry_points(5, 9, 16, 0, 0)) == [5, 6, 7, 8, 9]
+    assert len(oracle.entry_points(5, 4, 16, 0, 0)) == 0
+
+
+def test_entry_points_stratified_distinct_in_range():
+    rng = np.random.default_rng(4)
+    for _ in range(200):
+        l = int(rng.integers(0, 1000))
+        cnt = int(rng.integers(17, 5000))
+        epn = int(rng.integers(1, 17))
+        ep = oracle.entry_points(l, l + cnt - 1, epn, 7, int(rng.integers(0, 1 << 20)))
+        assert len(ep) == epn and len(set(ep.tolist())) == epn
+        # entry j lies in stratum j of [l, r]
+        for j, v in enumerate(ep):
+            assert l + (j * cnt) // epn <= v <= l + ((j + 1) * cnt) // epn - 1
+
+
+def test_entry_points_roughly_uniform():
+    # jitter inside each stratum is uniform: over many queries the offset
+    # within a stratum of width 10 has a flat histogram
+    offs = []
+    for qi in range(4000):
+        ep = oracle.entry_points(0, 159, 16, 123, qi)
+        offs.extend((ep - np.arange(16) * 10).tolist())
+    h = np.bincount(offs, minlength=10)
+    assert h.min() > 0.85 * h.mean() and h.max() < 1.15 * h.mean()
+
+
+# ------------------------------------------------------------------ P6 EN(u)
+
+def _hand_index():
+    # n=12, H=3, m=4; rows handwritten, -1 tails, duplicates across layers
+    n, H, m = 12, 3, 4
+    E = -np.ones((n, H, m), np.int32)
+    E[5, 0] = [11, 0, 6, 3]
+    E[5, 1] = [3, 4, 6, -1]
+    E[5, 2] = [4, 6, -1, -1]
+    E[2, 0] = [9, 10, 11, 1]
+    E[2, 1] = [1, 0, 4, 5]
+    E[2, 2] = [1, 0, 3, -1]
+    return E
+
+
+def test_en_ident_hand_examples():
+    E = _hand_index()
+    # range [3,6], layers 0..2, budget 16: in stored order, duplicates kept
+    got, sc = oracle.en_ident(E, 5, 3, 6, 0, 2, 16)
+    assert got.tolist() == [6, 3, 3, 4, 6, 4, 6] and sc == 12
+    # budget 3 stops inside layer 1; entries scanned count whole layers
+    got, sc = oracle.en_ident(E, 5, 3, 6, 0, 2, 3)
+    assert got.tolist() == [6, 3, 3] and sc == 8
+    # hotspot restricted to layers 1..2
+    got, sc = oracle.en_ident(E, 5, 0, 11, 1, 2, 16)
+    assert got.tolist() == [3, 4, 6, 4, 6] and sc == 8
+    # nothing in range
+    got, sc = oracle.en_ident(E, 2, 6, 8, 0, 2, 16)
+    assert got.tolist() == [] and sc == 12
+    # list-comprehension restatement of Alg. 4 on random rows
+    rng = np.random.default_rng(5)
+    R = rng.integers(-1, 40, (40, 5, 8)).astype(np.int32)
+    for _ in range(300):
+        u = int(rng.integers(0, 40))
+        l, r = sorted(rng.integers(0, 40, 2).tolist())
+        Ls = int(rng.integers(0, 5))
+        Le = int(rng.integers(Ls, 5))
+        B = int(rng.integers(1, 20))
+        flat = [v for h in range(Ls, Le + 1) for v in R[u, h] if v != -1 and l <= v <= r]
+        got, _ = oracle.en_ident(R, u, l, r, Ls, Le, B)
+        assert got.tolist() == flat[:B]
+
+
+# ------------------------------------------------------------------ P2 exact
+
+def test_exact_matches_numpy_lexsort():
+    w = workloads.make("tiny", n=3000, nq=40)
+    perm = np.argsort(w.attr, kind="stable").astype(np.int32)
+    srt = w.attr[perm]
+    Xr = w.X[perm]
+    ids, ds = oracle.exact(Xr, srt, perm, w.Q, w.lo, w.hi, 10)
+    for i in range(w.nq):
+        l = np.searchsorted(srt, w.lo[i], "left")
+        r = np.searchsorted(srt, w.hi[i], "right") - 1
+        D = ((Xr[l:r + 1].astype(np.float64) - w.Q[i].astype(np.float64)) ** 2).sum(1).astype(np.float32)
+        rank = np.arange(l, r + 1)
+        o = np.lexsort((rank, D))[:10]
+        assert (ids[i, :len(o)] == perm[rank[o]]).all()
+        assert np.allclose(ds[i, :len(o)], D[o], rtol=1e-6, atol=0)
+        assert (ids[i, len(o):] == -1).all()
+
+
+def test_exact_empty_and_short_ranges():
+    w = workloads.make("tiny", n=500, nq=4)
+    perm = np.argsort(w.attr, kind="stable").astype(np.int32)
+    srt = w.attr[perm]
+    lo = np.array([10.0, 300.0, np.nan, 499.0])
+    hi = np.array([12.0, 200.0, 5.0, 1e9])
+    ids, ds = oracle.exact(w.X[perm], srt, perm, w.Q, lo, hi, 5)
+    assert (ids[0, :3] >= 0).all() and (ids[0, 3:] == -1).all() and np.isinf(ds[0, 3:]).all()
+    assert (ids[1] == -1).all() and (ids[2] == -1).all()
+    assert ids[3, 0] == perm[499] and (ids[3, 1:] == -1).all()
+
+
+# ------------------------------------------------------------------ fusion distance
+
+def test_fusion_special_values():
+    # beta = 0 reduces to the vector distance
+    assert oracle.fusion(9.0, 3, 70, 100, 0.0, 0.5) == 3.0
+    # maximal attribute distance (|ru - rv| = len - 1) leaves it unchanged
+    assert oracle.fusion(16.0, 0, 99, 100, 0.2, 0.5) == 4.0
+    # delta_a = 1/4, gamma = 1/2 -> weight 1 - 0.2 * (1 - 0.5) = 0.9
+    assert abs(oracle.fusion(4.0, 10, 35, 101, 0.2, 0.5) - 1.8) < 1e-15
+    # the weight only depends on |ru - rv| and grows with it
+    a = oracle.fusion(1.0, 10, 15, 101, 0.2, 0.5)
+    b = oracle.fusion(1.0, 15, 10, 101, 0.2, 0.5)
+    c = oracle.fusion(1.0, 10, 60, 101, 0.2, 0.5)
+    assert a == b and a < c < 1.0 and a > 0.8
+
+
+def test_fusion_shift_constant():
+    # Sec 5.2: C_gamma = Cov(Z, Z^gamma) = gamma / (2 (gamma+1)(gamma+2)) for Z ~ U(0,1);
+    # checked by quadrature, and 1/15 at gamma = 1/2
+    z = (np.arange(2_000_000) + 0.5) / 2_000_000
+    for g in (0.25, 0.5, 1.0, 2.0):
+        cov = (z * z ** g).mean() - z.mean() * (z ** g).mean()
+        assert abs(cov - g / (2 * (g + 1) * (g + 2))) < 1e-6
+    assert abs(0.5 / (2 * 1.5 * 2.5) - 1 / 15) < 1e-15
+
+
+# ------------------------------------------------------------------ build
+
+@pytest.fixture(scope="module")
+def tiny_index():
+    w = workloads.make("tiny", n=3000, nq=200)
+    ix = oracle.build(w.X, w.attr)
+    return w, ix
+
+
+def test_build_structure(tiny_index):
+    w, ix = tiny_index
+    n, H, m = ix.ENC.shape
+    assert H == oracle.num_layers(n, 7) and m == 16
+    assert (ix.perm == np.argsort(w.attr, kind="stable")).all()
+    assert (ix.X_rank == w.X[ix.perm]).all()
+    for h in range(H):
+        for u in range(0, n, 7):
+            row = ix.ENC[u, h]
+            valid = row[row != -1]
+            # -1 only at the tail, no self, distinct, inside u's layer-h segment
+            assert (row[len(valid):] == -1).all()
+            assert u not in valid and len(set(valid.tolist())) == len(valid)
+            s, e = oracle.segment(n, h, u)
+            assert ((valid >= s) & (valid <= e)).all()
+            # ascending fusion distance w.r.t. the segment length
+            keys = [oracle.fusion(oracle.dist(ix.X_rank[u], ix.X_rank[v]), u, int(v), e - s + 1, 0.2, 0.5)
+                    for v in valid]
+            assert all(keys[i] <= keys[i + 1] for i in range(len(keys) - 1))
+            if e - s + 1 > m:
+                assert len(valid) == m
+
+
+def test_build_leaf_layer_is_exact_fusion_topm(tiny_index):
+    w, ix = tiny_index
+    n, H, m = ix.ENC.shape
+    h = H - 1
+    Xr = ix.X_rank.astype(np.float64)
+    for u in range(0, n, 37):
+        s, e = oracle.segment(n, h, u)
+        cand = [v for v in range(s, e + 1) if v != u]
+        D = ((Xr[cand] - Xr[u]) ** 2).sum(1).astype(np.float32)
+        keys = np.array([oracle.fusion(float(dv), u, v, e - s + 1, 0.2, 0.5) for dv, v in zip(D, cand)])
+        order = np.lexsort((np.array(cand), keys))[:m]
+        assert ix.ENC[u, h].tolist() == [cand[i] for i in order]
+
+
+def test_build_beta0_leaf_is_vector_topm():
+    # with beta = 0 the leaf ENC rows are the plain vector top-m (numpy)
+    w = workloads.make("tiny", n=700, nq=1)
+    ix = oracle.build(w.X, w.attr, beta=0.0)
+    n, H, m = ix.ENC.shape
+    Xr = ix.X_rank.astype(np.float64)
+    for u in range(0, n, 11):
+        s, e = oracle.segment(n, H - 1, u)
+        cand = np.array([v for v in range(s, e + 1) if v != u])
+        D = ((Xr[cand] - Xr[u]) ** 2).sum(1).astype(np.float32)
+        assert ix.ENC[u, H - 1].tolist() == cand[np.lexsort((cand, D))[:m]].tolist()
+
+
+def test_boundary_effect_closed_form():
+    # Eq. naive_attr_dist: vector top-m inside a segment with attributes
+    # independent of vectors -> mean rank distance (l+1)/3 over positions,
+    # l/2 at the boundary.  The beta=0 leaf layer is exactly that method.
+    rng = np.random.default_rng(6)
+    n, d = 4096, 8
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    attr = rng.permutation(n).astype(np.float64)
+    ix = oracle.build(X, attr, beta=0.0, n_inv=5, m=1)   # leaves of 256, nearest neighbour only
+    H = ix.H
+    seglen = n >> (H - 1)
+    u = np.arange(n)
+    v = ix.ENC[:, H - 1, 0]
+    dist = np.abs(u - v)
+    assert abs(dist.mean() - (seglen + 1) / 3) < 0.05 * seglen / 3
+    t = u % seglen
+    bd = dist[(t == 0) | (t == seglen - 1)].mean()
+    assert abs(bd - seglen / 2) < 0.1 * seglen / 2
+    # fusion (beta > 0) pulls candidates closer in rank (Eq. fusion_attr_first_order)
+    ix2 = oracle.build(X, attr, beta=0.5, n_inv=5, m=1)
+    assert np.abs(u - ix2.ENC[:, H - 1, 0]).mean() < dist.mean()
+
+
+# ------------------------------------------------------------------ search
+
+def _bruteforce_rank_space(ix, q, l, r, k):
+    D = ((ix.X_rank[l:r + 1].astype(np.float64) - q.astype(np.float64)) ** 2).sum(1).astype(np.float32)
+    rank = np.arange(l, r + 1)
+    o = np.lexsort((rank, D))[:k]
+    return rank[o], D[o]
+
+
+def test_search_equals_bruteforce_when_range_fits_entry_set(tiny_index):
+    # P8a: cnt <= epn -> every in-range vertex is an entry point -> exact
+    w, ix = tiny_index
+    rng = np.random.default_rng(7)
+    nq = 60
+    start = rng.integers(0, ix.n - 40, nq)
+    cnt = rng.integers(1, 40, nq)
+    lo = start.astype(np.float64)
+    hi = (start + cnt - 1).astype(np.float64)
+    Q = w.Q[:nq]
+    ids, ds, st = oracle.search(ix, Q, lo, hi, 10, 64, epn=48, rank_ids=True)
+    gi, gd = oracle.exact(ix.X_rank, ix.attr_sorted, None, Q, lo, hi, 10, rank_ids=True)
+    assert (ids == gi).all() and (ds == gd).all()
+
+
+def test_search_large_pool_equals_closure_topk(tiny_index):
+    # P8b: with L >= n nothing is evicted, so the result is the exact top-k of
+    # the closure of the entry set under EN(.)
+    w, ix = tiny_index
+    n = ix.n
+    for i in range(0, 24):
+        q, lo, hi = w.Q[i], w.lo[i], w.hi[i]
+        l, r = oracle.rank_bounds(ix.attr_sorted, lo, hi)
+        Ls, Le = oracle.hotspot(l, r, ix.H, n)
+        ep = oracle.entry_points(l, r, 16, 0, i)
+        reach = oracle.closure(ix, l, r, Ls, Le, 16, ep)
+        ids, ds, st = oracle.search(ix, q[None], [lo], [hi], 10, n, qidx=[i], rank_ids=True)
+        vs = np.nonzero(reach)[0]
+        D = ((ix.X_rank[vs].astype(np.float64) - q.astype(np.float64)) ** 2).sum(1).astype(np.float32)
+        o = np.lexsort((vs, D))[:10]
+        kk = len(o)
+        assert ids[0, :kk].tolist() == vs[o].tolist()
+        assert st[0, oracle.STAT_DIST] == reach.sum()          # every reachable vertex evaluated once
+        assert st[0, oracle.STAT_EXPANSIONS] == reach.sum()    # and expanded once
+        if reach.sum() == r - l + 1:                            # closure = whole range -> brute force
+            bi, _ = _bruteforce_rank_space(ix, q, l, r, 10)
+            assert ids[0, :kk].tolist() == bi.tolist()
+
+
+def _textbook_kann(adj, dist_fn, entries, ef, k):
+    """Alg. 1 written independently: pool of (dist, id) kept sorted, expand the
+    closest unexpanded, insert every not-yet-computed neighbour, truncate."""
+    computed = set()
+    pool = []
+    for e in entries:
+        if e not in computed:
+            computed.add(e)
+            pool.append((dist_fn(e), e))
+    pool = sorted(pool)[:ef]
+    expanded = set()
+    while True:
+        nxt = [p for p in pool if p[1] not in expanded]
+        if not nxt:
+            break
+        u = nxt[0][1]
+        expanded.add(u)
+        for v in adj(u):
+            if v not in computed:
+                computed.add(v)
+                pool.append((dist_fn(v), v))
+        pool = sorted(pool)[:ef]
+    return [p[1] for p in pool[:k]], [p[0] for p in pool[:k]]
+
+
+def test_search_full_range_equals_textbook_greedy(tiny_index):
+    # P8c: full range, B <= m, no -1 in layer 0 -> L_start = 0 and EN(u) is the
+    # first B entries of u's layer-0 row, so FROGSearch is Alg. 1 over that graph
+    w, ix = tiny_index
+    assert (ix.ENC[:, 0, :] != -1).all()
+    n = ix.n
+    B = 12
+    for i in range(12):
+        q = w.Q[i]
+        ep = oracle.entry_points(0, n - 1, 16, 0, i)
+        qd = q.astype(np.float64)
+        Xr = ix.X_rank.astype(np.float64)
+        ref_ids, ref_d = _textbook_kann(lambda u: ix.ENC[u, 0, :B].tolist(),
+                                        lambda v: np.float32(((Xr[v] - qd) ** 2).sum()),
+                                        ep.tolist(), 32, 10)
+        ids, ds, _ = oracle.search(ix, q[None], [-np.inf], [np.inf], 10, 32, B=B, qidx=[i], rank_ids=True)
+        assert ids[0].tolist() == ref_ids
+
+
+def test_search_invariants_tiny_workload():
+    # P9 on the tiny workload: ids in range, distinct, ascending, distances
+    # equal to a numpy recomputation, expansions <= distance evaluations
+    w = workloads.make("tiny")
+    ix = oracle.build(w.X, w.attr)
+    ids, ds, st = oracle.search(ix, w.Q, w.lo, w.hi, w.k, 64, rank_ids=True)
+    for i in range(w.nq):
+        l, r = oracle.rank_bounds(ix.attr_sorted, w.lo[i], w.hi[i])
+        row = ids[i][ids[i] >= 0]
+        assert ((row >= l) & (row <= r)).all() and len(set(row.tolist())) == len(row)
+        assert (np.diff(ds[i][:len(row)]) >= 0).all()
+        ref = ((ix.X_rank[row].astype(np.float64) - w.Q[i].astype(np.float64)) ** 2).sum(1)
+        assert np.allclose(ds[i][:len(row)], ref.astype(np.float32), rtol=2e-7, atol=0)
+        assert st[i, oracle.STAT_EXPANSIONS] <= st[i, oracle.STAT_DIST]
+        assert len(row) == min(w.k, r - l + 1)
+    # recall against exhaustive search is high on this easy workload
+    gi, _ = oracle.exact(ix.X_rank, ix.attr_sorted, None, w.Q, w.lo, w.hi, w.k, rank_ids=True)
+    rec = np.mean([len(set(ids[i]) & set(gi[i])) / w.k for i in range(w.nq)])
+    assert rec > 0.8
+
+
+def test_search_degenerate_queries(tiny_index):
+    w, ix = tiny_index
+    Q = w.Q[:5]
+    lo = np.array([100.0, 5.0, np.nan, 0.0, 2999.0])
+    hi = np.array([99.0, 5.0, 10.0, 2.0, 5000.0])
+    ids, ds, st = oracle.search(ix, Q, lo, hi, 10, 64, rank_ids=True)
+    assert (ids[0] == -1).all() and np.isinf(ds[0]).all()
+    assert ids[1, 0] == 5 and (ids[1, 1:] == -1).all()
+    assert (ids[2] == -1).all()
+    assert sorted(ids[3, :3].tolist()) == [0, 1, 2] and (ids[3, 3:] == -1).all()
+    assert ids[4, 0] == 2999 and (ids[4, 1:] == -1).all()
