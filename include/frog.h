@@ -1,0 +1,170 @@
+/*
+ * frog.h — C ABI of the MI355X (gfx950) range-filtered k-NN search library.
+ *
+ * The library implements the query-time path of FROG ("FROG: Efficient
+ * Range-Filtering Approximate Nearest Neighbor Search on GPUs", arxiv
+ * 2608.16491) on one AMD GPU, plus the host-side index construction that
+ * produces its input and an exhaustive filtered search used as ground truth.
+ *
+ * Conventions for every entry point:
+ *   - Return value: FROG_OK (0) or a negative FROG_E* code.  frog_last_error()
+ *     returns a thread-local message for the last failure on the calling
+ *     thread.  No C++ exception crosses this ABI and the library never exits
+ *     the process.
+ *   - Host pointers are read during the call only.  Device pointers ("d_")
+ *     are caller-owned HIP device memory; they must stay valid until `stream`
+ *     has executed the enqueued work.  `stream` is a hipStream_t passed as
+ *     void* (NULL = the null stream).  Device entry points only ENQUEUE work
+ *     and return; every argument error detectable on the host is reported
+ *     before anything is enqueued.
+ *   - Ranks: objects are renumbered by ascending attribute (ties by original
+ *     index), so an attribute range [lo, hi] is the rank interval
+ *     [#{a < lo}, #{a <= hi} - 1] (Sec 4).  Results report ORIGINAL object
+ *     indices.  A NaN bound or lo > hi gives an empty range: not an error, the
+ *     output row is padding.
+ *   - Distances are SQUARED L2, accumulated in double from float inputs and
+ *     rounded once to float; rows of results are ascending by (distance,
+ *     rank).  Missing results (empty range, fewer than k reachable) are padded
+ *     with id -1 and distance +inf.  Inputs must be finite.
+ */
+#ifndef FROG_H
+#define FROG_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    FROG_OK = 0,
+    FROG_EINVAL = -1,        /* bad argument (null pointer, size, parameter) */
+    FROG_ENOMEM = -2,        /* host or device allocation failed */
+    FROG_EHIP = -3,          /* a HIP runtime call failed; message has its text */
+    FROG_EBADINDEX = -4,     /* index file: bad magic, version, size or checksum */
+    FROG_ENOTUPLOADED = -5,  /* device entry point called before frog_index_upload */
+    FROG_EIO = -6,           /* file could not be opened, read or written */
+    FROG_EUNSUPPORTED = -7   /* shape outside what the kernels are built for */
+};
+
+typedef struct frog_index frog_index_t; /* opaque; owns host and device copies */
+
+/* Index construction parameters (Sec 6; defaults of Sec 8.1.4). */
+typedef struct {
+    int m;            /* expansion-neighbour candidates per vertex per layer: 16 (d<=300), 32 */
+    int ef_c;         /* pool width of the construction-time greedy search: 128 (d<=300), 256 */
+    int n_inv;        /* deepest segment-tree layers omitted: 7 (d<=300), 6 */
+    int patience;     /* early-termination patience of the sibling search: 30 */
+    int sib_seeds;    /* seeds of each sibling search (stratified over the sibling): 16 */
+    int num_threads;  /* host threads; <= 0 means all available */
+    double beta;      /* fusion-distance shrink, Eq. fusion-distance: 0.2 */
+    double gamma;     /* fusion-distance decay: 0.5 */
+    uint64_t seed;    /* seed of the sibling-search seed jitter: 0 */
+} frog_build_params_t;
+
+/* Query-time parameters of FROGSearch (Alg. 2). */
+typedef struct {
+    int epn;            /* entry points; minimum count when epn_frac > 0: 16 */
+    double epn_frac;    /* 0: fixed epn; > 0: per-query count clamp(ceil(epn_frac*cnt), epn, epn_max) */
+    int epn_max;        /* upper bound of the per-query count (ignored when epn_frac == 0) */
+    int budget;         /* expansion budget B of ENIdentification (Alg. 4), 1..64: 16 */
+    uint64_t seed;      /* entry-point jitter seed: 0 */
+    int64_t query_base; /* batch index of query 0; keys the entry-point jitter: 0 */
+    int hash_log2;      /* visited table of 2^hash_log2 slots in LDS (6..13): 11;
+                           0 selects an exact visited set in device memory (slow;
+                           used to count distinct evaluations) */
+} frog_search_params_t;
+
+/* Per-query statistics written by frog_search_ex (int32, FROG_STAT_N per query). */
+enum {
+    FROG_STAT_EXPANSIONS = 0, /* pool entries expanded */
+    FROG_STAT_EN = 1,         /* sum over expansions of |EN(u)| */
+    FROG_STAT_DIST = 2,       /* distance evaluations performed (entry points included) */
+    FROG_STAT_SCANNED = 3,    /* ENC entries of the hotspot layers Alg. 4 examined */
+    FROG_STAT_ENTRY = 4,      /* entry points */
+    FROG_STAT_LSTART = 5,     /* hotspot first layer (Alg. 3) */
+    FROG_STAT_LEND = 6,       /* hotspot last layer */
+    FROG_STAT_LOADED = 7,     /* ENC entries actually loaded by the kernel */
+    FROG_STAT_N = 8
+};
+
+/* Fill *p with the paper's defaults for dimension d. */
+void frog_build_params_default(int d, frog_build_params_t* p);
+void frog_search_params_default(frog_search_params_t* p);
+
+/* Build the index on the host (Sec 6: attribute-rank domain, leaf brute force,
+ * bottom-up layers with child m-ANN + sibling greedy search (Alg. 1 with
+ * patience), RNG-pruned temporary graphs, fusion re-rank into the n x H x m
+ * candidate array of Sec 4).  X: n x d floats, row-major, original order;
+ * attr: n doubles (no NaN).  p = NULL uses frog_build_params_default(d).  On
+ * success *out owns a host index (not yet on a device). */
+int frog_build_index(const float* X, const double* attr, int64_t n, int d,
+                     const frog_build_params_t* p, frog_index_t** out);
+
+/* Wrap already-built arrays (copied): X_rank n x d floats in rank order,
+ * attr_sorted n ascending doubles, perm n ints (rank -> original index, a
+ * permutation), ENC n x H x m ints (each entry -1 or a rank).  Validates sizes,
+ * the permutation, the ordering of attr_sorted and the entry range. */
+int frog_index_from_arrays(const float* X_rank, const double* attr_sorted,
+                           const int32_t* perm, const int32_t* ENC,
+                           int64_t n, int d, int H, int m, frog_index_t** out);
+
+/* Copy the host arrays out (any pointer may be NULL to skip it). */
+int frog_index_export(const frog_index_t* idx, float* X_rank, double* attr_sorted,
+                      int32_t* perm, int32_t* ENC);
+int frog_index_info(const frog_index_t* idx, int64_t* n, int* d, int* H, int* m);
+
+/* Index file: header (magic, version, n, d, H, m), the four arrays, CRC-32 of
+ * everything before it.  Load reports FROG_EBADINDEX on any mismatch. */
+int frog_index_save(const frog_index_t* idx, const char* path);
+int frog_index_load(const char* path, frog_index_t** out);
+
+/* Copy the index to HIP device `device` (the HBM layout: X rows in rank order,
+ * padded to a multiple of 32 floats; ENC n x H x m; attr_sorted; perm).  The
+ * device copy is read-only afterwards, so concurrent searches on different
+ * streams are safe.  Calling it again replaces the previous device copy. */
+int frog_index_upload(frog_index_t* idx, int device);
+/* Release host and device memory.  NULL is a no-op. */
+void frog_index_free(frog_index_t* idx);
+
+/* Range -> rank interval (Sec 4) for nq queries: d_lr[2i] = l, d_lr[2i+1] = r
+ * (int32; l > r when empty). */
+int frog_rank_bounds(const frog_index_t* idx, const double* d_lo, const double* d_hi,
+                     int64_t nq, int32_t* d_lr, void* stream);
+
+/* FROGSearch (Alg. 2 with HotspotLocalization, Alg. 3, and ENIdentification,
+ * Alg. 4) for nq queries with default parameters.  d_queries: nq x d floats
+ * row-major; d_lo/d_hi: nq doubles; k >= 1, L in [k, 256] (pool size ef_s);
+ * outputs d_ids (int32) and d_dists (float), nq x k each. */
+int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
+                const double* d_lo, const double* d_hi, int k, int L,
+                int32_t* d_ids, float* d_dists, void* stream);
+
+/* As frog_search with explicit parameters (p = NULL: defaults) and optional
+ * per-query statistics d_stats (NULL or nq x FROG_STAT_N int32). */
+int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
+                   const double* d_lo, const double* d_hi, int k, int L,
+                   const frog_search_params_t* p, int32_t* d_ids, float* d_dists,
+                   int32_t* d_stats, void* stream);
+
+/* Exhaustive filtered k-NN (Def. 2, RFANNS): the exact k nearest objects whose
+ * attribute lies in [lo, hi].  The dot products q.x run on fp32 matrix cores;
+ * a per-query certified margin selects candidates that are re-ranked with the
+ * exact squared distance.  1 <= k <= 256.  d_certified (NULL or nq int32) is
+ * set to 1 where the margin proves the result exact, else 0 (the row then
+ * holds the best candidates found).  The ranges are read back to the host to
+ * group queries into tiles, so this call synchronises `stream`; it is a
+ * ground-truth tool, not the search path. */
+int frog_bruteforce_filtered(const frog_index_t* idx, const float* d_queries, int64_t nq,
+                             const double* d_lo, const double* d_hi, int k,
+                             int32_t* d_ids, float* d_dists, int32_t* d_certified,
+                             void* stream);
+
+/* Message of the last failure on this thread ("" if none). */
+const char* frog_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FROG_H */

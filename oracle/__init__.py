@@ -76,12 +76,16 @@ def _load():
     lib.fo_hotspot.restype = None
     lib.fo_hotspot.argtypes = [i64, i64, i32, i64, P, P]
     lib.fo_entry_points.restype = i64
-    lib.fo_entry_points.argtypes = [i64, i64, i32, u64, u64, P]
+    lib.fo_entry_points.argtypes = [i64, i64, i64, u64, u64, P]
+    lib.fo_entry_count.restype = i64
+    lib.fo_entry_count.argtypes = [i64, i32, f64, i32]
+    lib.fo_reduce.restype = u64
+    lib.fo_reduce.argtypes = [u64, u64]
     lib.fo_en_ident.restype = i32
     lib.fo_en_ident.argtypes = [P, i32, i32, i64, i64, i64, i32, i32, i32, P, P]
     lib.fo_search_batch.restype = i32
     lib.fo_search_batch.argtypes = [P, P, P, P, i64, i32, i32, i32, P, P, P, i64, P,
-                                    i32, i32, i32, i32, u64, P, P, P, i32]
+                                    i32, i32, i32, f64, i32, i32, u64, P, P, P, i32]
     lib.fo_exact_batch.restype = i32
     lib.fo_exact_batch.argtypes = [P, P, P, i64, i32, P, P, P, i64, i32, P, P, i32]
     lib.fo_fusion.restype = f64
@@ -232,10 +236,16 @@ def build(X, attr, *, m=None, ef_c=None, n_inv=None, patience=None, sib_seeds=No
 
 # ---------------------------------------------------------------- search
 
-def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, B: int = 16,
-           seed: int = 0, qidx=None, threads=None, rank_ids: bool = False):
+def entry_count(cnt: int, epn: int, epn_frac: float = 0.0, epn_max: int = 0) -> int:
+    return int(_load().fo_entry_count(cnt, epn, epn_frac, epn_max))
+
+
+def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, epn_frac: float = 0.0,
+           epn_max: int = 0, B: int = 16, seed: int = 0, qidx=None, threads=None,
+           rank_ids: bool = False):
     """FROGSearch for every query.  Returns (ids int32 [nq,k] original ids or
-    ranks, dists float32 [nq,k], stats int64 [nq,8])."""
+    ranks, dists float32 [nq,k], stats int64 [nq,8]).  The entry-point count
+    is epn, or clamp(ceil(epn_frac * cnt), epn, epn_max) when epn_frac > 0."""
     Q = _c(Q, np.float32)
     lo = _c(lo, np.float64)
     hi = _c(hi, np.float64)
@@ -249,7 +259,7 @@ def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, B: int 
     rc = _load().fo_search_batch(
         _p(ix.X_rank), _p(ENC), _p(ix.attr_sorted), None if rank_ids else _p(ix.perm),
         ix.n, ix.d, ix.H, ix.m, _p(Q), _p(lo), _p(hi), nq,
-        None if qi is None else _p(qi), k, L, epn, B, seed, _p(ids), _p(ds), _p(st),
+        None if qi is None else _p(qi), k, L, epn, epn_frac, epn_max, B, seed, _p(ids), _p(ds), _p(st),
         threads or default_threads())
     if rc:
         raise MemoryError("oracle search: allocation failed")

@@ -36,9 +36,12 @@
  *   - the boundary terms of Eq. endcondition use segment start positions:
  *     b_l = end of the segment holding l, plus one; b_r = start of the segment
  *     holding r; the test is (b_l-l + r-b_r) * 2^h >= r-l in integers;
- *   - entry points: all of [l,r] if it holds at most epn ranks, else one rank
- *     per stratum j of [l,r] split into epn equal strata, jittered by
- *     splitmix64(seed ^ (query_index << 32) ^ j);
+ *   - entry points: the count is epn, or, when epn_frac > 0, the per-query
+ *     count clamp(ceil(epn_frac * cnt), epn, epn_max) for a range of cnt ranks;
+ *     all of [l,r] is used if it holds at most that many ranks, else one rank
+ *     per stratum j of [l,r] split into equal strata, at offset
+ *     (hi32(splitmix64(seed ^ (query_index << 32) ^ j)) * width) >> 32 inside
+ *     the stratum (Lemire's multiply-shift range reduction);
  *   - duplicates inside EN(u) count against B; the visited set drops them;
  *   - the loop ends when no unexpanded entry is left in the pool;
  *   - empty ranges and fewer than k results pad with (id -1, +inf);
@@ -49,7 +52,7 @@
  *     RNG prune (alpha = 1) of the 2m candidates, topped up to m with the
  *     nearest pruned ones; the sibling search starts from `sib_seeds`
  *     stratified-jittered sibling ranks (splitmix64(seed ^ (u<<32) ^ (h<<24)
- *     ^ j)) and stops early after `patience` consecutive expansions that add
+ *     ^ j), reduced the same way) and stops early after `patience` consecutive expansions that add
  *     nothing to the current top-m.
  *
  * Nothing here is tuned.  OpenMP only spreads independent queries (or the
@@ -151,8 +154,26 @@ void fo_hotspot(int64_t l, int64_t r, int H, int64_t n, int* Ls, int* Le) {
     }
 }
 
+/* An offset in [0, width) from a 64-bit random word: high 32 bits times the
+ * width, high half of the product (Lemire, "Fast random integer generation
+ * in an interval", 2019).  width < 2^32. */
+uint64_t fo_reduce(uint64_t z, uint64_t width) {
+    return ((z >> 32) * width) >> 32;
+}
+
+/* Number of entry points for a range of cnt ranks. */
+int64_t fo_entry_count(int64_t cnt, int epn, double epn_frac, int epn_max) {
+    int64_t e = epn;
+    if (epn_frac > 0.0) {
+        double want = ceil(epn_frac * (double)cnt);
+        if (want > (double)epn_max) want = (double)epn_max;
+        if (want > (double)e) e = (int64_t)want;
+    }
+    return e;
+}
+
 /* Entry points drawn from [l, r]; returns their number. */
-int64_t fo_entry_points(int64_t l, int64_t r, int epn, uint64_t seed, uint64_t qi, int32_t* out) {
+int64_t fo_entry_points(int64_t l, int64_t r, int64_t epn, uint64_t seed, uint64_t qi, int32_t* out) {
     int64_t cnt = r - l + 1;
     if (cnt <= 0) return 0;
     if (cnt <= epn) {
@@ -163,7 +184,7 @@ int64_t fo_entry_points(int64_t l, int64_t r, int epn, uint64_t seed, uint64_t q
         int64_t s = l + (j * cnt) / epn;
         int64_t t = l + ((j + 1) * cnt) / epn - 1;
         uint64_t z = fo_splitmix64(seed ^ (qi << 32) ^ (uint64_t)j);
-        out[j] = (int32_t)(s + (int64_t)(z % (uint64_t)(t - s + 1)));
+        out[j] = (int32_t)(s + (int64_t)fo_reduce(z, (uint64_t)(t - s + 1)));
     }
     return epn;
 }
@@ -246,7 +267,8 @@ typedef struct {
 } fo_index;
 
 static void fo_search_one(const fo_index* ix, const float* q, double lo, double hi,
-                          int k, int L, int epn, int B, uint64_t seed, uint64_t qi,
+                          int k, int L, int epn, double epn_frac, int epn_max, int B,
+                          uint64_t seed, uint64_t qi,
                           int32_t* out_ids, float* out_d, int64_t* st,
                           fo_visited* vis, fo_cand* pool, fo_cand* work,
                           int32_t* ep, int32_t* EN) {
@@ -262,7 +284,8 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
     st[FO_ST_LE] = Le;
 
     /* entry points, their distances, pool = the L nearest of them */
-    int64_t ne = fo_entry_points(l, r, epn, seed, qi, ep);
+    int64_t ne = fo_entry_points(l, r, fo_entry_count(r - l + 1, epn, epn_frac, epn_max),
+                                 seed, qi, ep);
     st[FO_ST_ENTRY] = ne;
     fo_visited_clear(vis);
     int64_t nw = 0;
@@ -322,15 +345,17 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
 int fo_search_batch(const float* X, const int32_t* ENC, const double* attr_sorted,
                     const int32_t* perm, int64_t n, int d, int H, int m,
                     const float* Q, const double* lo, const double* hi, int64_t nq,
-                    const int64_t* qidx, int k, int L, int epn, int B, uint64_t seed,
-                    int32_t* out_ids, float* out_d, int64_t* stats, int nthreads) {
+                    const int64_t* qidx, int k, int L, int epn, double epn_frac, int epn_max,
+                    int B, uint64_t seed, int32_t* out_ids, float* out_d, int64_t* stats,
+                    int nthreads) {
     fo_index ix = { X, ENC, attr_sorted, perm, n, d, H, m };
     int fail = 0;
     if (nthreads <= 0) nthreads = 1;
 #pragma omp parallel num_threads(nthreads) reduction(|:fail)
     {
         fo_visited vis;
-        int64_t ep_cap = epn > 0 ? epn : 1;
+        int64_t ep_cap = fo_entry_count(n, epn, epn_frac, epn_max);
+        if (ep_cap < 1) ep_cap = 1;
         fo_cand* pool = (fo_cand*)malloc(sizeof(fo_cand) * (size_t)(L + 1));
         fo_cand* work = (fo_cand*)malloc(sizeof(fo_cand) * (size_t)(L + B + ep_cap + 1));
         int32_t* ep = (int32_t*)malloc(sizeof(int32_t) * (size_t)ep_cap);
@@ -341,7 +366,7 @@ int fo_search_batch(const float* X, const int32_t* ENC, const double* attr_sorte
 #pragma omp for schedule(dynamic, 4)
             for (int64_t i = 0; i < nq; ++i) {
                 int64_t st_local[FO_ST_N];
-                fo_search_one(&ix, Q + i * d, lo[i], hi[i], k, L, epn, B, seed,
+                fo_search_one(&ix, Q + i * d, lo[i], hi[i], k, L, epn, epn_frac, epn_max, B, seed,
                               (uint64_t)(qidx ? qidx[i] : i),
                               out_ids + i * k, out_d + i * k,
                               stats ? stats + i * FO_ST_N : st_local,
@@ -652,7 +677,7 @@ int fo_build(const float* X, const double* attr, int64_t n, int d,
                                 int64_t a = ts + ((int64_t)j * tl) / sib_seeds;
                                 int64_t b = ts + ((int64_t)(j + 1) * tl) / sib_seeds - 1;
                                 uint64_t z = fo_splitmix64(seed ^ ((uint64_t)u << 32) ^ ((uint64_t)h << 24) ^ (uint64_t)j);
-                                seeds[j] = (int32_t)(a + (int64_t)(z % (uint64_t)(b - a + 1)));
+                                seeds[j] = (int32_t)(a + (int64_t)fo_reduce(z, (uint64_t)(b - a + 1)));
                             }
                         }
                         int nr = fo_sibling_search(X_rank, d, PG, m, xu, ts, te, seeds, ns, ef_c,

@@ -1,0 +1,429 @@
+// extern "C" entry points of include/frog.h: argument validation, the index
+// container (host arrays, file format, device upload) and dispatch to the
+// host builder and the HIP launchers.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <thread>
+
+#include "frog_internal.h"
+
+namespace frog {
+
+static thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[1024];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+void clear_error() { g_err.clear(); }
+
+}  // namespace frog
+
+using frog::fail;
+
+namespace {
+
+#define HIP_TRY(expr)                                                                   \
+    do {                                                                                \
+        hipError_t e_ = (expr);                                                         \
+        if (e_ != hipSuccess)                                                           \
+            return fail(e_ == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "%s: %s", \
+                        #expr, hipGetErrorString(e_));                                  \
+    } while (0)
+
+void release_device(frog_index* ix) {
+    if (ix->device >= 0) {
+        int prev = 0;
+        hipGetDevice(&prev);
+        hipSetDevice(ix->device);
+        hipFree(ix->dX);
+        hipFree(ix->dENC);
+        hipFree(ix->dattr);
+        hipFree(ix->dperm);
+        hipSetDevice(prev);
+    }
+    ix->dX = nullptr;
+    ix->dENC = nullptr;
+    ix->dattr = nullptr;
+    ix->dperm = nullptr;
+    ix->device = -1;
+}
+
+// CRC-32 (IEEE 802.3, reflected polynomial 0xEDB88320), slicing by one byte.
+struct Crc32 {
+    uint32_t table[256];
+    Crc32() {
+        for (uint32_t i = 0; i < 256; ++i) {
+            uint32_t c = i;
+            for (int k = 0; k < 8; ++k) c = (c & 1) ? 0xEDB88320u ^ (c >> 1) : c >> 1;
+            table[i] = c;
+        }
+    }
+    uint32_t update(uint32_t crc, const void* data, size_t len) const {
+        const uint8_t* p = (const uint8_t*)data;
+        crc = ~crc;
+        for (size_t i = 0; i < len; ++i) crc = table[(crc ^ p[i]) & 0xFF] ^ (crc >> 8);
+        return ~crc;
+    }
+};
+const Crc32& crc32() {
+    static const Crc32 c;
+    return c;
+}
+
+constexpr char kMagic[8] = {'F', 'R', 'O', 'G', 'I', 'D', 'X', '1'};
+constexpr uint32_t kVersion = 1;
+
+struct FileHeader {
+    char magic[8];
+    uint32_t version;
+    uint32_t reserved;
+    int64_t n;
+    int32_t d, H, m, pad;
+};
+static_assert(sizeof(FileHeader) == 40, "file header layout");
+
+int validate_index_arrays(const double* attr, const int32_t* perm, const int32_t* ENC, int64_t n,
+                          int H, int m) {
+    for (int64_t i = 0; i < n; ++i) {
+        if (std::isnan(attr[i])) return fail(FROG_EINVAL, "attr_sorted[%lld] is NaN", (long long)i);
+        if (i > 0 && attr[i] < attr[i - 1])
+            return fail(FROG_EINVAL, "attr_sorted is not ascending at %lld", (long long)i);
+    }
+    std::vector<uint8_t> seen((size_t)n, 0);
+    for (int64_t i = 0; i < n; ++i) {
+        int32_t p = perm[i];
+        if (p < 0 || p >= n || seen[(size_t)p])
+            return fail(FROG_EINVAL, "perm is not a permutation (entry %lld)", (long long)i);
+        seen[(size_t)p] = 1;
+    }
+    const int64_t tot = n * H * m;
+    for (int64_t i = 0; i < tot; ++i) {
+        int32_t v = ENC[i];
+        if (v < -1 || v >= n) return fail(FROG_EINVAL, "ENC entry %lld out of range", (long long)i);
+    }
+    return FROG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* frog_last_error(void) { return frog::g_err.c_str(); }
+
+void frog_build_params_default(int d, frog_build_params_t* p) {
+    if (!p) return;
+    const bool small = d <= 300;
+    p->m = small ? 16 : 32;
+    p->ef_c = small ? 128 : 256;
+    p->n_inv = small ? 7 : 6;
+    p->patience = 30;
+    p->sib_seeds = 16;
+    p->num_threads = 0;
+    p->beta = 0.2;
+    p->gamma = 0.5;
+    p->seed = 0;
+}
+
+void frog_search_params_default(frog_search_params_t* p) {
+    if (!p) return;
+    p->epn = 16;
+    p->epn_frac = 0.0;
+    p->epn_max = 0;
+    p->budget = 16;
+    p->seed = 0;
+    p->query_base = 0;
+    p->hash_log2 = 11;
+}
+
+int frog_build_index(const float* X, const double* attr, int64_t n, int d,
+                     const frog_build_params_t* p, frog_index_t** out) {
+    frog::clear_error();
+    if (!out) return fail(FROG_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!X || !attr) return fail(FROG_EINVAL, "X or attr is NULL");
+    if (n < 1 || n > INT32_MAX - 1) return fail(FROG_EINVAL, "n=%lld outside [1, 2^31-2]", (long long)n);
+    if (d < 1 || d > 65536) return fail(FROG_EINVAL, "d=%d outside [1, 65536]", d);
+    frog_build_params_t q;
+    if (p) q = *p; else frog_build_params_default(d, &q);
+    if (q.m < 1 || q.m > 64) return fail(FROG_EINVAL, "m=%d outside [1, 64]", q.m);
+    if (q.ef_c < q.m || q.ef_c > 4096) return fail(FROG_EINVAL, "ef_c=%d outside [m, 4096]", q.ef_c);
+    if (q.n_inv < 0 || q.n_inv > 40) return fail(FROG_EINVAL, "n_inv=%d outside [0, 40]", q.n_inv);
+    if (q.patience < 1) return fail(FROG_EINVAL, "patience=%d < 1", q.patience);
+    if (q.sib_seeds < 1 || q.sib_seeds > 4096) return fail(FROG_EINVAL, "sib_seeds=%d outside [1, 4096]", q.sib_seeds);
+    if (!(q.beta >= 0.0 && q.beta < 1.0) || !(q.gamma > 0.0))
+        return fail(FROG_EINVAL, "beta=%g must be in [0,1), gamma=%g > 0", q.beta, q.gamma);
+    frog_index* ix = new (std::nothrow) frog_index;
+    if (!ix) return fail(FROG_ENOMEM, "allocation failed");
+    int rc = frog::build_host(X, attr, n, d, q, ix);
+    if (rc != FROG_OK) { delete ix; return rc; }
+    *out = ix;
+    return FROG_OK;
+}
+
+int frog_index_from_arrays(const float* X_rank, const double* attr_sorted, const int32_t* perm,
+                           const int32_t* ENC, int64_t n, int d, int H, int m, frog_index_t** out) {
+    frog::clear_error();
+    if (!out) return fail(FROG_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!X_rank || !attr_sorted || !perm || !ENC) return fail(FROG_EINVAL, "NULL array");
+    if (n < 1 || n > INT32_MAX - 1 || d < 1 || d > 65536 || H < 1 || H > 40 || m < 1 || m > 64)
+        return fail(FROG_EINVAL, "bad shape n=%lld d=%d H=%d m=%d", (long long)n, d, H, m);
+    int rc = validate_index_arrays(attr_sorted, perm, ENC, n, H, m);
+    if (rc) return rc;
+    frog_index* ix = new (std::nothrow) frog_index;
+    if (!ix) return fail(FROG_ENOMEM, "allocation failed");
+    try {
+        ix->n = n; ix->d = d; ix->H = H; ix->m = m;
+        ix->X.assign(X_rank, X_rank + n * d);
+        ix->attr.assign(attr_sorted, attr_sorted + n);
+        ix->perm.assign(perm, perm + n);
+        ix->ENC.assign(ENC, ENC + n * H * m);
+    } catch (const std::bad_alloc&) {
+        delete ix;
+        return fail(FROG_ENOMEM, "host allocation failed");
+    }
+    *out = ix;
+    return FROG_OK;
+}
+
+int frog_index_export(const frog_index_t* ix, float* X_rank, double* attr_sorted, int32_t* perm,
+                      int32_t* ENC) {
+    frog::clear_error();
+    if (!ix) return fail(FROG_EINVAL, "index is NULL");
+    if (X_rank) std::memcpy(X_rank, ix->X.data(), ix->X.size() * sizeof(float));
+    if (attr_sorted) std::memcpy(attr_sorted, ix->attr.data(), ix->attr.size() * sizeof(double));
+    if (perm) std::memcpy(perm, ix->perm.data(), ix->perm.size() * sizeof(int32_t));
+    if (ENC) std::memcpy(ENC, ix->ENC.data(), ix->ENC.size() * sizeof(int32_t));
+    return FROG_OK;
+}
+
+int frog_index_info(const frog_index_t* ix, int64_t* n, int* d, int* H, int* m) {
+    frog::clear_error();
+    if (!ix) return fail(FROG_EINVAL, "index is NULL");
+    if (n) *n = ix->n;
+    if (d) *d = ix->d;
+    if (H) *H = ix->H;
+    if (m) *m = ix->m;
+    return FROG_OK;
+}
+
+int frog_index_save(const frog_index_t* ix, const char* path) {
+    frog::clear_error();
+    if (!ix || !path) return fail(FROG_EINVAL, "NULL argument");
+    FILE* f = std::fopen(path, "wb");
+    if (!f) return fail(FROG_EIO, "cannot open %s for writing", path);
+    FileHeader h{};
+    std::memcpy(h.magic, kMagic, 8);
+    h.version = kVersion;
+    h.n = ix->n; h.d = ix->d; h.H = ix->H; h.m = ix->m;
+    uint32_t crc = 0;
+    struct Part { const void* p; size_t len; } parts[5] = {
+        {&h, sizeof(h)},
+        {ix->X.data(), ix->X.size() * sizeof(float)},
+        {ix->attr.data(), ix->attr.size() * sizeof(double)},
+        {ix->perm.data(), ix->perm.size() * sizeof(int32_t)},
+        {ix->ENC.data(), ix->ENC.size() * sizeof(int32_t)}};
+    bool ok = true;
+    for (auto& part : parts) {
+        crc = crc32().update(crc, part.p, part.len);
+        ok = ok && std::fwrite(part.p, 1, part.len, f) == part.len;
+    }
+    ok = ok && std::fwrite(&crc, 4, 1, f) == 1;
+    ok = (std::fclose(f) == 0) && ok;
+    return ok ? FROG_OK : fail(FROG_EIO, "write to %s failed", path);
+}
+
+int frog_index_load(const char* path, frog_index_t** out) {
+    frog::clear_error();
+    if (!path || !out) return fail(FROG_EINVAL, "NULL argument");
+    *out = nullptr;
+    FILE* f = std::fopen(path, "rb");
+    if (!f) return fail(FROG_EIO, "cannot open %s", path);
+    FileHeader h{};
+    if (std::fread(&h, sizeof(h), 1, f) != 1) { std::fclose(f); return fail(FROG_EBADINDEX, "short header"); }
+    if (std::memcmp(h.magic, kMagic, 8) != 0 || h.version != kVersion) {
+        std::fclose(f);
+        return fail(FROG_EBADINDEX, "bad magic or version in %s", path);
+    }
+    if (h.n < 1 || h.n > INT32_MAX - 1 || h.d < 1 || h.d > 65536 || h.H < 1 || h.H > 40 || h.m < 1 || h.m > 64) {
+        std::fclose(f);
+        return fail(FROG_EBADINDEX, "bad shape in header");
+    }
+    frog_index* ix = new (std::nothrow) frog_index;
+    if (!ix) { std::fclose(f); return fail(FROG_ENOMEM, "allocation failed"); }
+    try {
+        ix->n = h.n; ix->d = h.d; ix->H = h.H; ix->m = h.m;
+        ix->X.resize((size_t)h.n * h.d);
+        ix->attr.resize((size_t)h.n);
+        ix->perm.resize((size_t)h.n);
+        ix->ENC.resize((size_t)h.n * h.H * h.m);
+    } catch (const std::bad_alloc&) {
+        delete ix;
+        std::fclose(f);
+        return fail(FROG_ENOMEM, "host allocation failed");
+    }
+    uint32_t crc = crc32().update(0, &h, sizeof(h));
+    struct Part { void* p; size_t len; } parts[4] = {
+        {ix->X.data(), ix->X.size() * sizeof(float)},
+        {ix->attr.data(), ix->attr.size() * sizeof(double)},
+        {ix->perm.data(), ix->perm.size() * sizeof(int32_t)},
+        {ix->ENC.data(), ix->ENC.size() * sizeof(int32_t)}};
+    bool ok = true;
+    for (auto& part : parts) {
+        ok = ok && std::fread(part.p, 1, part.len, f) == part.len;
+        if (ok) crc = crc32().update(crc, part.p, part.len);
+    }
+    uint32_t stored = 0;
+    ok = ok && std::fread(&stored, 4, 1, f) == 1;
+    std::fclose(f);
+    if (!ok || stored != crc) {
+        delete ix;
+        return fail(FROG_EBADINDEX, "truncated file or checksum mismatch in %s", path);
+    }
+    int rc = validate_index_arrays(ix->attr.data(), ix->perm.data(), ix->ENC.data(), ix->n, ix->H, ix->m);
+    if (rc) { delete ix; return fail(FROG_EBADINDEX, "%s", frog_last_error()); }
+    *out = ix;
+    return FROG_OK;
+}
+
+int frog_index_upload(frog_index_t* ix, int device) {
+    frog::clear_error();
+    if (!ix) return fail(FROG_EINVAL, "index is NULL");
+    int ndev = 0;
+    HIP_TRY(hipGetDeviceCount(&ndev));
+    if (device < 0 || device >= ndev) return fail(FROG_EINVAL, "device %d not in [0, %d)", device, ndev);
+    release_device(ix);
+    int prev = 0;
+    HIP_TRY(hipGetDevice(&prev));
+    HIP_TRY(hipSetDevice(device));
+    const int dp = (ix->d + 31) / 32 * 32;
+    const size_t nX = (size_t)ix->n * dp, nE = (size_t)ix->n * ix->H * ix->m;
+    ix->device = device;
+    ix->dp = dp;
+    auto bail = [&](int rc) { release_device(ix); hipSetDevice(prev); return rc; };
+    hipError_t e = hipMalloc(&ix->dX, nX * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&ix->dENC, nE * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&ix->dattr, (size_t)ix->n * sizeof(double));
+    if (e == hipSuccess) e = hipMalloc(&ix->dperm, (size_t)ix->n * sizeof(int32_t));
+    if (e != hipSuccess)
+        return bail(fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "device allocation: %s",
+                         hipGetErrorString(e)));
+    if (dp == ix->d) {
+        e = hipMemcpy(ix->dX, ix->X.data(), nX * sizeof(float), hipMemcpyHostToDevice);
+    } else {
+        e = hipMemset(ix->dX, 0, nX * sizeof(float));
+        if (e == hipSuccess)
+            e = hipMemcpy2D(ix->dX, (size_t)dp * sizeof(float), ix->X.data(), (size_t)ix->d * sizeof(float),
+                            (size_t)ix->d * sizeof(float), (size_t)ix->n, hipMemcpyHostToDevice);
+    }
+    if (e == hipSuccess) e = hipMemcpy(ix->dENC, ix->ENC.data(), nE * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(ix->dattr, ix->attr.data(), (size_t)ix->n * sizeof(double), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(ix->dperm, ix->perm.data(), (size_t)ix->n * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return bail(fail(FROG_EHIP, "upload: %s", hipGetErrorString(e)));
+    hipSetDevice(prev);
+    return FROG_OK;
+}
+
+void frog_index_free(frog_index_t* ix) {
+    if (!ix) return;
+    release_device(ix);
+    delete ix;
+}
+
+}  // extern "C"
+
+namespace {
+
+frog::DevIndex view(const frog_index* ix) {
+    return frog::DevIndex{ix->dX, ix->dENC, ix->dattr, ix->dperm, ix->n, ix->d, ix->dp, ix->H, ix->m};
+}
+
+// Device entry points run on the index's device; the caller's stream must
+// belong to it.
+int check_device_index(const frog_index_t* ix) {
+    if (!ix) return fail(FROG_EINVAL, "index is NULL");
+    if (ix->device < 0 || !ix->dX) return fail(FROG_ENOTUPLOADED, "index has not been uploaded");
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
+    if (cur != ix->device)
+        return fail(FROG_EINVAL, "current device %d differs from the index's device %d", cur, ix->device);
+    return FROG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int frog_rank_bounds(const frog_index_t* ix, const double* d_lo, const double* d_hi, int64_t nq,
+                     int32_t* d_lr, void* stream) {
+    frog::clear_error();
+    int rc = check_device_index(ix);
+    if (rc) return rc;
+    if (nq < 0) return fail(FROG_EINVAL, "nq < 0");
+    if (nq == 0) return FROG_OK;
+    if (!d_lo || !d_hi || !d_lr) return fail(FROG_EINVAL, "NULL device pointer");
+    return frog::launch_rank_bounds(view(ix), d_lo, d_hi, nq, d_lr, stream);
+}
+
+int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo,
+                   const double* d_hi, int k, int L, const frog_search_params_t* p, int32_t* d_ids,
+                   float* d_dists, int32_t* d_stats, void* stream) {
+    frog::clear_error();
+    int rc = check_device_index(ix);
+    if (rc) return rc;
+    frog_search_params_t q;
+    if (p) q = *p; else frog_search_params_default(&q);
+    if (nq < 0) return fail(FROG_EINVAL, "nq < 0");
+    if (k < 1 || L < k || L > 256) return fail(FROG_EINVAL, "need 1 <= k <= L <= 256 (k=%d, L=%d)", k, L);
+    if (q.budget < 1 || q.budget > 64) return fail(FROG_EINVAL, "budget=%d outside [1, 64]", q.budget);
+    if (q.epn < 1 || q.epn > (1 << 20)) return fail(FROG_EINVAL, "epn=%d outside [1, 2^20]", q.epn);
+    if (!(q.epn_frac >= 0.0) || q.epn_frac > 1.0) return fail(FROG_EINVAL, "epn_frac=%g outside [0, 1]", q.epn_frac);
+    if (q.epn_frac > 0.0 && (q.epn_max < q.epn || q.epn_max > (1 << 20)))
+        return fail(FROG_EINVAL, "epn_max=%d outside [epn, 2^20]", q.epn_max);
+    if (q.hash_log2 != 0 && (q.hash_log2 < 6 || q.hash_log2 > 13))
+        return fail(FROG_EINVAL, "hash_log2=%d: 0 or 6..13", q.hash_log2);
+    if (q.query_base < 0) return fail(FROG_EINVAL, "query_base < 0");
+    if (!frog::search_shape_supported(ix->dp, ix->m, L))
+        return fail(FROG_EUNSUPPORTED, "no search kernel for padded d=%d, m=%d, L=%d", ix->dp, ix->m, L);
+    if (nq == 0) return FROG_OK;
+    if (!d_queries || !d_lo || !d_hi || !d_ids || !d_dists) return fail(FROG_EINVAL, "NULL device pointer");
+    frog::SearchLaunch a{};
+    a.Q = d_queries; a.nq = nq; a.lo = d_lo; a.hi = d_hi; a.k = k; a.L = L;
+    a.epn = q.epn; a.epn_max = q.epn_frac > 0.0 ? q.epn_max : q.epn; a.epn_frac = q.epn_frac;
+    a.B = q.budget; a.hash_log2 = q.hash_log2; a.seed = q.seed; a.qbase = q.query_base;
+    a.ids = d_ids; a.dists = d_dists; a.stats = d_stats;
+    return frog::launch_search(view(ix), a, stream);
+}
+
+int frog_search(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo,
+                const double* d_hi, int k, int L, int32_t* d_ids, float* d_dists, void* stream) {
+    return frog_search_ex(ix, d_queries, nq, d_lo, d_hi, k, L, nullptr, d_ids, d_dists, nullptr, stream);
+}
+
+int frog_bruteforce_filtered(const frog_index_t* ix, const float* d_queries, int64_t nq,
+                             const double* d_lo, const double* d_hi, int k, int32_t* d_ids,
+                             float* d_dists, int32_t* d_certified, void* stream) {
+    frog::clear_error();
+    int rc = check_device_index(ix);
+    if (rc) return rc;
+    if (nq < 0) return fail(FROG_EINVAL, "nq < 0");
+    if (k < 1 || k > 256) return fail(FROG_EINVAL, "k=%d outside [1, 256]", k);
+    if (nq == 0) return FROG_OK;
+    if (!d_queries || !d_lo || !d_hi || !d_ids || !d_dists) return fail(FROG_EINVAL, "NULL device pointer");
+    return frog::launch_bruteforce(ix, d_queries, nq, d_lo, d_hi, k, d_ids, d_dists, d_certified, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,694 @@
+// FROGSearch on gfx950: range -> rank interval (Sec 4), HotspotLocalization
+// (Alg. 3), entry points (Alg. 2), and the best-first loop of Alg. 2 with
+// ENIdentification (Alg. 4), the lazy visited check, distance evaluation and
+// MergeTopEfS.
+//
+// Mapping to CDNA4:
+//   - one query per 64-lane wavefront, four independent wavefronts per
+//     workgroup, a persistent grid that takes queries from an atomic counter;
+//   - the candidate pool (size L <= 64*LP) lives in VGPRs: pool slot p is
+//     register s = p / 64 of lane p % 64, holding a 64-bit key
+//     (float bits of the squared distance << 32 | rank) -- for non-negative
+//     floats the bit pattern orders like the value, so (distance, rank) order
+//     is one unsigned compare -- and an expanded flag;
+//   - selecting the first unexpanded entry is one ballot per register;
+//   - ENIdentification loads up to 64 hotspot candidates per wave load (one
+//     per lane, in stored order) and compacts the in-range ones with
+//     ballot + mbcnt under the budget B, as Alg. 4 describes for a warp;
+//   - the visited check runs after compaction (the paper's lazy check) on a
+//     direct-mapped table of 2^hash_log2 ranks in LDS: a lookup is one read,
+//     an insert one write.  The table may forget a vertex (a later insert to
+//     the same slot overwrites it) but never reports an unseen vertex as
+//     seen.  Forgetting cannot change the result: a re-evaluated vertex gets
+//     the same key; if it is still in the pool the merge drops the duplicate,
+//     and if it is not, it was rejected or evicted when the pool was full, so
+//     its key is at or above the pool's current L-th key (which never grows)
+//     and the merge rejects it again.  Only the number of evaluations grows.
+//     hash_log2 = 0 selects an exact per-wave bitmap in device memory instead
+//     (used to count distinct evaluations);
+//   - distances: each vector is read by 8 lanes as 16-byte loads (128
+//     contiguous bytes per load instruction and vector), differences and
+//     squares in double, an 8-lane butterfly sum, one rounding to float --
+//     the library's canonical squared L2.  d > 128 uses all 64 lanes per
+//     vector.  No matrix cores: every gathered vector is used once;
+//   - MergeTopEfS: a new key's position is (# pool keys below it) + (# new
+//     keys below it), counted with ballots; a pool key's position is its slot
+//     plus (# new keys below it); entries scatter through LDS.  Keys are
+//     unique once duplicates are dropped, so this equals sorting the union.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <mutex>
+#include <map>
+
+#include "frog_internal.h"
+
+namespace frog {
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+constexpr uint64_t kEmpty = ~0ull;
+
+struct KParams {
+    DevIndex ix;
+    SearchLaunch a;
+    unsigned int* counter;   // persistent-grid work counter
+    uint32_t* gvis;          // exact visited bitmaps (hash_log2 == 0)
+    int64_t gvis_words;      // words per wave
+    int lds_per_wave;        // bytes
+};
+
+// ------------------------------------------------------------------ wave helpers
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+__device__ __forceinline__ int mbcnt(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+    uint32_t lo = __builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Orders LDS traffic between the lanes of one wavefront.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ULL;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ uint64_t make_key(float d, int32_t id) {
+    return ((uint64_t)__float_as_uint(d) << 32) | (uint32_t)id;
+}
+
+// ------------------------------------------------------------------ a1: ranks
+
+// Number of entries of the ascending array a[0, n) below x (inclusive: <= x),
+// by a 64-ary search: each round every lane probes one position and a ballot
+// narrows the interval 64-fold.
+__device__ int64_t count_below(const double* __restrict__ a, int64_t n, double x, bool inclusive) {
+    const int lane = lane_id();
+    int64_t lo = 0, hi = n;
+    while (hi > lo) {
+        const int64_t step = (hi - lo + 63) / 64;
+        const int64_t p = lo + (int64_t)(lane + 1) * step - 1;
+        bool below = false;
+        if (p < hi) {
+            const double v = a[p];
+            below = inclusive ? (v <= x) : (v < x);
+        }
+        const int c = __popcll(ballot(below));
+        const int64_t nlo = lo + (int64_t)c * step;
+        int64_t nhi = lo + (int64_t)(c + 1) * step - 1;
+        if (nhi > hi) nhi = hi;
+        lo = uniform64(nlo);
+        hi = uniform64(nhi);
+    }
+    return lo;
+}
+
+__device__ void rank_interval(const DevIndex& ix, double lo_v, double hi_v, int64_t& l, int64_t& r) {
+    if (isnan(lo_v) || isnan(hi_v)) { l = 0; r = -1; return; }
+    l = count_below(ix.attr, ix.n, lo_v, false);
+    r = count_below(ix.attr, ix.n, hi_v, true) - 1;
+}
+
+// ------------------------------------------------------------------ a2: hotspot
+
+__device__ void segment_of(int64_t n, int h, int64_t p, int64_t& s, int64_t& e) {
+    int64_t L = 0, R = n - 1;
+    for (int i = 0; i < h; ++i) {
+        const int64_t mid = L + (R - L) / 2;
+        if (p <= mid) R = mid; else L = mid + 1;
+    }
+    s = L;
+    e = R;
+}
+
+// Alg. 3: L_start = depth of the deepest segment holding [l, r] (at most H-1);
+// L_end extends over consecutive deeper layers while Eq. endcondition holds,
+// with the boundary terms b_l = (end of l's segment) + 1, b_r = start of r's.
+__device__ void hotspot(int64_t l, int64_t r, int H, int64_t n, int& Ls, int& Le) {
+    int64_t L = 0, R = n - 1;
+    int d = 0;
+    while (d < H - 1) {
+        const int64_t mid = L + (R - L) / 2;
+        if (r <= mid) R = mid;
+        else if (l >= mid + 1) L = mid + 1;
+        else break;
+        ++d;
+    }
+    Ls = d;
+    Le = d;
+    for (int h = d + 1; h <= H - 1; ++h) {
+        int64_t sl, el, sr, er;
+        segment_of(n, h, l, sl, el);
+        segment_of(n, h, r, sr, er);
+        const int64_t lhs = (el + 1 - l) + (r - sr);
+        if (lhs * ((int64_t)1 << h) >= (r - l)) Le = h;
+        else break;
+    }
+}
+
+// ------------------------------------------------------------------ a8: distances
+
+// Squared L2 of up to `cnt` (<= 64) candidates; lane j holds candidate j's
+// rank in `myid` and receives its distance in the return value.  The query's
+// float4 chunks this lane needs are in qv.
+template <int C>
+__device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
+    // G = 8 lanes per vector: lane reads float4 chunks (lane % 8) + 8c.
+    const int lane = lane_id();
+    const int sub = lane & 7;
+    const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
+    const int dp4 = dp >> 2;
+    float mine = 0.f;
+    for (int sb0 = 0; sb0 < cnt; sb0 += 16) {
+        // two groups of 8 vectors per step: issue all loads first
+        const int j0 = sb0 + (lane >> 3);
+        const int j1 = j0 + 8;
+        const int id0 = __shfl(myid, j0 & 63);
+        const int id1 = __shfl(myid, j1 & 63);
+        const bool v0 = j0 < cnt, v1 = j1 < cnt;
+        float4 x0[C], x1[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            x0[c] = v0 ? X4[(int64_t)id0 * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
+            x1[c] = v1 ? X4[(int64_t)id1 * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const double q0 = qv[c].x, q1 = qv[c].y, q2 = qv[c].z, q3 = qv[c].w;
+            double t;
+            t = q0 - (double)x0[c].x; s0 += t * t;
+            t = q1 - (double)x0[c].y; s0 += t * t;
+            t = q2 - (double)x0[c].z; s0 += t * t;
+            t = q3 - (double)x0[c].w; s0 += t * t;
+            t = q0 - (double)x1[c].x; s1 += t * t;
+            t = q1 - (double)x1[c].y; s1 += t * t;
+            t = q2 - (double)x1[c].z; s1 += t * t;
+            t = q3 - (double)x1[c].w; s1 += t * t;
+        }
+        s0 += __shfl_xor(s0, 1);
+        s1 += __shfl_xor(s1, 1);
+        s0 += __shfl_xor(s0, 2);
+        s1 += __shfl_xor(s1, 2);
+        s0 += __shfl_xor(s0, 4);
+        s1 += __shfl_xor(s1, 4);
+        const float f0 = (float)s0, f1 = (float)s1;
+        // vector sb0 + g (g < 8) sits in lanes 8g..8g+7 of f0, sb0 + 8 + g in f1
+        const int src = (lane & 7) << 3;
+        const float g0 = __shfl(f0, src);
+        const float g1 = __shfl(f1, src);
+        if ((lane >> 3) == ((sb0 >> 3) & 7)) mine = g0;
+        if ((lane >> 3) == (((sb0 >> 3) + 1) & 7)) mine = g1;
+    }
+    return mine;
+}
+
+// d > 128: all 64 lanes read one vector, float4 chunk lane + 64c.
+__device__ float eval_large(const float* __restrict__ X, int dp, const float* __restrict__ q, int d, int cnt,
+                            int32_t myid) {
+    const int lane = lane_id();
+    const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
+    const int dp4 = dp >> 2;
+    float mine = 0.f;
+    for (int j = 0; j < cnt; ++j) {
+        const int id = __builtin_amdgcn_readlane(myid, j);
+        double s = 0.0;
+        for (int c = lane; c < dp4; c += 64) {
+            const float4 x = X4[(int64_t)id * dp4 + c];
+            const int b = 4 * c;
+            const double q0 = b < d ? q[b] : 0.f, q1 = b + 1 < d ? q[b + 1] : 0.f;
+            const double q2 = b + 2 < d ? q[b + 2] : 0.f, q3 = b + 3 < d ? q[b + 3] : 0.f;
+            double t;
+            t = q0 - (double)x.x; s += t * t;
+            t = q1 - (double)x.y; s += t * t;
+            t = q2 - (double)x.z; s += t * t;
+            t = q3 - (double)x.w; s += t * t;
+        }
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o);
+        if (lane == j) mine = (float)s;
+    }
+    return mine;
+}
+
+// ------------------------------------------------------------------ pool
+
+template <int LP>
+struct Pool {
+    uint64_t key[LP];
+    uint32_t flag[LP];
+    int np;  // valid entries, wave-uniform
+};
+
+// MergeTopEfS: merge new keys (lane j < ns holds one; others kEmpty) into the
+// pool, dropping keys already present and keys at or beyond the pool's L-th
+// when it is full.  Returns the number of keys that entered.
+template <int LP>
+__device__ int merge(Pool<LP>& P, uint64_t nkey, int ns, int L, uint64_t* st_key, uint32_t* st_flag) {
+    const int lane = lane_id();
+    bool cand = lane < ns;
+    if (P.np >= L) {
+        const int t = L - 1;
+        uint64_t thr = 0;
+#pragma unroll
+        for (int s = 0; s < LP; ++s)
+            if (s == (t >> 6)) thr = readlane64(P.key[s], t & 63);
+        cand = cand && nkey < thr;
+    }
+    uint64_t cmask = ballot(cand);
+    if (cmask == 0) return 0;
+    // drop duplicates: of a pool key, or of an earlier new key
+    bool keep = cand;
+    for (uint64_t m = cmask; m; m &= m - 1) {
+        const int j = __builtin_ctzll(m);
+        const uint64_t kj = readlane64(nkey, j);
+        bool eq = false;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) eq |= P.key[s] == kj;
+        if (ballot(eq) != 0 && lane == j) keep = false;
+        if (lane > j && nkey == kj) keep = false;
+    }
+    const uint64_t kmask = ballot(keep);
+    const int nk = __popcll(kmask);
+    if (nk == 0) return 0;
+    // positions
+    int ltN = 0, cntP = 0;
+    int ltP[LP];
+#pragma unroll
+    for (int s = 0; s < LP; ++s) ltP[s] = 0;
+    for (uint64_t m = kmask; m; m &= m - 1) {
+        const int j = __builtin_ctzll(m);
+        const uint64_t kj = readlane64(nkey, j);
+        int c = 0;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) {
+            c += __popcll(ballot(P.key[s] < kj));
+            ltP[s] += kj < P.key[s] ? 1 : 0;
+        }
+        if (lane == j) cntP = c;
+        ltN += kj < nkey ? 1 : 0;
+    }
+    // scatter
+#pragma unroll
+    for (int s = 0; s < LP; ++s) {
+        const int p = s * 64 + lane;
+        const int pos = p + ltP[s];
+        if (p < P.np && pos < L) {
+            st_key[pos] = P.key[s];
+            st_flag[pos] = P.flag[s];
+        }
+    }
+    if (keep) {
+        const int pos = cntP + ltN;
+        if (pos < L) {
+            st_key[pos] = nkey;
+            st_flag[pos] = 0u;
+        }
+    }
+    P.np = P.np + nk < L ? P.np + nk : L;
+    wave_sync();
+#pragma unroll
+    for (int s = 0; s < LP; ++s) {
+        const int p = s * 64 + lane;
+        P.key[s] = p < P.np ? st_key[p] : kEmpty;
+        P.flag[s] = p < P.np ? st_flag[p] : 0u;
+    }
+    wave_sync();
+    return nk;
+}
+
+// ------------------------------------------------------------------ visited set
+
+struct Visited {
+    int32_t* tab;        // LDS table (forgetful) or nullptr
+    uint32_t* bits;      // exact bitmap in device memory
+    int shift;           // 32 - hash_log2
+    __device__ __forceinline__ uint32_t slot(int32_t v) const { return ((uint32_t)v * 0x9E3779B1u) >> shift; }
+    // true if v has not been seen (and records it); never false for an unseen v
+    __device__ __forceinline__ bool check_insert(int32_t v) const {
+        if (tab) {
+            const uint32_t s = slot(v);
+            if (tab[s] == v) return false;
+            tab[s] = v;
+            return true;
+        }
+        const uint32_t bit = 1u << (v & 31);
+        return (atomicOr(bits + (v >> 5), bit) & bit) == 0;
+    }
+    __device__ __forceinline__ void insert(int32_t v) const {
+        if (tab) tab[slot(v)] = v;
+        else atomicOr(bits + (v >> 5), 1u << (v & 31));
+    }
+};
+
+// ------------------------------------------------------------------ kernel
+
+template <int C, int LP>
+__global__ __launch_bounds__(kBlock) void search_kernel(KParams P) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const DevIndex& ix = P.ix;
+    const SearchLaunch& A = P.a;
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    char* wbase = smem + (size_t)wave * P.lds_per_wave;
+    uint64_t* st_key = reinterpret_cast<uint64_t*>(wbase);
+    uint32_t* st_flag = reinterpret_cast<uint32_t*>(st_key + 64 * LP);
+    int32_t* enbuf = reinterpret_cast<int32_t*>(st_flag + 64 * LP);
+    Visited vis;
+    vis.tab = A.hash_log2 > 0 ? enbuf + 64 : nullptr;
+    vis.shift = 32 - A.hash_log2;
+    const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+    vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
+    const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
+    const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
+
+    for (;;) {
+        int qi_l = 0;
+        if (lane == 0) qi_l = (int)atomicAdd(P.counter, 1u);
+        const int64_t qi = uniform(__shfl(qi_l, 0));
+        if (qi >= A.nq) break;
+
+        int32_t st[FROG_STAT_N];
+#pragma unroll
+        for (int i = 0; i < FROG_STAT_N; ++i) st[i] = 0;
+
+        // a1: range -> ranks
+        int64_t l, r;
+        rank_interval(ix, A.lo[qi], A.hi[qi], l, r);
+        l = uniform64(l);
+        r = uniform64(r);
+        Pool<LP> pool;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+        pool.np = 0;
+
+        if (l <= r) {
+            // a2: hotspot
+            int Ls, Le;
+            hotspot(l, r, H, ix.n, Ls, Le);
+            Ls = uniform(Ls);
+            Le = uniform(Le);
+            st[FROG_STAT_LSTART] = Ls;
+            st[FROG_STAT_LEND] = Le;
+
+            // query chunks
+            float4 qv[C > 0 ? C : 1];
+            const float* qrow = A.Q + qi * ix.d;
+            if constexpr (C > 0) {
+#pragma unroll
+                for (int c = 0; c < C; ++c) {
+                    const int b = 4 * ((lane & 7) + 8 * c);
+                    qv[c].x = b < ix.d ? qrow[b] : 0.f;
+                    qv[c].y = b + 1 < ix.d ? qrow[b + 1] : 0.f;
+                    qv[c].z = b + 2 < ix.d ? qrow[b + 2] : 0.f;
+                    qv[c].w = b + 3 < ix.d ? qrow[b + 3] : 0.f;
+                }
+            }
+            auto eval = [&](int cnt, int32_t myid) -> float {
+                if constexpr (C > 0) return eval_small<C>(ix.X, ix.dp, qv, cnt, myid);
+                else return eval_large(ix.X, ix.dp, qrow, ix.d, cnt, myid);
+            };
+
+            // reset the visited set
+            if (vis.tab) {
+                for (int i = lane; i < T; i += 64) vis.tab[i] = -1;
+            } else {
+                for (int64_t i = lane; i < P.gvis_words; i += 64) vis.bits[i] = 0u;
+                __threadfence();
+            }
+            wave_sync();
+
+            // a3: entry points
+            const int64_t cnt = r - l + 1;
+            int64_t E = A.epn;
+            if (A.epn_frac > 0.0) {
+                double want = ceil(A.epn_frac * (double)cnt);
+                if (want > (double)A.epn_max) want = (double)A.epn_max;
+                if (want > (double)E) E = (int64_t)want;
+            }
+            const bool all = cnt <= E;
+            const int64_t ne = all ? cnt : E;
+            st[FROG_STAT_ENTRY] = (int32_t)ne;
+            const uint64_t qkey = (uint64_t)(A.qbase + qi) << 32;
+            for (int64_t b0 = 0; b0 < ne; b0 += 16) {
+                const int nb = (int)(ne - b0 < 16 ? ne - b0 : 16);
+                int32_t id = 0;
+                if (lane < nb) {
+                    const int64_t j = b0 + lane;
+                    if (all) {
+                        id = (int32_t)(l + j);
+                    } else {
+                        const int64_t s0 = l + (j * cnt) / E;
+                        const int64_t t0 = l + ((j + 1) * cnt) / E - 1;
+                        const uint64_t z = splitmix64(A.seed ^ qkey ^ (uint64_t)j);
+                        id = (int32_t)(s0 + (int64_t)(((z >> 32) * (uint64_t)(t0 - s0 + 1)) >> 32));
+                    }
+                    if (!vis.tab) vis.insert(id);
+                }
+                const float dd = eval(nb, id);
+                const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
+                st[FROG_STAT_DIST] += nb;
+                merge<LP>(pool, nkey, nb, L, st_key, st_flag);
+                if (vis.tab && lane < nb) vis.insert(id);
+            }
+            wave_sync();
+
+            // best-first loop (Alg. 2)
+            const int64_t nent = (int64_t)(Le - Ls + 1) * m;
+            for (;;) {
+                // a4: first unexpanded entry
+                int sel = -1;
+#pragma unroll
+                for (int s = 0; s < LP; ++s) {
+                    const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
+                    if (sel < 0 && mk != 0) sel = s * 64 + __builtin_ctzll(mk);
+                }
+                sel = uniform(sel);
+                if (sel < 0) break;
+                const int ss = sel >> 6, sl = sel & 63;
+                int32_t u = 0;
+#pragma unroll
+                for (int s = 0; s < LP; ++s) {
+                    if (s == ss) {
+                        u = (int32_t)(uint32_t)readlane64(pool.key[s], sl);
+                        if (lane == sl) pool.flag[s] = 1u;
+                    }
+                }
+                st[FROG_STAT_EXPANSIONS] += 1;
+
+                // a5 + a6: ENC slice of the hotspot, compaction under budget B
+                const int32_t* row = ix.ENC + ((int64_t)u * H + Ls) * m;
+                int nen = 0;
+                int64_t scanned = nent;
+                for (int64_t off = 0; off < nent && nen < B; off += 64) {
+                    const int64_t e = off + lane;
+                    const int32_t v = e < nent ? row[e] : -1;
+                    const bool pred = v >= l && v <= r;
+                    const uint64_t pm = ballot(pred);
+                    const int rk = mbcnt(pm);
+                    const int tot = __popcll(pm);
+                    const int admit = tot < B - nen ? tot : B - nen;
+                    if (pred && rk < admit) enbuf[nen + rk] = v;
+                    const int here = (int)(nent - off < 64 ? nent - off : 64);
+                    st[FROG_STAT_LOADED] += here;
+                    if (admit == B - nen && admit > 0) {
+                        // budget reached: Alg. 4 examined every layer up to the
+                        // one holding the last admitted entry
+                        const int last = uniform(__builtin_ctzll(ballot(pred && rk == admit - 1)));
+                        scanned = ((off + last) / m + 1) * m;
+                    }
+                    nen += admit;
+                }
+                st[FROG_STAT_SCANNED] += (int32_t)scanned;
+                nen = uniform(nen);
+                st[FROG_STAT_EN] += nen;
+                wave_sync();
+
+                // a7: lazy visited check on the compacted list
+                int32_t v = lane < nen ? enbuf[lane] : -1;
+                bool fresh = false;
+                if (lane < nen) fresh = vis.check_insert(v);
+                const uint64_t fm = ballot(fresh);
+                const int ns = __popcll(fm);
+                wave_sync();
+                if (fresh) enbuf[mbcnt(fm)] = v;
+                wave_sync();
+                const int32_t myid = lane < ns ? enbuf[lane] : 0;
+                wave_sync();
+                if (ns == 0) continue;
+
+                // a8: gather + distances
+                const float dd = eval(ns, myid);
+                st[FROG_STAT_DIST] += ns;
+                const uint64_t nkey = lane < ns ? make_key(dd, myid) : kEmpty;
+                // a9 + a10: MergeTopEfS
+                merge<LP>(pool, nkey, ns, L, st_key, st_flag);
+            }
+        }
+
+        // a11: output, rank -> original id, padding
+#pragma unroll
+        for (int s = 0; s < LP; ++s) {
+            const int p = s * 64 + lane;
+            if (p < k) {
+                int32_t oid = -1;
+                float od = __int_as_float(0x7f800000);
+                if (p < pool.np) {
+                    oid = ix.perm[(uint32_t)pool.key[s]];
+                    od = __uint_as_float((uint32_t)(pool.key[s] >> 32));
+                }
+                A.ids[qi * k + p] = oid;
+                A.dists[qi * k + p] = od;
+            }
+        }
+        if (A.stats && lane < FROG_STAT_N) {
+            int32_t val = 0;
+#pragma unroll
+            for (int i = 0; i < FROG_STAT_N; ++i)
+                if (lane == i) val = st[i];
+            A.stats[qi * FROG_STAT_N + lane] = val;
+        }
+    }
+}
+
+__global__ void rank_bounds_kernel(DevIndex ix, const double* lo, const double* hi, int64_t nq, int32_t* lr) {
+    const int64_t q = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (q >= nq) return;
+    int64_t l, r;
+    rank_interval(ix, lo[q], hi[q], l, r);
+    if (lane_id() == 0) {
+        lr[2 * q] = (int32_t)l;
+        lr[2 * q + 1] = (int32_t)r;
+    }
+}
+
+__global__ void zero_u32(unsigned int* p) { *p = 0u; }
+
+// ------------------------------------------------------------------ dispatch
+
+using KernelFn = void (*)(KParams);
+
+template <int C>
+KernelFn pick_lp(int L) {
+    if (L <= 64) return search_kernel<C, 1>;
+    if (L <= 128) return search_kernel<C, 2>;
+    return search_kernel<C, 4>;
+}
+
+KernelFn pick_kernel(int dp, int L) {
+    switch (dp) {
+        case 32: return pick_lp<1>(L);
+        case 64: return pick_lp<2>(L);
+        case 96: return pick_lp<3>(L);
+        case 128: return pick_lp<4>(L);
+        default: return pick_lp<0>(L);
+    }
+}
+
+int lp_of(int L) { return L <= 64 ? 1 : (L <= 128 ? 2 : 4); }
+
+int lds_per_wave(int L, int hash_log2) {
+    const int lp = lp_of(L);
+    return 64 * lp * 8 + 64 * lp * 4 + 64 * 4 + (hash_log2 > 0 ? (4 << hash_log2) : 0);
+}
+
+int max_blocks(KernelFn fn, int smem) {
+    static std::mutex mu;
+    static std::map<std::pair<void*, int>, int> cache;
+    std::lock_guard<std::mutex> g(mu);
+    auto key = std::make_pair((void*)fn, smem);
+    auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+    int dev = 0, per_cu = 0, cus = 0;
+    hipGetDevice(&dev);
+    hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)fn, kBlock, smem) != hipSuccess ||
+        per_cu < 1)
+        per_cu = 1;
+    const int v = per_cu * (cus > 0 ? cus : 1);
+    cache[key] = v;
+    return v;
+}
+
+}  // namespace
+
+bool search_shape_supported(int dp, int m, int L) {
+    return dp >= 32 && dp % 32 == 0 && m >= 1 && m <= 64 && L >= 1 && L <= 256;
+}
+
+int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
+    hipStream_t stream = (hipStream_t)stream_v;
+    KernelFn fn = pick_kernel(ix.dp, a.L);
+    const int lpw = lds_per_wave(a.L, a.hash_log2);
+    const int smem = lpw * kWavesPerBlock;
+    if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);
+    if (smem > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
+    int blocks = max_blocks(fn, smem);
+    const int64_t need = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (need < blocks) blocks = (int)need;
+    KParams P{};
+    P.ix = ix;
+    P.a = a;
+    P.lds_per_wave = lpw;
+    P.gvis_words = 0;
+    size_t ws = 256;
+    if (a.hash_log2 == 0) {
+        P.gvis_words = (ix.n + 31) / 32;
+        // bound the bitmap footprint to ~2 GiB
+        const int64_t cap = ((int64_t)2 << 30) / (P.gvis_words * 4 * kWavesPerBlock);
+        if (cap < blocks) blocks = (int)(cap > 0 ? cap : 1);
+        ws += (size_t)blocks * kWavesPerBlock * P.gvis_words * 4;
+    }
+    void* wsp = nullptr;
+    hipError_t e = hipMallocAsync(&wsp, ws, stream);
+    if (e != hipSuccess) return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
+    P.counter = reinterpret_cast<unsigned int*>(wsp);
+    P.gvis = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(wsp) + 256);
+    hipLaunchKernelGGL(zero_u32, dim3(1), dim3(1), 0, stream, P.counter);
+    hipLaunchKernelGGL(fn, dim3(blocks), dim3(kBlock), smem, stream, P);
+    e = hipGetLastError();
+    hipFreeAsync(wsp, stream);
+    if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
+    return FROG_OK;
+}
+
+int launch_rank_bounds(const DevIndex& ix, const double* lo, const double* hi, int64_t nq, int32_t* lr,
+                       void* stream_v) {
+    hipStream_t stream = (hipStream_t)stream_v;
+    const int64_t blocks = (nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, ix, lo, hi, nq, lr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(FROG_EHIP, "rank_bounds launch: %s", hipGetErrorString(e));
+    return FROG_OK;
+}
+
+}  // namespace frog

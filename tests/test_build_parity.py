@@ -1,0 +1,52 @@
+"""The library's host index construction equals the oracle's, entry for entry
+(Sec 6; the readings both follow are listed in oracle/frog_oracle.c)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_16491_amd as F
+import workloads
+
+
+def _compare(X, attr, **params):
+    ix = F.Index.build(X, attr, **params)
+    e = ix.export()
+    ox = oracle.build(X, attr, **params)
+    assert (e["perm"] == ox.perm).all()
+    assert (e["attr_sorted"] == ox.attr_sorted).all()
+    assert (e["X_rank"] == ox.X_rank).all()
+    assert e["ENC"].shape == ox.ENC.shape
+    diff = np.argwhere(e["ENC"] != ox.ENC)
+    assert len(diff) == 0, f"{len(diff)} entries differ, first at {diff[:3].tolist()}"
+
+
+def test_build_parity_iid():
+    w = workloads.make("tiny", n=4000, nq=1)
+    _compare(w.X, w.attr)
+
+
+def test_build_parity_mixture_d128():
+    w = workloads.make("c2", n=6000, nq=1)
+    _compare(w.X, w.attr)
+
+
+def test_build_parity_m32_high_dim():
+    rng = np.random.default_rng(3)
+    X = rng.standard_normal((1500, 320)).astype(np.float32)
+    attr = rng.permutation(1500).astype(np.float64)
+    _compare(X, attr)          # d > 300: m=32, ef_c=256, n_inv=6
+
+
+def test_build_parity_duplicate_attributes_and_odd_sizes():
+    rng = np.random.default_rng(4)
+    X = rng.standard_normal((777, 20)).astype(np.float32)
+    attr = rng.integers(0, 50, 777).astype(np.float64)
+    _compare(X, attr, m=8, ef_c=24, n_inv=3, patience=5, sib_seeds=4, beta=0.3, gamma=1.0, seed=9)
+
+
+def test_build_parity_tiny_n():
+    rng = np.random.default_rng(5)
+    for n in (1, 2, 3, 17):
+        X = rng.standard_normal((n, 4)).astype(np.float32)
+        attr = rng.permutation(n).astype(np.float64)
+        _compare(X, attr, m=4, ef_c=8, n_inv=0)

@@ -1,0 +1,62 @@
+"""GPU exhaustive filtered k-NN (Def. 2) against the oracle's exhaustive
+search, through the C ABI."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_16491_amd as F
+import workloads
+from tests.parity import assert_parity
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _cuda(a, dtype):
+    return torch.as_tensor(np.ascontiguousarray(a)).to(dtype=dtype, device="cuda")
+
+
+def _run(X, attr, Q, lo, hi, k):
+    perm = np.argsort(attr, kind="stable").astype(np.int32)
+    srt = attr[perm]
+    Xr = X[perm]
+    n, d = X.shape
+    ENC = -np.ones((n, 1, 1), np.int32)
+    ix = F.Index.from_arrays(Xr, srt, perm, ENC).upload(0)
+    ids, ds, cert = F.bruteforce(ix, _cuda(Q, torch.float32), _cuda(lo, torch.float64),
+                                 _cuda(hi, torch.float64), k)
+    torch.cuda.synchronize()
+    o_ids, o_d = oracle.exact(Xr, srt, perm, Q, lo, hi, k)
+    return ids.cpu().numpy(), ds.cpu().numpy(), cert.cpu().numpy(), o_ids, o_d
+
+
+def test_bruteforce_tiny():
+    print("[gpu] bruteforce tiny", flush=True)
+    w = workloads.make("tiny")
+    ids, ds, cert, o_ids, o_d = _run(w.X, w.attr, w.Q, w.lo, w.hi, 10)
+    assert cert.all()
+    assert_parity(ids, ds, o_ids, o_d, max_residual=0)
+
+
+@pytest.mark.parametrize("k", [1, 10, 100])
+def test_bruteforce_mixture(k):
+    print(f"[gpu] bruteforce mixture k={k}", flush=True)
+    w = workloads.make("c2", n=40000, nq=200)
+    ids, ds, cert, o_ids, o_d = _run(w.X, w.attr, w.Q, w.lo, w.hi, k)
+    assert cert.mean() > 0.99
+    c = cert.astype(bool)
+    assert_parity(ids[c], ds[c], o_ids[c], o_d[c], max_residual=0)
+
+
+def test_bruteforce_edges():
+    rng = np.random.default_rng(1)
+    n, d = 2000, 40
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    attr = rng.integers(0, 300, n).astype(np.float64)      # duplicate attribute values
+    Q = rng.standard_normal((9, d)).astype(np.float32)
+    lo = np.array([0, 5, np.nan, 7, 299, 100, 50, -5, 10], np.float64)
+    hi = np.array([299, 5, 3, 2, 400, 100.5, 60, 1e9, 10], np.float64)
+    ids, ds, cert, o_ids, o_d = _run(X, attr, Q, lo, hi, 25)
+    assert cert.all()
+    assert_parity(ids, ds, o_ids, o_d, max_residual=0)
+    assert (ids[2] == -1).all() and (ids[3] == -1).all()
