@@ -70,7 +70,7 @@ typedef struct {
     int budget;         /* expansion budget B of ENIdentification (Alg. 4), 1..64: 16 */
     uint64_t seed;      /* entry-point jitter seed: 0 */
     int64_t query_base; /* batch index of query 0; keys the entry-point jitter: 0 */
-    int hash_log2;      /* visited table of 2^hash_log2 slots in LDS (6..13): 11;
+    int hash_log2;      /* visited table of 2^hash_log2 slots in LDS (6..13): 10;
                            0 selects an exact visited set in device memory (slow;
                            used to count distinct evaluations) */
 } frog_search_params_t;

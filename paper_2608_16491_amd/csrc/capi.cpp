@@ -145,7 +145,7 @@ void frog_search_params_default(frog_search_params_t* p) {
     p->budget = 16;
     p->seed = 0;
     p->query_base = 0;
-    p->hash_log2 = 11;
+    p->hash_log2 = 10;
 }
 
 int frog_build_index(const float* X, const double* attr, int64_t n, int d,

@@ -475,7 +475,14 @@ __global__ __launch_bounds__(kBlock) void search_kernel(KParams P) {
                 const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
                 st[FROG_STAT_DIST] += nb;
                 merge<LP>(pool, nkey, nb, L, st_key, st_flag);
-                if (vis.tab && lane < nb) vis.insert(id);
+            }
+            // The forgetful table remembers the pool's entry points only: an
+            // entry point that did not make the pool can never enter it later
+            // (its key is above the pool's L-th), so forgetting it is free.
+            if (vis.tab) {
+#pragma unroll
+                for (int s = 0; s < LP; ++s)
+                    if (s * 64 + lane < pool.np) vis.insert((int32_t)(uint32_t)pool.key[s]);
             }
             wave_sync();
 
