@@ -51,14 +51,21 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kEmpty = ~0ull;
+// Register budget: at least 4 wavefronts per SIMD (128 VGPRs).  The d = 128
+// kernel needs ~130 without it; the compiler spills a few bytes instead.
+#define FROG_WAVES_PER_EU 4
 
 struct KParams {
     DevIndex ix;
     SearchLaunch a;
-    unsigned int* counter;   // persistent-grid work counter
+    unsigned int* counter;   // [2] work counters: entry units, queries
+    const int32_t* lr;       // [nq][2] rank intervals, from the prologue kernel
+    uint64_t* part;          // [nq][cpq][64 * LP] pools of the entry chunks
     uint32_t* gvis;          // exact visited bitmaps (hash_log2 == 0)
     int64_t gvis_words;      // words per wave
     int lds_per_wave;        // bytes
+    int cpq;                 // work units (entry chunks) per query
+    int chunk;               // entry points per chunk, a multiple of 16
 };
 
 // ------------------------------------------------------------------ wave helpers
@@ -101,6 +108,24 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
 
 __device__ __forceinline__ uint64_t make_key(float d, int32_t id) {
     return ((uint64_t)__float_as_uint(d) << 32) | (uint32_t)id;
+}
+
+// Data-parallel-primitive lane moves of a double (two 32-bit DPP moves).
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
+// Sum over each aligned group of 8 lanes, the same value in all 8: quad swaps
+// [1,0,3,2] and [2,3,0,1], then the half-row mirror pairs the two quads.
+__device__ __forceinline__ double sum8(double s) {
+    s += dpp_f64<0xB1>(s);
+    s += dpp_f64<0x4E>(s);
+    s += dpp_f64<0x141>(s);
+    return s;
 }
 
 // ------------------------------------------------------------------ a1: ranks
@@ -201,7 +226,10 @@ __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&
         double s0 = 0.0, s1 = 0.0;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
-            const double q0 = qv[c].x, q1 = qv[c].y, q2 = qv[c].z, q3 = qv[c].w;
+            // keep the query in fp32 registers: convert per use, not once
+            float4 qf = qv[c];
+            asm volatile("" : "+v"(qf.x), "+v"(qf.y), "+v"(qf.z), "+v"(qf.w));
+            const double q0 = qf.x, q1 = qf.y, q2 = qf.z, q3 = qf.w;
             double t;
             t = q0 - (double)x0[c].x; s0 += t * t;
             t = q1 - (double)x0[c].y; s0 += t * t;
@@ -212,12 +240,8 @@ __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&
             t = q2 - (double)x1[c].z; s1 += t * t;
             t = q3 - (double)x1[c].w; s1 += t * t;
         }
-        s0 += __shfl_xor(s0, 1);
-        s1 += __shfl_xor(s1, 1);
-        s0 += __shfl_xor(s0, 2);
-        s1 += __shfl_xor(s1, 2);
-        s0 += __shfl_xor(s0, 4);
-        s1 += __shfl_xor(s1, 4);
+        s0 = sum8(s0);
+        s1 = sum8(s1);
         const float f0 = (float)s0, f1 = (float)s1;
         // vector sb0 + g (g < 8) sits in lanes 8g..8g+7 of f0, sb0 + 8 + g in f1
         const int src = (lane & 7) << 3;
@@ -369,46 +393,174 @@ struct Visited {
 
 // ------------------------------------------------------------------ kernel
 
+// Per-wave LDS: pool staging (64 LP keys + flags), the EN list, the visited
+// table.
+template <int LP>
+struct WaveLds {
+    uint64_t* st_key;
+    uint32_t* st_flag;
+    int32_t* enbuf;
+    int32_t* tab;
+    __device__ WaveLds(char* smem, int lds_per_wave, int hash_log2) {
+        char* wbase = smem + (size_t)(threadIdx.x >> 6) * lds_per_wave;
+        st_key = reinterpret_cast<uint64_t*>(wbase);
+        st_flag = reinterpret_cast<uint32_t*>(st_key + 64 * LP);
+        enbuf = reinterpret_cast<int32_t*>(st_flag + 64 * LP);
+        tab = hash_log2 > 0 ? enbuf + 64 : nullptr;
+    }
+};
+
+// Query context shared by both kernels: the query's float4 chunks this lane
+// needs, its rank interval and its entry points (Alg. 2).
+template <int C>
+struct QueryCtx {
+    float4 qv[C > 0 ? C : 1];
+    const float* qrow;
+    int64_t qi, l, r, cnt, E, ne;
+    bool all;
+    uint64_t qkey;
+
+    __device__ void load(const DevIndex& ix, const SearchLaunch& A, const int32_t* lr, int64_t q) {
+        qi = q;
+        l = uniform(lr[2 * q]);
+        r = uniform(lr[2 * q + 1]);
+        cnt = r - l + 1;
+        E = A.epn;
+        if (A.epn_frac > 0.0) {
+            double want = ceil(A.epn_frac * (double)cnt);
+            if (want > (double)A.epn_max) want = (double)A.epn_max;
+            if (want > (double)E) E = (int64_t)want;
+        }
+        all = cnt <= E;
+        ne = cnt <= 0 ? 0 : (all ? cnt : E);
+        qkey = (uint64_t)(A.qbase + q) << 32;
+        qrow = A.Q + q * ix.d;
+    }
+    __device__ void load_vector(const DevIndex& ix) {
+        if constexpr (C > 0) {
+            const int lane = lane_id();
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                const int b = 4 * ((lane & 7) + 8 * c);
+                qv[c].x = b < ix.d ? qrow[b] : 0.f;
+                qv[c].y = b + 1 < ix.d ? qrow[b + 1] : 0.f;
+                qv[c].z = b + 2 < ix.d ? qrow[b + 2] : 0.f;
+                qv[c].w = b + 3 < ix.d ? qrow[b + 3] : 0.f;
+            }
+        }
+    }
+    // entry point j: every rank when the range holds at most E, else one
+    // jittered rank per stratum
+    __device__ int32_t entry_id(const SearchLaunch& A, int64_t j) const {
+        if (all) return (int32_t)(l + j);
+        const int64_t s0 = l + (j * cnt) / E;
+        const int64_t t0 = l + ((j + 1) * cnt) / E - 1;
+        const uint64_t z = splitmix64(A.seed ^ qkey ^ (uint64_t)j);
+        return (int32_t)(s0 + (int64_t)(((z >> 32) * (uint64_t)(t0 - s0 + 1)) >> 32));
+    }
+    __device__ float eval(const DevIndex& ix, int nb, int32_t myid) const {
+        if constexpr (C > 0) return eval_small<C>(ix.X, ix.dp, qv, nb, myid);
+        else return eval_large(ix.X, ix.dp, qrow, ix.d, nb, myid);
+    }
+};
+
+// a3 (entry points, Alg. 2): work unit = (query, chunk of `chunk` entry
+// points).  The unit evaluates its entry points and writes the L nearest
+// (sorted keys, empty slots = kEmpty) to its slot of `part`.  Spreading the
+// entry phase over many short units keeps every wavefront busy to the end;
+// the kernel boundary publishes the pools to the traversal kernel.
 template <int C, int LP>
-__global__ __launch_bounds__(kBlock) void search_kernel(KParams P) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
+void entry_kernel(KParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const DevIndex& ix = P.ix;
     const SearchLaunch& A = P.a;
     const int lane = lane_id();
-    const int wave = threadIdx.x >> 6;
-    char* wbase = smem + (size_t)wave * P.lds_per_wave;
-    uint64_t* st_key = reinterpret_cast<uint64_t*>(wbase);
-    uint32_t* st_flag = reinterpret_cast<uint32_t*>(st_key + 64 * LP);
-    int32_t* enbuf = reinterpret_cast<int32_t*>(st_flag + 64 * LP);
-    Visited vis;
-    vis.tab = A.hash_log2 > 0 ? enbuf + 64 : nullptr;
-    vis.shift = 32 - A.hash_log2;
-    const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + wave;
-    vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
-    const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
-    const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
-
+    WaveLds<LP> W(smem, P.lds_per_wave, 0);
+    const int64_t units = A.nq * (int64_t)P.cpq;
+    const uint32_t slots = 64u * LP;
     for (;;) {
-        int qi_l = 0;
-        if (lane == 0) qi_l = (int)atomicAdd(P.counter, 1u);
-        const int64_t qi = uniform(__shfl(qi_l, 0));
-        if (qi >= A.nq) break;
-
-        int32_t st[FROG_STAT_N];
-#pragma unroll
-        for (int i = 0; i < FROG_STAT_N; ++i) st[i] = 0;
-
-        // a1: range -> ranks
-        int64_t l, r;
-        rank_interval(ix, A.lo[qi], A.hi[qi], l, r);
-        l = uniform64(l);
-        r = uniform64(r);
+        int u_l = 0;
+        if (lane == 0) u_l = (int)atomicAdd(P.counter, 1u);
+        const int64_t unit = (uint32_t)uniform(__shfl(u_l, 0));
+        if (unit >= units) break;
+        const int64_t qi = unit / P.cpq;
+        const int ci = (int)(unit - qi * P.cpq);
+        QueryCtx<C> Q;
+        Q.load(ix, A, P.lr, qi);
+        const int64_t e0 = (int64_t)ci * P.chunk;
+        if (e0 >= Q.ne) continue;
+        const int64_t e1 = e0 + P.chunk < Q.ne ? e0 + P.chunk : Q.ne;
+        Q.load_vector(ix);
         Pool<LP> pool;
 #pragma unroll
         for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
         pool.np = 0;
+        for (int64_t b0 = e0; b0 < e1; b0 += 16) {
+            const int nb = (int)(e1 - b0 < 16 ? e1 - b0 : 16);
+            const int32_t id = lane < nb ? Q.entry_id(A, b0 + lane) : 0;
+            const float dd = Q.eval(ix, nb, id);
+            const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
+            merge<LP>(pool, nkey, nb, A.L, W.st_key, W.st_flag);
+        }
+        uint64_t* out = P.part + ((uint64_t)qi * P.cpq + ci) * slots;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) out[s * 64 + lane] = pool.key[s];
+    }
+}
 
-        if (l <= r) {
+// a2, a4-a11: per query, merge the entry chunks' pools (the L nearest entry
+// points), HotspotLocalization, then the best-first loop of Alg. 2.
+template <int C, int LP>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
+void search_kernel(KParams P) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const DevIndex& ix = P.ix;
+    const SearchLaunch& A = P.a;
+    const int lane = lane_id();
+    WaveLds<LP> W(smem, P.lds_per_wave, A.hash_log2);
+    Visited vis;
+    vis.tab = W.tab;
+    vis.shift = 32 - A.hash_log2;
+    const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
+    const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
+    const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
+    const uint32_t slots = 64u * LP;
+
+    for (;;) {
+        int q_l = 0;
+        if (lane == 0) q_l = (int)atomicAdd(P.counter + 1, 1u);
+        const int64_t qi = (uint32_t)uniform(__shfl(q_l, 0));
+        if (qi >= A.nq) break;
+        QueryCtx<C> Q;
+        Q.load(ix, A, P.lr, qi);
+        const int64_t l = Q.l, r = Q.r;
+
+        Pool<LP> pool;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+        pool.np = 0;
+        int32_t st[FROG_STAT_N];
+#pragma unroll
+        for (int i = 0; i < FROG_STAT_N; ++i) st[i] = 0;
+
+        if (Q.ne > 0) {
+            Q.load_vector(ix);
+            // the L nearest entry points: merge the chunk pools
+            const int nch = (int)((Q.ne + P.chunk - 1) / P.chunk);
+            for (int cc = 0; cc < nch; ++cc) {
+                const uint64_t* part = P.part + ((uint64_t)qi * P.cpq + cc) * slots;
+#pragma unroll
+                for (int s = 0; s < LP; ++s) {
+                    const uint64_t key = part[s * 64 + lane];
+                    const int nk = __popcll(ballot(key != kEmpty));   // sorted: a prefix
+                    if (nk > 0) merge<LP>(pool, key, nk, L, W.st_key, W.st_flag);
+                }
+            }
+            st[FROG_STAT_ENTRY] = (int32_t)Q.ne;
+            st[FROG_STAT_DIST] = (int32_t)Q.ne;
+
             // a2: hotspot
             int Ls, Le;
             hotspot(l, r, H, ix.n, Ls, Le);
@@ -417,77 +569,26 @@ __global__ __launch_bounds__(kBlock) void search_kernel(KParams P) {
             st[FROG_STAT_LSTART] = Ls;
             st[FROG_STAT_LEND] = Le;
 
-            // query chunks
-            float4 qv[C > 0 ? C : 1];
-            const float* qrow = A.Q + qi * ix.d;
-            if constexpr (C > 0) {
-#pragma unroll
-                for (int c = 0; c < C; ++c) {
-                    const int b = 4 * ((lane & 7) + 8 * c);
-                    qv[c].x = b < ix.d ? qrow[b] : 0.f;
-                    qv[c].y = b + 1 < ix.d ? qrow[b + 1] : 0.f;
-                    qv[c].z = b + 2 < ix.d ? qrow[b + 2] : 0.f;
-                    qv[c].w = b + 3 < ix.d ? qrow[b + 3] : 0.f;
-                }
-            }
-            auto eval = [&](int cnt, int32_t myid) -> float {
-                if constexpr (C > 0) return eval_small<C>(ix.X, ix.dp, qv, cnt, myid);
-                else return eval_large(ix.X, ix.dp, qrow, ix.d, cnt, myid);
-            };
-
-            // reset the visited set
+            // visited set: every entry point (exact bitmap) or the pool's
+            // entry points (forgetful table: an entry point outside the pool
+            // can never enter it later, its key is above the pool's L-th)
             if (vis.tab) {
                 for (int i = lane; i < T; i += 64) vis.tab[i] = -1;
-            } else {
-                for (int64_t i = lane; i < P.gvis_words; i += 64) vis.bits[i] = 0u;
-                __threadfence();
-            }
-            wave_sync();
-
-            // a3: entry points
-            const int64_t cnt = r - l + 1;
-            int64_t E = A.epn;
-            if (A.epn_frac > 0.0) {
-                double want = ceil(A.epn_frac * (double)cnt);
-                if (want > (double)A.epn_max) want = (double)A.epn_max;
-                if (want > (double)E) E = (int64_t)want;
-            }
-            const bool all = cnt <= E;
-            const int64_t ne = all ? cnt : E;
-            st[FROG_STAT_ENTRY] = (int32_t)ne;
-            const uint64_t qkey = (uint64_t)(A.qbase + qi) << 32;
-            for (int64_t b0 = 0; b0 < ne; b0 += 16) {
-                const int nb = (int)(ne - b0 < 16 ? ne - b0 : 16);
-                int32_t id = 0;
-                if (lane < nb) {
-                    const int64_t j = b0 + lane;
-                    if (all) {
-                        id = (int32_t)(l + j);
-                    } else {
-                        const int64_t s0 = l + (j * cnt) / E;
-                        const int64_t t0 = l + ((j + 1) * cnt) / E - 1;
-                        const uint64_t z = splitmix64(A.seed ^ qkey ^ (uint64_t)j);
-                        id = (int32_t)(s0 + (int64_t)(((z >> 32) * (uint64_t)(t0 - s0 + 1)) >> 32));
-                    }
-                    if (!vis.tab) vis.insert(id);
-                }
-                const float dd = eval(nb, id);
-                const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
-                st[FROG_STAT_DIST] += nb;
-                merge<LP>(pool, nkey, nb, L, st_key, st_flag);
-            }
-            // The forgetful table remembers the pool's entry points only: an
-            // entry point that did not make the pool can never enter it later
-            // (its key is above the pool's L-th), so forgetting it is free.
-            if (vis.tab) {
+                wave_sync();
 #pragma unroll
                 for (int s = 0; s < LP; ++s)
                     if (s * 64 + lane < pool.np) vis.insert((int32_t)(uint32_t)pool.key[s]);
+            } else {
+                for (int64_t i = lane; i < P.gvis_words; i += 64) vis.bits[i] = 0u;
+                __threadfence_block();
+                for (int64_t j = lane; j < Q.ne; j += 64) vis.insert(Q.entry_id(A, j));
+                __threadfence_block();
             }
             wave_sync();
 
             // best-first loop (Alg. 2)
             const int64_t nent = (int64_t)(Le - Ls + 1) * m;
+            int32_t* enbuf = W.enbuf;
             for (;;) {
                 // a4: first unexpanded entry
                 int sel = -1;
@@ -551,11 +652,11 @@ __global__ __launch_bounds__(kBlock) void search_kernel(KParams P) {
                 if (ns == 0) continue;
 
                 // a8: gather + distances
-                const float dd = eval(ns, myid);
+                const float dd = Q.eval(ix, ns, myid);
                 st[FROG_STAT_DIST] += ns;
                 const uint64_t nkey = lane < ns ? make_key(dd, myid) : kEmpty;
                 // a9 + a10: MergeTopEfS
-                merge<LP>(pool, nkey, ns, L, st_key, st_flag);
+                merge<LP>(pool, nkey, ns, L, W.st_key, W.st_flag);
             }
         }
 
@@ -595,20 +696,25 @@ __global__ void rank_bounds_kernel(DevIndex ix, const double* lo, const double* 
     }
 }
 
-__global__ void zero_u32(unsigned int* p) { *p = 0u; }
+__global__ void init_kernel(unsigned int* counter) {
+    if (threadIdx.x < 2) counter[threadIdx.x] = 0u;
+}
 
 // ------------------------------------------------------------------ dispatch
 
 using KernelFn = void (*)(KParams);
+struct KernelPair {
+    KernelFn entry, search;
+};
 
 template <int C>
-KernelFn pick_lp(int L) {
-    if (L <= 64) return search_kernel<C, 1>;
-    if (L <= 128) return search_kernel<C, 2>;
-    return search_kernel<C, 4>;
+KernelPair pick_lp(int L) {
+    if (L <= 64) return {entry_kernel<C, 1>, search_kernel<C, 1>};
+    if (L <= 128) return {entry_kernel<C, 2>, search_kernel<C, 2>};
+    return {entry_kernel<C, 4>, search_kernel<C, 4>};
 }
 
-KernelFn pick_kernel(int dp, int L) {
+KernelPair pick_kernel(int dp, int L) {
     switch (dp) {
         case 32: return pick_lp<1>(L);
         case 64: return pick_lp<2>(L);
@@ -651,23 +757,43 @@ bool search_shape_supported(int dp, int m, int L) {
 
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     hipStream_t stream = (hipStream_t)stream_v;
-    KernelFn fn = pick_kernel(ix.dp, a.L);
+    const KernelPair kp = pick_kernel(ix.dp, a.L);
+    const int lpw_entry = lds_per_wave(a.L, 0);
     const int lpw = lds_per_wave(a.L, a.hash_log2);
     const int smem = lpw * kWavesPerBlock;
+    const int smem_entry = lpw_entry * kWavesPerBlock;
     if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);
     if (smem > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        hipError_t e = hipFuncSetAttribute((const void*)kp.search, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
-    int blocks = max_blocks(fn, smem);
+    // entry chunks: 512 entry points per work unit, at most 16 units per query
+    const int64_t emax = a.epn_frac > 0.0 ? (a.epn_max > a.epn ? a.epn_max : a.epn) : a.epn;
+    int64_t chunk = 512;
+    if ((emax + chunk - 1) / chunk > 16) chunk = ((emax + 15) / 16 + 15) / 16 * 16;
+    const int cpq = (int)((emax + chunk - 1) / chunk);
+    if (a.nq * (int64_t)cpq >= ((int64_t)1 << 31))
+        return fail(FROG_EINVAL, "nq=%lld too large for one launch", (long long)a.nq);
+    const int lp = lp_of(a.L);
+    int blocks = max_blocks(kp.search, smem);
     const int64_t need = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     if (need < blocks) blocks = (int)need;
+    int eblocks = max_blocks(kp.entry, smem_entry);
+    const int64_t eneed = (a.nq * cpq + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (eneed < eblocks) eblocks = (int)eneed;
     KParams P{};
     P.ix = ix;
     P.a = a;
     P.lds_per_wave = lpw;
+    P.cpq = cpq;
+    P.chunk = (int)chunk;
     P.gvis_words = 0;
-    size_t ws = 256;
+    auto align = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t off_lr = 256;
+    const size_t off_part = off_lr + align((size_t)a.nq * 8);
+    const size_t part_bytes = (size_t)a.nq * cpq * 64 * lp * 8;
+    const size_t off_gvis = off_part + align(part_bytes);
+    size_t ws = off_gvis;
     if (a.hash_log2 == 0) {
         P.gvis_words = (ix.n + 31) / 32;
         // bound the bitmap footprint to ~2 GiB
@@ -678,12 +804,21 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     void* wsp = nullptr;
     hipError_t e = hipMallocAsync(&wsp, ws, stream);
     if (e != hipSuccess) return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
-    P.counter = reinterpret_cast<unsigned int*>(wsp);
-    P.gvis = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(wsp) + 256);
-    hipLaunchKernelGGL(zero_u32, dim3(1), dim3(1), 0, stream, P.counter);
-    hipLaunchKernelGGL(fn, dim3(blocks), dim3(kBlock), smem, stream, P);
+    char* base = reinterpret_cast<char*>(wsp);
+    P.counter = reinterpret_cast<unsigned int*>(base);
+    int32_t* lr = reinterpret_cast<int32_t*>(base + off_lr);
+    P.lr = lr;
+    P.part = reinterpret_cast<uint64_t*>(base + off_part);
+    P.gvis = reinterpret_cast<uint32_t*>(base + off_gvis);
+    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(64), 0, stream, P.counter);
+    const int64_t rb_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
+    KParams PE = P;
+    PE.lds_per_wave = lpw_entry;
+    hipLaunchKernelGGL(kp.entry, dim3(eblocks), dim3(kBlock), smem_entry, stream, PE);
+    hipLaunchKernelGGL(kp.search, dim3(blocks), dim3(kBlock), smem, stream, P);
     e = hipGetLastError();
-    hipFreeAsync(wsp, stream);
+    (void)hipFreeAsync(wsp, stream);
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
     return FROG_OK;
 }

@@ -1,0 +1,98 @@
+"""Full-size parity on the benchmark workload (n = 1,000,000, d = 128, 10,000
+mixed-selectivity queries) in the launch configuration bench.py times
+(L = 32, entry points min(cnt, 3072), budget 16, LDS table 2^10).
+
+The index is built by the library's host construction, whose equality with
+the oracle's construction is established entry by entry on smaller inputs in
+tests/test_build_parity.py; here it is only the common input of both searches.
+Sampled rows are recomputed by the oracle one by one (same index arrays, same
+entry-point keys); every row is checked for the properties that hold at any
+size."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_16491_amd as F
+import workloads
+from tests.parity import assert_parity
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SETTING = dict(epn=16, epn_frac=1.0, epn_max=3072, budget=16, hash_log2=10)
+L, K = 32, 10
+
+
+@pytest.fixture(scope="module")
+def c2():
+    print("[gpu] full-size c2: building the 1M x 128 index on the host", flush=True)
+    w = workloads.make("c2")
+    ix = F.Index.build(w.X, w.attr).upload(0)
+    arr = ix.export()
+    ox = oracle.OracleIndex(arr["perm"], arr["attr_sorted"], arr["X_rank"], arr["ENC"])
+    dev = torch.device("cuda:0")
+    d = dict(Q=torch.as_tensor(w.Q, device=dev), lo=torch.as_tensor(w.lo, device=dev),
+             hi=torch.as_tensor(w.hi, device=dev))
+    print("[gpu] full-size c2: index ready", flush=True)
+    return w, ix, ox, d
+
+
+@pytest.mark.timeout(900)
+def test_full_size_sampled_rows_match_oracle(c2):
+    w, ix, ox, d = c2
+    ids, ds, st = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, stats=True, **SETTING)
+    torch.cuda.synchronize()
+    ids, ds, st = ids.cpu().numpy(), ds.cpu().numpy(), st.cpu().numpy()
+    rng = np.random.default_rng(0)
+    sample = np.sort(rng.choice(w.nq, 400, replace=False))
+    o_ids, o_d, o_st = oracle.search(ox, w.Q[sample], w.lo[sample], w.hi[sample], K, L, qidx=sample,
+                                     epn=16, epn_frac=1.0, epn_max=3072, B=16)
+    res = assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
+    ok = np.setdiff1d(np.arange(len(sample)), res)
+    # the search took the same path: expansions, |EN| sums, ENC entries, hotspot
+    for gc, oc in [(F.STAT_EXPANSIONS, oracle.STAT_EXPANSIONS), (F.STAT_EN, oracle.STAT_EN),
+                   (F.STAT_SCANNED, oracle.STAT_SCANNED), (F.STAT_ENTRY, oracle.STAT_ENTRY),
+                   (F.STAT_LSTART, oracle.STAT_LS), (F.STAT_LEND, oracle.STAT_LE)]:
+        assert (st[sample][ok, gc] == o_st[ok, oc]).all(), gc
+    assert (st[sample][ok, F.STAT_DIST] >= o_st[ok, oracle.STAT_DIST]).all()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_properties_every_row(c2):
+    w, ix, ox, d = c2
+    ids, ds = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTING)
+    torch.cuda.synchronize()
+    ids, ds = ids.cpu().numpy(), ds.cpu().numpy()
+    cnt = (w.hi - w.lo + 1).astype(np.int64)
+    valid = ids >= 0
+    # every row holds min(k, cnt) results: the entry points alone give that many
+    assert (valid.sum(1) == np.minimum(K, cnt)).all()
+    # ids inside the query's attribute range, distinct, distances ascending
+    a = w.attr[np.where(valid, ids, 0)]
+    assert ((a >= w.lo[:, None]) & (a <= w.hi[:, None]) | ~valid).all()
+    for i in range(w.nq):
+        row = ids[i][valid[i]]
+        assert len(np.unique(row)) == len(row)
+    assert (np.diff(np.where(valid, ds, np.inf), axis=1) >= 0).all()
+    # every distance is the squared L2 recomputed in fp64 (one rounding)
+    qi, kj = np.nonzero(valid)
+    ref = ((w.X[ids[qi, kj]].astype(np.float64) - w.Q[qi].astype(np.float64)) ** 2).sum(1).astype(np.float32)
+    got = ds[qi, kj]
+    assert (np.abs(got - ref) <= np.spacing(ref)).all()
+    # determinism of the timed launch
+    ids2, ds2 = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTING)
+    torch.cuda.synchronize()
+    assert (ids2.cpu().numpy() == ids).all()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_bruteforce_sample(c2):
+    w, ix, ox, d = c2
+    gt, gd, cert = F.bruteforce(ix, d["Q"], d["lo"], d["hi"], K)
+    torch.cuda.synchronize()
+    gt, gd, cert = gt.cpu().numpy(), gd.cpu().numpy(), cert.cpu().numpy()
+    assert cert.all()
+    rng = np.random.default_rng(1)
+    sample = np.sort(rng.choice(w.nq, 60, replace=False))
+    o_ids, o_d = oracle.exact(ox.X_rank, ox.attr_sorted, ox.perm, w.Q[sample], w.lo[sample], w.hi[sample], K)
+    assert_parity(gt[sample], gd[sample], o_ids, o_d, max_residual=0)
