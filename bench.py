@@ -119,9 +119,9 @@ def main():
     k = w.k
     stream = torch.cuda.current_stream()
 
-    def run(L, epn, frac, emax, hl2=args.hash_log2, stats=False):
+    def run(L, epn, frac, emax, hl2=args.hash_log2, stats=False, events=None):
         return F.search(ix, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax,
-                        hash_log2=hl2, stats=stats)
+                        hash_log2=hl2, stats=stats, events=events)
 
     def timed(fn, reps):
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -182,23 +182,30 @@ def main():
     log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} recall={chosen['recall']:.4f}"
         + ("" if met else "  (recall target NOT met)"))
 
-    # timed steps
+    # timed steps; each step also records three events around the library's
+    # two kernels (entry points, traversal) on the same stream
     for _ in range(args.warmup):
         run(L, epn, frac, emax)
+    phase = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for trio in phase:
+        for ev in trio:
+            ev.record(stream)            # materialise the events
     torch.cuda.synchronize()
     ev_s, ev_e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     ev_s.record(stream)
-    for _ in range(args.steps):
-        run(L, epn, frac, emax)
+    for i in range(args.steps):
+        run(L, epn, frac, emax, events=phase[i])
     ev_e.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     per_step = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
+    t_entry = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
+    t_trav = sum(t[1].elapsed_time(t[2]) for t in phase) / 1000.0 / args.steps
     qps = w.nq / per_step
     log(f"timed {args.steps} steps: {per_step * 1e3:.3f} ms/step (events), wall {wall / args.steps * 1e3:.3f} ms/step, "
-        f"{qps:.0f} QPS")
+        f"{qps:.0f} QPS; entry kernel {t_entry * 1e3:.3f} ms, traversal kernel {t_trav * 1e3:.3f} ms")
 
     # algorithmic bytes: distinct evaluations and ENC entries from the exact-visited pass
     ids_e, _, st_e = run(L, epn, frac, emax, hl2=0, stats=True)
@@ -208,14 +215,27 @@ def main():
     st_f = st_f.cpu().numpy().astype(np.int64)
     D = st_e[:, F.STAT_DIST].sum()
     S = st_e[:, F.STAT_SCANNED].sum()
+    NE = st_e[:, F.STAT_ENTRY].sum()
     nonempty = int((cnt > 0).sum())
-    per_query_fixed = 4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k
-    alg_bytes = 4.0 * d * D + 4.0 * S + per_query_fixed * nonempty
-    achieved = alg_bytes / per_step / 1e9
+    # entry kernel: the entry vectors and each query vector; traversal kernel:
+    # the traversal's distinct vectors, the ENC entries Alg. 4 examines, the
+    # query, the rank search, the output and its id map
+    bytes_entry = 4.0 * d * NE + 4.0 * d * nonempty
+    bytes_trav = (4.0 * d * (D - NE) + 4.0 * S
+                  + (4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k) * nonempty)
+    alg_bytes = bytes_entry + bytes_trav
     overhead = st_f[:, F.STAT_DIST].sum() / max(D, 1)
-    log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, ENC entries {S}); "
-        f"{achieved:.0f} GB/s = {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s; "
-        f"forgetful-table evaluations x{overhead:.3f}")
+    kernels = {
+        "entry_kernel": dict(bytes=bytes_entry, s=t_entry, gbs=bytes_entry / t_entry / 1e9),
+        "search_kernel": dict(bytes=bytes_trav, s=t_trav, gbs=bytes_trav / t_trav / 1e9),
+    }
+    dominant = max(kernels, key=lambda kname: kernels[kname]["s"])
+    achieved = kernels[dominant]["gbs"]
+    log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, entry points {NE}, "
+        f"ENC entries {S}); whole step {alg_bytes / per_step / 1e9:.0f} GB/s; "
+        + "; ".join(f"{kname} {v['bytes'] / 1e6:.0f} MB in {v['s'] * 1e3:.3f} ms = {v['gbs']:.0f} GB/s"
+                    for kname, v in kernels.items())
+        + f"; forgetful-table evaluations x{overhead:.3f}")
 
     traffic = None
     sha = source_sha()
@@ -223,8 +243,9 @@ def main():
         tf = json.load(open(TRAFFIC_FILE))
         same = (tf.get("source_sha") == sha and tf.get("setting") == [L, epn, frac, emax]
                 and tf.get("n") == n and tf.get("nq") == w.nq)
-        if same:
-            traffic = 1024.0 * (tf["fetch_kib"] * tf["fetch_factor"] + tf["write_kib"] * tf["write_factor"])
+        if same and dominant in tf.get("kernels", {}):
+            kc = tf["kernels"][dominant]
+            traffic = 1024.0 * (kc["fetch_kib"] * tf["fetch_factor"] + kc["write_kib"] * tf["write_factor"])
 
     # CPU oracle on a bounded sample (same index arrays, same parameters)
     cpu = None
@@ -271,8 +292,11 @@ def main():
             "hash_log2": args.hash_log2, "recall@10": chosen["recall"], "recall_target_met": met,
             "index": {"H": H, "m": m, "build_s": round(t_build, 1)},
         },
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "step_achieved": alg_bytes / per_step / 1e9,
+                     "kernels": {kname: {"ms": v["s"] * 1e3, "alg_bytes": v["bytes"], "GB/s": v["gbs"]}
+                                 for kname, v in kernels.items()}},
         "cpu_baseline": cpu,
         "bruteforce": {"ms": bf_time * 1e3, "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,

@@ -73,6 +73,9 @@ typedef struct {
     int hash_log2;      /* visited table of 2^hash_log2 slots in LDS (6..13): 10;
                            0 selects an exact visited set in device memory (slow;
                            used to count distinct evaluations) */
+    void** phase_events;/* NULL, or 3 caller-created hipEvent_t recorded on `stream`
+                           before the entry-point kernel, between it and the
+                           traversal kernel, and after the traversal kernel */
 } frog_search_params_t;
 
 /* Per-query statistics written by frog_search_ex (int32, FROG_STAT_N per query). */

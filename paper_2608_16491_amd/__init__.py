@@ -44,7 +44,8 @@ class BuildParams(C.Structure):
 
 class SearchParams(C.Structure):
     _fields_ = [("epn", C.c_int), ("epn_frac", C.c_double), ("epn_max", C.c_int), ("budget", C.c_int),
-                ("seed", C.c_uint64), ("query_base", C.c_int64), ("hash_log2", C.c_int)]
+                ("seed", C.c_uint64), ("query_base", C.c_int64), ("hash_log2", C.c_int),
+                ("phase_events", C.c_void_p)]
 
 
 _lib = None
@@ -230,7 +231,8 @@ def search(index: Index, Q, lo, hi, k: int, L: int, *, stats: bool = False, stre
     """FROGSearch for a batch: Q [nq, d] float32, lo/hi [nq] float64, all on
     the index's device.  Returns (ids int32 [nq, k], dists float32 [nq, k]) and,
     with stats=True, the per-query statistics int32 [nq, 8].  Keyword params:
-    epn, epn_frac, epn_max, budget, seed, query_base, hash_log2."""
+    epn, epn_frac, epn_max, budget, seed, query_base, hash_log2, and events
+    (three torch.cuda.Event recorded around the two kernels)."""
     import torch
     nq = Q.shape[0]
     if out is None:
@@ -239,7 +241,13 @@ def search(index: Index, Q, lo, hi, k: int, L: int, *, stats: bool = False, stre
     else:
         ids, ds = out
     st = torch.empty((nq, STAT_N), dtype=torch.int32, device=Q.device) if stats else None
+    events = params.pop("events", None)
     p = search_params(**params)
+    if events is not None:
+        # three torch.cuda.Event(enable_timing=True): before the entry-point
+        # kernel, between the kernels, after the traversal kernel
+        ev_arr = (C.c_void_p * 3)(*[C.c_void_p(e.cuda_event) for e in events])
+        p.phase_events = C.cast(ev_arr, C.c_void_p)
     _check(lib().frog_search_ex(index.handle, _dev(Q, torch.float32), nq, _dev(lo, torch.float64),
                                 _dev(hi, torch.float64), k, L, C.byref(p), _dev(ids, torch.int32),
                                 _dev(ds, torch.float32), None if st is None else _dev(st, torch.int32),

@@ -146,6 +146,7 @@ void frog_search_params_default(frog_search_params_t* p) {
     p->seed = 0;
     p->query_base = 0;
     p->hash_log2 = 10;
+    p->phase_events = nullptr;
 }
 
 int frog_build_index(const float* X, const double* attr, int64_t n, int d,
@@ -404,7 +405,7 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
     a.Q = d_queries; a.nq = nq; a.lo = d_lo; a.hi = d_hi; a.k = k; a.L = L;
     a.epn = q.epn; a.epn_max = q.epn_frac > 0.0 ? q.epn_max : q.epn; a.epn_frac = q.epn_frac;
     a.B = q.budget; a.hash_log2 = q.hash_log2; a.seed = q.seed; a.qbase = q.query_base;
-    a.ids = d_ids; a.dists = d_dists; a.stats = d_stats;
+    a.ids = d_ids; a.dists = d_dists; a.stats = d_stats; a.events = q.phase_events;
     return frog::launch_search(view(ix), a, stream);
 }
 

@@ -59,6 +59,7 @@ struct SearchLaunch {
     int32_t* ids;
     float* dists;
     int32_t* stats;
+    void** events;   // NULL or 3 hipEvent_t
 };
 
 // search.hip

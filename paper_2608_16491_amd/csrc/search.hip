@@ -815,8 +815,12 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
     KParams PE = P;
     PE.lds_per_wave = lpw_entry;
+    hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(a.events);
+    if (ev) (void)hipEventRecord(ev[0], stream);
     hipLaunchKernelGGL(kp.entry, dim3(eblocks), dim3(kBlock), smem_entry, stream, PE);
+    if (ev) (void)hipEventRecord(ev[1], stream);
     hipLaunchKernelGGL(kp.search, dim3(blocks), dim3(kBlock), smem, stream, P);
+    if (ev) (void)hipEventRecord(ev[2], stream);
     e = hipGetLastError();
     (void)hipFreeAsync(wsp, stream);
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
