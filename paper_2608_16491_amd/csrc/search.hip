@@ -253,6 +253,68 @@ __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&
     return mine;
 }
 
+// Same result as eval_small for the entry-point batches (up to 64 candidates),
+// with two steps of 16 vectors in flight: the loads of step i+1 are issued
+// before step i is reduced, so the arithmetic overlaps the memory latency.
+template <int C>
+struct Gather16 {
+    float4 x[2][C];
+    __device__ __forceinline__ void issue(const float4* __restrict__ X4, int dp4, int cnt, int32_t myid, int sb0) {
+        const int lane = lane_id();
+        const int sub = lane & 7;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+            const int j = sb0 + 8 * g + (lane >> 3);
+            const int id = __shfl(myid, j & 63);
+            const bool v = j < cnt;
+#pragma unroll
+            for (int c = 0; c < C; ++c)
+                x[g][c] = v ? X4[(int64_t)id * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+    __device__ __forceinline__ void consume(const float4 (&qv)[C], int sb0, float& mine) const {
+        const int lane = lane_id();
+        double s[2] = {0.0, 0.0};
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            float4 qf = qv[c];
+            asm volatile("" : "+v"(qf.x), "+v"(qf.y), "+v"(qf.z), "+v"(qf.w));
+            const double q0 = qf.x, q1 = qf.y, q2 = qf.z, q3 = qf.w;
+#pragma unroll
+            for (int g = 0; g < 2; ++g) {
+                double t;
+                t = q0 - (double)x[g][c].x; s[g] += t * t;
+                t = q1 - (double)x[g][c].y; s[g] += t * t;
+                t = q2 - (double)x[g][c].z; s[g] += t * t;
+                t = q3 - (double)x[g][c].w; s[g] += t * t;
+            }
+        }
+        const int src = (lane & 7) << 3;
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+            const float f = (float)sum8(s[g]);
+            const float got = __shfl(f, src);
+            if ((lane >> 3) == (((sb0 >> 3) + g) & 7)) mine = got;
+        }
+    }
+};
+
+template <int C>
+__device__ float eval_pipelined(const float* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
+    const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
+    const int dp4 = dp >> 2;
+    float mine = 0.f;
+    Gather16<C> a, b;
+    a.issue(X4, dp4, cnt, myid, 0);
+    for (int sb0 = 0; sb0 < cnt; sb0 += 32) {
+        if (sb0 + 16 < cnt) b.issue(X4, dp4, cnt, myid, sb0 + 16);
+        a.consume(qv, sb0, mine);
+        if (sb0 + 32 < cnt) a.issue(X4, dp4, cnt, myid, sb0 + 32);
+        if (sb0 + 16 < cnt) b.consume(qv, sb0 + 16, mine);
+    }
+    return mine;
+}
+
 // d > 128: all 64 lanes read one vector, float4 chunk lane + 64c.
 __device__ float eval_large(const float* __restrict__ X, int dp, const float* __restrict__ q, int d, int cnt,
                             int32_t myid) {
@@ -412,11 +474,21 @@ struct WaveLds {
 
 // Query context shared by both kernels: the query's float4 chunks this lane
 // needs, its rank interval and its entry points (Alg. 2).
+// floor(a / b) for 0 <= a < 2^51, b > 0, given rb ~ 1/b: the double estimate is
+// off by at most one, which the integer check corrects.
+__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b, double rb) {
+    int64_t f = (int64_t)((double)a * rb);
+    if (f * b > a) --f;
+    else if ((f + 1) * b <= a) ++f;
+    return f;
+}
+
 template <int C>
 struct QueryCtx {
     float4 qv[C > 0 ? C : 1];
     const float* qrow;
     int64_t qi, l, r, cnt, E, ne;
+    double rE;
     bool all;
     uint64_t qkey;
 
@@ -433,6 +505,7 @@ struct QueryCtx {
         }
         all = cnt <= E;
         ne = cnt <= 0 ? 0 : (all ? cnt : E);
+        rE = 1.0 / (double)E;
         qkey = (uint64_t)(A.qbase + q) << 32;
         qrow = A.Q + q * ix.d;
     }
@@ -453,13 +526,17 @@ struct QueryCtx {
     // jittered rank per stratum
     __device__ int32_t entry_id(const SearchLaunch& A, int64_t j) const {
         if (all) return (int32_t)(l + j);
-        const int64_t s0 = l + (j * cnt) / E;
-        const int64_t t0 = l + ((j + 1) * cnt) / E - 1;
+        const int64_t s0 = l + floor_div(j * cnt, E, rE);
+        const int64_t t0 = l + floor_div((j + 1) * cnt, E, rE) - 1;
         const uint64_t z = splitmix64(A.seed ^ qkey ^ (uint64_t)j);
         return (int32_t)(s0 + (int64_t)(((z >> 32) * (uint64_t)(t0 - s0 + 1)) >> 32));
     }
     __device__ float eval(const DevIndex& ix, int nb, int32_t myid) const {
         if constexpr (C > 0) return eval_small<C>(ix.X, ix.dp, qv, nb, myid);
+        else return eval_large(ix.X, ix.dp, qrow, ix.d, nb, myid);
+    }
+    __device__ float eval_batch(const DevIndex& ix, int nb, int32_t myid) const {
+        if constexpr (C > 0) return eval_pipelined<C>(ix.X, ix.dp, qv, nb, myid);
         else return eval_large(ix.X, ix.dp, qrow, ix.d, nb, myid);
     }
 };
@@ -496,10 +573,11 @@ void entry_kernel(KParams P) {
 #pragma unroll
         for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
         pool.np = 0;
-        for (int64_t b0 = e0; b0 < e1; b0 += 16) {
-            const int nb = (int)(e1 - b0 < 16 ? e1 - b0 : 16);
+        // 64 entry points per batch: one id per lane, one merge per batch
+        for (int64_t b0 = e0; b0 < e1; b0 += 64) {
+            const int nb = (int)(e1 - b0 < 64 ? e1 - b0 : 64);
             const int32_t id = lane < nb ? Q.entry_id(A, b0 + lane) : 0;
-            const float dd = Q.eval(ix, nb, id);
+            const float dd = Q.eval_batch(ix, nb, id);
             const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
             merge<LP>(pool, nkey, nb, A.L, W.st_key, W.st_flag);
         }
