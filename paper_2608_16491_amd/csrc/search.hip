@@ -204,26 +204,23 @@ __device__ void hotspot(int64_t l, int64_t r, int H, int64_t n, int& Ls, int& Le
 // float4 chunks this lane needs are in qv.
 template <int C>
 __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
-    // G = 8 lanes per vector: lane reads float4 chunks (lane % 8) + 8c.
+    // G = 8 lanes per vector: lane reads float4 chunks (lane % 8) + 8c; one
+    // group of 8 vectors per step (an expansion rarely yields more than 8)
     const int lane = lane_id();
     const int sub = lane & 7;
     const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
     const int dp4 = dp >> 2;
+    const int src = (lane & 7) << 3;
     float mine = 0.f;
-    for (int sb0 = 0; sb0 < cnt; sb0 += 16) {
-        // two groups of 8 vectors per step: issue all loads first
-        const int j0 = sb0 + (lane >> 3);
-        const int j1 = j0 + 8;
-        const int id0 = __shfl(myid, j0 & 63);
-        const int id1 = __shfl(myid, j1 & 63);
-        const bool v0 = j0 < cnt, v1 = j1 < cnt;
-        float4 x0[C], x1[C];
+    for (int sb0 = 0; sb0 < cnt; sb0 += 8) {
+        const int j = sb0 + (lane >> 3);
+        const int id = __shfl(myid, j & 63);
+        const bool v = j < cnt;
+        float4 x[C];
 #pragma unroll
-        for (int c = 0; c < C; ++c) {
-            x0[c] = v0 ? X4[(int64_t)id0 * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
-            x1[c] = v1 ? X4[(int64_t)id1 * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        double s0 = 0.0, s1 = 0.0;
+        for (int c = 0; c < C; ++c)
+            x[c] = v ? X4[(int64_t)id * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        double s = 0.0;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
             // keep the query in fp32 registers: convert per use, not once
@@ -231,24 +228,15 @@ __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&
             asm volatile("" : "+v"(qf.x), "+v"(qf.y), "+v"(qf.z), "+v"(qf.w));
             const double q0 = qf.x, q1 = qf.y, q2 = qf.z, q3 = qf.w;
             double t;
-            t = q0 - (double)x0[c].x; s0 += t * t;
-            t = q1 - (double)x0[c].y; s0 += t * t;
-            t = q2 - (double)x0[c].z; s0 += t * t;
-            t = q3 - (double)x0[c].w; s0 += t * t;
-            t = q0 - (double)x1[c].x; s1 += t * t;
-            t = q1 - (double)x1[c].y; s1 += t * t;
-            t = q2 - (double)x1[c].z; s1 += t * t;
-            t = q3 - (double)x1[c].w; s1 += t * t;
+            t = q0 - (double)x[c].x; s += t * t;
+            t = q1 - (double)x[c].y; s += t * t;
+            t = q2 - (double)x[c].z; s += t * t;
+            t = q3 - (double)x[c].w; s += t * t;
         }
-        s0 = sum8(s0);
-        s1 = sum8(s1);
-        const float f0 = (float)s0, f1 = (float)s1;
-        // vector sb0 + g (g < 8) sits in lanes 8g..8g+7 of f0, sb0 + 8 + g in f1
-        const int src = (lane & 7) << 3;
-        const float g0 = __shfl(f0, src);
-        const float g1 = __shfl(f1, src);
-        if ((lane >> 3) == ((sb0 >> 3) & 7)) mine = g0;
-        if ((lane >> 3) == (((sb0 >> 3) + 1) & 7)) mine = g1;
+        s = sum8(s);
+        // vector sb0 + g sits in lanes 8g..8g+7; lane sb0 + g takes it
+        const float got = __shfl((float)s, src);
+        if ((lane >> 3) == ((sb0 >> 3) & 7)) mine = got;
     }
     return mine;
 }
@@ -627,13 +615,22 @@ void search_kernel(KParams P) {
             Q.load_vector(ix);
             // the L nearest entry points: merge the chunk pools
             const int nch = (int)((Q.ne + P.chunk - 1) / P.chunk);
-            for (int cc = 0; cc < nch; ++cc) {
-                const uint64_t* part = P.part + ((uint64_t)qi * P.cpq + cc) * slots;
+            for (int c0 = 0; c0 < nch; c0 += 8) {
+                // issue up to eight chunk pools' loads, then merge them
+                uint64_t keys[8][LP];
 #pragma unroll
-                for (int s = 0; s < LP; ++s) {
-                    const uint64_t key = part[s * 64 + lane];
-                    const int nk = __popcll(ballot(key != kEmpty));   // sorted: a prefix
-                    if (nk > 0) merge<LP>(pool, key, nk, L, W.st_key, W.st_flag);
+                for (int i = 0; i < 8; ++i) {
+                    const uint64_t* part = P.part + ((uint64_t)qi * P.cpq + c0 + i) * slots;
+#pragma unroll
+                    for (int s = 0; s < LP; ++s) keys[i][s] = c0 + i < nch ? part[s * 64 + lane] : kEmpty;
+                }
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+#pragma unroll
+                    for (int s = 0; s < LP; ++s) {
+                        const int nk = __popcll(ballot(keys[i][s] != kEmpty));   // sorted: a prefix
+                        if (nk > 0) merge<LP>(pool, keys[i][s], nk, L, W.st_key, W.st_flag);
+                    }
                 }
             }
             st[FROG_STAT_ENTRY] = (int32_t)Q.ne;
@@ -667,6 +664,11 @@ void search_kernel(KParams P) {
             // best-first loop (Alg. 2)
             const int64_t nent = (int64_t)(Le - Ls + 1) * m;
             int32_t* enbuf = W.enbuf;
+            // The first 64 hotspot entries of the next unexpanded pool entry
+            // are loaded while the current candidates are gathered; they are
+            // used only if that entry is the one selected next.
+            int32_t pre_u = -1;
+            int32_t pre_v = -1;
             for (;;) {
                 // a4: first unexpanded entry
                 int sel = -1;
@@ -686,23 +688,44 @@ void search_kernel(KParams P) {
                         if (lane == sl) pool.flag[s] = 1u;
                     }
                 }
+                u = uniform(u);
                 st[FROG_STAT_EXPANSIONS] += 1;
 
                 // a5 + a6: ENC slice of the hotspot, compaction under budget B
                 const int32_t* row = ix.ENC + ((int64_t)u * H + Ls) * m;
+                const bool hit = u == pre_u;
+                // next prefetch: the first unexpanded entry after u
+                int nsel = -1;
+#pragma unroll
+                for (int s = 0; s < LP; ++s) {
+                    const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
+                    if (nsel < 0 && mk != 0) nsel = s * 64 + __builtin_ctzll(mk);
+                }
+                nsel = uniform(nsel);
+                int32_t nu = -1;
+#pragma unroll
+                for (int s = 0; s < LP; ++s)
+                    if (s == (nsel >> 6) && nsel >= 0) nu = (int32_t)(uint32_t)readlane64(pool.key[s], nsel & 63);
+                nu = uniform(nu);
+                const int32_t cur_pre = pre_v;
+                pre_u = nu;
+                if (nu >= 0) {
+                    const int32_t* nrow = ix.ENC + ((int64_t)nu * H + Ls) * m;
+                    pre_v = lane < nent ? nrow[lane] : -1;
+                    st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
+                }
                 int nen = 0;
                 int64_t scanned = nent;
                 for (int64_t off = 0; off < nent && nen < B; off += 64) {
                     const int64_t e = off + lane;
-                    const int32_t v = e < nent ? row[e] : -1;
+                    const int32_t v = (off == 0 && hit) ? cur_pre : (e < nent ? row[e] : -1);
                     const bool pred = v >= l && v <= r;
                     const uint64_t pm = ballot(pred);
                     const int rk = mbcnt(pm);
                     const int tot = __popcll(pm);
                     const int admit = tot < B - nen ? tot : B - nen;
                     if (pred && rk < admit) enbuf[nen + rk] = v;
-                    const int here = (int)(nent - off < 64 ? nent - off : 64);
-                    st[FROG_STAT_LOADED] += here;
+                    if (!(off == 0 && hit)) st[FROG_STAT_LOADED] += (int32_t)(nent - off < 64 ? nent - off : 64);
                     if (admit == B - nen && admit > 0) {
                         // budget reached: Alg. 4 examined every layer up to the
                         // one holding the last admitted entry
