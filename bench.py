@@ -35,15 +35,16 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "search_c2_traffic.json")
 
-# (L, epn, epn_frac, epn_max): the paper's fixed 16 entry points, then the
-# per-query count min(cnt, epn_max) -- on the clustered mixture a query must
-# start inside its own cluster, which takes a few thousand uniform samples
+# (L, epn, epn_frac, epn_max, budget): the paper's fixed 16 entry points, then
+# the per-query count min(cnt, epn_max) -- on the clustered mixture a query
+# must start inside its own cluster, which takes a few thousand uniform samples
 SWEEP = [
-    (32, 16, 0.0, 0), (64, 16, 0.0, 0),
-    (32, 16, 1.0, 2048), (64, 16, 1.0, 2048),
-    (32, 16, 1.0, 2560), (64, 16, 1.0, 2560),
-    (32, 16, 1.0, 3072), (64, 16, 1.0, 3072),
-    (32, 16, 1.0, 4096), (64, 16, 1.0, 4096),
+    (32, 16, 0.0, 0, 16), (64, 16, 0.0, 0, 16),
+    (32, 16, 1.0, 2048, 16), (64, 16, 1.0, 2048, 16),
+    (32, 16, 1.0, 2560, 16), (48, 16, 1.0, 2560, 16), (64, 16, 1.0, 2560, 16), (48, 16, 1.0, 2560, 32),
+    (32, 16, 1.0, 2816, 16), (40, 16, 1.0, 2816, 16), (48, 16, 1.0, 2816, 16), (32, 16, 1.0, 2816, 32),
+    (32, 16, 1.0, 3072, 16), (64, 16, 1.0, 3072, 16),
+    (32, 16, 1.0, 4096, 16), (64, 16, 1.0, 4096, 16),
 ]
 
 
@@ -79,7 +80,7 @@ def main():
     ap.add_argument("--n", type=int, default=None, help="override n (smaller runs)")
     ap.add_argument("--nq", type=int, default=None, help="override the number of queries")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle time")
-    ap.add_argument("--setting", default=None, help="L,epn,epn_frac,epn_max: skip the sweep")
+    ap.add_argument("--setting", default=None, help="L,epn,epn_frac,epn_max,budget: skip the sweep")
     ap.add_argument("--hash-log2", type=int, default=10)
     ap.add_argument("--profile-pass", action="store_true",
                     help="run the chosen setting once plus a 1 GiB copy, for rocprofv3 counters")
@@ -119,9 +120,15 @@ def main():
     k = w.k
     stream = torch.cuda.current_stream()
 
-    def run(L, epn, frac, emax, hl2=args.hash_log2, stats=False, events=None):
-        return F.search(ix, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax,
+    def run(L, epn, frac, emax, B=16, hl2=args.hash_log2, stats=False, events=None):
+        return F.search(ix, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
                         hash_log2=hl2, stats=stats, events=events)
+
+    def parse_setting(text):
+        v = [float(x) for x in text.split(",")]
+        if len(v) == 4:
+            v.append(16)
+        return int(v[0]), int(v[1]), v[2], int(v[3]), int(v[4])
 
     def timed(fn, reps):
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -134,8 +141,8 @@ def main():
         return s.elapsed_time(e) / 1000.0 / reps
 
     if args.profile_pass:
-        L, epn, frac, emax = (float(x) for x in args.setting.split(","))
-        run(int(L), int(epn), frac, int(emax))
+        L, epn, frac, emax, B = parse_setting(args.setting)
+        run(L, epn, frac, emax, B)
         torch.cuda.synchronize()
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
         b = torch.empty_like(a)
@@ -160,32 +167,31 @@ def main():
 
     # sweep
     rows = []
-    settings = SWEEP if args.setting is None else [tuple(float(x) for x in args.setting.split(","))]
-    for (L, epn, frac, emax) in settings:
-        L, epn, emax = int(L), int(epn), int(emax)
+    settings = SWEEP if args.setting is None else [parse_setting(args.setting)]
+    for (L, epn, frac, emax, B) in settings:
         if L < k:
             continue
-        ids, _ = run(L, epn, frac, emax)
+        ids, _ = run(L, epn, frac, emax, B)
         torch.cuda.synchronize()
         rec = recall_at_k(ids.cpu().numpy(), gt_ids)
-        t = timed(lambda: run(L, epn, frac, emax), 3)
-        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, recall=float(rec.mean()),
+        t = timed(lambda: run(L, epn, frac, emax, B), 3)
+        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, recall=float(rec.mean()),
                          qps=w.nq / t, ms=t * 1e3,
                          recall_band=[float(rec[band == b].mean()) if (band == b).any() else None
                                       for b in range(10)]))
-        log(f"L={L:4d} epn={epn} frac={frac:<6} max={emax:5d}  recall={rec.mean():.4f}  "
+        log(f"L={L:4d} epn={epn} frac={frac:<6} max={emax:5d} B={B:2d}  recall={rec.mean():.4f}  "
             f"{t * 1e3:8.3f} ms  {w.nq / t:12.0f} QPS")
     ok = [r for r in rows if r["recall"] >= 0.9]
     chosen = max(ok, key=lambda r: r["qps"]) if ok else max(rows, key=lambda r: r["recall"])
     met = bool(ok)
-    L, epn, frac, emax = chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"]
-    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} recall={chosen['recall']:.4f}"
+    L, epn, frac, emax, B = chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"], chosen["budget"]
+    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} recall={chosen['recall']:.4f}"
         + ("" if met else "  (recall target NOT met)"))
 
-    # timed steps; each step also records three events around the library's
-    # two kernels (entry points, traversal) on the same stream
+    # timed steps; each step also records events around the library's search
+    # kernel on the same stream
     for _ in range(args.warmup):
-        run(L, epn, frac, emax)
+        run(L, epn, frac, emax, B)
     phase = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     for trio in phase:
         for ev in trio:
@@ -196,20 +202,19 @@ def main():
     wall0 = time.perf_counter()
     ev_s.record(stream)
     for i in range(args.steps):
-        run(L, epn, frac, emax, events=phase[i])
+        run(L, epn, frac, emax, B, events=phase[i])
     ev_e.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     per_step = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
-    t_entry = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
-    t_trav = sum(t[1].elapsed_time(t[2]) for t in phase) / 1000.0 / args.steps
+    t_kernel = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
     qps = w.nq / per_step
     log(f"timed {args.steps} steps: {per_step * 1e3:.3f} ms/step (events), wall {wall / args.steps * 1e3:.3f} ms/step, "
-        f"{qps:.0f} QPS; entry kernel {t_entry * 1e3:.3f} ms, traversal kernel {t_trav * 1e3:.3f} ms")
+        f"{qps:.0f} QPS; search kernel {t_kernel * 1e3:.3f} ms")
 
     # algorithmic bytes: distinct evaluations and ENC entries from the exact-visited pass
-    ids_e, _, st_e = run(L, epn, frac, emax, hl2=0, stats=True)
-    _, _, st_f = run(L, epn, frac, emax, stats=True)
+    ids_e, _, st_e = run(L, epn, frac, emax, B, hl2=0, stats=True)
+    _, _, st_f = run(L, epn, frac, emax, B, stats=True)
     torch.cuda.synchronize()
     st_e = st_e.cpu().numpy().astype(np.int64)
     st_f = st_f.cpu().numpy().astype(np.int64)
@@ -217,31 +222,23 @@ def main():
     S = st_e[:, F.STAT_SCANNED].sum()
     NE = st_e[:, F.STAT_ENTRY].sum()
     nonempty = int((cnt > 0).sum())
-    # entry kernel: the entry vectors and each query vector; traversal kernel:
-    # the traversal's distinct vectors, the ENC entries Alg. 4 examines, the
-    # query, the rank search, the output and its id map
-    bytes_entry = 4.0 * d * NE + 4.0 * d * nonempty
-    bytes_trav = (4.0 * d * (D - NE) + 4.0 * S
-                  + (4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k) * nonempty)
-    alg_bytes = bytes_entry + bytes_trav
+    # the search kernel reads every distinct evaluated vector (entry points and
+    # traversal), the ENC entries Alg. 4 examines, the query, its rank search,
+    # and writes the output through the id map
+    alg_bytes = (4.0 * d * D + 4.0 * S
+                 + (4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k) * nonempty)
     overhead = st_f[:, F.STAT_DIST].sum() / max(D, 1)
-    kernels = {
-        "entry_kernel": dict(bytes=bytes_entry, s=t_entry, gbs=bytes_entry / t_entry / 1e9),
-        "search_kernel": dict(bytes=bytes_trav, s=t_trav, gbs=bytes_trav / t_trav / 1e9),
-    }
-    dominant = max(kernels, key=lambda kname: kernels[kname]["s"])
-    achieved = kernels[dominant]["gbs"]
+    dominant = "coop_kernel"
+    achieved = alg_bytes / t_kernel / 1e9
     log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, entry points {NE}, "
-        f"ENC entries {S}); whole step {alg_bytes / per_step / 1e9:.0f} GB/s; "
-        + "; ".join(f"{kname} {v['bytes'] / 1e6:.0f} MB in {v['s'] * 1e3:.3f} ms = {v['gbs']:.0f} GB/s"
-                    for kname, v in kernels.items())
-        + f"; forgetful-table evaluations x{overhead:.3f}")
+        f"ENC entries {S}); search kernel {achieved:.0f} GB/s = {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s, "
+        f"whole step {alg_bytes / per_step / 1e9:.0f} GB/s; forgetful-table evaluations x{overhead:.3f}")
 
     traffic = None
     sha = source_sha()
     if os.path.exists(TRAFFIC_FILE):
         tf = json.load(open(TRAFFIC_FILE))
-        same = (tf.get("source_sha") == sha and tf.get("setting") == [L, epn, frac, emax]
+        same = (tf.get("source_sha") == sha and tf.get("setting") == [L, epn, frac, emax, B]
                 and tf.get("n") == n and tf.get("nq") == w.nq)
         if same and dominant in tf.get("kernels", {}):
             kc = tf["kernels"][dominant]
@@ -257,13 +254,13 @@ def main():
         probe = min(200, w.nq)
         t0 = time.time()
         oracle.search(ox, w.Q[:probe], w.lo[:probe], w.hi[:probe], k, L, epn=epn, epn_frac=frac,
-                      epn_max=emax, threads=threads)
+                      epn_max=emax, B=B, threads=threads)
         tp = max(time.time() - t0, 1e-3)
         ns = int(min(w.nq, max(probe, probe * args.cpu_seconds / tp)))
         if ns > probe:
             t0 = time.time()
             oracle.search(ox, w.Q[:ns], w.lo[:ns], w.hi[:ns], k, L, epn=epn, epn_frac=frac,
-                          epn_max=emax, threads=threads)
+                          epn_max=emax, B=B, threads=threads)
             tp = time.time() - t0
         cpu = {"value": ns / tp, "unit": "queries/s", "cores": threads, "kind": "oracle",
                "sample": f"first {ns} of the {w.nq} queries, same index and setting, {tp:.1f}s"}
@@ -288,15 +285,14 @@ def main():
             "workload": f"{w.name}: n={n} d={d} Gaussian mixture (1000 centres, noise 0.3), "
                         f"random-permutation attribute, {w.nq} queries, selectivity log-uniform "
                         f"[2^-10,1], k={k}",
-            "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": 16,
+            "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": B,
             "hash_log2": args.hash_log2, "recall@10": chosen["recall"], "recall_target_met": met,
             "index": {"H": H, "m": m, "build_s": round(t_build, 1)},
         },
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "step_achieved": alg_bytes / per_step / 1e9,
-                     "kernels": {kname: {"ms": v["s"] * 1e3, "alg_bytes": v["bytes"], "GB/s": v["gbs"]}
-                                 for kname, v in kernels.items()}},
+                     "alg_bytes_per_launch": alg_bytes, "kernel_ms": t_kernel * 1e3,
+                     "step_achieved": alg_bytes / per_step / 1e9},
         "cpu_baseline": cpu,
         "bruteforce": {"ms": bf_time * 1e3, "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,

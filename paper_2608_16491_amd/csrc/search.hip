@@ -51,9 +51,15 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kEmpty = ~0ull;
-// Register budget: at least 4 wavefronts per SIMD (128 VGPRs).  The d = 128
-// kernel needs ~130 without it; the compiler spills a few bytes instead.
-#define FROG_WAVES_PER_EU 4
+// Register budget: at least 3 wavefronts per SIMD (168 VGPRs); four would
+// make the d = 128 kernel spill, which costs more than the lost wave.
+#ifndef FROG_WAVES_PER_EU
+#define FROG_WAVES_PER_EU 3
+#endif
+// Entry points per work unit (a chunk of a query's entry phase).
+#ifndef FROG_CHUNK
+#define FROG_CHUNK 768
+#endif
 
 struct KParams {
     DevIndex ix;
@@ -61,6 +67,7 @@ struct KParams {
     unsigned int* counter;   // [2] work counters: entry units, queries
     const int32_t* lr;       // [nq][2] rank intervals, from the prologue kernel
     uint64_t* part;          // [nq][cpq][64 * LP] pools of the entry chunks
+    unsigned int* done;      // [nq] finished entry chunks per query
     uint32_t* gvis;          // exact visited bitmaps (hash_log2 == 0)
     int64_t gvis_words;      // words per wave
     int lds_per_wave;        // bytes
@@ -529,260 +536,342 @@ struct QueryCtx {
     }
 };
 
-// a3 (entry points, Alg. 2): work unit = (query, chunk of `chunk` entry
-// points).  The unit evaluates its entry points and writes the L nearest
-// (sorted keys, empty slots = kEmpty) to its slot of `part`.  Spreading the
-// entry phase over many short units keeps every wavefront busy to the end;
-// the kernel boundary publishes the pools to the traversal kernel.
+// a3 (entry points, Alg. 2): evaluate entry points [e0, e1) of a query into
+// a pool holding their L nearest.
 template <int C, int LP>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
-void entry_kernel(KParams P) {
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    const DevIndex& ix = P.ix;
-    const SearchLaunch& A = P.a;
+__device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const QueryCtx<C>& Q, int64_t e0,
+                            int64_t e1, Pool<LP>& pool, const WaveLds<LP>& W) {
     const int lane = lane_id();
-    WaveLds<LP> W(smem, P.lds_per_wave, 0);
-    const int64_t units = A.nq * (int64_t)P.cpq;
-    const uint32_t slots = 64u * LP;
-    for (;;) {
-        int u_l = 0;
-        if (lane == 0) u_l = (int)atomicAdd(P.counter, 1u);
-        const int64_t unit = (uint32_t)uniform(__shfl(u_l, 0));
-        if (unit >= units) break;
-        const int64_t qi = unit / P.cpq;
-        const int ci = (int)(unit - qi * P.cpq);
-        QueryCtx<C> Q;
-        Q.load(ix, A, P.lr, qi);
-        const int64_t e0 = (int64_t)ci * P.chunk;
-        if (e0 >= Q.ne) continue;
-        const int64_t e1 = e0 + P.chunk < Q.ne ? e0 + P.chunk : Q.ne;
-        Q.load_vector(ix);
-        Pool<LP> pool;
 #pragma unroll
-        for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
-        pool.np = 0;
-        // 64 entry points per batch: one id per lane, one merge per batch
-        for (int64_t b0 = e0; b0 < e1; b0 += 64) {
-            const int nb = (int)(e1 - b0 < 64 ? e1 - b0 : 64);
-            const int32_t id = lane < nb ? Q.entry_id(A, b0 + lane) : 0;
-            const float dd = Q.eval_batch(ix, nb, id);
-            const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
-            merge<LP>(pool, nkey, nb, A.L, W.st_key, W.st_flag);
-        }
-        uint64_t* out = P.part + ((uint64_t)qi * P.cpq + ci) * slots;
-#pragma unroll
-        for (int s = 0; s < LP; ++s) out[s * 64 + lane] = pool.key[s];
+    for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+    pool.np = 0;
+    // 64 entry points per batch: one id per lane, one merge per batch
+    for (int64_t b0 = e0; b0 < e1; b0 += 64) {
+        const int nb = (int)(e1 - b0 < 64 ? e1 - b0 : 64);
+        const int32_t id = lane < nb ? Q.entry_id(A, b0 + lane) : 0;
+        const float dd = Q.eval_batch(ix, nb, id);
+        const uint64_t nkey = lane < nb ? make_key(dd, id) : kEmpty;
+        merge<LP>(pool, nkey, nb, A.L, W.st_key, W.st_flag);
     }
 }
 
-// a2, a4-a11: per query, merge the entry chunks' pools (the L nearest entry
-// points), HotspotLocalization, then the best-first loop of Alg. 2.
+// a2, a4-a11 for one query whose pool holds the L nearest entry points:
+// HotspotLocalization, the best-first loop of Alg. 2, output and statistics.
+template <int C, int LP>
+__device__ void traverse(const KParams& P, const QueryCtx<C>& Q, Pool<LP>& pool, const WaveLds<LP>& W,
+                         const Visited& vis) {
+    const DevIndex& ix = P.ix;
+    const SearchLaunch& A = P.a;
+    const int lane = lane_id();
+    const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
+    const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
+    const int64_t qi = Q.qi, l = Q.l, r = Q.r;
+    int32_t st[FROG_STAT_N];
+#pragma unroll
+    for (int i = 0; i < FROG_STAT_N; ++i) st[i] = 0;
+    if (Q.ne > 0) {
+    st[FROG_STAT_ENTRY] = (int32_t)Q.ne;
+    st[FROG_STAT_DIST] = (int32_t)Q.ne;
+
+    // a2: hotspot
+    int Ls, Le;
+    hotspot(l, r, H, ix.n, Ls, Le);
+    Ls = uniform(Ls);
+    Le = uniform(Le);
+    st[FROG_STAT_LSTART] = Ls;
+    st[FROG_STAT_LEND] = Le;
+
+    // visited set: every entry point (exact bitmap) or the pool's
+    // entry points (forgetful table: an entry point outside the pool
+    // can never enter it later, its key is above the pool's L-th)
+    if (vis.tab) {
+        for (int i = lane; i < T; i += 64) vis.tab[i] = -1;
+        wave_sync();
+#pragma unroll
+        for (int s = 0; s < LP; ++s)
+            if (s * 64 + lane < pool.np) vis.insert((int32_t)(uint32_t)pool.key[s]);
+    } else {
+        for (int64_t i = lane; i < P.gvis_words; i += 64) vis.bits[i] = 0u;
+        __threadfence_block();
+        for (int64_t j = lane; j < Q.ne; j += 64) vis.insert(Q.entry_id(A, j));
+        __threadfence_block();
+    }
+    wave_sync();
+
+    // best-first loop (Alg. 2)
+    const int64_t nent = (int64_t)(Le - Ls + 1) * m;
+    int32_t* enbuf = W.enbuf;
+    // The first 64 hotspot entries of the next unexpanded pool entry
+    // are loaded while the current candidates are gathered; they are
+    // used only if that entry is the one selected next.
+    int32_t pre_u = -1;
+    int32_t pre_v = -1;
+    for (;;) {
+        // a4: first unexpanded entry
+        int sel = -1;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) {
+            const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
+            if (sel < 0 && mk != 0) sel = s * 64 + __builtin_ctzll(mk);
+        }
+        sel = uniform(sel);
+        if (sel < 0) break;
+        const int ss = sel >> 6, sl = sel & 63;
+        int32_t u = 0;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) {
+            if (s == ss) {
+                u = (int32_t)(uint32_t)readlane64(pool.key[s], sl);
+                if (lane == sl) pool.flag[s] = 1u;
+            }
+        }
+        u = uniform(u);
+        st[FROG_STAT_EXPANSIONS] += 1;
+
+        // a5 + a6: ENC slice of the hotspot, compaction under budget B
+        const int32_t* row = ix.ENC + ((int64_t)u * H + Ls) * m;
+        const bool hit = u == pre_u;
+        // next prefetch: the first unexpanded entry after u
+        int nsel = -1;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) {
+            const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
+            if (nsel < 0 && mk != 0) nsel = s * 64 + __builtin_ctzll(mk);
+        }
+        nsel = uniform(nsel);
+        int32_t nu = -1;
+#pragma unroll
+        for (int s = 0; s < LP; ++s)
+            if (s == (nsel >> 6) && nsel >= 0) nu = (int32_t)(uint32_t)readlane64(pool.key[s], nsel & 63);
+        nu = uniform(nu);
+        const int32_t cur_pre = pre_v;
+        pre_u = nu;
+        if (nu >= 0) {
+            const int32_t* nrow = ix.ENC + ((int64_t)nu * H + Ls) * m;
+            pre_v = lane < nent ? nrow[lane] : -1;
+            st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
+        }
+        int nen = 0;
+        int64_t scanned = nent;
+        for (int64_t off = 0; off < nent && nen < B; off += 64) {
+            const int64_t e = off + lane;
+            const int32_t v = (off == 0 && hit) ? cur_pre : (e < nent ? row[e] : -1);
+            const bool pred = v >= l && v <= r;
+            const uint64_t pm = ballot(pred);
+            const int rk = mbcnt(pm);
+            const int tot = __popcll(pm);
+            const int admit = tot < B - nen ? tot : B - nen;
+            if (pred && rk < admit) enbuf[nen + rk] = v;
+            if (!(off == 0 && hit)) st[FROG_STAT_LOADED] += (int32_t)(nent - off < 64 ? nent - off : 64);
+            if (admit == B - nen && admit > 0) {
+                // budget reached: Alg. 4 examined every layer up to the
+                // one holding the last admitted entry
+                const int last = uniform(__builtin_ctzll(ballot(pred && rk == admit - 1)));
+                scanned = ((off + last) / m + 1) * m;
+            }
+            nen += admit;
+        }
+        st[FROG_STAT_SCANNED] += (int32_t)scanned;
+        nen = uniform(nen);
+        st[FROG_STAT_EN] += nen;
+        wave_sync();
+
+        // a7: lazy visited check on the compacted list
+        int32_t v = lane < nen ? enbuf[lane] : -1;
+        bool fresh = false;
+        if (lane < nen) fresh = vis.check_insert(v);
+        const uint64_t fm = ballot(fresh);
+        const int ns = __popcll(fm);
+        wave_sync();
+        if (fresh) enbuf[mbcnt(fm)] = v;
+        wave_sync();
+        const int32_t myid = lane < ns ? enbuf[lane] : 0;
+        wave_sync();
+        if (ns == 0) continue;
+
+        // a8: gather + distances
+        const float dd = Q.eval(ix, ns, myid);
+        st[FROG_STAT_DIST] += ns;
+        const uint64_t nkey = lane < ns ? make_key(dd, myid) : kEmpty;
+        // a9 + a10: MergeTopEfS
+        merge<LP>(pool, nkey, ns, L, W.st_key, W.st_flag);
+    }
+    }
+
+    // a11: output, rank -> original id, padding
+#pragma unroll
+    for (int s = 0; s < LP; ++s) {
+        const int p = s * 64 + lane;
+        if (p < k) {
+            int32_t oid = -1;
+            float od = __int_as_float(0x7f800000);
+            if (p < pool.np) {
+                oid = ix.perm[(uint32_t)pool.key[s]];
+                od = __uint_as_float((uint32_t)(pool.key[s] >> 32));
+            }
+            A.ids[qi * k + p] = oid;
+            A.dists[qi * k + p] = od;
+        }
+    }
+    if (A.stats && lane < FROG_STAT_N) {
+        int32_t val = 0;
+#pragma unroll
+        for (int i = 0; i < FROG_STAT_N; ++i)
+            if (lane == i) val = st[i];
+        A.stats[qi * FROG_STAT_N + lane] = val;
+    }
+}
+
+// The whole search in one persistent kernel.  The four wavefronts of a
+// workgroup share queries: a 64-bit LDS word holds the workgroup's open query
+// and the next unclaimed entry chunk (claimed by compare-and-swap); a wave
+// that finds the open query exhausted opens the next one from the global
+// counter.  A wave evaluates one chunk (512 entry points) into a pool, writes
+// it to global memory and counts the query's finished chunks with a
+// workgroup-scope atomic; the wave that finishes the last chunk merges the
+// chunk pools (the L nearest entry points) and runs the query's traversal,
+// while its siblings go on with the next query's chunks -- so the traversal's
+// dependent round trips overlap other queries' bandwidth-bound entry work.
+// Only the waves of one workgroup ever touch a query, so workgroup-scope
+// release/acquire orders the chunk pools (no cache maintenance on gfx950).
+constexpr uint32_t kCtlNone = 0xFFFFFFFFu;       // no open query
+constexpr uint32_t kCtlOpening = 0xFFFFFFFEu;    // a wave is opening one
+constexpr uint32_t kCtlExhausted = 0xFFFFFFFDu;  // no queries left
+
+__device__ __forceinline__ uint64_t ctl_word(uint32_t q, uint32_t next, uint32_t nch) {
+    return ((uint64_t)q << 32) | ((uint64_t)next << 16) | nch;
+}
+
 template <int C, int LP>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
-void search_kernel(KParams P) {
+void coop_kernel(KParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const DevIndex& ix = P.ix;
     const SearchLaunch& A = P.a;
     const int lane = lane_id();
+    uint64_t* ctl = reinterpret_cast<uint64_t*>(smem + (size_t)kWavesPerBlock * P.lds_per_wave);
+    if (threadIdx.x == 0) *ctl = ctl_word(kCtlNone, 0, 0);
+    __syncthreads();
     WaveLds<LP> W(smem, P.lds_per_wave, A.hash_log2);
     Visited vis;
     vis.tab = W.tab;
     vis.shift = 32 - A.hash_log2;
     const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
-    const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
-    const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
     const uint32_t slots = 64u * LP;
 
     for (;;) {
-        int q_l = 0;
-        if (lane == 0) q_l = (int)atomicAdd(P.counter + 1, 1u);
-        const int64_t qi = (uint32_t)uniform(__shfl(q_l, 0));
-        if (qi >= A.nq) break;
+        // ---- claim an entry chunk of the workgroup's open query
+        uint32_t cq = 0, cc = 0, cn = 0;
+        bool done = false;
+        for (;;) {
+            uint64_t w = 0;
+            int state = 0;   // 0 retry, 1 claimed, 2 exhausted
+            if (lane == 0) {
+                w = __hip_atomic_load(ctl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                const uint32_t q = (uint32_t)(w >> 32), nx = (uint32_t)(w >> 16) & 0xFFFFu, nc = (uint32_t)w & 0xFFFFu;
+                if (q == kCtlExhausted) {
+                    state = 2;
+                } else if (q == kCtlOpening) {
+                    __builtin_amdgcn_s_sleep(2);
+                } else if (q == kCtlNone || nx >= nc) {
+                    uint64_t expect = w;
+                    if (__hip_atomic_compare_exchange_strong(ctl, &expect, ctl_word(kCtlOpening, 0, 0), __ATOMIC_RELAXED,
+                                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                        // open the next non-empty query
+                        uint64_t nw = ctl_word(kCtlExhausted, 0, 0);
+                        for (;;) {
+                            const uint32_t g = atomicAdd(P.counter, 1u);
+                            if ((int64_t)g >= A.nq) break;
+                            const int64_t l = P.lr[2 * (int64_t)g], r = P.lr[2 * (int64_t)g + 1];
+                            const int64_t cnt = r - l + 1;
+                            if (cnt <= 0) {
+                                // empty range: padding and zero statistics
+                                for (int j = 0; j < A.k; ++j) {
+                                    A.ids[(int64_t)g * A.k + j] = -1;
+                                    A.dists[(int64_t)g * A.k + j] = __int_as_float(0x7f800000);
+                                }
+                                if (A.stats)
+                                    for (int j = 0; j < FROG_STAT_N; ++j) A.stats[(int64_t)g * FROG_STAT_N + j] = 0;
+                                continue;
+                            }
+                            int64_t E = A.epn;
+                            if (A.epn_frac > 0.0) {
+                                double want = ceil(A.epn_frac * (double)cnt);
+                                if (want > (double)A.epn_max) want = (double)A.epn_max;
+                                if (want > (double)E) E = (int64_t)want;
+                            }
+                            const int64_t ne = cnt <= E ? cnt : E;
+                            nw = ctl_word(g, 0, (uint32_t)((ne + P.chunk - 1) / P.chunk));
+                            break;
+                        }
+                        __hip_atomic_store(ctl, nw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    }
+                } else {
+                    uint64_t expect = w;
+                    if (__hip_atomic_compare_exchange_strong(ctl, &expect, w + ((uint64_t)1 << 16), __ATOMIC_RELAXED,
+                                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) {
+                        state = 1;
+                        cq = q;
+                        cc = nx;
+                        cn = nc;
+                    }
+                }
+            }
+            state = uniform(__shfl(state, 0));
+            if (state == 2) { done = true; break; }
+            if (state == 1) {
+                cq = (uint32_t)uniform((int)__shfl((int)cq, 0));
+                cc = (uint32_t)uniform((int)__shfl((int)cc, 0));
+                cn = (uint32_t)uniform((int)__shfl((int)cn, 0));
+                break;
+            }
+        }
+        if (done) break;
+
+        // ---- the chunk's entry points
+        const int64_t qi = cq;
+        const int ci = (int)cc, nch = (int)cn;
         QueryCtx<C> Q;
         Q.load(ix, A, P.lr, qi);
-        const int64_t l = Q.l, r = Q.r;
-
+        Q.load_vector(ix);
         Pool<LP> pool;
-#pragma unroll
-        for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
-        pool.np = 0;
-        int32_t st[FROG_STAT_N];
-#pragma unroll
-        for (int i = 0; i < FROG_STAT_N; ++i) st[i] = 0;
+        const int64_t e0 = (int64_t)ci * P.chunk;
+        const int64_t e1 = e0 + P.chunk < Q.ne ? e0 + P.chunk : Q.ne;
+        entry_chunk<C, LP>(ix, A, Q, e0, e1, pool, W);
 
-        if (Q.ne > 0) {
-            Q.load_vector(ix);
-            // the L nearest entry points: merge the chunk pools
-            const int nch = (int)((Q.ne + P.chunk - 1) / P.chunk);
+        if (nch > 1) {
+            uint64_t* mine = P.part + ((uint64_t)qi * P.cpq + ci) * slots;
+#pragma unroll
+            for (int s = 0; s < LP; ++s) mine[s * 64 + lane] = pool.key[s];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            uint32_t old = 0;
+            if (lane == 0)
+                old = __hip_atomic_fetch_add(P.done + qi, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            old = (uint32_t)uniform((int)__shfl((int)old, 0));
+            if ((int)old != nch - 1) continue;
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            // the L nearest entry points: merge the other chunks' pools
             for (int c0 = 0; c0 < nch; c0 += 8) {
-                // issue up to eight chunk pools' loads, then merge them
                 uint64_t keys[8][LP];
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
                     const uint64_t* part = P.part + ((uint64_t)qi * P.cpq + c0 + i) * slots;
 #pragma unroll
-                    for (int s = 0; s < LP; ++s) keys[i][s] = c0 + i < nch ? part[s * 64 + lane] : kEmpty;
+                    for (int s = 0; s < LP; ++s)
+                        keys[i][s] = (c0 + i < nch && c0 + i != ci) ? part[s * 64 + lane] : kEmpty;
                 }
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
 #pragma unroll
                     for (int s = 0; s < LP; ++s) {
                         const int nk = __popcll(ballot(keys[i][s] != kEmpty));   // sorted: a prefix
-                        if (nk > 0) merge<LP>(pool, keys[i][s], nk, L, W.st_key, W.st_flag);
+                        if (nk > 0) merge<LP>(pool, keys[i][s], nk, A.L, W.st_key, W.st_flag);
                     }
                 }
             }
-            st[FROG_STAT_ENTRY] = (int32_t)Q.ne;
-            st[FROG_STAT_DIST] = (int32_t)Q.ne;
-
-            // a2: hotspot
-            int Ls, Le;
-            hotspot(l, r, H, ix.n, Ls, Le);
-            Ls = uniform(Ls);
-            Le = uniform(Le);
-            st[FROG_STAT_LSTART] = Ls;
-            st[FROG_STAT_LEND] = Le;
-
-            // visited set: every entry point (exact bitmap) or the pool's
-            // entry points (forgetful table: an entry point outside the pool
-            // can never enter it later, its key is above the pool's L-th)
-            if (vis.tab) {
-                for (int i = lane; i < T; i += 64) vis.tab[i] = -1;
-                wave_sync();
-#pragma unroll
-                for (int s = 0; s < LP; ++s)
-                    if (s * 64 + lane < pool.np) vis.insert((int32_t)(uint32_t)pool.key[s]);
-            } else {
-                for (int64_t i = lane; i < P.gvis_words; i += 64) vis.bits[i] = 0u;
-                __threadfence_block();
-                for (int64_t j = lane; j < Q.ne; j += 64) vis.insert(Q.entry_id(A, j));
-                __threadfence_block();
-            }
-            wave_sync();
-
-            // best-first loop (Alg. 2)
-            const int64_t nent = (int64_t)(Le - Ls + 1) * m;
-            int32_t* enbuf = W.enbuf;
-            // The first 64 hotspot entries of the next unexpanded pool entry
-            // are loaded while the current candidates are gathered; they are
-            // used only if that entry is the one selected next.
-            int32_t pre_u = -1;
-            int32_t pre_v = -1;
-            for (;;) {
-                // a4: first unexpanded entry
-                int sel = -1;
-#pragma unroll
-                for (int s = 0; s < LP; ++s) {
-                    const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
-                    if (sel < 0 && mk != 0) sel = s * 64 + __builtin_ctzll(mk);
-                }
-                sel = uniform(sel);
-                if (sel < 0) break;
-                const int ss = sel >> 6, sl = sel & 63;
-                int32_t u = 0;
-#pragma unroll
-                for (int s = 0; s < LP; ++s) {
-                    if (s == ss) {
-                        u = (int32_t)(uint32_t)readlane64(pool.key[s], sl);
-                        if (lane == sl) pool.flag[s] = 1u;
-                    }
-                }
-                u = uniform(u);
-                st[FROG_STAT_EXPANSIONS] += 1;
-
-                // a5 + a6: ENC slice of the hotspot, compaction under budget B
-                const int32_t* row = ix.ENC + ((int64_t)u * H + Ls) * m;
-                const bool hit = u == pre_u;
-                // next prefetch: the first unexpanded entry after u
-                int nsel = -1;
-#pragma unroll
-                for (int s = 0; s < LP; ++s) {
-                    const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
-                    if (nsel < 0 && mk != 0) nsel = s * 64 + __builtin_ctzll(mk);
-                }
-                nsel = uniform(nsel);
-                int32_t nu = -1;
-#pragma unroll
-                for (int s = 0; s < LP; ++s)
-                    if (s == (nsel >> 6) && nsel >= 0) nu = (int32_t)(uint32_t)readlane64(pool.key[s], nsel & 63);
-                nu = uniform(nu);
-                const int32_t cur_pre = pre_v;
-                pre_u = nu;
-                if (nu >= 0) {
-                    const int32_t* nrow = ix.ENC + ((int64_t)nu * H + Ls) * m;
-                    pre_v = lane < nent ? nrow[lane] : -1;
-                    st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
-                }
-                int nen = 0;
-                int64_t scanned = nent;
-                for (int64_t off = 0; off < nent && nen < B; off += 64) {
-                    const int64_t e = off + lane;
-                    const int32_t v = (off == 0 && hit) ? cur_pre : (e < nent ? row[e] : -1);
-                    const bool pred = v >= l && v <= r;
-                    const uint64_t pm = ballot(pred);
-                    const int rk = mbcnt(pm);
-                    const int tot = __popcll(pm);
-                    const int admit = tot < B - nen ? tot : B - nen;
-                    if (pred && rk < admit) enbuf[nen + rk] = v;
-                    if (!(off == 0 && hit)) st[FROG_STAT_LOADED] += (int32_t)(nent - off < 64 ? nent - off : 64);
-                    if (admit == B - nen && admit > 0) {
-                        // budget reached: Alg. 4 examined every layer up to the
-                        // one holding the last admitted entry
-                        const int last = uniform(__builtin_ctzll(ballot(pred && rk == admit - 1)));
-                        scanned = ((off + last) / m + 1) * m;
-                    }
-                    nen += admit;
-                }
-                st[FROG_STAT_SCANNED] += (int32_t)scanned;
-                nen = uniform(nen);
-                st[FROG_STAT_EN] += nen;
-                wave_sync();
-
-                // a7: lazy visited check on the compacted list
-                int32_t v = lane < nen ? enbuf[lane] : -1;
-                bool fresh = false;
-                if (lane < nen) fresh = vis.check_insert(v);
-                const uint64_t fm = ballot(fresh);
-                const int ns = __popcll(fm);
-                wave_sync();
-                if (fresh) enbuf[mbcnt(fm)] = v;
-                wave_sync();
-                const int32_t myid = lane < ns ? enbuf[lane] : 0;
-                wave_sync();
-                if (ns == 0) continue;
-
-                // a8: gather + distances
-                const float dd = Q.eval(ix, ns, myid);
-                st[FROG_STAT_DIST] += ns;
-                const uint64_t nkey = lane < ns ? make_key(dd, myid) : kEmpty;
-                // a9 + a10: MergeTopEfS
-                merge<LP>(pool, nkey, ns, L, W.st_key, W.st_flag);
-            }
         }
-
-        // a11: output, rank -> original id, padding
-#pragma unroll
-        for (int s = 0; s < LP; ++s) {
-            const int p = s * 64 + lane;
-            if (p < k) {
-                int32_t oid = -1;
-                float od = __int_as_float(0x7f800000);
-                if (p < pool.np) {
-                    oid = ix.perm[(uint32_t)pool.key[s]];
-                    od = __uint_as_float((uint32_t)(pool.key[s] >> 32));
-                }
-                A.ids[qi * k + p] = oid;
-                A.dists[qi * k + p] = od;
-            }
-        }
-        if (A.stats && lane < FROG_STAT_N) {
-            int32_t val = 0;
-#pragma unroll
-            for (int i = 0; i < FROG_STAT_N; ++i)
-                if (lane == i) val = st[i];
-            A.stats[qi * FROG_STAT_N + lane] = val;
-        }
+        traverse<C, LP>(P, Q, pool, W, vis);
     }
 }
 
@@ -797,25 +886,24 @@ __global__ void rank_bounds_kernel(DevIndex ix, const double* lo, const double* 
     }
 }
 
-__global__ void init_kernel(unsigned int* counter) {
-    if (threadIdx.x < 2) counter[threadIdx.x] = 0u;
+__global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t nq) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) *counter = 0u;
+    if (i < nq) done[i] = 0u;
 }
 
 // ------------------------------------------------------------------ dispatch
 
 using KernelFn = void (*)(KParams);
-struct KernelPair {
-    KernelFn entry, search;
-};
 
 template <int C>
-KernelPair pick_lp(int L) {
-    if (L <= 64) return {entry_kernel<C, 1>, search_kernel<C, 1>};
-    if (L <= 128) return {entry_kernel<C, 2>, search_kernel<C, 2>};
-    return {entry_kernel<C, 4>, search_kernel<C, 4>};
+KernelFn pick_lp(int L) {
+    if (L <= 64) return coop_kernel<C, 1>;
+    if (L <= 128) return coop_kernel<C, 2>;
+    return coop_kernel<C, 4>;
 }
 
-KernelPair pick_kernel(int dp, int L) {
+KernelFn pick_kernel(int dp, int L) {
     switch (dp) {
         case 32: return pick_lp<1>(L);
         case 64: return pick_lp<2>(L);
@@ -858,30 +946,24 @@ bool search_shape_supported(int dp, int m, int L) {
 
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     hipStream_t stream = (hipStream_t)stream_v;
-    const KernelPair kp = pick_kernel(ix.dp, a.L);
-    const int lpw_entry = lds_per_wave(a.L, 0);
+    const KernelFn fn = pick_kernel(ix.dp, a.L);
     const int lpw = lds_per_wave(a.L, a.hash_log2);
-    const int smem = lpw * kWavesPerBlock;
-    const int smem_entry = lpw_entry * kWavesPerBlock;
+    const int smem = lpw * kWavesPerBlock + 16;
     if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);
     if (smem > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute((const void*)kp.search, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
         if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
-    // entry chunks: 512 entry points per work unit, at most 16 units per query
+    // entry chunks: FROG_CHUNK entry points per work unit, at most 16 units per query
     const int64_t emax = a.epn_frac > 0.0 ? (a.epn_max > a.epn ? a.epn_max : a.epn) : a.epn;
-    int64_t chunk = 512;
+    int64_t chunk = FROG_CHUNK;
     if ((emax + chunk - 1) / chunk > 16) chunk = ((emax + 15) / 16 + 15) / 16 * 16;
     const int cpq = (int)((emax + chunk - 1) / chunk);
-    if (a.nq * (int64_t)cpq >= ((int64_t)1 << 31))
-        return fail(FROG_EINVAL, "nq=%lld too large for one launch", (long long)a.nq);
+    if (a.nq >= ((int64_t)1 << 31) - 1) return fail(FROG_EINVAL, "nq=%lld too large", (long long)a.nq);
     const int lp = lp_of(a.L);
-    int blocks = max_blocks(kp.search, smem);
-    const int64_t need = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    int blocks = max_blocks(fn, smem);
+    const int64_t need = (a.nq * cpq + kWavesPerBlock - 1) / kWavesPerBlock;
     if (need < blocks) blocks = (int)need;
-    int eblocks = max_blocks(kp.entry, smem_entry);
-    const int64_t eneed = (a.nq * cpq + kWavesPerBlock - 1) / kWavesPerBlock;
-    if (eneed < eblocks) eblocks = (int)eneed;
     KParams P{};
     P.ix = ix;
     P.a = a;
@@ -891,8 +973,9 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     P.gvis_words = 0;
     auto align = [](size_t x) { return (x + 255) / 256 * 256; };
     const size_t off_lr = 256;
-    const size_t off_part = off_lr + align((size_t)a.nq * 8);
-    const size_t part_bytes = (size_t)a.nq * cpq * 64 * lp * 8;
+    const size_t off_done = off_lr + align((size_t)a.nq * 8);
+    const size_t off_part = off_done + align((size_t)a.nq * 4);
+    const size_t part_bytes = cpq > 1 ? (size_t)a.nq * cpq * 64 * lp * 8 : 0;
     const size_t off_gvis = off_part + align(part_bytes);
     size_t ws = off_gvis;
     if (a.hash_log2 == 0) {
@@ -909,19 +992,19 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     P.counter = reinterpret_cast<unsigned int*>(base);
     int32_t* lr = reinterpret_cast<int32_t*>(base + off_lr);
     P.lr = lr;
+    P.done = reinterpret_cast<unsigned int*>(base + off_done);
     P.part = reinterpret_cast<uint64_t*>(base + off_part);
     P.gvis = reinterpret_cast<uint32_t*>(base + off_gvis);
-    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(64), 0, stream, P.counter);
+    hipLaunchKernelGGL(init_kernel, dim3((unsigned)((a.nq + 255) / 256)), dim3(256), 0, stream, P.counter, P.done, a.nq);
     const int64_t rb_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
-    KParams PE = P;
-    PE.lds_per_wave = lpw_entry;
     hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(a.events);
     if (ev) (void)hipEventRecord(ev[0], stream);
-    hipLaunchKernelGGL(kp.entry, dim3(eblocks), dim3(kBlock), smem_entry, stream, PE);
-    if (ev) (void)hipEventRecord(ev[1], stream);
-    hipLaunchKernelGGL(kp.search, dim3(blocks), dim3(kBlock), smem, stream, P);
-    if (ev) (void)hipEventRecord(ev[2], stream);
+    hipLaunchKernelGGL(fn, dim3(blocks), dim3(kBlock), smem, stream, P);
+    if (ev) {
+        (void)hipEventRecord(ev[1], stream);
+        (void)hipEventRecord(ev[2], stream);
+    }
     e = hipGetLastError();
     (void)hipFreeAsync(wsp, stream);
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
