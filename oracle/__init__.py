@@ -60,7 +60,12 @@ def _load():
     if _lib is not None:
         return _lib
     compile_oracle()
-    lib = C.CDLL(_LIB)
+    _lib = configure(C.CDLL(_LIB))
+    return _lib
+
+
+def configure(lib):
+    """Declare the C signatures on a loaded oracle library."""
     P = C.c_void_p
     i64, i32, f64, u64 = C.c_int64, C.c_int, C.c_double, C.c_uint64
     lib.fo_dist.restype = C.c_float
@@ -97,7 +102,6 @@ def _load():
                              P, P, P, P]
     lib.fo_closure.restype = i64
     lib.fo_closure.argtypes = [P, i32, i32, i64, i64, i64, i32, i32, i32, P, i64, P]
-    _lib = lib
     return lib
 
 

@@ -96,3 +96,25 @@ def test_full_size_bruteforce_sample(c2):
     sample = np.sort(rng.choice(w.nq, 60, replace=False))
     o_ids, o_d = oracle.exact(ox.X_rank, ox.attr_sorted, ox.perm, w.Q[sample], w.lo[sample], w.hi[sample], K)
     assert_parity(gt[sample], gd[sample], o_ids, o_d, max_residual=0)
+
+
+@pytest.mark.timeout(900)
+def test_full_size_k100_pool256_sampled(c2):
+    """The sweep configuration's k = 100, L = 256 on the same 1M index: fixed
+    selectivities 0.1%, 1%, 10%, 50%, 100%, sampled rows vs the oracle."""
+    w, ix, ox, d = c2
+    rng = np.random.default_rng(5)
+    nq = 2000
+    sigma = np.array([0.001, 0.01, 0.10, 0.50, 1.00])[np.arange(nq) % 5]
+    lo, hi = workloads.ranges_for_selectivity(rng, sigma, w.n)
+    Q = w.Q[:nq]
+    dev = torch.device("cuda:0")
+    p = dict(epn=16, epn_frac=1.0, epn_max=3072, budget=16)
+    ids, ds = F.search(ix, d["Q"][:nq].contiguous(), torch.as_tensor(lo, device=dev),
+                       torch.as_tensor(hi, device=dev), 100, 256, **p)
+    torch.cuda.synchronize()
+    ids, ds = ids.cpu().numpy(), ds.cpu().numpy()
+    sample = np.sort(rng.choice(nq, 100, replace=False))
+    o_ids, o_d, _ = oracle.search(ox, Q[sample], lo[sample], hi[sample], 100, 256, qidx=sample,
+                                  epn=16, epn_frac=1.0, epn_max=3072, B=16)
+    assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)

@@ -1,0 +1,75 @@
+"""The pins catch plausible mistakes.  Each case plants one mistake in a copy
+of the oracle's source (never in the oracle itself), compiles it, points the
+oracle module at the mutant, and requires the matching pin test to fail."""
+import ctypes as C
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "frog_oracle.c")
+
+# (name, text in frog_oracle.c, replacement, pin tests that must fail)
+MUTANTS = [
+    ("distance sign", "double t = (double)a[i] - (double)b[i];", "double t = (double)a[i] + (double)b[i];",
+     ["test_dist_matches_numpy_fp64"]),
+    ("distance drops a term", "for (int i = 0; i < d; ++i) {\n        double t = (double)a[i]",
+     "for (int i = 1; i < d; ++i) {\n        double t = (double)a[i]", ["test_dist_exact_small_integers"]),
+    ("lower bound uses <=", "if (attr_sorted[mid] < lo) a = mid + 1;", "if (attr_sorted[mid] <= lo) a = mid + 1;",
+     ["test_rank_bounds_match_searchsorted"]),
+    ("hotspot boundary term", "int64_t bl = el + 1, br = sr;", "int64_t bl = el, br = sr;",
+     ["test_hotspot_hand_examples", "test_hotspot_bruteforce"]),
+    ("hotspot descent bound", "while (d < H - 1) {\n        int64_t mid = L + (R - L) / 2;\n        if (r <= mid) R = mid;",
+     "while (d < H) {\n        int64_t mid = L + (R - L) / 2;\n        if (r <= mid) R = mid;",
+     ["test_hotspot_hand_examples", "test_hotspot_bruteforce"]),
+    ("range test off by one", "if (v != FO_NONE && v >= l && v <= r) {", "if (v != FO_NONE && v >= l && v < r) {",
+     ["test_en_ident_hand_examples"]),
+    ("budget stops one early", "if (cnt == B) return cnt;", "if (cnt + 1 >= B) return cnt;",
+     ["test_en_ident_hand_examples"]),
+    ("stratum bound", "int64_t s = l + (j * cnt) / epn;", "int64_t s = l + (j * cnt) / (epn + 1);",
+     ["test_entry_points_stratified_distinct_in_range"]),
+    ("tie order reversed", "if (a->id < b->id) return -1;\n    if (a->id > b->id) return 1;\n    return 0;\n}\n\n/* A visited",
+     "if (a->id < b->id) return 1;\n    if (a->id > b->id) return -1;\n    return 0;\n}\n\n/* A visited",
+     ["test_exact_breaks_distance_ties_by_rank"]),
+    ("pool truncation", "np = np + nnew < L ? np + nnew : L;", "np = np + nnew < L ? np + nnew : L - 1;",
+     ["test_search_full_range_equals_textbook_greedy"]),
+    ("visited check skipped", "            if (fo_visited_insert(vis, v)) {\n                work[np + nnew].dist = fo_dist(q,",
+     "            if (fo_visited_insert(vis, v) || 1) {\n                work[np + nnew].dist = fo_dist(q,",
+     ["test_search_invariants_tiny_workload"]),
+    ("fusion weight", "double w = 1.0 - beta * (1.0 - pow(da, gamma));", "double w = 1.0 - beta * pow(da, gamma);",
+     ["test_fusion_special_values"]),
+    ("fusion attribute scale", "double da = (double)diff / (double)(seglen - 1);",
+     "double da = (double)diff / (double)seglen;", ["test_fusion_special_values"]),
+    ("leaf keeps farthest", "qsort(fu, (size_t)c, sizeof(fo_ranked), fo_ranked_cmp);\n                    qsort(ve",
+     "qsort(fu, (size_t)c, sizeof(fo_ranked), fo_ranked_cmp);\n                    for (int z = 0; z < c / 2; ++z) { fo_ranked tz = fu[z]; fu[z] = fu[c - 1 - z]; fu[c - 1 - z] = tz; }\n                    qsort(ve",
+     ["test_build_leaf_layer_is_exact_fusion_topm"]),
+]
+
+
+@pytest.mark.parametrize("name,old,new,tests", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(name, old, new, tests, tmp_path, monkeypatch):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation site not found: {name}"
+    mutated = src.replace(old, new, 1)
+    c_path = tmp_path / "mutant.c"
+    so_path = tmp_path / "libmutant.so"
+    c_path.write_text(mutated)
+    subprocess.check_call(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+                           "-w", "-o", str(so_path), str(c_path), "-lm"])
+    mutant = oracle.configure(C.CDLL(str(so_path)))
+    monkeypatch.setattr(oracle, "_lib", mutant)
+    for tname in tests:
+        fn = getattr(pins, tname)
+        kwargs = {}
+        if "tiny_index" in fn.__code__.co_varnames[:fn.__code__.co_argcount]:
+            import workloads
+            w = workloads.make("tiny", n=3000, nq=200)
+            kwargs["tiny_index"] = (w, oracle.build(w.X, w.attr))
+        argnames = fn.__code__.co_varnames[:fn.__code__.co_argcount]
+        if "n" in argnames and "H" in argnames:
+            kwargs.update(n=16, H=4)
+        with pytest.raises(AssertionError):
+            fn(**kwargs)

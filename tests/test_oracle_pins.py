@@ -269,6 +269,25 @@ def test_exact_matches_numpy_lexsort():
         assert (ids[i, len(o):] == -1).all()
 
 
+def test_exact_breaks_distance_ties_by_rank():
+    # integer-valued vectors: many exactly equal distances; order must be
+    # (distance, rank), as numpy lexsort gives
+    rng = np.random.default_rng(11)
+    n, d = 2000, 4
+    X = rng.integers(-2, 3, (n, d)).astype(np.float32)
+    attr = rng.permutation(n).astype(np.float64)
+    perm = np.argsort(attr, kind="stable").astype(np.int32)
+    Xr, srt = X[perm], attr[perm]
+    Q = rng.integers(-2, 3, (30, d)).astype(np.float32)
+    lo = np.zeros(30)
+    hi = np.full(30, n - 1.0)
+    ids, ds = oracle.exact(Xr, srt, None, Q, lo, hi, 25, rank_ids=True)
+    for i in range(30):
+        D = ((Xr.astype(np.float64) - Q[i].astype(np.float64)) ** 2).sum(1)
+        o = np.lexsort((np.arange(n), D))[:25]
+        assert ids[i].tolist() == o.tolist()
+
+
 def test_exact_empty_and_short_ranges():
     w = workloads.make("tiny", n=500, nq=4)
     perm = np.argsort(w.attr, kind="stable").astype(np.int32)
@@ -474,10 +493,11 @@ def test_search_full_range_equals_textbook_greedy(tiny_index):
         ep = oracle.entry_points(0, n - 1, 16, 0, i)
         qd = q.astype(np.float64)
         Xr = ix.X_rank.astype(np.float64)
+        # the whole pool (k = L), not only the top 10
         ref_ids, ref_d = _textbook_kann(lambda u: ix.ENC[u, 0, :B].tolist(),
                                         lambda v: np.float32(((Xr[v] - qd) ** 2).sum()),
-                                        ep.tolist(), 32, 10)
-        ids, ds, _ = oracle.search(ix, q[None], [-np.inf], [np.inf], 10, 32, B=B, qidx=[i], rank_ids=True)
+                                        ep.tolist(), 32, 32)
+        ids, ds, _ = oracle.search(ix, q[None], [-np.inf], [np.inf], 32, 32, B=B, qidx=[i], rank_ids=True)
         assert ids[0].tolist() == ref_ids
 
 
