@@ -45,6 +45,7 @@ SWEEP = [
     (32, 16, 1.0, 2816, 16), (40, 16, 1.0, 2816, 16), (48, 16, 1.0, 2816, 16), (32, 16, 1.0, 2816, 32),
     (32, 16, 1.0, 3072, 16), (64, 16, 1.0, 3072, 16),
     (32, 16, 1.0, 4096, 16), (64, 16, 1.0, 4096, 16),
+    (32, 16, 1.0, 2304, 32), (32, 16, 1.0, 2560, 32), (40, 16, 1.0, 2560, 32), (32, 16, 1.0, 2560, 24),
 ]
 
 
@@ -244,6 +245,24 @@ def main():
             kc = tf["kernels"][dominant]
             traffic = 1024.0 * (kc["fetch_kib"] * tf["fetch_factor"] + kc["write_kib"] * tf["write_factor"])
 
+    # per selectivity band: each octave of the mixed batch re-run as a batch of
+    # its own (smaller batches, so lower QPS than the mixed batch)
+    per_band = []
+    for b in range(10):
+        sel = np.nonzero(band == b)[0]
+        if len(sel) == 0:
+            continue
+        sel_t = torch.as_tensor(sel, device=dev)
+        Qb, lob, hib = Q[sel_t].contiguous(), lo[sel_t].contiguous(), hi[sel_t].contiguous()
+        fb = lambda: F.search(ix, Qb, lob, hib, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
+                              hash_log2=args.hash_log2, query_base=0)
+        idb, _ = fb()
+        torch.cuda.synchronize()
+        tb = timed(fb, 5)
+        per_band.append(dict(band=f"[2^-{b + 1}, 2^-{b}]", nq=int(len(sel)), qps=len(sel) / tb, ms=tb * 1e3,
+                             recall_in_mixed_batch=chosen["recall_band"][b]))
+    log("per band (own batch): " + ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M" for r in per_band))
+
     # CPU oracle on a bounded sample (same index arrays, same parameters)
     cpu = None
     try:
@@ -300,7 +319,7 @@ def main():
     }
     if args.details:
         with open(args.details, "w") as f:
-            json.dump(dict(result=result, sweep=rows, alg_bytes=alg_bytes, source_sha=sha,
+            json.dump(dict(result=result, sweep=rows, per_band=per_band, alg_bytes=alg_bytes, source_sha=sha,
                            eval_overhead=float(overhead),
                            mean_stats_exact=st_e.mean(0).tolist(),
                            mean_stats_timed=st_f.mean(0).tolist()), f, indent=1)

@@ -4,18 +4,21 @@
 //   1. Host: each query's rank interval [l, r] (Sec 4) from the index's host
 //      copy of the sorted attributes; queries are grouped into tiles of 16
 //      with the same octave of range size, ordered by l, so a tile's rows are
-//      the union of 16 overlapping intervals.
-//   2. Device, one workgroup (4 wavefronts) per tile: the dot products of the
-//      16 queries with 16-row blocks of X run on the fp32 matrix cores
-//      (v_mfma_f32_16x16x4_f32, K = 4 per instruction); the approximate
-//      squared distance |q|^2 + |x|^2 - 2 q.x masks rows outside each query's
-//      own interval.  Each wavefront keeps, per query, the K' = 64 smallest
-//      approximate distances it has seen (threshold test, then replace-max).
-//   3. Device, same workgroup: the up-to 4 K' candidates of each query are
-//      re-ranked with the exact canonical distance (double accumulation,
-//      rounded once to float), and the k smallest (distance, rank) kept.
-//      Every row a wavefront did not keep has an approximate distance at or
-//      above that wavefront's final threshold; if the smallest such threshold
+//      the union of 16 overlapping intervals.  Each tile's union is cut into
+//      row chunks; (tile, chunk) is a work item.
+//   2. bf_scan_kernel, one wavefront per work item: the dot products of the
+//      tile's 16 queries with 16-row blocks of X run on the fp32 matrix cores
+//      (v_mfma_f32_16x16x4_f32, K = 4 per instruction, query operand resident
+//      in VGPRs, the next block's rows loaded while the current one is
+//      multiplied); the approximate squared distance |q|^2 + |x|^2 - 2 q.x
+//      masks rows outside each query's own interval; per query the wavefront
+//      keeps the K' smallest approximate distances of its chunk (K' = 2k
+//      rounded up to 64, at most 256) and writes them out with its threshold.
+//   3. bf_merge_kernel, one wavefront per query: the K' smallest over the
+//      tile's chunks, re-ranked with the exact canonical distance (double
+//      accumulation, rounded once to float); the k smallest (distance, rank)
+//      are the result.  Every row not re-ranked has an approximate distance at
+//      or above some kept list's threshold; if the smallest such threshold
 //      minus the approximation bound exceeds the k-th exact distance, the
 //      result is certified exact (reported per query).
 //
@@ -25,7 +28,7 @@
 // that with |x|^2 replaced by the largest squared norm in the index.
 //
 // The host step reads the query ranges back, so this entry point synchronises
-// `stream` once; it is a ground-truth tool, not the search path.
+// `stream`; it is a ground-truth tool, not the search path.
 
 #include <hip/hip_runtime.h>
 
@@ -39,9 +42,8 @@
 namespace frog {
 namespace {
 
-constexpr int kQT = 16;       // queries per tile
-constexpr int kKeep = 64;     // approximate candidates kept per query per wavefront
-constexpr int kWaves = 4;
+constexpr int kQT = 16;       // queries per tile (one MFMA row block)
+constexpr int kWaves = 4;     // independent wavefronts per workgroup
 constexpr int kThreads = 64 * kWaves;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -51,7 +53,17 @@ struct Tile {
     int32_t l[kQT];
     int32_t r[kQT];
     int32_t ul, ur;   // union of the intervals
+    int32_t ib, ie;   // its work items
 };
+
+struct Item {
+    int32_t tile, rb, re;   // rows [rb, re] of the tile's union
+};
+
+__host__ __device__ constexpr size_t scan_lds_per_wave(int kkeep) {
+    return (size_t)kQT * kkeep * 8 + kQT * 4 + kQT * 16;
+}
+__host__ __device__ constexpr size_t merge_lds_per_wave(int kkeep) { return (size_t)kkeep * 8 + 16; }
 
 struct BFParams {
     const float* X;       // [n][dp]
@@ -60,8 +72,15 @@ struct BFParams {
     int d, dp;
     const float* Q;       // [nq][d]
     const Tile* tiles;
+    const Item* items;
+    int64_t ntiles, nitems;
+    int kkeep;            // approximate candidates kept per query and chunk
     int k;
     float maxnorm;        // largest |x|^2 in the index
+    float* pv;            // [nitems][16][kkeep] approximate distances
+    int32_t* pr;          // [nitems][16][kkeep] rows
+    float* pthr;          // [nitems][16] threshold of a full list, else +inf
+    int32_t* pfill;       // [nitems][16] entries kept
     int32_t* ids;
     float* dists;
     int32_t* cert;
@@ -69,8 +88,14 @@ struct BFParams {
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ float wave_max_pos(float v, int& pos) {
-    // max over the wavefront with the lowest lane among equals
+    // max over the wavefront with the lowest position among equals
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
         const float ov = __shfl_xor(v, o);
@@ -80,188 +105,312 @@ __device__ __forceinline__ float wave_max_pos(float v, int& pos) {
     return v;
 }
 
-__global__ __launch_bounds__(kThreads) void bf_tile_kernel(BFParams P) {
+// A list of at most `cap` (approximate distance, row) pairs in LDS (cap a
+// multiple of 64) and its state, also in LDS: the number of entries, and once
+// the list is full, the value and slot of its largest entry (the threshold a
+// new candidate has to beat).  Every row offered to the list and not kept has
+// a value at or above the final threshold.
+struct TopList {
+    float* v;
+    int32_t* r;
+    int32_t* st;   // [0] fill, [1] threshold (float bits), [2] slot of the largest
+};
+
+__device__ __forceinline__ float list_threshold(const int32_t* st) { return __int_as_float(st[1]); }
+
+// recompute the largest entry of a full list (all lanes)
+__device__ __forceinline__ void list_refresh(const TopList& Lst, int cap, float& thr, int& mpos) {
+    const int lane = lane_id();
+    float best = Lst.v[lane];
+    int pos = lane;
+    for (int j = 64 + lane; j < cap; j += 64)
+        if (Lst.v[j] > best) { best = Lst.v[j]; pos = j; }
+    best = wave_max_pos(best, pos);
+    thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(best)));
+    mpos = __builtin_amdgcn_readfirstlane(pos);
+}
+
+// Offer the candidates held by the lanes of `group_mask` (value a, row rw in
+// each such lane) to the list.  Returns true if a candidate was dropped or an
+// entry evicted.
+__device__ __noinline__ bool offer(TopList Lst, int cap, uint64_t group_mask, float a, int32_t rw) {
+    const int lane = lane_id();
+    int f = __builtin_amdgcn_readfirstlane(Lst.st[0]);
+    float thr = __int_as_float(__builtin_amdgcn_readfirstlane(Lst.st[1]));
+    int mpos = __builtin_amdgcn_readfirstlane(Lst.st[2]);
+    bool dropped = false;
+    const int c = __popcll(group_mask);
+    if (f + c <= cap) {
+        // room for all: append in parallel
+        if ((group_mask >> lane) & 1) {
+            const int pos = f + __popcll(group_mask & ((1ull << lane) - 1));
+            Lst.v[pos] = a;
+            Lst.r[pos] = rw;
+        }
+        f += c;
+        wave_sync();
+        if (f == cap) list_refresh(Lst, cap, thr, mpos);
+    } else {
+        for (uint64_t m = group_mask; m; m &= m - 1) {
+            const int src = __builtin_ctzll(m);
+            const float av = __shfl(a, src);
+            const int32_t rv = __shfl(rw, src);
+            if (f < cap) {
+                if (lane == 0) { Lst.v[f] = av; Lst.r[f] = rv; }
+                ++f;
+                wave_sync();
+                if (f == cap) list_refresh(Lst, cap, thr, mpos);
+                continue;
+            }
+            dropped = true;   // av itself, or the entry it evicts
+            if (!(av < thr)) continue;
+            if (lane == 0) { Lst.v[mpos] = av; Lst.r[mpos] = rv; }
+            wave_sync();
+            list_refresh(Lst, cap, thr, mpos);
+        }
+    }
+    if (lane == 0) {
+        Lst.st[0] = f;
+        Lst.st[1] = __float_as_int(thr);
+        Lst.st[2] = mpos;
+    }
+    wave_sync();
+    return dropped;
+}
+
+// Stage 2.  KT = dp/16 float4 chunks of the query operand kept in registers
+// (d <= 128); KT = 0 reloads the operand from global memory for each block.
+template <int KT>
+__global__ __launch_bounds__(kThreads) void bf_scan_kernel(BFParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    const Tile& T = P.tiles[blockIdx.x];
     const int lane = lane_id();
     const int wave = threadIdx.x >> 6;
-    const int dp = P.dp;
-    // LDS: queries [16][dp] floats, |q|^2 [16], per wave: lists [16][kKeep]
-    // (approx float, row int), thresholds [16], fill counts [16], max slot [16]
-    float* Qs = reinterpret_cast<float*>(smem);
-    float* qn = Qs + kQT * dp;
-    char* wb = reinterpret_cast<char*>(qn + kQT) + (size_t)wave * (kQT * kKeep * 8 + kQT * 12);
+    const int64_t item = (int64_t)blockIdx.x * kWaves + wave;
+    if (item >= P.nitems) return;   // no workgroup barrier follows
+    const Item it = P.items[item];
+    const Tile& T = P.tiles[it.tile];
+    const int dp = P.dp, dp4 = dp >> 2, d = P.d;
+    const int kkeep = P.kkeep;
+    // per-wave LDS: lists [16][kkeep] (value, row), |q|^2 [16], list state [16][4]
+    char* wb = smem + (size_t)wave * scan_lds_per_wave(kkeep);
     float* lv = reinterpret_cast<float*>(wb);
-    int32_t* lr = reinterpret_cast<int32_t*>(lv + kQT * kKeep);
-    float* thr = reinterpret_cast<float*>(lr + kQT * kKeep);
-    int32_t* fill = reinterpret_cast<int32_t*>(thr + kQT);
-    int32_t* mpos = fill + kQT;
-
-    for (int i = threadIdx.x; i < kQT * dp; i += kThreads) {
-        const int qi = i / dp, c = i % dp;
-        const int q = T.q[qi];
-        Qs[i] = (q >= 0 && c < P.d) ? P.Q[(int64_t)q * P.d + c] : 0.f;
-    }
-    if (lane < kQT) {
-        thr[lane] = __int_as_float(0x7f800000);
-        fill[lane] = 0;
-        mpos[lane] = 0;
-    }
-    __syncthreads();
-    if (threadIdx.x < kQT) {
-        float s = 0.f;
-        for (int c = 0; c < dp; ++c) s += Qs[threadIdx.x * dp + c] * Qs[threadIdx.x * dp + c];
-        qn[threadIdx.x] = s;
-    }
-    __syncthreads();
+    int32_t* lr = reinterpret_cast<int32_t*>(lv + kQT * kkeep);
+    float* qnl = reinterpret_cast<float*>(lr + kQT * kkeep);
+    int32_t* lst = reinterpret_cast<int32_t*>(qnl + kQT);
 
     // MFMA operand mapping (16x16x4 f32): A[i][kk] in lane i + 16 kk, B[kk][j]
     // in lane j + 16 kk, D[4 (lane/16) + e][lane % 16] in element e.  The K
     // loop walks float4 chunks: lane group kk takes dims 16t + 4kk + {0..3}.
-    const int ii = lane & 15;   // query (A) / row (B) index
+    const int ii = lane & 15;
     const int kk = lane >> 4;
-    const int nblk = (T.ur - T.ul + 16) / 16;
-    const int ql[4] = {T.l[4 * kk], T.l[4 * kk + 1], T.l[4 * kk + 2], T.l[4 * kk + 3]};
-    const int qr[4] = {T.r[4 * kk], T.r[4 * kk + 1], T.r[4 * kk + 2], T.r[4 * kk + 3]};
-    const bool qv[4] = {T.q[4 * kk] >= 0, T.q[4 * kk + 1] >= 0, T.q[4 * kk + 2] >= 0, T.q[4 * kk + 3] >= 0};
-    const float4* Qs4 = reinterpret_cast<const float4*>(Qs);
+    const int qrow = T.q[ii];
+    const float* Qr = P.Q + (int64_t)(qrow >= 0 ? qrow : 0) * d;
+    auto qchunk = [&](int t) -> float4 {
+        const int b = 16 * t + 4 * kk;
+        float4 v;
+        v.x = (qrow >= 0 && b < d) ? Qr[b] : 0.f;
+        v.y = (qrow >= 0 && b + 1 < d) ? Qr[b + 1] : 0.f;
+        v.z = (qrow >= 0 && b + 2 < d) ? Qr[b + 2] : 0.f;
+        v.w = (qrow >= 0 && b + 3 < d) ? Qr[b + 3] : 0.f;
+        return v;
+    };
+    float4 qa[KT > 0 ? KT : 1];
+    float qs = 0.f;
+    for (int t = 0; t < dp / 16; ++t) {
+        const float4 v = qchunk(t);
+        if constexpr (KT > 0) {
+#pragma unroll
+            for (int u = 0; u < KT; ++u)
+                if (u == t) qa[u] = v;
+        }
+        qs += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    qs += __shfl_xor(qs, 16);
+    qs += __shfl_xor(qs, 32);
+    if (kk == 0) {
+        qnl[ii] = qs;
+        lst[4 * ii + 0] = 0;
+        lst[4 * ii + 1] = 0x7f800000;
+        lst[4 * ii + 2] = 0;
+    }
+    wave_sync();
+    float qn[4];
+    int ql[4], qr[4];
+    bool qv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        qn[e] = qnl[4 * kk + e];
+        ql[e] = T.l[4 * kk + e];
+        qr[e] = T.r[4 * kk + e];
+        qv[e] = T.q[4 * kk + e] >= 0;
+    }
     const float4* X4 = reinterpret_cast<const float4*>(P.X);
-    const int dp4 = dp >> 2;
-    for (int blk = wave; blk < nblk; blk += kWaves) {
-        const int row = T.ul + blk * 16 + ii;
-        const int rowc = row <= T.ur ? row : T.ur;
+    const int nblk = (it.re - it.rb + 16) / 16;
+    float4 xa[KT > 0 ? KT : 1], xb[KT > 0 ? KT : 1];
+    auto load_block = [&](int blk, float4 (&x)[KT > 0 ? KT : 1]) {
+        if constexpr (KT > 0) {
+            const int row = it.rb + blk * 16 + ii;
+            const int rowc = row <= it.re ? row : it.re;
+#pragma unroll
+            for (int t = 0; t < KT; ++t) x[t] = X4[(int64_t)rowc * dp4 + 4 * t + kk];
+        }
+    };
+    load_block(0, xa);
+    for (int blk = 0; blk < nblk; ++blk) {
+        const int row = it.rb + blk * 16 + ii;
+        const int rowc = row <= it.re ? row : it.re;
+        if (blk + 1 < nblk) load_block(blk + 1, xb);
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
         float xn = 0.f;
-        for (int t = 0; t < dp / 16; ++t) {
-            const float4 x = X4[(int64_t)rowc * dp4 + 4 * t + kk];
-            const float4 q = Qs4[ii * dp4 + 4 * t + kk];
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.x, x.x, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, x.y, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.z, x.z, acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, x.w, acc, 0, 0, 0);
-            xn += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+        if constexpr (KT > 0) {
+#pragma unroll
+            for (int t = 0; t < KT; ++t) {
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].x, xa[t].x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].y, xa[t].y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].z, xa[t].z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].w, xa[t].w, acc, 0, 0, 0);
+                xn += xa[t].x * xa[t].x + xa[t].y * xa[t].y + xa[t].z * xa[t].z + xa[t].w * xa[t].w;
+            }
+#pragma unroll
+            for (int t = 0; t < KT; ++t) xa[t] = xb[t];
+        } else {
+            for (int t = 0; t < dp / 16; ++t) {
+                const float4 x = X4[(int64_t)rowc * dp4 + 4 * t + kk];
+                const float4 q = qchunk(t);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.x, x.x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, x.y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.z, x.z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, x.w, acc, 0, 0, 0);
+                xn += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+            }
         }
         xn += __shfl_xor(xn, 16);
         xn += __shfl_xor(xn, 32);
-        // lane holds D[4kk + e][ii]: query 4kk + e, row ul + blk*16 + ii
-        float ap[4];
-        bool cand[4];
+        // lane holds D[4kk + e][ii]: query 4kk + e, row rb + blk*16 + ii
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int qi = 4 * kk + e;
-            ap[e] = qn[qi] + xn - 2.f * acc[e];
-            cand[e] = qv[e] && row <= T.ur && row >= ql[e] && row <= qr[e] && ap[e] < thr[qi];
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            uint64_t m = __ballot(cand[e]);
+            const float ap = qn[e] + xn - 2.f * acc[e];
+            const bool cand = qv[e] && row <= it.re && row >= ql[e] && row <= qr[e] &&
+                              ap < list_threshold(lst + 4 * (4 * kk + e));
+            uint64_t m = __ballot(cand);
             while (m) {
-                const int src = __builtin_ctzll(m);
-                m &= m - 1;
-                const int qi = 4 * (src >> 4) + e;
-                const float a = __shfl(ap[e], src);
-                const int rw = T.ul + blk * 16 + (src & 15);
-                if (!(a < thr[qi])) continue;
-                const int f = fill[qi];
-                int slot;
-                if (f < kKeep) {
-                    slot = f;
-                } else {
-                    slot = mpos[qi];
-                }
-                if (lane == 0) {
-                    lv[qi * kKeep + slot] = a;
-                    lr[qi * kKeep + slot] = rw;
-                    if (f < kKeep) fill[qi] = f + 1;
-                }
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-                if (f + 1 >= kKeep) {
-                    // list full: the threshold is its largest entry
-                    float v = lv[qi * kKeep + lane];
-                    int pos = lane;
-                    v = wave_max_pos(v, pos);
-                    if (lane == 0) {
-                        thr[qi] = v;
-                        mpos[qi] = pos;
-                    }
-                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                    __builtin_amdgcn_wave_barrier();
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-                }
+                const int g = __builtin_ctzll(m) >> 4;
+                const uint64_t gm = m & (0xFFFFull << (16 * g));
+                m &= ~gm;
+                const int qi = 4 * g + e;
+                offer(TopList{lv + qi * kkeep, lr + qi * kkeep, lst + 4 * qi}, kkeep, gm, ap, rowc);
             }
         }
     }
-    __syncthreads();
+    // write the chunk's lists
+    const int64_t base = item * kQT;
+    for (int i = 0; i < kQT; ++i) {
+        const int fi = lst[4 * i];
+        for (int j = lane; j < kkeep; j += 64) {
+            P.pv[(base + i) * kkeep + j] = j < fi ? lv[i * kkeep + j] : __int_as_float(0x7f800000);
+            P.pr[(base + i) * kkeep + j] = j < fi ? lr[i * kkeep + j] : -1;
+        }
+        if (lane == 0) {
+            P.pthr[base + i] = fi >= kkeep ? list_threshold(lst + 4 * i) : __int_as_float(0x7f800000);
+            P.pfill[base + i] = fi;
+        }
+    }
+}
 
-    // exact re-rank: wavefront w finalises queries w, w + 4, w + 8, w + 12
-    const int lists_stride = kQT * kKeep * 8 + kQT * 12;
-    for (int qi = wave; qi < kQT; qi += kWaves) {
-        const int q = T.q[qi];
-        if (q < 0) continue;
-        uint64_t key[kWaves];
-        float tmin = __int_as_float(0x7f800000);
-        int total = 0;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-            char* b = reinterpret_cast<char*>(qn + kQT) + (size_t)w * lists_stride;
-            const float* wlv = reinterpret_cast<const float*>(b);
-            const int32_t* wlr = reinterpret_cast<const int32_t*>(wlv + kQT * kKeep);
-            const float* wthr = reinterpret_cast<const float*>(wlr + kQT * kKeep);
-            const int32_t* wfill = reinterpret_cast<const int32_t*>(wthr + kQT);
-            const int f = wfill[qi];
-            total += f;
-            if (f >= kKeep) tmin = fminf(tmin, wthr[qi]);
-            key[w] = ~0ull;
-            if (lane < f) {
-                const int rw = wlr[qi * kKeep + lane];
-                const float* xr = P.X + (int64_t)rw * dp;
-                const float* qq = Qs + qi * dp;
-                double s = 0.0;
-                for (int c = 0; c < P.d; ++c) {
-                    const double t = (double)qq[c] - (double)xr[c];
-                    s += t * t;
-                }
-                key[w] = ((uint64_t)__float_as_uint((float)s) << 32) | (uint32_t)rw;
-            }
+// Stage 3: one wavefront per (tile, query slot).
+__global__ __launch_bounds__(kThreads) void bf_merge_kernel(BFParams P) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    const int64_t gw = (int64_t)blockIdx.x * kWaves + wave;
+    if (gw >= P.ntiles * kQT) return;
+    const Tile& T = P.tiles[gw / kQT];
+    const int qi = (int)(gw % kQT);
+    const int q = T.q[qi];
+    if (q < 0) return;
+    const int kkeep = P.kkeep, d = P.d, dp = P.dp;
+    char* wb = smem + (size_t)wave * merge_lds_per_wave(kkeep);
+    const TopList Lst{reinterpret_cast<float*>(wb), reinterpret_cast<int32_t*>(wb) + kkeep,
+                      reinterpret_cast<int32_t*>(wb) + 2 * kkeep};
+    if (lane == 0) {
+        Lst.st[0] = 0;
+        Lst.st[1] = 0x7f800000;
+        Lst.st[2] = 0;
+    }
+    wave_sync();
+    float texcl = __int_as_float(0x7f800000);   // every row not kept is at or above this
+    bool dropped = false;
+    for (int item = T.ib; item < T.ie; ++item) {
+        const int64_t base = (int64_t)item * kQT + qi;
+        texcl = fminf(texcl, P.pthr[base]);
+        const int fi = P.pfill[base];
+        for (int j0 = 0; j0 < fi; j0 += 64) {
+            const int j = j0 + lane;
+            const bool have = j < fi;
+            const float a = have ? P.pv[base * kkeep + j] : 0.f;
+            const int32_t rw = have ? P.pr[base * kkeep + j] : -1;
+            const int f = Lst.st[0];
+            const uint64_t gm = __ballot(have && (f < kkeep || a < list_threshold(Lst.st)));
+            const uint64_t all = __ballot(have);
+            if (gm != all) dropped = true;   // candidates at or above a full list's threshold
+            if (gm) dropped |= offer(Lst, kkeep, gm, a, rw);
         }
-        // k smallest keys by repeated wave minimum
-        float kth = __int_as_float(0x7f800000);
-        int found = 0;
-        for (int j = 0; j < P.k; ++j) {
-            uint64_t best = key[0];
+    }
+    if (dropped) texcl = fminf(texcl, list_threshold(Lst.st));
+    const int f = Lst.st[0];
+    // exact re-rank
+    const float* Qq = P.Q + (int64_t)q * d;
+    uint64_t key[4];
 #pragma unroll
-            for (int w = 1; w < kWaves; ++w) best = key[w] < best ? key[w] : best;
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) {
-                const uint64_t other = __shfl_xor(best, o);
-                best = other < best ? other : best;
+    for (int j = 0; j < 4; ++j) {
+        key[j] = ~0ull;
+        const int slot = lane + 64 * j;
+        if (slot < kkeep && slot < f) {
+            const int rw = Lst.r[slot];
+            const float* xr = P.X + (int64_t)rw * dp;
+            double sacc = 0.0;
+            for (int c = 0; c < d; ++c) {
+                const double t = (double)Qq[c] - (double)xr[c];
+                sacc += t * t;
             }
-            int32_t oid = -1;
-            float od = __int_as_float(0x7f800000);
-            if (best != ~0ull) {
-                oid = P.perm[(uint32_t)best];
-                od = __uint_as_float((uint32_t)(best >> 32));
-                kth = od;
-                found = j + 1;
-#pragma unroll
-                for (int w = 0; w < kWaves; ++w)
-                    if (key[w] == best) key[w] = ~0ull;
-            }
-            if (lane == 0) {
-                P.ids[(int64_t)q * P.k + j] = oid;
-                P.dists[(int64_t)q * P.k + j] = od;
-            }
+            key[j] = ((uint64_t)__float_as_uint((float)sacc) << 32) | (uint32_t)rw;
         }
-        if (P.cert && lane == 0) {
-            const double eps = 2.0 * (2.0 * P.d + 4.0) * 5.9604644775390625e-08 * ((double)qn[qi] + (double)P.maxnorm);
-            bool ok;
-            if (isinf(tmin)) ok = true;                       // no wavefront dropped a row
-            else ok = found == P.k && (double)tmin - eps > (double)kth;
-            P.cert[q] = ok ? 1 : 0;
+    }
+    float kth = __int_as_float(0x7f800000);
+    int found = 0;
+    for (int j = 0; j < P.k; ++j) {
+        uint64_t best = key[0];
+#pragma unroll
+        for (int u = 1; u < 4; ++u) best = key[u] < best ? key[u] : best;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const uint64_t other = __shfl_xor(best, o);
+            best = other < best ? other : best;
         }
-        (void)total;
+        int32_t oid = -1;
+        float od = __int_as_float(0x7f800000);
+        if (best != ~0ull) {
+            oid = P.perm[(uint32_t)best];
+            od = __uint_as_float((uint32_t)(best >> 32));
+            kth = od;
+            found = j + 1;
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (key[u] == best) key[u] = ~0ull;
+        }
+        if (lane == 0) {
+            P.ids[(int64_t)q * P.k + j] = oid;
+            P.dists[(int64_t)q * P.k + j] = od;
+        }
+    }
+    if (P.cert && lane == 0) {
+        double qn = 0.0;
+        for (int c = 0; c < d; ++c) qn += (double)Qq[c] * Qq[c];
+        const double eps = 2.0 * (2.0 * d + 4.0) * 5.9604644775390625e-08 * (qn + (double)P.maxnorm);
+        bool ok;
+        if (isinf(texcl)) ok = true;                       // no row was dropped
+        else ok = found == P.k && (double)texcl - eps > (double)kth;
+        P.cert[q] = ok ? 1 : 0;
     }
 }
 
@@ -308,6 +457,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         return x < y;
     });
     std::vector<Tile> tiles;
+    int64_t total_rows = 0;
     for (size_t i = 0; i < order.size();) {
         Tile t;
         const int b = band(order[i]);
@@ -324,7 +474,20 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
             ++c;
         }
         for (; c < kQT; ++c) { t.q[c] = -1; t.l[c] = 0; t.r[c] = -1; }
+        total_rows += (int64_t)t.ur - t.ul + 1;
         tiles.push_back(t);
+    }
+    // work items: about 8192 row chunks in all (a multiple of 16 rows each)
+    int64_t chunk = total_rows / 8192 + 1;
+    chunk = std::max<int64_t>(1024, std::min<int64_t>(1 << 18, (chunk + 15) / 16 * 16));
+    std::vector<Item> items;
+    for (size_t t = 0; t < tiles.size(); ++t) {
+        tiles[t].ib = (int32_t)items.size();
+        for (int64_t rb = tiles[t].ul; rb <= tiles[t].ur; rb += chunk) {
+            const int64_t re = std::min<int64_t>(tiles[t].ur, rb + chunk - 1);
+            items.push_back(Item{(int32_t)t, (int32_t)rb, (int32_t)re});
+        }
+        tiles[t].ie = (int32_t)items.size();
     }
     if (ix->maxnorm < 0.f) {
         double mx = 0.0;
@@ -335,15 +498,31 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         }
         const_cast<frog_index*>(ix)->maxnorm = (float)(mx * (1.0 + 1e-6));
     }
-    const size_t tbytes = tiles.size() * sizeof(Tile);
+    int kkeep = 2 * k < 64 ? 64 : (2 * k + 63) / 64 * 64;
+    if (kkeep > 256) kkeep = 256;
+    auto align = [](size_t x) { return (x + 255) / 256 * 256; };
+    const size_t tbytes = align(tiles.size() * sizeof(Tile));
+    const size_t ibytes = align(items.size() * sizeof(Item));
+    const size_t ebytes = align((size_t)nq);
+    const size_t lbytes = align(items.size() * kQT * (size_t)kkeep * 4);
+    const size_t sbytes = align(items.size() * kQT * 4);
+    const size_t ws_bytes = tbytes + ibytes + ebytes + 2 * lbytes + 2 * sbytes + 256;
     void* ws = nullptr;
-    e = hipMallocAsync(&ws, tbytes + (size_t)nq + 64, stream);
+    e = hipMallocAsync(&ws, ws_bytes, stream);
     if (e != hipSuccess) return fail(FROG_ENOMEM, "bruteforce workspace: %s", hipGetErrorString(e));
-    Tile* dT = reinterpret_cast<Tile*>(ws);
-    uint8_t* dE = reinterpret_cast<uint8_t*>(ws) + tbytes;
-    if (tbytes) e = hipMemcpyAsync(dT, tiles.data(), tbytes, hipMemcpyHostToDevice, stream);
+    char* base = reinterpret_cast<char*>(ws);
+    Tile* dT = reinterpret_cast<Tile*>(base);
+    Item* dI = reinterpret_cast<Item*>(base + tbytes);
+    uint8_t* dE = reinterpret_cast<uint8_t*>(base + tbytes + ibytes);
+    char* lists = base + tbytes + ibytes + ebytes;
+    if (!tiles.empty()) e = hipMemcpyAsync(dT, tiles.data(), tiles.size() * sizeof(Tile), hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess && !items.empty())
+        e = hipMemcpyAsync(dI, items.data(), items.size() * sizeof(Item), hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(dE, empty.data(), (size_t)nq, hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) { hipFreeAsync(ws, stream); return fail(FROG_EHIP, "bruteforce upload: %s", hipGetErrorString(e)); }
+    if (e != hipSuccess) {
+        (void)hipFreeAsync(ws, stream);
+        return fail(FROG_EHIP, "bruteforce upload: %s", hipGetErrorString(e));
+    }
     hipLaunchKernelGGL(bf_pad_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, nq, k, dE, ids, dists, cert);
     if (!tiles.empty()) {
         BFParams P{};
@@ -354,20 +533,40 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         P.dp = ix->dp;
         P.Q = Q;
         P.tiles = dT;
+        P.items = dI;
+        P.ntiles = (int64_t)tiles.size();
+        P.nitems = (int64_t)items.size();
+        P.kkeep = kkeep;
         P.k = k;
         P.maxnorm = ix->maxnorm;
+        P.pv = reinterpret_cast<float*>(lists);
+        P.pr = reinterpret_cast<int32_t*>(lists + lbytes);
+        P.pthr = reinterpret_cast<float*>(lists + 2 * lbytes);
+        P.pfill = reinterpret_cast<int32_t*>(lists + 2 * lbytes + sbytes);
         P.ids = ids;
         P.dists = dists;
         P.cert = cert;
-        const int smem = kQT * ix->dp * 4 + kQT * 4 + kWaves * (kQT * kKeep * 8 + kQT * 12);
-        if (smem > 160 * 1024) { hipFreeAsync(ws, stream); return fail(FROG_EUNSUPPORTED, "bruteforce: d too large"); }
-        if (smem > 64 * 1024) hipFuncSetAttribute((const void*)bf_tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
-        hipLaunchKernelGGL(bf_tile_kernel, dim3((unsigned)tiles.size()), dim3(kThreads), smem, stream, P);
+        const int smem_scan = (int)(kWaves * scan_lds_per_wave(kkeep));
+        void (*scan)(BFParams) = bf_scan_kernel<0>;
+        switch (ix->dp) {
+            case 32: scan = bf_scan_kernel<2>; break;
+            case 64: scan = bf_scan_kernel<4>; break;
+            case 96: scan = bf_scan_kernel<6>; break;
+            case 128: scan = bf_scan_kernel<8>; break;
+            default: break;
+        }
+        if (smem_scan > 64 * 1024)
+            (void)hipFuncSetAttribute((const void*)scan, hipFuncAttributeMaxDynamicSharedMemorySize, smem_scan);
+        hipLaunchKernelGGL(scan, dim3((unsigned)((items.size() + kWaves - 1) / kWaves)), dim3(kThreads), smem_scan,
+                           stream, P);
+        const int smem_merge = (int)(kWaves * merge_lds_per_wave(kkeep));
+        hipLaunchKernelGGL(bf_merge_kernel, dim3((unsigned)((tiles.size() * kQT + kWaves - 1) / kWaves)), dim3(kThreads),
+                           smem_merge, stream, P);
     }
     e = hipGetLastError();
-    hipFreeAsync(ws, stream);
-    // keep the host-side tile array alive until the copy has run
-    hipStreamSynchronize(stream);
+    (void)hipFreeAsync(ws, stream);
+    // keep the host-side arrays alive until the copies have run
+    (void)hipStreamSynchronize(stream);
     if (e != hipSuccess) return fail(FROG_EHIP, "bruteforce launch: %s", hipGetErrorString(e));
     return FROG_OK;
 }
