@@ -12,7 +12,8 @@ Functions and the passages of the paper they follow:
 * :func:`rank_bounds`    attribute range -> rank interval (Sec 4)
 * :func:`num_layers`, :func:`segment`   segment-tree geometry (Sec 4, Alg 3)
 * :func:`hotspot`        HotspotLocalization (Alg 3, Eq. endcondition)
-* :func:`entry_points`   entry-point sampling (Alg 2)
+* :func:`entry_points`   entry-point sampling (Alg 2), stratified per query
+* :func:`entry_points_shared`  the same with a rank priority shared by all queries
 * :func:`en_ident`       ENIdentification (Alg 4)
 * :func:`search`         FROGSearch (Alg 2) with an exact visited set
 * :func:`exact`          exhaustive filtered k-NN (Def. 2)
@@ -90,7 +91,13 @@ def configure(lib):
     lib.fo_en_ident.argtypes = [P, i32, i32, i64, i64, i64, i32, i32, i32, P, P]
     lib.fo_search_batch.restype = i32
     lib.fo_search_batch.argtypes = [P, P, P, P, i64, i32, i32, i32, P, P, P, i64, P,
-                                    i32, i32, i32, f64, i32, i32, u64, P, P, P, i32]
+                                    i32, i32, i32, f64, i32, i32, u64, i32, P, P, P, i32]
+    lib.fo_entry_priority.restype = C.c_uint32
+    lib.fo_entry_priority.argtypes = [u64, i64]
+    lib.fo_entry_threshold.restype = u64
+    lib.fo_entry_threshold.argtypes = [i64, i64]
+    lib.fo_entry_points_shared.restype = i64
+    lib.fo_entry_points_shared.argtypes = [i64, i64, i64, u64, P]
     lib.fo_exact_batch.restype = i32
     lib.fo_exact_batch.argtypes = [P, P, P, i64, i32, P, P, P, i64, i32, P, P, i32]
     lib.fo_fusion.restype = f64
@@ -163,6 +170,23 @@ def entry_points(l: int, r: int, epn: int, seed: int, qi: int) -> np.ndarray:
     cnt = max(0, r - l + 1)
     out = np.empty(max(1, min(cnt, epn)), dtype=np.int32)
     k = _load().fo_entry_points(l, r, epn, seed, qi, _p(out))
+    return out[:k].copy()
+
+
+def entry_priority(seed: int, i: int) -> int:
+    return int(_load().fo_entry_priority(C.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), i))
+
+
+def entry_threshold(cnt: int, E: int) -> int:
+    return int(_load().fo_entry_threshold(cnt, E))
+
+
+def entry_points_shared(l: int, r: int, E: int, seed: int) -> np.ndarray:
+    """Ranks i of [l, r] whose shared priority is below the threshold for E
+    expected entry points."""
+    cnt = max(0, r - l + 1)
+    out = np.empty(max(1, cnt), dtype=np.int32)
+    k = _load().fo_entry_points_shared(l, r, E, C.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), _p(out))
     return out[:k].copy()
 
 
@@ -245,11 +269,13 @@ def entry_count(cnt: int, epn: int, epn_frac: float = 0.0, epn_max: int = 0) -> 
 
 
 def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, epn_frac: float = 0.0,
-           epn_max: int = 0, B: int = 16, seed: int = 0, qidx=None, threads=None,
+           epn_max: int = 0, B: int = 16, seed: int = 0, entry_mode: int = 0, qidx=None, threads=None,
            rank_ids: bool = False):
     """FROGSearch for every query.  Returns (ids int32 [nq,k] original ids or
     ranks, dists float32 [nq,k], stats int64 [nq,8]).  The entry-point count
-    is epn, or clamp(ceil(epn_frac * cnt), epn, epn_max) when epn_frac > 0."""
+    is epn, or clamp(ceil(epn_frac * cnt), epn, epn_max) when epn_frac > 0;
+    entry_mode 0 draws them stratified per query, 1 from the shared-priority
+    sample (that count is then the expected size)."""
     Q = _c(Q, np.float32)
     lo = _c(lo, np.float64)
     hi = _c(hi, np.float64)
@@ -263,7 +289,7 @@ def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, epn_fra
     rc = _load().fo_search_batch(
         _p(ix.X_rank), _p(ENC), _p(ix.attr_sorted), None if rank_ids else _p(ix.perm),
         ix.n, ix.d, ix.H, ix.m, _p(Q), _p(lo), _p(hi), nq,
-        None if qi is None else _p(qi), k, L, epn, epn_frac, epn_max, B, seed, _p(ids), _p(ds), _p(st),
+        None if qi is None else _p(qi), k, L, epn, epn_frac, epn_max, B, seed, entry_mode, _p(ids), _p(ds), _p(st),
         threads or default_threads())
     if rc:
         raise MemoryError("oracle search: allocation failed")

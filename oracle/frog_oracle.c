@@ -18,6 +18,8 @@
  *   fo_hotspot         HotspotLocalization (Alg. 3, Rules 1-2, Eq. endcondition)
  *   fo_entry_points    entry-point sampling (Alg. 2, uniform sampling from the
  *                      range; deterministic stratified reading)
+ *   fo_entry_points_shared  the same sampling with a per-rank random priority
+ *                      shared by all queries (second reading, below)
  *   fo_en_ident        ENIdentification (Alg. 4): scan hotspot layers in stored
  *                      order, keep in-range candidates, stop at budget B
  *   fo_search_batch    FROGSearch (Alg. 2) with an exact visited set
@@ -42,6 +44,15 @@
  *     per stratum j of [l,r] split into equal strata, at offset
  *     (hi32(splitmix64(seed ^ (query_index << 32) ^ j)) * width) >> 32 inside
  *     the stratum (Lemire's multiply-shift range reduction);
+ *   - second entry-point reading (entry_mode 1): every rank i carries the
+ *     priority p(i) = hi32(splitmix64(splitmix64(seed) ^ i)) (the seed is
+ *     mixed first so that different seeds give unrelated samples); a query whose range holds
+ *     cnt ranks and asks for E entry points takes every i in [l,r] with
+ *     p(i) < T, T = min(2^32, ceil(E * 2^32 / cnt)), in rank order.  Each
+ *     rank of the range is included with probability E/cnt independently of
+ *     the others (a uniform random sample of expected size E, all of [l,r]
+ *     when cnt <= E); the sample depends on (seed, rank) only, so queries over
+ *     overlapping ranges draw from the same random subset;
  *   - duplicates inside EN(u) count against B; the visited set drops them;
  *   - the loop ends when no unexpanded entry is left in the pool;
  *   - empty ranges and fewer than k results pad with (id -1, +inf);
@@ -189,6 +200,30 @@ int64_t fo_entry_points(int64_t l, int64_t r, int64_t epn, uint64_t seed, uint64
     return epn;
 }
 
+/* Second reading of the sampling: the rank's shared priority, the threshold
+ * for E expected entry points out of cnt, and the sample itself. */
+uint32_t fo_entry_priority(uint64_t seed, int64_t i) {
+    return (uint32_t)(fo_splitmix64(fo_splitmix64(seed) ^ (uint64_t)i) >> 32);
+}
+
+uint64_t fo_entry_threshold(int64_t cnt, int64_t E) {
+    const uint64_t full = (uint64_t)1 << 32;
+    if (cnt <= E) return full;
+    /* ceil(E * 2^32 / cnt); E < cnt < 2^31, so E * 2^32 < 2^63 */
+    uint64_t t = (((uint64_t)E << 32) + (uint64_t)cnt - 1) / (uint64_t)cnt;
+    return t < full ? t : full;
+}
+
+int64_t fo_entry_points_shared(int64_t l, int64_t r, int64_t E, uint64_t seed, int32_t* out) {
+    int64_t cnt = r - l + 1;
+    if (cnt <= 0) return 0;
+    uint64_t T = fo_entry_threshold(cnt, E);
+    int64_t c = 0;
+    for (int64_t i = l; i <= r; ++i)
+        if ((uint64_t)fo_entry_priority(seed, i) < T) out[c++] = (int32_t)i;
+    return c;
+}
+
 /* ENIdentification: layers L_start..L_end of u's ENC block in stored order,
  * keep v != -1 with l <= v <= r, stop once B are kept.  Adds to *scanned the
  * entries of every layer touched (a layer is one chunk when m <= 64). */
@@ -268,7 +303,7 @@ typedef struct {
 
 static void fo_search_one(const fo_index* ix, const float* q, double lo, double hi,
                           int k, int L, int epn, double epn_frac, int epn_max, int B,
-                          uint64_t seed, uint64_t qi,
+                          uint64_t seed, int entry_mode, uint64_t qi,
                           int32_t* out_ids, float* out_d, int64_t* st,
                           fo_visited* vis, fo_cand* pool, fo_cand* work,
                           int32_t* ep, int32_t* EN) {
@@ -284,8 +319,9 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
     st[FO_ST_LE] = Le;
 
     /* entry points, their distances, pool = the L nearest of them */
-    int64_t ne = fo_entry_points(l, r, fo_entry_count(r - l + 1, epn, epn_frac, epn_max),
-                                 seed, qi, ep);
+    int64_t E = fo_entry_count(r - l + 1, epn, epn_frac, epn_max);
+    int64_t ne = entry_mode == 1 ? fo_entry_points_shared(l, r, E, seed, ep)
+                                 : fo_entry_points(l, r, E, seed, qi, ep);
     st[FO_ST_ENTRY] = ne;
     fo_visited_clear(vis);
     int64_t nw = 0;
@@ -340,21 +376,24 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
 }
 
 /* Batch driver.  qidx (may be NULL) gives each query's index in its batch,
- * which keys its entry-point jitter; NULL means 0..nq-1.  Returns 0 or -1 on
- * allocation failure.  stats (may be NULL) is [nq][8] int64. */
+ * which keys its entry-point jitter (entry_mode 0); NULL means 0..nq-1.
+ * entry_mode 0: stratified per-query sample; 1: shared-priority sample.
+ * Returns 0 or -1 on allocation failure.  stats (may be NULL) is [nq][8]
+ * int64. */
 int fo_search_batch(const float* X, const int32_t* ENC, const double* attr_sorted,
                     const int32_t* perm, int64_t n, int d, int H, int m,
                     const float* Q, const double* lo, const double* hi, int64_t nq,
                     const int64_t* qidx, int k, int L, int epn, double epn_frac, int epn_max,
-                    int B, uint64_t seed, int32_t* out_ids, float* out_d, int64_t* stats,
-                    int nthreads) {
+                    int B, uint64_t seed, int entry_mode, int32_t* out_ids, float* out_d,
+                    int64_t* stats, int nthreads) {
     fo_index ix = { X, ENC, attr_sorted, perm, n, d, H, m };
     int fail = 0;
     if (nthreads <= 0) nthreads = 1;
 #pragma omp parallel num_threads(nthreads) reduction(|:fail)
     {
         fo_visited vis;
-        int64_t ep_cap = fo_entry_count(n, epn, epn_frac, epn_max);
+        /* the shared-priority sample has no fixed size: room for a whole range */
+        int64_t ep_cap = entry_mode == 1 ? n : fo_entry_count(n, epn, epn_frac, epn_max);
         if (ep_cap < 1) ep_cap = 1;
         fo_cand* pool = (fo_cand*)malloc(sizeof(fo_cand) * (size_t)(L + 1));
         fo_cand* work = (fo_cand*)malloc(sizeof(fo_cand) * (size_t)(L + B + ep_cap + 1));
@@ -367,7 +406,7 @@ int fo_search_batch(const float* X, const int32_t* ENC, const double* attr_sorte
             for (int64_t i = 0; i < nq; ++i) {
                 int64_t st_local[FO_ST_N];
                 fo_search_one(&ix, Q + i * d, lo[i], hi[i], k, L, epn, epn_frac, epn_max, B, seed,
-                              (uint64_t)(qidx ? qidx[i] : i),
+                              entry_mode, (uint64_t)(qidx ? qidx[i] : i),
                               out_ids + i * k, out_d + i * k,
                               stats ? stats + i * FO_ST_N : st_local,
                               &vis, pool, work, ep, EN);

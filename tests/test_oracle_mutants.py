@@ -31,6 +31,14 @@ MUTANTS = [
      ["test_en_ident_hand_examples"]),
     ("stratum bound", "int64_t s = l + (j * cnt) / epn;", "int64_t s = l + (j * cnt) / (epn + 1);",
      ["test_entry_points_stratified_distinct_in_range"]),
+    ("shared threshold rounds down", "uint64_t t = (((uint64_t)E << 32) + (uint64_t)cnt - 1) / (uint64_t)cnt;",
+     "uint64_t t = ((uint64_t)E << 32) / (uint64_t)cnt;", ["test_entry_threshold_closed_form"]),
+    ("shared sample keeps the threshold", "if ((uint64_t)fo_entry_priority(seed, i) < T) out[c++]",
+     "if ((uint64_t)fo_entry_priority(seed, i) <= T + 20000000) out[c++]", ["test_entry_points_shared_membership"]),
+    ("shared priority low word", "return (uint32_t)(fo_splitmix64(fo_splitmix64(seed) ^ (uint64_t)i) >> 32);",
+     "return (uint32_t)fo_splitmix64(fo_splitmix64(seed) ^ (uint64_t)i);", ["test_entry_priority_is_splitmix_high_word"]),
+    ("shared priority seed unmixed", "return (uint32_t)(fo_splitmix64(fo_splitmix64(seed) ^ (uint64_t)i) >> 32);",
+     "return (uint32_t)(fo_splitmix64(seed ^ (uint64_t)i) >> 32);", ["test_entry_points_shared_size_nesting_and_sharing"]),
     ("tie order reversed", "if (a->id < b->id) return -1;\n    if (a->id > b->id) return 1;\n    return 0;\n}\n\n/* A visited",
      "if (a->id < b->id) return 1;\n    if (a->id > b->id) return -1;\n    return 0;\n}\n\n/* A visited",
      ["test_exact_breaks_distance_ties_by_rank"]),

@@ -209,6 +209,64 @@ def test_entry_points_roughly_uniform():
 
 # ------------------------------------------------------------------ P6 EN(u)
 
+# second sampling reading: a rank priority shared by all queries
+
+def _shared_sample_python(l, r, E, seed):
+    """The sample written out with Python integers: priorities from the
+    (pinned) SplitMix64, threshold ceil(E * 2^32 / cnt) in exact arithmetic."""
+    cnt = r - l + 1
+    T = 1 << 32 if cnt <= E else min(1 << 32, -((-E << 32) // cnt))
+    key = oracle.splitmix64(seed)
+    return [i for i in range(l, r + 1) if (oracle.splitmix64(key ^ i) >> 32) < T]
+
+
+def test_entry_threshold_closed_form():
+    for cnt, E in [(1, 16), (16, 16), (17, 16), (1000, 3), (999_999, 2560), (1_000_000, 2560),
+                   (3, 2), (2 ** 31 - 1, 2 ** 30), (123_457, 1)]:
+        want = 1 << 32 if cnt <= E else min(1 << 32, -((-E << 32) // cnt))
+        assert oracle.entry_threshold(cnt, E) == want, (cnt, E)
+
+
+def test_entry_priority_is_splitmix_high_word():
+    for seed in (0, 1, 0xDEADBEEF, 2 ** 63 + 5):
+        for i in (0, 1, 2, 999_999, 2 ** 31 - 1):
+            assert oracle.entry_priority(seed, i) == oracle.splitmix64(oracle.splitmix64(seed) ^ i) >> 32
+
+
+def test_entry_points_shared_membership():
+    for (l, r, E, seed) in [(0, 9, 16, 0), (5, 5, 16, 3), (100, 5099, 64, 0), (0, 99_999, 2560, 0),
+                            (31_000, 95_000, 700, 7), (10, 400, 390, 1)]:
+        got = oracle.entry_points_shared(l, r, E, seed).tolist()
+        assert got == _shared_sample_python(l, r, E, seed), (l, r, E, seed)
+        if r - l + 1 <= E:
+            assert got == list(range(l, r + 1))
+
+
+def test_entry_points_shared_size_nesting_and_sharing():
+    # each rank is included with probability E/cnt, independently: the size is
+    # binomial around E and the positions are uniform over the range
+    l, r, E = 1000, 200_999, 2560
+    sizes, hist = [], np.zeros(10)
+    for seed in range(40):
+        s = oracle.entry_points_shared(l, r, E, seed)
+        sizes.append(len(s))
+        hist += np.histogram(s, bins=10, range=(l, r + 1))[0]
+    p = E / (r - l + 1)
+    sd = np.sqrt(E * (1 - p) / len(sizes))
+    assert abs(np.mean(sizes) - E) < 4 * sd
+    exp_bin = hist.sum() / 10
+    assert (np.abs(hist - exp_bin) < 5 * np.sqrt(exp_bin)).all()
+    # a larger E keeps every rank of a smaller one (thresholds are nested)
+    a = set(oracle.entry_points_shared(l, r, 500, 3).tolist())
+    b = set(oracle.entry_points_shared(l, r, 2000, 3).tolist())
+    assert a <= b and len(b) > len(a)
+    # two ranges with the same density agree on their overlap
+    x = oracle.entry_points_shared(0, 99_999, 1000, 5)
+    y = oracle.entry_points_shared(50_000, 149_999, 1000, 5)
+    ov = lambda z: z[(z >= 50_000) & (z <= 99_999)].tolist()
+    assert ov(x) == ov(y)
+
+
 def _hand_index():
     # n=12, H=3, m=4; rows handwritten, -1 tails, duplicates across layers
     n, H, m = 12, 3, 4
@@ -533,3 +591,58 @@ def test_search_degenerate_queries(tiny_index):
     assert (ids[2] == -1).all()
     assert sorted(ids[3, :3].tolist()) == [0, 1, 2] and (ids[3, 3:] == -1).all()
     assert ids[4, 0] == 2999 and (ids[4, 1:] == -1).all()
+
+
+def test_search_shared_entries_without_edges_is_entry_topk(tiny_index):
+    # an index without edges: the result is the k nearest of the entry sample,
+    # which is rebuilt here from its definition
+    w, ix = tiny_index
+    bare = oracle.OracleIndex(ix.perm, ix.attr_sorted, ix.X_rank, np.full_like(ix.ENC, -1))
+    rng = np.random.default_rng(11)
+    for i in range(16):
+        l = int(rng.integers(0, ix.n - 200))
+        r = int(rng.integers(l, min(ix.n, l + 2500)))
+        E = 150
+        sample = np.array(_shared_sample_python(l, r, E, 9), np.int64)
+        q = w.Q[i]
+        ids, ds, st = oracle.search(bare, q[None], [float(l)], [float(r)], 10, 32, epn=16, epn_frac=1.0,
+                                    epn_max=E, seed=9, entry_mode=1, rank_ids=True)
+        D = ((ix.X_rank[sample].astype(np.float64) - q.astype(np.float64)) ** 2).sum(1).astype(np.float32)
+        o = np.lexsort((sample, D))[:10]
+        assert ids[0, :len(o)].tolist() == sample[o].tolist()
+        assert ds[0, :len(o)].tolist() == D[o].tolist()
+        assert st[0, oracle.STAT_ENTRY] == len(sample) == st[0, oracle.STAT_DIST]
+        assert st[0, oracle.STAT_EXPANSIONS] == min(32, len(sample))
+
+
+def test_search_shared_full_range_equals_textbook_greedy(tiny_index):
+    # P8c with the shared sample as the entry set (entry points are visited)
+    w, ix = tiny_index
+    n = ix.n
+    B = 12
+    for i in range(8):
+        q = w.Q[i]
+        ep = _shared_sample_python(0, n - 1, 40, i)
+        qd = q.astype(np.float64)
+        Xr = ix.X_rank.astype(np.float64)
+        ref_ids, ref_d = _textbook_kann(lambda u: ix.ENC[u, 0, :B].tolist(),
+                                        lambda v: np.float32(((Xr[v] - qd) ** 2).sum()),
+                                        ep, 32, 32)
+        ids, ds, st = oracle.search(ix, q[None], [-np.inf], [np.inf], 32, 32, B=B, epn=16, epn_frac=1.0,
+                                    epn_max=40, seed=i, entry_mode=1, rank_ids=True)
+        assert ids[0].tolist() == ref_ids
+        assert st[0, oracle.STAT_ENTRY] == len(ep)
+
+
+def test_search_shared_small_range_is_exact(tiny_index):
+    # cnt <= E: the shared sample is the whole range, so the result is exact
+    w, ix = tiny_index
+    rng = np.random.default_rng(12)
+    nq = 40
+    start = rng.integers(0, ix.n - 60, nq)
+    cnt = rng.integers(1, 60, nq)
+    lo = start.astype(np.float64)
+    hi = (start + cnt - 1).astype(np.float64)
+    ids, ds, _ = oracle.search(ix, w.Q[:nq], lo, hi, 10, 32, epn=64, entry_mode=1, rank_ids=True)
+    gi, gd = oracle.exact(ix.X_rank, ix.attr_sorted, None, w.Q[:nq], lo, hi, 10, rank_ids=True)
+    assert (ids == gi).all() and (ds == gd).all()
