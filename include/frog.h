@@ -74,8 +74,18 @@ typedef struct {
                            0 selects an exact visited set in device memory (slow;
                            used to count distinct evaluations) */
     void** phase_events;/* NULL, or 3 caller-created hipEvent_t recorded on `stream`
-                           before the entry-point kernel, between it and the
-                           traversal kernel, and after the traversal kernel */
+                           before the search kernels, between the entry-point
+                           kernels and the traversal kernel (entry_mode 1; the
+                           same as the third otherwise), and after the last */
+    int entry_mode;     /* how the entry points of Alg. 2 are drawn uniformly from
+                           the range: 0 (default) one per stratum, jittered per
+                           query; 1 every rank whose priority, a hash of (seed,
+                           rank) shared by all queries, is below count/cnt of
+                           its range: a sample of expected size count that
+                           overlapping queries share, evaluated on matrix
+                           cores in tiles of 16 queries.  Mode 1 builds and
+                           uploads the seed's rank lists on its first call
+                           (synchronously; about n int32 of device memory) */
 } frog_search_params_t;
 
 /* Per-query statistics written by frog_search_ex (int32, FROG_STAT_N per query). */

@@ -38,9 +38,12 @@
 #include <vector>
 
 #include "frog_internal.h"
+#include "wave_topk.h"
 
 namespace frog {
 namespace {
+
+using namespace topk;
 
 constexpr int kQT = 16;       // queries per tile (one MFMA row block)
 constexpr int kWaves = 4;     // independent wavefronts per workgroup
@@ -92,90 +95,6 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ float wave_max_pos(float v, int& pos) {
-    // max over the wavefront with the lowest position among equals
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const float ov = __shfl_xor(v, o);
-        const int op = __shfl_xor(pos, o);
-        if (ov > v || (ov == v && op < pos)) { v = ov; pos = op; }
-    }
-    return v;
-}
-
-// A list of at most `cap` (approximate distance, row) pairs in LDS (cap a
-// multiple of 64) and its state, also in LDS: the number of entries, and once
-// the list is full, the value and slot of its largest entry (the threshold a
-// new candidate has to beat).  Every row offered to the list and not kept has
-// a value at or above the final threshold.
-struct TopList {
-    float* v;
-    int32_t* r;
-    int32_t* st;   // [0] fill, [1] threshold (float bits), [2] slot of the largest
-};
-
-__device__ __forceinline__ float list_threshold(const int32_t* st) { return __int_as_float(st[1]); }
-
-// recompute the largest entry of a full list (all lanes)
-__device__ __forceinline__ void list_refresh(const TopList& Lst, int cap, float& thr, int& mpos) {
-    const int lane = lane_id();
-    float best = Lst.v[lane];
-    int pos = lane;
-    for (int j = 64 + lane; j < cap; j += 64)
-        if (Lst.v[j] > best) { best = Lst.v[j]; pos = j; }
-    best = wave_max_pos(best, pos);
-    thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(best)));
-    mpos = __builtin_amdgcn_readfirstlane(pos);
-}
-
-// Offer the candidates held by the lanes of `group_mask` (value a, row rw in
-// each such lane) to the list.  Returns true if a candidate was dropped or an
-// entry evicted.
-__device__ __noinline__ bool offer(TopList Lst, int cap, uint64_t group_mask, float a, int32_t rw) {
-    const int lane = lane_id();
-    int f = __builtin_amdgcn_readfirstlane(Lst.st[0]);
-    float thr = __int_as_float(__builtin_amdgcn_readfirstlane(Lst.st[1]));
-    int mpos = __builtin_amdgcn_readfirstlane(Lst.st[2]);
-    bool dropped = false;
-    const int c = __popcll(group_mask);
-    if (f + c <= cap) {
-        // room for all: append in parallel
-        if ((group_mask >> lane) & 1) {
-            const int pos = f + __popcll(group_mask & ((1ull << lane) - 1));
-            Lst.v[pos] = a;
-            Lst.r[pos] = rw;
-        }
-        f += c;
-        wave_sync();
-        if (f == cap) list_refresh(Lst, cap, thr, mpos);
-    } else {
-        for (uint64_t m = group_mask; m; m &= m - 1) {
-            const int src = __builtin_ctzll(m);
-            const float av = __shfl(a, src);
-            const int32_t rv = __shfl(rw, src);
-            if (f < cap) {
-                if (lane == 0) { Lst.v[f] = av; Lst.r[f] = rv; }
-                ++f;
-                wave_sync();
-                if (f == cap) list_refresh(Lst, cap, thr, mpos);
-                continue;
-            }
-            dropped = true;   // av itself, or the entry it evicts
-            if (!(av < thr)) continue;
-            if (lane == 0) { Lst.v[mpos] = av; Lst.r[mpos] = rv; }
-            wave_sync();
-            list_refresh(Lst, cap, thr, mpos);
-        }
-    }
-    if (lane == 0) {
-        Lst.st[0] = f;
-        Lst.st[1] = __float_as_int(thr);
-        Lst.st[2] = mpos;
-    }
-    wave_sync();
-    return dropped;
 }
 
 // Stage 2.  KT = dp/16 float4 chunks of the query operand kept in registers
@@ -489,15 +408,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         }
         tiles[t].ie = (int32_t)items.size();
     }
-    if (ix->maxnorm < 0.f) {
-        double mx = 0.0;
-        for (int64_t i = 0; i < n; ++i) {
-            double s = 0.0;
-            for (int c = 0; c < ix->d; ++c) s += (double)ix->X[(size_t)(i * ix->d + c)] * ix->X[(size_t)(i * ix->d + c)];
-            mx = std::max(mx, s);
-        }
-        const_cast<frog_index*>(ix)->maxnorm = (float)(mx * (1.0 + 1e-6));
-    }
+    const float maxnorm = index_maxnorm(const_cast<frog_index*>(ix));
     int kkeep = 2 * k < 64 ? 64 : (2 * k + 63) / 64 * 64;
     if (kkeep > 256) kkeep = 256;
     auto align = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -538,7 +449,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         P.nitems = (int64_t)items.size();
         P.kkeep = kkeep;
         P.k = k;
-        P.maxnorm = ix->maxnorm;
+        P.maxnorm = maxnorm;
         P.pv = reinterpret_cast<float*>(lists);
         P.pr = reinterpret_cast<int32_t*>(lists + lbytes);
         P.pthr = reinterpret_cast<float*>(lists + 2 * lbytes);

@@ -52,8 +52,11 @@ void release_device(frog_index* ix) {
         hipFree(ix->dENC);
         hipFree(ix->dattr);
         hipFree(ix->dperm);
+        if (ix->dshared) hipFree(ix->dshared);
         hipSetDevice(prev);
     }
+    ix->dshared = nullptr;
+    ix->shared_valid = false;
     ix->dX = nullptr;
     ix->dENC = nullptr;
     ix->dattr = nullptr;
@@ -147,6 +150,7 @@ void frog_search_params_default(frog_search_params_t* p) {
     p->query_base = 0;
     p->hash_log2 = 10;
     p->phase_events = nullptr;
+    p->entry_mode = 0;
 }
 
 int frog_build_index(const float* X, const double* attr, int64_t n, int d,
@@ -397,6 +401,7 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
     if (q.hash_log2 != 0 && (q.hash_log2 < 6 || q.hash_log2 > 13))
         return fail(FROG_EINVAL, "hash_log2=%d: 0 or 6..13", q.hash_log2);
     if (q.query_base < 0) return fail(FROG_EINVAL, "query_base < 0");
+    if (q.entry_mode != 0 && q.entry_mode != 1) return fail(FROG_EINVAL, "entry_mode=%d: 0 or 1", q.entry_mode);
     if (!frog::search_shape_supported(ix->dp, ix->m, L))
         return fail(FROG_EUNSUPPORTED, "no search kernel for padded d=%d, m=%d, L=%d", ix->dp, ix->m, L);
     if (nq == 0) return FROG_OK;
@@ -406,6 +411,13 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
     a.epn = q.epn; a.epn_max = q.epn_frac > 0.0 ? q.epn_max : q.epn; a.epn_frac = q.epn_frac;
     a.B = q.budget; a.hash_log2 = q.hash_log2; a.seed = q.seed; a.qbase = q.query_base;
     a.ids = d_ids; a.dists = d_dists; a.stats = d_stats; a.events = q.phase_events;
+    a.entry_mode = q.entry_mode;
+    if (q.entry_mode == 1) {
+        frog_index* mix = const_cast<frog_index*>(ix);
+        a.maxnorm = frog::index_maxnorm(mix);
+        rc = frog::shared_levels(mix, q.seed, &a.lv);
+        if (rc) return rc;
+    }
     return frog::launch_search(view(ix), a, stream);
 }
 
@@ -428,3 +440,82 @@ int frog_bruteforce_filtered(const frog_index_t* ix, const float* d_queries, int
 }
 
 }  // extern "C"
+
+namespace frog {
+
+static uint64_t mix64(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ULL;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+    return z ^ (z >> 31);
+}
+
+float index_maxnorm(frog_index* ix) {
+    std::lock_guard<std::mutex> g(ix->shared_mu);
+    if (ix->maxnorm < 0.f) {
+        double mx = 0.0;
+        for (int64_t i = 0; i < ix->n; ++i) {
+            const float* x = ix->X.data() + (size_t)i * ix->d;
+            double s = 0.0;
+            for (int c = 0; c < ix->d; ++c) s += (double)x[c] * x[c];
+            mx = std::max(mx, s);
+        }
+        ix->maxnorm = (float)(mx * (1.0 + 1e-6));
+    }
+    return ix->maxnorm;
+}
+
+// Level j (1 <= j <= nlev) holds the ranks whose priority p has at least j
+// leading zero bits (p < 2^(32-j)); nlev covers the smallest threshold any
+// query can ask for (one entry point out of n).
+int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
+    std::lock_guard<std::mutex> g(ix->shared_mu);
+    const uint64_t key = mix64(seed);
+    if (!ix->shared_valid || ix->shared_seed != seed) {
+        const int64_t n = ix->n;
+        const uint64_t tmin = ((uint64_t)1 << 32) / (uint64_t)n + 1;   // >= ceil(2^32 / n)
+        int cl = 0;
+        while (((uint64_t)1 << cl) < tmin) ++cl;
+        const int nlev = std::max(1, std::min(31, 32 - cl + 1));
+        std::vector<uint8_t> depth((size_t)n);
+        std::vector<int64_t> cnt((size_t)nlev + 2, 0);
+        for (int64_t i = 0; i < n; ++i) {
+            const uint32_t p = (uint32_t)(mix64(key ^ (uint64_t)i) >> 32);
+            const int z = p == 0 ? 32 : __builtin_clz(p);
+            depth[(size_t)i] = (uint8_t)std::min(z, nlev);
+            for (int j = 1; j <= depth[(size_t)i]; ++j) ++cnt[(size_t)j];
+        }
+        int64_t off[34] = {};
+        off[1] = 0;
+        for (int j = 1; j <= nlev; ++j) off[j + 1] = off[j] + cnt[(size_t)j];
+        std::vector<int32_t> ranks((size_t)std::max<int64_t>(off[nlev + 1], 1));
+        std::vector<int64_t> fill(off, off + nlev + 2);
+        for (int64_t i = 0; i < n; ++i)
+            for (int j = 1; j <= depth[(size_t)i]; ++j) ranks[(size_t)fill[(size_t)j]++] = (int32_t)i;
+        int prev = 0;
+        if (hipGetDevice(&prev) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
+        if (hipSetDevice(ix->device) != hipSuccess) return fail(FROG_EHIP, "hipSetDevice failed");
+        if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
+        ix->shared_valid = false;
+        hipError_t e = hipMalloc(&ix->dshared, ranks.size() * sizeof(int32_t));
+        if (e == hipSuccess)
+            e = hipMemcpy(ix->dshared, ranks.data(), ranks.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+        (void)hipSetDevice(prev);
+        if (e != hipSuccess) {
+            if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
+            return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "shared sample levels: %s",
+                        hipGetErrorString(e));
+        }
+        std::copy(off, off + 34, ix->shared_off);
+        ix->shared_nlev = nlev;
+        ix->shared_seed = seed;
+        ix->shared_valid = true;
+    }
+    out->ranks = ix->dshared;
+    std::copy(ix->shared_off, ix->shared_off + 34, out->off);
+    out->nlev = ix->shared_nlev;
+    out->key = key;
+    return FROG_OK;
+}
+
+}  // namespace frog

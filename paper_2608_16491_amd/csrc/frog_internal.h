@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cstdint>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -24,6 +25,15 @@ struct frog_index {
     double* dattr = nullptr;
     int32_t* dperm = nullptr;
     float maxnorm = -1.f;        // largest squared row norm, computed on first use
+    // shared entry sample (entry_mode 1): for one seed, the ascending rank
+    // lists of levels 1..nlev (level j: ranks whose priority is below
+    // 2^(32-j)), concatenated on the device; built on first use
+    std::mutex shared_mu;
+    bool shared_valid = false;
+    uint64_t shared_seed = 0;
+    int shared_nlev = 0;
+    int64_t shared_off[34] = {};
+    int32_t* dshared = nullptr;
 };
 
 namespace frog {
@@ -47,6 +57,15 @@ struct DevIndex {
     int d, dp, H, m;
 };
 
+// Levels of the shared entry sample, as the kernels see them: level j's list
+// is ranks[off[j], off[j + 1]) for 1 <= j <= nlev; level 0 is every rank.
+struct SharedLevels {
+    const int32_t* ranks;
+    int64_t off[34];
+    int nlev;
+    uint64_t key;      // splitmix64(seed): priority(i) = hi32(splitmix64(key ^ i))
+};
+
 struct SearchLaunch {
     const float* Q;
     int64_t nq;
@@ -60,7 +79,15 @@ struct SearchLaunch {
     float* dists;
     int32_t* stats;
     void** events;   // NULL or 3 hipEvent_t
+    int entry_mode;  // 0 stratified per query, 1 shared sample
+    SharedLevels lv; // entry_mode 1
+    float maxnorm;   // entry_mode 1: largest squared row norm of the index
 };
+
+// capi.cpp: the shared sample's levels for `seed` on the index's device
+// (built and uploaded on first use), and the largest squared row norm
+int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out);
+float index_maxnorm(frog_index* ix);
 
 // search.hip
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream);

@@ -43,6 +43,7 @@
 #include <map>
 
 #include "frog_internal.h"
+#include "wave_topk.h"
 
 namespace frog {
 namespace {
@@ -51,6 +52,7 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr uint64_t kEmpty = ~0ull;
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
 // Register budget: at least 3 wavefronts per SIMD (168 VGPRs); four would
 // make the d = 128 kernel spill, which costs more than the lost wave.
 #ifndef FROG_WAVES_PER_EU
@@ -486,6 +488,11 @@ struct QueryCtx {
     double rE;
     bool all;
     uint64_t qkey;
+    // shared entry sample: rank i of [l, r] is an entry point iff
+    // hi32(splitmix64(pkey ^ i)) < T
+    bool shared = false;
+    uint32_t T = 0;
+    uint64_t pkey = 0;
 
     __device__ void load(const DevIndex& ix, const SearchLaunch& A, const int32_t* lr, int64_t q) {
         qi = q;
@@ -526,6 +533,12 @@ struct QueryCtx {
         const uint64_t z = splitmix64(A.seed ^ qkey ^ (uint64_t)j);
         return (int32_t)(s0 + (int64_t)(((z >> 32) * (uint64_t)(t0 - s0 + 1)) >> 32));
     }
+    // whether an in-range rank is one of the query's entry points (then it is
+    // in the visited set from the start)
+    __device__ __forceinline__ bool is_entry(int32_t v) const {
+        if (all) return true;
+        return shared && (uint32_t)(splitmix64(pkey ^ (uint64_t)(uint32_t)v) >> 32) < T;
+    }
     __device__ float eval(const DevIndex& ix, int nb, int32_t myid) const {
         if constexpr (C > 0) return eval_small<C>(ix.X, ix.dp, qv, nb, myid);
         else return eval_large(ix.X, ix.dp, qrow, ix.d, nb, myid);
@@ -558,10 +571,8 @@ __device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const Que
 // a2, a4-a11 for one query whose pool holds the L nearest entry points:
 // HotspotLocalization, the best-first loop of Alg. 2, output and statistics.
 template <int C, int LP>
-__device__ void traverse(const KParams& P, const QueryCtx<C>& Q, Pool<LP>& pool, const WaveLds<LP>& W,
-                         const Visited& vis) {
-    const DevIndex& ix = P.ix;
-    const SearchLaunch& A = P.a;
+__device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis_words, const QueryCtx<C>& Q,
+                         Pool<LP>& pool, const WaveLds<LP>& W, const Visited& vis) {
     const int lane = lane_id();
     const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
     const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
@@ -591,9 +602,11 @@ __device__ void traverse(const KParams& P, const QueryCtx<C>& Q, Pool<LP>& pool,
         for (int s = 0; s < LP; ++s)
             if (s * 64 + lane < pool.np) vis.insert((int32_t)(uint32_t)pool.key[s]);
     } else {
-        for (int64_t i = lane; i < P.gvis_words; i += 64) vis.bits[i] = 0u;
+        for (int64_t i = lane; i < gvis_words; i += 64) vis.bits[i] = 0u;
         __threadfence_block();
-        for (int64_t j = lane; j < Q.ne; j += 64) vis.insert(Q.entry_id(A, j));
+        // entry points the membership test cannot tell
+        if (!Q.shared && !Q.all)
+            for (int64_t j = lane; j < Q.ne; j += 64) vis.insert(Q.entry_id(A, j));
         __threadfence_block();
     }
     wave_sync();
@@ -679,7 +692,7 @@ __device__ void traverse(const KParams& P, const QueryCtx<C>& Q, Pool<LP>& pool,
         // a7: lazy visited check on the compacted list
         int32_t v = lane < nen ? enbuf[lane] : -1;
         bool fresh = false;
-        if (lane < nen) fresh = vis.check_insert(v);
+        if (lane < nen) fresh = !Q.is_entry(v) && vis.check_insert(v);
         const uint64_t fm = ballot(fresh);
         const int ns = __popcll(fm);
         wave_sync();
@@ -871,7 +884,7 @@ void coop_kernel(KParams P) {
                 }
             }
         }
-        traverse<C, LP>(P, Q, pool, W, vis);
+        traverse<C, LP>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
     }
 }
 
@@ -890,6 +903,551 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i == 0) *counter = 0u;
     if (i < nq) done[i] = 0u;
+}
+
+// ================================================================== shared entry sample
+//
+// Second reading of the entry-point sampling (entry_mode 1).  Rank i carries
+// the priority p(i) = hi32(splitmix64(key ^ i)), key = splitmix64(seed); a
+// query asking for E entry points out of cnt ranks takes the ranks of [l, r]
+// with p(i) < T, T = ceil(E 2^32 / cnt) (every rank when cnt <= E).  Level
+// j >= 1 lists, in rank order, the ranks with p < 2^(32-j); level 0 is every
+// rank.  A query's sample lies in the coarsest level whose bound is at least
+// T, where it is the run of the list between l and r, filtered by T.
+//
+// The sample depends on (seed, rank) only, so queries over overlapping ranges
+// at the same level draw from the same rows, and their entry distances form
+// a dense product (16 queries x a run of rows) for the fp32 matrix cores in
+// place of per-query gathers:
+//   s_plan_kernel     per query: threshold, level, run in the level's list,
+//                     and a bucket (level, position of l) for grouping
+//   s_offsets_kernel  bucket offsets (one workgroup)
+//   s_order_kernel    the queries in bucket order
+//   s_tile_kernel     tiles of 16 consecutive queries: the union of their
+//                     runs in the finest level among them
+//   s_scan_kernel     one wavefront per (tile, eighth of the union): 16 x 16
+//                     blocks of q.x on the matrix cores, the approximate
+//                     squared distance |q|^2 + |x|^2 - 2 q.x of each query's
+//                     sample rows, the kkeep smallest per query kept in LDS
+//   s_search_kernel   one wavefront per query (persistent grid): the kkeep
+//                     smallest of its tile's lists, re-ranked with the exact
+//                     canonical distance into the pool (the L nearest entry
+//                     points); a margin test proves that no row left out
+//                     could enter the pool, else the whole sample is
+//                     evaluated exactly; then the traversal, where the
+//                     sample's ranks count as visited by their priority.
+// Bucket order inside a bucket follows atomic arrival, so tiles differ from
+// run to run; results do not, since every pool is the exact L nearest of the
+// sample.
+
+constexpr int kSQ = 16;        // queries per tile
+constexpr int kSChunks = 8;    // work items per tile
+constexpr int kSBins = 256;    // buckets of l per level
+
+struct SPlan {
+    int32_t l, r;
+    uint32_t T;      // threshold
+    int32_t all;     // every rank of the range is an entry point
+    int32_t lev;     // level whose list holds the sample
+    int32_t a, b;    // run [a, b) of [l, r] in that list
+    int32_t bin, pos;
+    int32_t tslot;   // tile * 16 + slot (-1: empty range)
+    int32_t pad[2];
+};
+
+struct STile {
+    int32_t q[kSQ];
+    int32_t l[kSQ];
+    int32_t r[kSQ];
+    uint32_t T[kSQ];
+    uint32_t allmask;
+    int32_t lev;      // finest level among the tile's queries
+    int32_t ua, ub;   // run of the union of their intervals in that level's list
+    int32_t nq;       // 0: unused tile
+    int32_t pad[3];
+};
+
+struct SParams {
+    DevIndex ix;
+    SearchLaunch a;
+    const int32_t* lr;
+    SPlan* plan;
+    uint32_t* hist;     // [nbins] queries per bucket
+    uint32_t* bstart;   // [nbins] first place of each bucket
+    uint32_t* meta;     // [0] places used in `order`, [1] tiles, [2] query counter
+    int32_t* order;     // [nq + 16 (nlev + 1)] queries by bucket, each level's run
+                        // padded to a multiple of 16 with -1 (no tile spans two levels)
+    STile* tiles;       // [tmax]
+    int64_t tmax;
+    int nbins;
+    int kkeep;
+    float* pv;          // [tmax * kSChunks][16][kkeep] approximate distances
+    int32_t* pr;        // [tmax * kSChunks][16][kkeep] ranks
+    float* pthr;        // [tmax * kSChunks][16] threshold of a full list, else +inf
+    int32_t* pfill;     // [tmax * kSChunks][16] entries kept
+    int32_t* pcnt;      // [tmax * kSChunks][16] sample rows seen
+    uint32_t* gvis;
+    int64_t gvis_words;
+    int lds_per_wave;   // s_search_kernel, bytes
+    int lds_list;       // offset of the re-rank list inside a wave's LDS
+};
+
+__device__ __forceinline__ int32_t level_rank(const SharedLevels& lv, int j, int64_t pos) {
+    return j == 0 ? (int32_t)pos : lv.ranks[lv.off[j] + pos];
+}
+
+// first position of level j's list whose rank is >= x
+__device__ int64_t level_lower(const SharedLevels& lv, int64_t n, int j, int64_t x) {
+    if (j == 0) return x < 0 ? 0 : (x > n ? n : x);
+    const int32_t* a = lv.ranks + lv.off[j];
+    int64_t lo = 0, hi = lv.off[j + 1] - lv.off[j];
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (a[mid] < x) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint32_t s_priority(uint64_t key, int32_t i) {
+    return (uint32_t)(splitmix64(key ^ (uint64_t)(uint32_t)i) >> 32);
+}
+
+__global__ void s_init_kernel(uint32_t* meta, uint32_t* hist, int nbins, int32_t* order, int64_t norder) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < 4) meta[i] = 0u;
+    if (i < nbins) hist[i] = 0u;
+    if (i < norder) order[i] = -1;
+}
+
+__global__ void s_plan_kernel(SParams P) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= P.a.nq) return;
+    const SharedLevels& lv = P.a.lv;
+    const int64_t n = P.ix.n;
+    SPlan p{};
+    p.l = P.lr[2 * q];
+    p.r = P.lr[2 * q + 1];
+    p.tslot = -1;
+    if (p.l > p.r) {
+        p.bin = P.nbins - 1;
+    } else {
+        const int64_t cnt = (int64_t)p.r - p.l + 1;
+        int64_t E = P.a.epn;
+        if (P.a.epn_frac > 0.0) {
+            double want = ceil(P.a.epn_frac * (double)cnt);
+            if (want > (double)P.a.epn_max) want = (double)P.a.epn_max;
+            if (want > (double)E) E = (int64_t)want;
+        }
+        if (cnt <= E) {
+            p.all = 1;
+            p.T = 0xFFFFFFFFu;
+            p.lev = 0;
+        } else {
+            // ceil(E 2^32 / cnt) < 2^32 since E < cnt < 2^31
+            const uint64_t t = (((uint64_t)E << 32) + (uint64_t)cnt - 1) / (uint64_t)cnt;
+            p.T = (uint32_t)t;
+            const int cl = t <= 1 ? 0 : 64 - __builtin_clzll(t - 1);   // ceil(log2 t)
+            p.lev = 32 - cl < lv.nlev ? 32 - cl : lv.nlev;
+        }
+        p.a = (int32_t)level_lower(lv, n, p.lev, p.l);
+        p.b = (int32_t)level_lower(lv, n, p.lev, (int64_t)p.r + 1);
+        p.bin = p.lev * kSBins + (int)(((int64_t)p.l * kSBins) / n);
+    }
+    p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
+    P.plan[q] = p;
+}
+
+// Bucket offsets: level by level, each level's run of places padded to a
+// multiple of 16; inside a level, buckets in order of l.  The empty ranges'
+// bucket comes last.  One thread per level.
+__global__ __launch_bounds__(64) void s_offsets_kernel(SParams P) {
+    __shared__ uint32_t start[34];
+    const int j = threadIdx.x;
+    const int nlev = P.a.lv.nlev;
+    uint32_t tot = 0;
+    if (j <= nlev)
+        for (int b = 0; b < kSBins; ++b) tot += P.hist[j * kSBins + b];
+    if (j <= nlev) start[j + 1] = (tot + kSQ - 1) / kSQ * kSQ;
+    __syncthreads();
+    if (j == 0) {
+        start[0] = 0;
+        for (int i = 1; i <= nlev + 1; ++i) start[i] += start[i - 1];
+        P.bstart[P.nbins - 1] = start[nlev + 1];
+        P.meta[0] = start[nlev + 1];
+        P.meta[1] = start[nlev + 1] / kSQ;
+    }
+    __syncthreads();
+    if (j <= nlev) {
+        uint32_t run = start[j];
+        for (int b = 0; b < kSBins; ++b) {
+            P.bstart[j * kSBins + b] = run;
+            run += P.hist[j * kSBins + b];
+        }
+    }
+}
+
+__global__ void s_order_kernel(SParams P) {
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= P.a.nq) return;
+    const SPlan& p = P.plan[q];
+    P.order[P.bstart[p.bin] + p.pos] = (int32_t)q;
+}
+
+__global__ void s_tile_kernel(SParams P) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= P.tmax) return;
+    const int64_t places = P.meta[0];
+    STile T{};
+    T.nq = 0;
+    int lev = 64;
+    int32_t ul = 0x7FFFFFFF, ur = -1;
+    for (int s = 0; s < kSQ; ++s) {
+        const int64_t i = t * kSQ + s;
+        T.q[s] = -1;
+        T.l[s] = 0;
+        T.r[s] = -1;
+        T.T[s] = 0u;
+        if (i >= places) continue;
+        const int32_t q = P.order[i];
+        if (q < 0) continue;
+        SPlan& p = P.plan[q];
+        T.q[s] = q;
+        T.l[s] = p.l;
+        T.r[s] = p.r;
+        T.T[s] = p.T;
+        if (p.all) T.allmask |= 1u << s;
+        lev = p.lev < lev ? p.lev : lev;
+        ul = p.l < ul ? p.l : ul;
+        ur = p.r > ur ? p.r : ur;
+        p.tslot = (int32_t)(t * kSQ + s);
+        ++T.nq;
+    }
+    if (T.nq > 0) {
+        T.lev = lev;
+        T.ua = (int32_t)level_lower(P.a.lv, P.ix.n, lev, ul);
+        T.ub = (int32_t)level_lower(P.a.lv, P.ix.n, lev, (int64_t)ur + 1);
+    }
+    P.tiles[t] = T;
+}
+
+// per wave: 16 buffers of 2 kkeep keys, |q|^2 of the 16 queries, 16 list states
+__host__ __device__ constexpr size_t s_scan_lds_per_wave(int kkeep) {
+    return (size_t)kSQ * 2 * kkeep * 8 + kSQ * 4 + kSQ * 8;
+}
+
+// KT = dp / 16 float4 chunks of the query operand in registers (d <= 128);
+// KT = 0 reloads it for every block.
+template <int KT, int KK>
+__global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
+    using namespace topk;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    const int64_t item = (int64_t)blockIdx.x * (blockDim.x >> 6) + wave;
+    const int64_t t = item / kSChunks;
+    const int c = (int)(item % kSChunks);
+    if (t >= P.tmax) return;        // wave-uniform; no workgroup barrier follows
+    const STile& T = P.tiles[t];
+    if (T.nq == 0) return;
+    const SharedLevels& lv = P.a.lv;
+    const int lev = T.lev;
+    const int64_t len = (int64_t)T.ub - T.ua;
+    const int64_t c0 = T.ua + len * c / kSChunks;
+    const int64_t c1 = T.ua + len * (c + 1) / kSChunks;
+    const int dp = P.ix.dp, dp4 = dp >> 2, d = P.ix.d;
+    constexpr int kkeep = KK;
+    char* wb = smem + (size_t)wave * s_scan_lds_per_wave(kkeep);
+    uint64_t* lkey = reinterpret_cast<uint64_t*>(wb);
+    float* qnl = reinterpret_cast<float*>(lkey + kSQ * 2 * kkeep);
+    int32_t* lst = reinterpret_cast<int32_t*>(qnl + kSQ);
+    auto list_of = [&](int sl) { return BufList{lkey + (size_t)sl * 2 * kkeep, lst + 2 * sl}; };
+
+    // MFMA operand mapping (16x16x4 f32): A[i][kk] in lane i + 16 kk, B[kk][j]
+    // in lane j + 16 kk, D[4 (lane/16) + e][lane % 16] in element e.  Lane
+    // group kk takes dimensions 16 u + 4 kk + {0..3} of K step u.
+    const int ii = lane & 15;
+    const int kk = lane >> 4;
+    const int qrow = T.q[ii];
+    const float* Qr = P.a.Q + (int64_t)(qrow >= 0 ? qrow : 0) * d;
+    auto qchunk = [&](int u) -> float4 {
+        const int b = 16 * u + 4 * kk;
+        float4 v;
+        v.x = (qrow >= 0 && b < d) ? Qr[b] : 0.f;
+        v.y = (qrow >= 0 && b + 1 < d) ? Qr[b + 1] : 0.f;
+        v.z = (qrow >= 0 && b + 2 < d) ? Qr[b + 2] : 0.f;
+        v.w = (qrow >= 0 && b + 3 < d) ? Qr[b + 3] : 0.f;
+        return v;
+    };
+    float4 qa[KT > 0 ? KT : 1];
+    float qs = 0.f;
+    for (int u = 0; u < dp / 16; ++u) {
+        const float4 v = qchunk(u);
+        if constexpr (KT > 0) {
+#pragma unroll
+            for (int w = 0; w < KT; ++w)
+                if (w == u) qa[w] = v;
+        }
+        qs += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+    qs += __shfl_xor(qs, 16);
+    qs += __shfl_xor(qs, 32);
+    if (kk == 0) {
+        qnl[ii] = qs;
+        lst[2 * ii + 0] = 0;
+        lst[2 * ii + 1] = 0x7f800000;
+    }
+    wave_sync();
+    float qn[4];
+    int32_t ql[4], qr[4];
+    uint32_t qT[4];
+    bool qv[4], qall[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int sl = 4 * kk + e;
+        qn[e] = qnl[sl];
+        ql[e] = T.l[sl];
+        qr[e] = T.r[sl];
+        qT[e] = T.T[sl];
+        qv[e] = T.q[sl] >= 0;
+        qall[e] = (T.allmask >> sl) & 1u;
+    }
+    uint32_t scount[kSQ];
+#pragma unroll
+    for (int i = 0; i < kSQ; ++i) scount[i] = 0u;
+
+    const float4* X4 = reinterpret_cast<const float4*>(P.ix.X);
+    const int64_t nblk = (c1 - c0 + 15) / 16;
+    // the level's list (level 0: every rank, no list)
+    const int32_t* lranks = lev == 0 ? nullptr : lv.ranks + lv.off[lev];
+    auto rank_at = [&](int64_t blk) -> int32_t {
+        int64_t pos = c0 + blk * 16 + ii;
+        pos = pos < c1 ? pos : c1 - 1;
+        return lranks ? lranks[pos] : (int32_t)pos;
+    };
+    auto load_rows = [&](int32_t rk, float4 (&x)[KT > 0 ? KT : 1]) {
+        if constexpr (KT > 0) {
+#pragma unroll
+            for (int u = 0; u < KT; ++u) x[u] = X4[(int64_t)rk * dp4 + 4 * u + kk];
+        }
+    };
+    // one 16-row block: q.x on the matrix cores, then the candidates
+    auto process = [&](const float4 (&x)[KT > 0 ? KT : 1], int32_t rk, int64_t blk) {
+        const bool inrun = c0 + blk * 16 + ii < c1;
+        // a block adds at most 16 entries to a list: cut those that could overflow
+        {
+            const int fl = lane < kSQ ? lst[2 * lane] : 0;
+            uint64_t over = __ballot(lane < kSQ && fl > 2 * kkeep - 16);
+            while (over) {
+                const int sl = __builtin_ctzll(over);
+                over &= over - 1;
+                buf_cut<kkeep>(list_of(sl));
+            }
+        }
+        floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+        float xn = 0.f;
+        if constexpr (KT > 0) {
+#pragma unroll
+            for (int u = 0; u < KT; ++u) {
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].x, x[u].x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].y, x[u].y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].z, x[u].z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].w, x[u].w, acc, 0, 0, 0);
+                xn += x[u].x * x[u].x + x[u].y * x[u].y + x[u].z * x[u].z + x[u].w * x[u].w;
+            }
+        } else {
+            for (int u = 0; u < dp / 16; ++u) {
+                const float4 xv = X4[(int64_t)rk * dp4 + 4 * u + kk];
+                const float4 q = qchunk(u);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.x, xv.x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, xv.y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.z, xv.z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, xv.w, acc, 0, 0, 0);
+                xn += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
+            }
+        }
+        xn += __shfl_xor(xn, 16);
+        xn += __shfl_xor(xn, 32);
+        const uint32_t pri = s_priority(P.a.lv.key, rk);
+        // lane holds D[4kk + e][ii]: query slot 4kk + e, the block's row ii
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bool insample = inrun && qv[e] && rk >= ql[e] && rk <= qr[e] && (qall[e] || pri < qT[e]);
+            const uint64_t ms = __ballot(insample);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) scount[4 * g + e] += (uint32_t)__popcll(ms & (0xFFFFull << (16 * g)));
+            if (ms == 0) continue;
+            const float ap = qn[e] + xn - 2.f * acc[e];
+            const int sl = 4 * kk + e;
+            if (insample && ap < __int_as_float(lst[2 * sl + 1])) {
+                const int pos = atomicAdd(lst + 2 * sl, 1);
+                lkey[(size_t)sl * 2 * kkeep + pos] = ((uint64_t)ord_bits(ap) << 32) | (uint32_t)rk;
+            }
+        }
+        list_sync();
+    };
+    // two row buffers in turn: the loads of block b + 2 are issued as soon
+    // as block b is multiplied, ranks two blocks ahead of their rows
+    float4 xa[KT > 0 ? KT : 1], xb[KT > 0 ? KT : 1];
+    int32_t ra = 0, rb = 0, ra2 = 0, rb2 = 0;
+    if (nblk > 0) { ra = rank_at(0); load_rows(ra, xa); }
+    if (nblk > 1) { rb = rank_at(1); load_rows(rb, xb); }
+    if (nblk > 2) ra2 = rank_at(2);
+    if (nblk > 3) rb2 = rank_at(3);
+    for (int64_t blk = 0; blk < nblk; blk += 2) {
+        process(xa, ra, blk);
+        if (blk + 2 < nblk) {
+            ra = ra2;
+            load_rows(ra, xa);
+            if (blk + 4 < nblk) ra2 = rank_at(blk + 4);
+        }
+        if (blk + 1 < nblk) process(xb, rb, blk + 1);
+        if (blk + 3 < nblk) {
+            rb = rb2;
+            load_rows(rb, xb);
+            if (blk + 5 < nblk) rb2 = rank_at(blk + 5);
+        }
+    }
+    // the item's lists: entries kept, threshold, sample rows seen
+    const int64_t base = item * kSQ;
+#pragma unroll
+    for (int i = 0; i < kSQ; ++i) {
+        buf_cut<kkeep>(list_of(i));
+        const int fi = __builtin_amdgcn_readfirstlane(lst[2 * i]);
+        const uint64_t* kb = lkey + (size_t)i * 2 * kkeep;
+        for (int j = lane; j < fi; j += 64) {
+            const uint64_t key = kb[j];
+            P.pv[(base + i) * kkeep + j] = ord_value((uint32_t)(key >> 32));
+            P.pr[(base + i) * kkeep + j] = (int32_t)(uint32_t)key;
+        }
+        if (lane == 0) {
+            P.pthr[base + i] = __int_as_float(lst[2 * i + 1]);   // +inf unless a cut dropped rows
+            P.pfill[base + i] = fi;
+            P.pcnt[base + i] = (int32_t)scount[i];
+        }
+    }
+}
+
+template <int C, int LP, int KK>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
+void s_search_kernel(SParams P) {
+    using namespace topk;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const DevIndex& ix = P.ix;
+    const SearchLaunch& A = P.a;
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    WaveLds<LP> W(smem, P.lds_per_wave, A.hash_log2);
+    char* lbase = smem + (size_t)wave * P.lds_per_wave + P.lds_list;
+    constexpr int kkeep = KK;
+    const BufList Lst{reinterpret_cast<uint64_t*>(lbase), reinterpret_cast<int32_t*>(lbase + (size_t)2 * kkeep * 8)};
+    Visited vis;
+    vis.tab = W.tab;
+    vis.shift = 32 - A.hash_log2;
+    const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+    vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
+    const double u_round = 5.9604644775390625e-08;   // 2^-24
+
+    for (;;) {
+        uint32_t qq = 0;
+        if (lane == 0) qq = atomicAdd(P.meta + 2, 1u);
+        const int64_t qi = (int64_t)(uint32_t)uniform((int)__shfl((int)qq, 0));
+        if (qi >= A.nq) break;
+        const SPlan p = P.plan[qi];
+        if (p.l > p.r) {
+            for (int j = lane; j < A.k; j += 64) {
+                A.ids[qi * A.k + j] = -1;
+                A.dists[qi * A.k + j] = __int_as_float(0x7f800000);
+            }
+            if (A.stats && lane < FROG_STAT_N) A.stats[qi * FROG_STAT_N + lane] = 0;
+            continue;
+        }
+        QueryCtx<C> Q;
+        Q.load(ix, A, P.lr, qi);
+        Q.load_vector(ix);
+        Q.shared = true;
+        Q.T = p.T;
+        Q.pkey = A.lv.key;
+
+        // the kkeep smallest approximate distances over the tile's lists
+        buf_init(Lst);
+        const int64_t t = p.tslot / kSQ;
+        const int slot = p.tslot % kSQ;
+        float texcl = __int_as_float(0x7f800000);   // every row left out is at or above this
+        int64_t ne = 0;
+        for (int c = 0; c < kSChunks; ++c) {
+            const int64_t base = (t * kSChunks + c) * kSQ + slot;
+            ne += P.pcnt[base];
+            texcl = fminf(texcl, P.pthr[base]);
+            const int fi = P.pfill[base];
+            for (int j0 = 0; j0 < fi; j0 += 64) {
+                const int j = j0 + lane;
+                const bool have = j < fi;
+                const float av = have ? P.pv[base * kkeep + j] : 0.f;
+                const int32_t rw = have ? P.pr[base * kkeep + j] : -1;
+                const uint64_t gm = ballot(have && av < __int_as_float(Lst.st[1]));
+                if (gm) buf_offer<kkeep>(Lst, gm, av, rw);
+            }
+        }
+        buf_cut<kkeep>(Lst);
+        texcl = fminf(texcl, __int_as_float(Lst.st[1]));
+        const int f = uniform(Lst.st[0]);
+
+        // exact distances of the kept rows: the pool of the L nearest
+        Pool<LP> pool;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+        pool.np = 0;
+        for (int j0 = 0; j0 < f; j0 += 64) {
+            const int nb = f - j0 < 64 ? f - j0 : 64;
+            const int32_t id = lane < nb ? (int32_t)(uint32_t)Lst.key[j0 + lane] : 0;
+            const float dd = Q.eval_batch(ix, nb, id);
+            merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
+        }
+        // margin test: a row left out has exact distance >= texcl - eps
+        bool certified = true;
+        if (!(texcl == __int_as_float(0x7f800000))) {
+            certified = false;
+            if (pool.np >= A.L) {
+                double qsq = 0.0;
+                for (int cc = lane; cc < ix.d; cc += 64) qsq += (double)Q.qrow[cc] * (double)Q.qrow[cc];
+#pragma unroll
+                for (int o = 32; o >= 1; o >>= 1) qsq += __shfl_xor(qsq, o);
+                const double eps = 2.0 * (2.0 * ix.d + 4.0) * u_round * (qsq + (double)A.maxnorm);
+                uint64_t lk = 0;
+#pragma unroll
+                for (int s = 0; s < LP; ++s)
+                    if (s == ((A.L - 1) >> 6)) lk = readlane64(pool.key[s], (A.L - 1) & 63);
+                const double dL = (double)__uint_as_float((uint32_t)(lk >> 32));
+                certified = (double)texcl - eps > dL;
+            }
+        }
+        certified = uniform(certified ? 1 : 0) != 0;
+        if (!certified) {
+            // every sample row, exactly
+#pragma unroll
+            for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+            pool.np = 0;
+            ne = 0;
+            for (int64_t b0 = p.a; b0 < p.b; b0 += 64) {
+                const int64_t pos = b0 + lane;
+                const int32_t rk = pos < p.b ? level_rank(A.lv, p.lev, pos) : 0;
+                const bool in = pos < p.b && (p.all || s_priority(A.lv.key, rk) < p.T);
+                const uint64_t pm = ballot(in);
+                const int nb = __popcll(pm);
+                ne += nb;
+                if (nb == 0) continue;
+                if (in) W.enbuf[mbcnt(pm)] = rk;
+                wave_sync();
+                const int32_t id = lane < nb ? W.enbuf[lane] : 0;
+                wave_sync();
+                const float dd = Q.eval_batch(ix, nb, id);
+                merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
+            }
+        }
+        Q.ne = ne;
+        traverse<C, LP>(ix, A, P.gvis_words, Q, pool, W, vis);
+    }
 }
 
 // ------------------------------------------------------------------ dispatch
@@ -938,6 +1496,143 @@ int max_blocks(KernelFn fn, int smem) {
     return v;
 }
 
+
+// candidates kept per query and work item: K > L with room for the margin
+int shared_kkeep(int L) { return L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256); }
+
+template <int C>
+void (*pick_s_lp(int L))(SParams) {
+    const int kk = shared_kkeep(L);
+    if (L <= 64) return kk == 64 ? s_search_kernel<C, 1, 64> : s_search_kernel<C, 1, 128>;
+    if (L <= 128) return kk == 128 ? s_search_kernel<C, 2, 128> : s_search_kernel<C, 2, 256>;
+    return s_search_kernel<C, 4, 256>;
+}
+
+void (*pick_s_search(int dp, int L))(SParams) {
+    switch (dp) {
+        case 32: return pick_s_lp<1>(L);
+        case 64: return pick_s_lp<2>(L);
+        case 96: return pick_s_lp<3>(L);
+        case 128: return pick_s_lp<4>(L);
+        default: return pick_s_lp<0>(L);
+    }
+}
+
+template <int KK>
+void (*pick_s_scan_k(int dp))(SParams) {
+    switch (dp) {
+        case 32: return s_scan_kernel<2, KK>;
+        case 64: return s_scan_kernel<4, KK>;
+        case 96: return s_scan_kernel<6, KK>;
+        case 128: return s_scan_kernel<8, KK>;
+        default: return s_scan_kernel<0, KK>;
+    }
+}
+
+void (*pick_s_scan(int dp, int kkeep))(SParams) {
+    if (kkeep == 64) return pick_s_scan_k<64>(dp);
+    if (kkeep == 128) return pick_s_scan_k<128>(dp);
+    return pick_s_scan_k<256>(dp);
+}
+
+// entry_mode 1: plan, group, scan on the matrix cores, then search
+int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream) {
+    const int kkeep = shared_kkeep(a.L);
+    auto sfn = pick_s_search(ix.dp, a.L);
+    const int base_lds = lds_per_wave(a.L, a.hash_log2);
+    const int lpw = base_lds + 2 * kkeep * 8 + 16;
+    const int smem = lpw * kWavesPerBlock;
+    if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);
+    if (smem > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)sfn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
+    auto scan = pick_s_scan(ix.dp, kkeep);
+    // wavefronts per scan workgroup: as many as 160 KB of LDS hold (at most 4)
+    int scan_waves = (int)((160 * 1024) / s_scan_lds_per_wave(kkeep));
+    if (scan_waves > kWavesPerBlock) scan_waves = kWavesPerBlock;
+    if (scan_waves < 1) return fail(FROG_EUNSUPPORTED, "L=%d needs too much LDS for the entry scan", a.L);
+    const int smem_scan = (int)(scan_waves * s_scan_lds_per_wave(kkeep));
+    if (smem_scan > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)scan, hipFuncAttributeMaxDynamicSharedMemorySize, smem_scan);
+        if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
+    SParams P{};
+    P.ix = ix;
+    P.a = a;
+    const int64_t norder = a.nq + (int64_t)kSQ * (a.lv.nlev + 1);
+    P.tmax = (norder + kSQ - 1) / kSQ;
+    P.nbins = (a.lv.nlev + 1) * kSBins + 1;
+    P.kkeep = kkeep;
+    P.lds_per_wave = lpw;
+    P.lds_list = base_lds;
+    int blocks = max_blocks((KernelFn)sfn, smem);
+    const int64_t need = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (need < blocks) blocks = (int)need;
+    const int64_t items = P.tmax * kSChunks;
+    auto align = [](size_t x) { return (x + 255) / 256 * 256; };
+    size_t off = 0;
+    auto take = [&](size_t bytes) { const size_t o = off; off += align(bytes); return o; };
+    const size_t o_meta = take(16);
+    const size_t o_lr = take((size_t)a.nq * 8);
+    const size_t o_plan = take((size_t)a.nq * sizeof(SPlan));
+    const size_t o_hist = take((size_t)P.nbins * 4);
+    const size_t o_bstart = take((size_t)P.nbins * 4);
+    const size_t o_order = take((size_t)norder * 4);
+    const size_t o_tiles = take((size_t)P.tmax * sizeof(STile));
+    const size_t o_pv = take((size_t)items * kSQ * kkeep * 4);
+    const size_t o_pr = take((size_t)items * kSQ * kkeep * 4);
+    const size_t o_pthr = take((size_t)items * kSQ * 4);
+    const size_t o_pfill = take((size_t)items * kSQ * 4);
+    const size_t o_pcnt = take((size_t)items * kSQ * 4);
+    const size_t o_gvis = off;
+    if (a.hash_log2 == 0) {
+        P.gvis_words = (ix.n + 31) / 32;
+        const int64_t cap = ((int64_t)2 << 30) / (P.gvis_words * 4 * kWavesPerBlock);
+        if (cap < blocks) blocks = (int)(cap > 0 ? cap : 1);
+        off += (size_t)blocks * kWavesPerBlock * P.gvis_words * 4;
+    }
+    void* wsp = nullptr;
+    hipError_t e = hipMallocAsync(&wsp, off, stream);
+    if (e != hipSuccess) return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
+    char* base = reinterpret_cast<char*>(wsp);
+    P.meta = reinterpret_cast<uint32_t*>(base + o_meta);
+    int32_t* lr = reinterpret_cast<int32_t*>(base + o_lr);
+    P.lr = lr;
+    P.plan = reinterpret_cast<SPlan*>(base + o_plan);
+    P.hist = reinterpret_cast<uint32_t*>(base + o_hist);
+    P.bstart = reinterpret_cast<uint32_t*>(base + o_bstart);
+    P.order = reinterpret_cast<int32_t*>(base + o_order);
+    P.tiles = reinterpret_cast<STile*>(base + o_tiles);
+    P.pv = reinterpret_cast<float*>(base + o_pv);
+    P.pr = reinterpret_cast<int32_t*>(base + o_pr);
+    P.pthr = reinterpret_cast<float*>(base + o_pthr);
+    P.pfill = reinterpret_cast<int32_t*>(base + o_pfill);
+    P.pcnt = reinterpret_cast<int32_t*>(base + o_pcnt);
+    P.gvis = reinterpret_cast<uint32_t*>(base + o_gvis);
+    hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(a.events);
+    const unsigned qb = (unsigned)((a.nq + 255) / 256);
+    const int64_t ninit = norder > P.nbins ? norder : P.nbins;
+    hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.hist,
+                       P.nbins, P.order, norder);
+    const int64_t rb_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (ev) (void)hipEventRecord(ev[0], stream);
+    hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
+    hipLaunchKernelGGL(s_plan_kernel, dim3(qb), dim3(256), 0, stream, P);
+    hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(64), 0, stream, P);
+    hipLaunchKernelGGL(s_order_kernel, dim3(qb), dim3(256), 0, stream, P);
+    hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + 255) / 256)), dim3(256), 0, stream, P);
+    hipLaunchKernelGGL(scan, dim3((unsigned)((items + scan_waves - 1) / scan_waves)), dim3(64 * scan_waves), smem_scan,
+                       stream, P);
+    if (ev) (void)hipEventRecord(ev[1], stream);
+    hipLaunchKernelGGL(sfn, dim3(blocks), dim3(kBlock), smem, stream, P);
+    if (ev) (void)hipEventRecord(ev[2], stream);
+    e = hipGetLastError();
+    (void)hipFreeAsync(wsp, stream);
+    if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
+    return FROG_OK;
+}
+
 }  // namespace
 
 bool search_shape_supported(int dp, int m, int L) {
@@ -946,6 +1641,7 @@ bool search_shape_supported(int dp, int m, int L) {
 
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     hipStream_t stream = (hipStream_t)stream_v;
+    if (a.entry_mode == 1) return launch_shared(ix, a, stream);
     const KernelFn fn = pick_kernel(ix.dp, a.L);
     const int lpw = lds_per_wave(a.L, a.hash_log2);
     const int smem = lpw * kWavesPerBlock + 16;

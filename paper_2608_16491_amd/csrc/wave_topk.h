@@ -1,0 +1,202 @@
+// Per-query lists of the smallest (approximate distance, row) pairs, kept by
+// one wavefront in LDS.  The matrix-core scans (the brute force and the
+// shared entry sample of the search) offer each query's candidates of a
+// 16-row block to its list; a full list holds its largest value as the
+// threshold a candidate has to beat.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace frog {
+namespace topk {
+
+__device__ __forceinline__ void list_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ float wave_max_pos(float v, int& pos) {
+    // max over the wavefront with the lowest position among equals
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(v, o);
+        const int op = __shfl_xor(pos, o);
+        if (ov > v || (ov == v && op < pos)) { v = ov; pos = op; }
+    }
+    return v;
+}
+
+// A list of at most `cap` (approximate distance, row) pairs in LDS (cap a
+// multiple of 64) and its state, also in LDS: the number of entries, and once
+// the list is full, the value and slot of its largest entry (the threshold a
+// new candidate has to beat).  Every row offered to the list and not kept has
+// a value at or above the final threshold.
+struct TopList {
+    float* v;
+    int32_t* r;
+    int32_t* st;   // [0] fill, [1] threshold (float bits), [2] slot of the largest
+};
+
+__device__ __forceinline__ float list_threshold(const int32_t* st) { return __int_as_float(st[1]); }
+
+// recompute the largest entry of a full list (all lanes)
+__device__ __forceinline__ void list_refresh(const TopList& Lst, int cap, float& thr, int& mpos) {
+    const int lane = __lane_id();
+    float best = Lst.v[lane];
+    int pos = lane;
+    for (int j = 64 + lane; j < cap; j += 64)
+        if (Lst.v[j] > best) { best = Lst.v[j]; pos = j; }
+    best = wave_max_pos(best, pos);
+    thr = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(best)));
+    mpos = __builtin_amdgcn_readfirstlane(pos);
+}
+
+// Offer the candidates held by the lanes of `group_mask` (value a, row rw in
+// each such lane) to the list.  Returns true if a candidate was dropped or an
+// entry evicted.
+static __device__ __noinline__ bool offer(TopList Lst, int cap, uint64_t group_mask, float a, int32_t rw) {
+    const int lane = __lane_id();
+    int f = __builtin_amdgcn_readfirstlane(Lst.st[0]);
+    float thr = __int_as_float(__builtin_amdgcn_readfirstlane(Lst.st[1]));
+    int mpos = __builtin_amdgcn_readfirstlane(Lst.st[2]);
+    bool dropped = false;
+    const int c = __popcll(group_mask);
+    if (f + c <= cap) {
+        // room for all: append in parallel
+        if ((group_mask >> lane) & 1) {
+            const int pos = f + __popcll(group_mask & ((1ull << lane) - 1));
+            Lst.v[pos] = a;
+            Lst.r[pos] = rw;
+        }
+        f += c;
+        list_sync();
+        if (f == cap) list_refresh(Lst, cap, thr, mpos);
+    } else {
+        for (uint64_t m = group_mask; m; m &= m - 1) {
+            const int src = __builtin_ctzll(m);
+            const float av = __shfl(a, src);
+            const int32_t rv = __shfl(rw, src);
+            if (f < cap) {
+                if (lane == 0) { Lst.v[f] = av; Lst.r[f] = rv; }
+                ++f;
+                list_sync();
+                if (f == cap) list_refresh(Lst, cap, thr, mpos);
+                continue;
+            }
+            dropped = true;   // av itself, or the entry it evicts
+            if (!(av < thr)) continue;
+            if (lane == 0) { Lst.v[mpos] = av; Lst.r[mpos] = rv; }
+            list_sync();
+            list_refresh(Lst, cap, thr, mpos);
+        }
+    }
+    if (lane == 0) {
+        Lst.st[0] = f;
+        Lst.st[1] = __float_as_int(thr);
+        Lst.st[2] = mpos;
+    }
+    list_sync();
+    return dropped;
+}
+
+// Buffered variant for long streams: up to 2K keys (orderable float bits of
+// the value << 32 | row) in LDS.  Candidates below the threshold are
+// appended; a buffer about to overflow is cut to its K smallest (K-th value
+// found by bisection over the value bits, kept entries compacted in place),
+// whose largest value becomes the threshold (+inf until the first cut).
+// Every candidate offered and not kept has a value at or above the final
+// threshold.
+struct BufList {
+    uint64_t* key;   // [2K]
+    int32_t* st;     // [0] fill, [1] threshold (float bits)
+};
+
+__device__ __forceinline__ uint32_t ord_bits(float v) {
+    const uint32_t b = __float_as_uint(v);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ float ord_value(uint32_t o) {
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+
+__device__ __forceinline__ void buf_init(const BufList& B) {
+    if (__lane_id() == 0) {
+        B.st[0] = 0;
+        B.st[1] = 0x7f800000;
+    }
+    list_sync();
+}
+
+// Keep the K smallest of the buffer's entries (all of them if there are at
+// most K).  K is 64, 128 or 256.
+template <int K>
+__device__ __forceinline__ void buf_cut(const BufList& B) {
+    constexpr int R = 2 * K / 64;   // entries per lane
+    const int lane = __lane_id();
+    const int f = __builtin_amdgcn_readfirstlane(B.st[0]);
+    if (f <= K) return;
+    uint64_t k[R];
+#pragma unroll
+    for (int i = 0; i < R; ++i) k[i] = i * 64 + lane < f ? B.key[i * 64 + lane] : ~0ull;
+    // smallest value bits x with #(entries with value <= x) >= K
+    uint32_t lo = 0u, hi = 0xFFFFFFFFu;
+    while (lo < hi) {
+        const uint32_t mid = lo + ((hi - lo) >> 1);
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < R; ++i) c += __popcll(__ballot((uint32_t)(k[i] >> 32) <= mid));
+        if (c >= K) hi = mid;
+        else lo = mid + 1;
+    }
+    const uint32_t vk = lo;
+    // entries below vk, then entries equal to vk up to K in all
+    int below = 0;
+#pragma unroll
+    for (int i = 0; i < R; ++i) below += __popcll(__ballot((uint32_t)(k[i] >> 32) < vk));
+    list_sync();
+    int wr = 0, eq = 0;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const uint32_t v = (uint32_t)(k[i] >> 32);
+        const uint64_t mb = __ballot(v < vk);
+        const uint64_t me = __ballot(v == vk);
+        const uint64_t lt = (1ull << lane) - 1;
+        if (v < vk) B.key[wr + __popcll(mb & lt)] = k[i];
+        if (v == vk) {
+            const int pos = below + eq + __popcll(me & lt);
+            if (pos < K) B.key[pos] = k[i];
+        }
+        wr += __popcll(mb);
+        eq += __popcll(me);
+    }
+    if (lane == 0) {
+        B.st[0] = K;
+        B.st[1] = (int32_t)__float_as_uint(ord_value(vk));
+    }
+    list_sync();
+}
+
+// Append the candidates of the lanes in gm (value a, row rw), all of them
+// below the current threshold; at most 64 of them, so K >= 64 leaves room
+// after a cut.
+template <int K>
+__device__ __forceinline__ void buf_offer(const BufList& B, uint64_t gm, float a, int32_t rw) {
+    const int lane = __lane_id();
+    int f = __builtin_amdgcn_readfirstlane(B.st[0]);
+    if (f + __popcll(gm) > 2 * K) {
+        buf_cut<K>(B);
+        f = __builtin_amdgcn_readfirstlane(B.st[0]);
+        const float thr = __int_as_float(__builtin_amdgcn_readfirstlane(B.st[1]));
+        gm &= __ballot(a < thr);
+    }
+    if ((gm >> lane) & 1) B.key[f + __popcll(gm & ((1ull << lane) - 1))] = ((uint64_t)ord_bits(a) << 32) | (uint32_t)rw;
+    if (lane == 0) B.st[0] = f + __popcll(gm);
+    list_sync();
+}
+
+}  // namespace topk
+}  // namespace frog

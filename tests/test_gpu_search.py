@@ -34,7 +34,7 @@ class Case:
 
     def cpu(self, k, L, **p):
         kw = dict(epn=p.get("epn", 16), epn_frac=p.get("epn_frac", 0.0), epn_max=p.get("epn_max", 0),
-                  B=p.get("budget", 16), seed=p.get("seed", 0))
+                  B=p.get("budget", 16), seed=p.get("seed", 0), entry_mode=p.get("entry_mode", 0))
         qidx = np.arange(self.Q.shape[0]) + p.get("query_base", 0)
         return oracle.search(self.ox, self.Q, self.lo, self.hi, k, L, qidx=qidx, **kw)
 

@@ -1,0 +1,138 @@
+"""GPU parity of FROGSearch with the shared-priority entry sample
+(entry_mode 1: matrix-core scan of the sample, exact re-rank, margin test)
+against the CPU oracle's plain reading of the same sampling (every rank of the
+range whose priority is below the query's threshold, evaluated one by one).
+The index comes from the oracle's construction."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_16491_amd as F
+import workloads
+from tests.parity import assert_parity
+from tests.test_gpu_search import Case
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SH = dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=2000)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    print("[gpu] shared entry sample: tiny workload n=10000 d=32 nq=100", flush=True)
+    w = workloads.make("tiny")
+    return Case(w.X, w.attr, w.Q, w.lo, w.hi)
+
+
+@pytest.fixture(scope="module")
+def mix128():
+    print("[gpu] shared entry sample: mixture n=30000 d=128 nq=600", flush=True)
+    w = workloads.make("c2", n=30000, nq=600)
+    return Case(w.X, w.attr, w.Q, w.lo, w.hi)
+
+
+@pytest.mark.parametrize("L", [32, 56, 64, 128, 256])
+def test_shared_tiny_parity_pool_sizes(tiny, L):
+    g_ids, g_d = tiny.gpu(10, L, **SH)
+    o_ids, o_d, _ = tiny.cpu(10, L, **SH)
+    assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+@pytest.mark.parametrize("p", [dict(entry_mode=1), dict(entry_mode=1, epn=100),
+                               dict(entry_mode=1, epn=4, epn_frac=0.05, epn_max=700),
+                               dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=20000),
+                               dict(entry_mode=1, seed=12345, epn=16, epn_frac=0.2, epn_max=3000)])
+def test_shared_entry_counts_and_seeds(tiny, p):
+    g_ids, g_d = tiny.gpu(10, 64, **p)
+    o_ids, o_d, _ = tiny.cpu(10, 64, **p)
+    assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+def test_shared_stats_exact_visited_equal_oracle(tiny):
+    # exact visited set: expansions, |EN| sums, distinct evaluations, ENC
+    # entries, the sample size and the hotspot all equal the oracle's
+    g_ids, g_d, g_st = tiny.gpu(10, 64, stats=True, hash_log2=0, **SH)
+    o_ids, o_d, o_st = tiny.cpu(10, 64, **SH)
+    res = assert_parity(g_ids, g_d, o_ids, o_d)
+    ok = np.setdiff1d(np.arange(len(g_ids)), res)
+    cols = [(F.STAT_EXPANSIONS, oracle.STAT_EXPANSIONS), (F.STAT_EN, oracle.STAT_EN),
+            (F.STAT_DIST, oracle.STAT_DIST), (F.STAT_SCANNED, oracle.STAT_SCANNED),
+            (F.STAT_ENTRY, oracle.STAT_ENTRY), (F.STAT_LSTART, oracle.STAT_LS), (F.STAT_LEND, oracle.STAT_LE)]
+    for gc, oc in cols:
+        assert (g_st[ok, gc] == o_st[ok, oc]).all(), (gc, g_st[ok, gc][:8], o_st[ok, oc][:8])
+
+
+@pytest.mark.parametrize("hash_log2", [6, 10])
+def test_shared_forgetful_table_does_not_change_results(tiny, hash_log2):
+    ref_ids, ref_d, ref_st = tiny.gpu(10, 64, stats=True, hash_log2=0, **SH)
+    g_ids, g_d, g_st = tiny.gpu(10, 64, stats=True, hash_log2=hash_log2, **SH)
+    assert (g_ids == ref_ids).all() and (g_d.view(np.uint32) == ref_d.view(np.uint32)).all()
+    assert (g_st[:, F.STAT_EXPANSIONS] == ref_st[:, F.STAT_EXPANSIONS]).all()
+    assert (g_st[:, F.STAT_DIST] >= ref_st[:, F.STAT_DIST]).all()
+
+
+def test_shared_seed_change_rebuilds_levels(tiny):
+    # seed 0, then 99 (new levels), then 0 again (levels rebuilt): each run
+    # matches the oracle for its seed
+    a_ids, a_d = tiny.gpu(10, 64, **SH)
+    tiny.gpu(10, 64, **dict(SH, seed=99))
+    c_ids, c_d = tiny.gpu(10, 64, **SH)
+    assert (a_ids == c_ids).all() and (a_d.view(np.uint32) == c_d.view(np.uint32)).all()
+    o2_ids, o2_d, _ = tiny.cpu(10, 64, **dict(SH, seed=99))
+    g2_ids, g2_d = tiny.gpu(10, 64, **dict(SH, seed=99))
+    assert_parity(g2_ids, g2_d, o2_ids, o2_d)
+
+
+@pytest.mark.parametrize("L,emax,B", [(32, 2560, 24), (64, 2000, 16), (128, 800, 16)])
+def test_shared_mixture_d128_parity(mix128, L, emax, B):
+    p = dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=emax, budget=B)
+    g_ids, g_d, g_st = mix128.gpu(10, L, stats=True, **p)
+    o_ids, o_d, o_st = mix128.cpu(10, L, **p)
+    res = assert_parity(g_ids, g_d, o_ids, o_d)
+    ok = np.setdiff1d(np.arange(len(g_ids)), res)
+    assert (g_st[ok, F.STAT_ENTRY] == o_st[ok, oracle.STAT_ENTRY]).all()
+    assert (g_st[ok, F.STAT_EXPANSIONS] == o_st[ok, oracle.STAT_EXPANSIONS]).all()
+
+
+def test_shared_k100_pool256(mix128):
+    p = dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=3000)
+    g_ids, g_d = mix128.gpu(100, 256, **p)
+    o_ids, o_d, _ = mix128.cpu(100, 256, **p)
+    assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+def test_shared_degenerate_ranges(tiny):
+    n = tiny.ox.n
+    lo = np.array([5.0, 100.0, np.nan, 3.0, 0.0, -1e9, n - 1.0, 40.0, 10.0, 0.0])
+    hi = np.array([5.0, 99.0, 10.0, 3.5, n - 1.0, 1e9, n + 5.0, 39.0, 12.0, 15.0])
+    Q = tiny.Q[:10]
+    c = Case.__new__(Case)
+    c.ox, c.ix = tiny.ox, tiny.ix
+    c.Q, c.lo, c.hi = Q, lo, hi
+    c.dQ = torch.as_tensor(Q).cuda()
+    c.dlo = torch.as_tensor(lo).cuda()
+    c.dhi = torch.as_tensor(hi).cuda()
+    g_ids, g_d, g_st = c.gpu(10, 32, stats=True, **SH)
+    o_ids, o_d, o_st = c.cpu(10, 32, **SH)
+    assert_parity(g_ids, g_d, o_ids, o_d, max_residual=0)
+    assert (g_st[[1, 2, 7]] == 0).all()
+
+
+@pytest.mark.parametrize("d", [7, 96, 200])
+def test_shared_other_dimensions(d):
+    print(f"[gpu] shared entry sample, d={d}", flush=True)
+    rng = np.random.default_rng(d)
+    n, nq = 4000, 64
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    attr = rng.permutation(n).astype(np.float64)
+    Q = rng.standard_normal((nq, d)).astype(np.float32)
+    sig = 2.0 ** (-8 * rng.random(nq))
+    cnt = np.maximum(1, np.round(sig * n)).astype(np.int64)
+    lo = rng.integers(0, n - cnt + 1)
+    hi = lo + cnt - 1
+    c = Case(X, attr, Q, lo.astype(np.float64), hi.astype(np.float64), m=8, ef_c=32, n_inv=4)
+    p = dict(entry_mode=1, epn=8, epn_frac=0.5, epn_max=300)
+    g_ids, g_d = c.gpu(10, 32, **p)
+    o_ids, o_d, _ = c.cpu(10, 32, **p)
+    assert_parity(g_ids, g_d, o_ids, o_d)
