@@ -35,9 +35,11 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "search_c2_traffic.json")
 
-# (L, epn, epn_frac, epn_max, budget): the paper's fixed 16 entry points, then
-# the per-query count min(cnt, epn_max) -- on the clustered mixture a query
-# must start inside its own cluster, which takes a few thousand uniform samples
+# (L, epn, epn_frac, epn_max, budget[, entry_mode]): the paper's fixed 16
+# entry points, then the per-query count min(cnt, epn_max) -- on the clustered
+# mixture a query must start inside its own cluster, which takes a few
+# thousand uniform samples.  entry_mode 0 draws them per query (stratified),
+# 1 from the rank priority shared by all queries (matrix-core entry scan).
 SWEEP = [
     (32, 16, 0.0, 0, 16), (64, 16, 0.0, 0, 16),
     (32, 16, 1.0, 2048, 16), (64, 16, 1.0, 2048, 16),
@@ -47,7 +49,17 @@ SWEEP = [
     (32, 16, 1.0, 4096, 16), (64, 16, 1.0, 4096, 16),
     (32, 16, 1.0, 2304, 32), (32, 16, 1.0, 2560, 32), (40, 16, 1.0, 2560, 32), (32, 16, 1.0, 2560, 24),
     (32, 16, 1.0, 2560, 28), (24, 16, 1.0, 2560, 32),
+    (32, 16, 1.0, 2560, 24, 1), (24, 16, 1.0, 2560, 32, 1), (32, 16, 1.0, 2048, 32, 1),
+    (24, 16, 1.0, 2304, 32, 1), (32, 16, 1.0, 3072, 16, 1), (24, 16, 1.0, 3072, 24, 1),
+    (16, 16, 1.0, 3072, 32, 1), (32, 16, 1.0, 4096, 16, 1),
 ]
+
+
+def _plain(o):
+    """JSON for numpy scalars."""
+    if hasattr(o, "item"):
+        return o.item()
+    raise TypeError(f"not JSON serializable: {type(o).__name__}")
 
 
 def log(*a):
@@ -56,8 +68,9 @@ def log(*a):
 
 def source_sha():
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2608_16491_amd", "csrc", "search.hip"), "rb") as f:
-        h.update(f.read())
+    for name in ("search.hip", "wave_topk.h"):
+        with open(os.path.join(ROOT, "paper_2608_16491_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
@@ -125,15 +138,20 @@ def main():
     k = w.k
     stream = torch.cuda.current_stream()
 
-    def run(L, epn, frac, emax, B=16, hl2=args.hash_log2, stats=False, events=None):
+    def run(L, epn, frac, emax, B=16, mode=0, hl2=args.hash_log2, stats=False, events=None):
         return F.search(ix, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                        hash_log2=hl2, stats=stats, events=events)
+                        entry_mode=mode, hash_log2=hl2, stats=stats, events=events)
 
-    def parse_setting(text):
-        v = [float(x) for x in text.split(",")]
+    def norm_setting(v):
+        v = list(v)
         if len(v) == 4:
             v.append(16)
-        return int(v[0]), int(v[1]), v[2], int(v[3]), int(v[4])
+        if len(v) == 5:
+            v.append(0)
+        return int(v[0]), int(v[1]), float(v[2]), int(v[3]), int(v[4]), int(v[5])
+
+    def parse_setting(text):
+        return norm_setting([float(x) for x in text.split(",")])
 
     def timed(fn, reps):
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -147,8 +165,8 @@ def main():
 
     if args.profile_pass:
         settings = [parse_setting(t) for t in args.setting.split(";")]
-        for (L, epn, frac, emax, B) in settings:
-            run(L, epn, frac, emax, B)
+        for (L, epn, frac, emax, B, mode) in settings:
+            run(L, epn, frac, emax, B, mode)
             torch.cuda.synchronize()
         F.bruteforce(ix, Q, lo, hi, k)
         torch.cuda.synchronize()
@@ -176,31 +194,34 @@ def main():
 
     # sweep
     rows = []
-    settings = SWEEP if args.setting is None else [parse_setting(args.setting)]
-    for (L, epn, frac, emax, B) in settings:
+    settings = [norm_setting(x) for x in SWEEP] if args.setting is None else [parse_setting(args.setting)]
+    for (L, epn, frac, emax, B, mode) in settings:
         if L < k:
             continue
-        ids, _ = run(L, epn, frac, emax, B)
+        ids, _ = run(L, epn, frac, emax, B, mode)
         torch.cuda.synchronize()
         rec = recall_at_k(ids.cpu().numpy(), gt_ids)
-        t = timed(lambda: run(L, epn, frac, emax, B), 3)
-        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, recall=float(rec.mean()),
-                         qps=w.nq / t, ms=t * 1e3,
+        run(L, epn, frac, emax, B, mode)
+        t = timed(lambda: run(L, epn, frac, emax, B, mode), 3)
+        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, entry_mode=mode,
+                         recall=float(rec.mean()), qps=w.nq / t, ms=t * 1e3,
                          recall_band=[float(rec[band == b].mean()) if (band == b).any() else None
                                       for b in range(10)]))
-        log(f"L={L:4d} epn={epn} frac={frac:<6} max={emax:5d} B={B:2d}  recall={rec.mean():.4f}  "
+        log(f"L={L:4d} epn={epn} frac={frac:<6} max={emax:5d} B={B:2d} mode={mode}  recall={rec.mean():.4f}  "
             f"{t * 1e3:8.3f} ms  {w.nq / t:12.0f} QPS")
     ok = [r for r in rows if r["recall"] >= 0.9]
     chosen = max(ok, key=lambda r: r["qps"]) if ok else max(rows, key=lambda r: r["recall"])
     met = bool(ok)
-    L, epn, frac, emax, B = chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"], chosen["budget"]
-    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} recall={chosen['recall']:.4f}"
-        + ("" if met else "  (recall target NOT met)"))
+    L, epn, frac, emax, B, mode = (chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"],
+                                   chosen["budget"], chosen["entry_mode"])
+    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} entry_mode={mode} "
+        f"recall={chosen['recall']:.4f}" + ("" if met else "  (recall target NOT met)"))
 
-    # timed steps; each step also records events around the library's search
-    # kernel on the same stream
+    # timed steps; each step also records events around the library's kernels
+    # on the same stream (entry_mode 0: the search kernel; entry_mode 1: the
+    # matrix-core entry scan, then the search kernel)
     for _ in range(args.warmup):
-        run(L, epn, frac, emax, B)
+        run(L, epn, frac, emax, B, mode)
     phase = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     for trio in phase:
         for ev in trio:
@@ -211,19 +232,21 @@ def main():
     wall0 = time.perf_counter()
     ev_s.record(stream)
     for i in range(args.steps):
-        run(L, epn, frac, emax, B, events=phase[i])
+        run(L, epn, frac, emax, B, mode, events=phase[i])
     ev_e.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     per_step = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
-    t_kernel = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
+    t_a = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
+    t_b = sum(t[1].elapsed_time(t[2]) for t in phase) / 1000.0 / args.steps
     qps = w.nq / per_step
     log(f"timed {args.steps} steps: {per_step * 1e3:.3f} ms/step (events), wall {wall / args.steps * 1e3:.3f} ms/step, "
-        f"{qps:.0f} QPS; search kernel {t_kernel * 1e3:.3f} ms")
+        f"{qps:.0f} QPS; " + (f"search kernel {t_a * 1e3:.3f} ms" if mode == 0 else
+                              f"entry scan {t_a * 1e3:.3f} ms, search kernel {t_b * 1e3:.3f} ms"))
 
     # algorithmic bytes: distinct evaluations and ENC entries from the exact-visited pass
-    ids_e, _, st_e = run(L, epn, frac, emax, B, hl2=0, stats=True)
-    _, _, st_f = run(L, epn, frac, emax, B, stats=True)
+    ids_e, _, st_e = run(L, epn, frac, emax, B, mode, hl2=0, stats=True)
+    _, _, st_f = run(L, epn, frac, emax, B, mode, stats=True)
     torch.cuda.synchronize()
     st_e = st_e.cpu().numpy().astype(np.int64)
     st_f = st_f.cpu().numpy().astype(np.int64)
@@ -231,27 +254,55 @@ def main():
     S = st_e[:, F.STAT_SCANNED].sum()
     NE = st_e[:, F.STAT_ENTRY].sum()
     nonempty = int((cnt > 0).sum())
-    # the search kernel reads every distinct evaluated vector (entry points and
-    # traversal), the ENC entries Alg. 4 examines, the query, its rank search,
-    # and writes the output through the id map
-    alg_bytes = (4.0 * d * D + 4.0 * S
-                 + (4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k) * nonempty)
     overhead = st_f[:, F.STAT_DIST].sum() / max(D, 1)
-    dominant = "coop_kernel"
-    achieved = alg_bytes / t_kernel / 1e9
-    log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, entry points {NE}, "
-        f"ENC entries {S}); search kernel {achieved:.0f} GB/s = {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s, "
-        f"whole step {alg_bytes / per_step / 1e9:.0f} GB/s; forgetful-table evaluations x{overhead:.3f}")
+    per_query = (4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k) * nonempty
+    phases = None
+    if mode == 0:
+        # one kernel reads every distinct evaluated vector (entry points and
+        # traversal), the ENC entries Alg. 4 examines, the query, its rank
+        # search, and writes the output through the id map
+        alg_bytes = 4.0 * d * D + 4.0 * S + per_query
+        dominant, t_kernel = "coop_kernel", t_a
+        achieved = alg_bytes / t_kernel / 1e9
+        log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, entry points {NE}, "
+            f"ENC entries {S}); search kernel {achieved:.0f} GB/s = {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s, "
+            f"whole step {alg_bytes / per_step / 1e9:.0f} GB/s; forgetful-table evaluations x{overhead:.3f}")
+    else:
+        # entry scan: the rows of every tile's run, once per tile (row data
+        # and, above level 0, its rank); search kernel: the kept candidates
+        # re-ranked, the traversal's distinct evaluations, the ENC entries,
+        # the query, its rank search and the output
+        scan_rows = int(st_f[:, F.STAT_SCANROWS].sum())
+        kkeep = 64 if L + 8 <= 64 else (128 if L + 8 <= 128 else 256)
+        rerank = int(np.minimum(st_e[:, F.STAT_ENTRY], kkeep).sum())
+        scan_bytes = (4.0 * d + 4.0) * scan_rows
+        search_bytes = 4.0 * d * (rerank + D - NE) + 4.0 * S + per_query
+        scan_flops = 2.0 * d * 16 * scan_rows
+        a_scan, a_search = scan_bytes / t_a / 1e9, search_bytes / t_b / 1e9
+        phases = {"entry_scan": {"kernel": "s_scan_kernel", "ms": t_a * 1e3, "rows": scan_rows,
+                                 "alg_bytes": scan_bytes, "GB_s": a_scan,
+                                 "matrix_TFLOP_s": scan_flops / t_a / 1e12},
+                  "search": {"kernel": "s_search_kernel", "ms": t_b * 1e3, "alg_bytes": search_bytes,
+                             "GB_s": a_search}}
+        if t_a >= t_b:
+            dominant, t_kernel, alg_bytes, achieved = "s_scan_kernel", t_a, scan_bytes, a_scan
+        else:
+            dominant, t_kernel, alg_bytes, achieved = "s_search_kernel", t_b, search_bytes, a_search
+        log(f"entry scan: {scan_rows} tile rows, {scan_bytes / 1e6:.1f} MB, {a_scan:.0f} GB/s, "
+            f"{scan_flops / t_a / 1e12:.1f} TFLOP/s on the matrix cores; search kernel: "
+            f"{search_bytes / 1e6:.1f} MB (re-ranked {rerank}, traversal evaluations {D - NE}, ENC entries {S}), "
+            f"{a_search:.0f} GB/s; dominant {dominant} {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s; "
+            f"forgetful-table evaluations x{overhead:.3f}")
 
-    # HBM traffic of the search kernel from the committed rocprofv3 counters,
-    # if they were taken on this source, workload and setting
+    # HBM traffic of the dominant kernel from the committed rocprofv3
+    # counters, if they were taken on this source, workload and setting
     traffic = None
     sha = source_sha()
     if os.path.exists(TRAFFIC_FILE):
         tf = json.load(open(TRAFFIC_FILE))
         if tf.get("source_sha") == sha and tf.get("n") == n and tf.get("nq") == w.nq:
             for ent in tf.get("settings", []):
-                if ent["setting"] == [L, epn, frac, emax, B] and dominant in ent["kernels"]:
+                if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode) and dominant in ent["kernels"]:
                     kc = ent["kernels"][dominant]
                     traffic = 1024.0 * (kc["fetch_kib"] * tf["fetch_factor"]
                                         + kc["write_kib"] * tf["write_factor"])
@@ -266,7 +317,7 @@ def main():
         sel_t = torch.as_tensor(sel, device=dev)
         Qb, lob, hib = Q[sel_t].contiguous(), lo[sel_t].contiguous(), hi[sel_t].contiguous()
         fb = lambda: F.search(ix, Qb, lob, hib, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                              hash_log2=args.hash_log2, query_base=0)
+                              entry_mode=mode, hash_log2=args.hash_log2, query_base=0)
         idb, _ = fb()
         torch.cuda.synchronize()
         tb = timed(fb, 5)
@@ -284,14 +335,14 @@ def main():
         probe = min(200, w.nq)
         t0 = time.time()
         oracle.search(ox, w.Q[:probe], w.lo[:probe], w.hi[:probe], k, L, epn=epn, epn_frac=frac,
-                      epn_max=emax, B=B, threads=threads)
+                      epn_max=emax, B=B, entry_mode=mode, threads=threads)
         tp = max(time.time() - t0, 1e-3)
         ns = int(min(w.nq, max(probe, probe * args.cpu_seconds / tp)))
         reps = 1
         if ns > probe:
             t0 = time.time()
             oracle.search(ox, w.Q[:ns], w.lo[:ns], w.hi[:ns], k, L, epn=epn, epn_frac=frac,
-                          epn_max=emax, B=B, threads=threads)
+                          epn_max=emax, B=B, entry_mode=mode, threads=threads)
             tp = time.time() - t0
             # the whole batch takes less than the target: repeat it
             reps = max(1, min(100, int(args.cpu_seconds / max(tp, 1e-3))))
@@ -299,7 +350,7 @@ def main():
                 t0 = time.time()
                 for _ in range(reps):
                     oracle.search(ox, w.Q, w.lo, w.hi, k, L, epn=epn, epn_frac=frac, epn_max=emax,
-                                  B=B, threads=threads)
+                                  B=B, entry_mode=mode, threads=threads)
                 tp = (time.time() - t0) / reps
             else:
                 reps = 1
@@ -327,7 +378,7 @@ def main():
             "workload": f"{w.name}: n={n} d={d} Gaussian mixture (1000 centres, noise 0.3), "
                         f"random-permutation attribute, {w.nq} queries, selectivity log-uniform "
                         f"[2^-10,1], k={k}",
-            "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": B,
+            "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": B, "entry_mode": mode,
             "hash_log2": args.hash_log2, "recall@10": chosen["recall"], "recall_target_met": met,
             "index": {"H": H, "m": m, "build_s": round(t_build, 1)},
         },
@@ -335,6 +386,7 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "alg_bytes_per_launch": alg_bytes, "kernel_ms": t_kernel * 1e3,
                      "step_achieved": alg_bytes / per_step / 1e9},
+        "phases": phases,
         "cpu_baseline": cpu,
         "bruteforce": {"ms": bf_time * 1e3, "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,
@@ -345,8 +397,8 @@ def main():
             json.dump(dict(result=result, sweep=rows, per_band=per_band, alg_bytes=alg_bytes, source_sha=sha,
                            eval_overhead=float(overhead),
                            mean_stats_exact=st_e.mean(0).tolist(),
-                           mean_stats_timed=st_f.mean(0).tolist()), f, indent=1)
-    print(json.dumps(result), flush=True)
+                           mean_stats_timed=st_f.mean(0).tolist()), f, indent=1, default=_plain)
+    print(json.dumps(result, default=_plain), flush=True)
 
 
 if __name__ == "__main__":

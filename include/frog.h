@@ -73,10 +73,11 @@ typedef struct {
     int hash_log2;      /* visited table of 2^hash_log2 slots in LDS (6..13): 10;
                            0 selects an exact visited set in device memory (slow;
                            used to count distinct evaluations) */
-    void** phase_events;/* NULL, or 3 caller-created hipEvent_t recorded on `stream`
-                           before the search kernels, between the entry-point
-                           kernels and the traversal kernel (entry_mode 1; the
-                           same as the third otherwise), and after the last */
+    void** phase_events;/* NULL, or 3 caller-created hipEvent_t recorded on `stream`:
+                           entry_mode 0: before and after the search kernel (the
+                           second and third together); entry_mode 1: before the
+                           matrix-core entry scan, between it and the search
+                           kernel, and after the search kernel */
     int entry_mode;     /* how the entry points of Alg. 2 are drawn uniformly from
                            the range: 0 (default) one per stratum, jittered per
                            query; 1 every rank whose priority, a hash of (seed,
@@ -98,7 +99,10 @@ enum {
     FROG_STAT_LSTART = 5,     /* hotspot first layer (Alg. 3) */
     FROG_STAT_LEND = 6,       /* hotspot last layer */
     FROG_STAT_LOADED = 7,     /* ENC entries actually loaded by the kernel */
-    FROG_STAT_N = 8
+    FROG_STAT_SCANROWS = 8,   /* entry_mode 1: rows the shared entry scan read for the
+                                 query's tile of 16, credited to the tile's first query
+                                 (0 for the others and in entry_mode 0) */
+    FROG_STAT_N = 9
 };
 
 /* Fill *p with the paper's defaults for dimension d. */

@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(_PKG, "libfrog.so")
 FROG_OK = 0
 ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "EBADINDEX", -5: "ENOTUPLOADED",
           -6: "EIO", -7: "EUNSUPPORTED"}
-STAT_EXPANSIONS, STAT_EN, STAT_DIST, STAT_SCANNED, STAT_ENTRY, STAT_LSTART, STAT_LEND, STAT_LOADED = range(8)
-STAT_N = 8
+(STAT_EXPANSIONS, STAT_EN, STAT_DIST, STAT_SCANNED, STAT_ENTRY, STAT_LSTART, STAT_LEND, STAT_LOADED,
+ STAT_SCANROWS) = range(9)
+STAT_N = 9
 
 SYMBOLS = (
     "frog_build_params_default", "frog_search_params_default", "frog_build_index",

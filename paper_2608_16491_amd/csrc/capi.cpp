@@ -53,9 +53,11 @@ void release_device(frog_index* ix) {
         hipFree(ix->dattr);
         hipFree(ix->dperm);
         if (ix->dshared) hipFree(ix->dshared);
+        if (ix->dshared_x) hipFree(ix->dshared_x);
         hipSetDevice(prev);
     }
     ix->dshared = nullptr;
+    ix->dshared_x = nullptr;
     ix->shared_valid = false;
     ix->dX = nullptr;
     ix->dENC = nullptr;
@@ -496,13 +498,24 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         if (hipGetDevice(&prev) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
         if (hipSetDevice(ix->device) != hipSuccess) return fail(FROG_EHIP, "hipSetDevice failed");
         if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
+        if (ix->dshared_x) { (void)hipFree(ix->dshared_x); ix->dshared_x = nullptr; }
         ix->shared_valid = false;
+        const int64_t total = off[nlev + 1];
         hipError_t e = hipMalloc(&ix->dshared, ranks.size() * sizeof(int32_t));
         if (e == hipSuccess)
             e = hipMemcpy(ix->dshared, ranks.data(), ranks.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+        // the listed rows of X, so that a scan over a list reads contiguous rows
+        if (e == hipSuccess) e = hipMalloc(&ix->dshared_x, (size_t)std::max<int64_t>(total, 1) * ix->dp * sizeof(float));
+        int rc = FROG_OK;
+        if (e == hipSuccess && total > 0) {
+            rc = launch_gather_rows(ix->dX, ix->dp, ix->dshared, total, ix->dshared_x, nullptr);
+            if (rc == FROG_OK) e = hipDeviceSynchronize();
+        }
         (void)hipSetDevice(prev);
-        if (e != hipSuccess) {
+        if (e != hipSuccess || rc != FROG_OK) {
             if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
+            if (ix->dshared_x) { (void)hipFree(ix->dshared_x); ix->dshared_x = nullptr; }
+            if (rc != FROG_OK) return rc;
             return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "shared sample levels: %s",
                         hipGetErrorString(e));
         }
@@ -512,6 +525,7 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         ix->shared_valid = true;
     }
     out->ranks = ix->dshared;
+    out->xrows = ix->dshared_x;
     std::copy(ix->shared_off, ix->shared_off + 34, out->off);
     out->nlev = ix->shared_nlev;
     out->key = key;

@@ -34,6 +34,7 @@ struct frog_index {
     int shared_nlev = 0;
     int64_t shared_off[34] = {};
     int32_t* dshared = nullptr;
+    float* dshared_x = nullptr;  // the levels' rows of X, in list order, dp floats each
 };
 
 namespace frog {
@@ -61,6 +62,7 @@ struct DevIndex {
 // is ranks[off[j], off[j + 1]) for 1 <= j <= nlev; level 0 is every rank.
 struct SharedLevels {
     const int32_t* ranks;
+    const float* xrows;  // row p of level j's list at xrows + (off[j] + p) * dp
     int64_t off[34];
     int nlev;
     uint64_t key;      // splitmix64(seed): priority(i) = hi32(splitmix64(key ^ i))
@@ -94,6 +96,8 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream);
 int launch_rank_bounds(const DevIndex& ix, const double* lo, const double* hi, int64_t nq,
                        int32_t* lr, void* stream);
 bool search_shape_supported(int dp, int m, int L);
+// copy the rows of the listed ranks: out[i] = X[ranks[i]] (dp floats each)
+int launch_gather_rows(const float* X, int dp, const int32_t* ranks, int64_t count, float* out, void* stream);
 // bruteforce.hip
 int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const double* lo,
                       const double* hi, int k, int32_t* ids, float* dists, int32_t* cert,

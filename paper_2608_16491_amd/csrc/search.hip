@@ -726,10 +726,11 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
             A.dists[qi * k + p] = od;
         }
     }
-    if (A.stats && lane < FROG_STAT_N) {
+    // the traversal's columns; the shared scan's row count is written by the scan
+    if (A.stats && lane < FROG_STAT_SCANROWS) {
         int32_t val = 0;
 #pragma unroll
-        for (int i = 0; i < FROG_STAT_N; ++i)
+        for (int i = 0; i < FROG_STAT_SCANROWS; ++i)
             if (lane == i) val = st[i];
         A.stats[qi * FROG_STAT_N + lane] = val;
     }
@@ -885,6 +886,7 @@ void coop_kernel(KParams P) {
             }
         }
         traverse<C, LP>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
+        if (A.stats && lane == 0) A.stats[qi * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
     }
 }
 
@@ -1056,6 +1058,7 @@ __global__ void s_plan_kernel(SParams P) {
     }
     p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
     P.plan[q] = p;
+    if (P.a.stats) P.a.stats[q * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
 }
 
 // Bucket offsets: level by level, each level's run of places padded to a
@@ -1212,52 +1215,80 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
         qv[e] = T.q[sl] >= 0;
         qall[e] = (T.allmask >> sl) & 1u;
     }
-    uint32_t scount[kSQ];
-#pragma unroll
-    for (int i = 0; i < kSQ; ++i) scount[i] = 0u;
+    uint32_t scnt[4] = {0u, 0u, 0u, 0u};   // sample rows of slot 4kk + e seen by this lane
 
-    const float4* X4 = reinterpret_cast<const float4*>(P.ix.X);
     const int64_t nblk = (c1 - c0 + 15) / 16;
-    // the level's list (level 0: every rank, no list)
+    // the level's list and its rows (level 0: every rank, rows of X)
     const int32_t* lranks = lev == 0 ? nullptr : lv.ranks + lv.off[lev];
+    const float4* X4 = reinterpret_cast<const float4*>(P.ix.X);
+    const float4* R4 = lev == 0 ? X4 : reinterpret_cast<const float4*>(lv.xrows + lv.off[lev] * dp);
+    auto pos_at = [&](int64_t blk) -> int64_t {
+        const int64_t pos = c0 + blk * 16 + ii;
+        return pos < c1 ? pos : c1 - 1;   // in bounds past the end
+    };
     auto rank_at = [&](int64_t blk) -> int32_t {
-        int64_t pos = c0 + blk * 16 + ii;
-        pos = pos < c1 ? pos : c1 - 1;
+        const int64_t pos = pos_at(blk);
         return lranks ? lranks[pos] : (int32_t)pos;
     };
-    auto load_rows = [&](int32_t rk, float4 (&x)[KT > 0 ? KT : 1]) {
+    auto load_rows = [&](int64_t blk, float4 (&x)[KT > 0 ? KT : 1]) {
         if constexpr (KT > 0) {
+            const int64_t pos = pos_at(blk);
 #pragma unroll
-            for (int u = 0; u < KT; ++u) x[u] = X4[(int64_t)rk * dp4 + 4 * u + kk];
+            for (int u = 0; u < KT; ++u) x[u] = R4[pos * dp4 + 4 * u + kk];
         }
     };
-    // one 16-row block: q.x on the matrix cores, then the candidates
+    // list state in registers: entries per slot (uniform) and the threshold
+    // of slot 4kk + e in each lane; LDS holds them only around a cut
+    int fill[kSQ];
+#pragma unroll
+    for (int i = 0; i < kSQ; ++i) fill[i] = 0;
+    float thr_l[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) thr_l[e] = __int_as_float(0x7f800000);
+    // cut every list that the next block (at most 16 entries each) could overflow
+    auto make_room = [&]() {
+        uint32_t over = 0u;
+#pragma unroll
+        for (int i = 0; i < kSQ; ++i) over |= (fill[i] > 2 * kkeep - 16 ? 1u : 0u) << i;
+        if (over == 0u) return;
+        int myfill = 0;
+#pragma unroll
+        for (int i = 0; i < kSQ; ++i) myfill = lane == i ? fill[i] : myfill;
+        if (lane < kSQ) lst[2 * lane] = myfill;
+        list_sync();
+        while (over) {
+            const int sl = __builtin_ctz(over);
+            over &= over - 1u;
+            buf_cut<kkeep>(list_of(sl), false);
+        }
+        const int nf = lane < kSQ ? lst[2 * lane] : 0;
+#pragma unroll
+        for (int i = 0; i < kSQ; ++i) fill[i] = __builtin_amdgcn_readlane(nf, i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) thr_l[e] = __int_as_float(lst[2 * (4 * kk + e) + 1]);
+    };
+    // one 16-row block: q.x on the matrix cores (four independent
+    // accumulation chains), then the candidates
     auto process = [&](const float4 (&x)[KT > 0 ? KT : 1], int32_t rk, int64_t blk) {
         const bool inrun = c0 + blk * 16 + ii < c1;
-        // a block adds at most 16 entries to a list: cut those that could overflow
-        {
-            const int fl = lane < kSQ ? lst[2 * lane] : 0;
-            uint64_t over = __ballot(lane < kSQ && fl > 2 * kkeep - 16);
-            while (over) {
-                const int sl = __builtin_ctzll(over);
-                over &= over - 1;
-                buf_cut<kkeep>(list_of(sl));
-            }
-        }
-        floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+        make_room();
+        floatx4_t acc;
         float xn = 0.f;
         if constexpr (KT > 0) {
+            floatx4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0, a2 = a0, a3 = a0;
 #pragma unroll
             for (int u = 0; u < KT; ++u) {
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].x, x[u].x, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].y, x[u].y, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].z, x[u].z, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].w, x[u].w, acc, 0, 0, 0);
+                a0 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].x, x[u].x, a0, 0, 0, 0);
+                a1 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].y, x[u].y, a1, 0, 0, 0);
+                a2 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].z, x[u].z, a2, 0, 0, 0);
+                a3 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].w, x[u].w, a3, 0, 0, 0);
                 xn += x[u].x * x[u].x + x[u].y * x[u].y + x[u].z * x[u].z + x[u].w * x[u].w;
             }
+            acc = (a0 + a1) + (a2 + a3);
         } else {
+            acc = floatx4_t{0.f, 0.f, 0.f, 0.f};
             for (int u = 0; u < dp / 16; ++u) {
-                const float4 xv = X4[(int64_t)rk * dp4 + 4 * u + kk];
+                const float4 xv = R4[pos_at(blk) * dp4 + 4 * u + kk];
                 const float4 q = qchunk(u);
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.x, xv.x, acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, xv.y, acc, 0, 0, 0);
@@ -1269,46 +1300,72 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
         xn += __shfl_xor(xn, 16);
         xn += __shfl_xor(xn, 32);
         const uint32_t pri = s_priority(P.a.lv.key, rk);
+        const uint64_t below = (1ull << lane) - 1;
         // lane holds D[4kk + e][ii]: query slot 4kk + e, the block's row ii
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const bool insample = inrun && qv[e] && rk >= ql[e] && rk <= qr[e] && (qall[e] || pri < qT[e]);
-            const uint64_t ms = __ballot(insample);
-#pragma unroll
-            for (int g = 0; g < 4; ++g) scount[4 * g + e] += (uint32_t)__popcll(ms & (0xFFFFull << (16 * g)));
-            if (ms == 0) continue;
+            scnt[e] += insample ? 1u : 0u;
             const float ap = qn[e] + xn - 2.f * acc[e];
-            const int sl = 4 * kk + e;
-            if (insample && ap < __int_as_float(lst[2 * sl + 1])) {
-                const int pos = atomicAdd(lst + 2 * sl, 1);
-                lkey[(size_t)sl * 2 * kkeep + pos] = ((uint64_t)ord_bits(ap) << 32) | (uint32_t)rk;
+            const bool cand = insample && ap < thr_l[e];
+            const uint64_t m = __ballot(cand);
+            if (m == 0) continue;
+            int myfill = fill[e];
+#pragma unroll
+            for (int g = 1; g < 4; ++g) myfill = kk == g ? fill[4 * g + e] : myfill;
+            if (cand) {
+                const uint64_t gm = m & (0xFFFFull << (16 * kk));
+                lkey[(size_t)(4 * kk + e) * 2 * kkeep + myfill + __popcll(gm & below)] =
+                    ((uint64_t)ord_bits(ap) << 32) | (uint32_t)rk;
             }
+#pragma unroll
+            for (int g = 0; g < 4; ++g) fill[4 * g + e] += __popcll(m & (0xFFFFull << (16 * g)));
         }
-        list_sync();
     };
     // two row buffers in turn: the loads of block b + 2 are issued as soon
     // as block b is multiplied, ranks two blocks ahead of their rows
-    float4 xa[KT > 0 ? KT : 1], xb[KT > 0 ? KT : 1];
-    int32_t ra = 0, rb = 0, ra2 = 0, rb2 = 0;
-    if (nblk > 0) { ra = rank_at(0); load_rows(ra, xa); }
-    if (nblk > 1) { rb = rank_at(1); load_rows(rb, xb); }
-    if (nblk > 2) ra2 = rank_at(2);
-    if (nblk > 3) rb2 = rank_at(3);
-    for (int64_t blk = 0; blk < nblk; blk += 2) {
-        process(xa, ra, blk);
-        if (blk + 2 < nblk) {
-            ra = ra2;
-            load_rows(ra, xa);
-            if (blk + 4 < nblk) ra2 = rank_at(blk + 4);
-        }
-        if (blk + 1 < nblk) process(xb, rb, blk + 1);
-        if (blk + 3 < nblk) {
-            rb = rb2;
-            load_rows(rb, xb);
-            if (blk + 5 < nblk) rb2 = rank_at(blk + 5);
+    // (positions past the end are clamped to the last one, so the loads are
+    // in bounds and unconditional: a load under a branch would make the
+    // compiler wait for it, and for every load issued before it, at once)
+    if (nblk > 0) {
+        float4 xa[KT > 0 ? KT : 1], xb[KT > 0 ? KT : 1];
+        load_rows(0, xa);
+        int32_t ra = rank_at(0);
+        load_rows(1, xb);
+        int32_t rb = rank_at(1);
+        for (int64_t blk = 0; blk < nblk; blk += 2) {
+            process(xa, ra, blk);
+            load_rows(blk + 2, xa);
+            ra = rank_at(blk + 2);
+            if (blk + 1 < nblk) process(xb, rb, blk + 1);
+            load_rows(blk + 3, xb);
+            rb = rank_at(blk + 3);
         }
     }
     // the item's lists: entries kept, threshold, sample rows seen
+    if (P.a.stats && lane == 0) {
+        int first = 0;
+        while (first < kSQ - 1 && T.q[first] < 0) ++first;
+        atomicAdd(P.a.stats + (int64_t)T.q[first] * FROG_STAT_N + FROG_STAT_SCANROWS, (int32_t)(nblk * 16));
+    }
+    // the lists' states to LDS for the last cuts and the write-out
+    {
+        int myfill = 0;
+#pragma unroll
+        for (int i = 0; i < kSQ; ++i) myfill = lane == i ? fill[i] : myfill;
+        if (lane < kSQ) lst[2 * lane] = myfill;
+        list_sync();
+    }
+    // per-slot sample counts: sum over the 16 lanes of each group
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) scnt[e] += __shfl_xor(scnt[e], o);
+    uint32_t scount[kSQ];
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) scount[4 * g + e] = (uint32_t)__shfl((int)scnt[e], 16 * g);
     const int64_t base = item * kSQ;
 #pragma unroll
     for (int i = 0; i < kSQ; ++i) {
@@ -1612,16 +1669,18 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     P.gvis = reinterpret_cast<uint32_t*>(base + o_gvis);
     hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(a.events);
     const unsigned qb = (unsigned)((a.nq + 255) / 256);
+    // events: before the matrix-core scan, between it and the search kernel,
+    // after the search kernel (the planning kernels come before the first)
     const int64_t ninit = norder > P.nbins ? norder : P.nbins;
     hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.hist,
                        P.nbins, P.order, norder);
     const int64_t rb_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
-    if (ev) (void)hipEventRecord(ev[0], stream);
     hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
     hipLaunchKernelGGL(s_plan_kernel, dim3(qb), dim3(256), 0, stream, P);
     hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(64), 0, stream, P);
     hipLaunchKernelGGL(s_order_kernel, dim3(qb), dim3(256), 0, stream, P);
     hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + 255) / 256)), dim3(256), 0, stream, P);
+    if (ev) (void)hipEventRecord(ev[0], stream);
     hipLaunchKernelGGL(scan, dim3((unsigned)((items + scan_waves - 1) / scan_waves)), dim3(64 * scan_waves), smem_scan,
                        stream, P);
     if (ev) (void)hipEventRecord(ev[1], stream);
@@ -1633,7 +1692,27 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     return FROG_OK;
 }
 
+__global__ void gather_rows_kernel(const float4* __restrict__ X, int dp4, const int32_t* __restrict__ ranks,
+                                   int64_t count, float4* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t row = i / dp4;
+    if (row >= count) return;
+    const int c = (int)(i % dp4);
+    out[i] = X[(int64_t)ranks[row] * dp4 + c];
+}
+
 }  // namespace
+
+int launch_gather_rows(const float* X, int dp, const int32_t* ranks, int64_t count, float* out, void* stream_v) {
+    hipStream_t stream = (hipStream_t)stream_v;
+    const int dp4 = dp / 4;
+    const int64_t total = count * dp4;
+    hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                       reinterpret_cast<const float4*>(X), dp4, ranks, count, reinterpret_cast<float4*>(out));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(FROG_EHIP, "gather rows: %s", hipGetErrorString(e));
+    return FROG_OK;
+}
 
 bool search_shape_supported(int dp, int m, int L) {
     return dp >= 32 && dp % 32 == 0 && m >= 1 && m <= 64 && L >= 1 && L <= 256;

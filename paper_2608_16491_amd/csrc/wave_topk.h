@@ -131,51 +131,102 @@ __device__ __forceinline__ void buf_init(const BufList& B) {
     list_sync();
 }
 
-// Keep the K smallest of the buffer's entries (all of them if there are at
-// most K).  K is 64, 128 or 256.
+// Cut the buffer: with exact = true keep its K smallest entries (all if
+// there are at most K); with exact = false keep every entry at or below some
+// value x with K <= #kept <= 3K/2 (a cheaper search; the exact cut when ties
+// leave no such x).  The new threshold is the smallest value a dropped entry
+// can have.  K is 64, 128 or 256.
 template <int K>
-__device__ __forceinline__ void buf_cut(const BufList& B) {
+__device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
     constexpr int R = 2 * K / 64;   // entries per lane
     const int lane = __lane_id();
     const int f = __builtin_amdgcn_readfirstlane(B.st[0]);
     if (f <= K) return;
     uint64_t k[R];
+    uint32_t vmin = 0xFFFFFFFFu, vmax = 0u;
 #pragma unroll
-    for (int i = 0; i < R; ++i) k[i] = i * 64 + lane < f ? B.key[i * 64 + lane] : ~0ull;
-    // smallest value bits x with #(entries with value <= x) >= K
-    uint32_t lo = 0u, hi = 0xFFFFFFFFu;
+    for (int i = 0; i < R; ++i) {
+        k[i] = i * 64 + lane < f ? B.key[i * 64 + lane] : ~0ull;
+        const uint32_t v = (uint32_t)(k[i] >> 32);
+        if (i * 64 + lane < f) {
+            vmin = v < vmin ? v : vmin;
+            vmax = v > vmax ? v : vmax;
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t a = __shfl_xor(vmin, o), b = __shfl_xor(vmax, o);
+        vmin = a < vmin ? a : vmin;
+        vmax = b > vmax ? b : vmax;
+    }
+    // smallest x in [vmin, vmax] with #(entries <= x) >= K, or (loose) any x
+    // with K <= #(entries <= x) <= 3K/2
+    uint32_t lo = __builtin_amdgcn_readfirstlane(vmin), hi = __builtin_amdgcn_readfirstlane(vmax);
+    int cx = f;
+    bool loose = false;
     while (lo < hi) {
         const uint32_t mid = lo + ((hi - lo) >> 1);
         int c = 0;
 #pragma unroll
         for (int i = 0; i < R; ++i) c += __popcll(__ballot((uint32_t)(k[i] >> 32) <= mid));
-        if (c >= K) hi = mid;
-        else lo = mid + 1;
-    }
-    const uint32_t vk = lo;
-    // entries below vk, then entries equal to vk up to K in all
-    int below = 0;
-#pragma unroll
-    for (int i = 0; i < R; ++i) below += __popcll(__ballot((uint32_t)(k[i] >> 32) < vk));
-    list_sync();
-    int wr = 0, eq = 0;
-#pragma unroll
-    for (int i = 0; i < R; ++i) {
-        const uint32_t v = (uint32_t)(k[i] >> 32);
-        const uint64_t mb = __ballot(v < vk);
-        const uint64_t me = __ballot(v == vk);
-        const uint64_t lt = (1ull << lane) - 1;
-        if (v < vk) B.key[wr + __popcll(mb & lt)] = k[i];
-        if (v == vk) {
-            const int pos = below + eq + __popcll(me & lt);
-            if (pos < K) B.key[pos] = k[i];
+        if (c < K) {
+            lo = mid + 1;
+        } else {
+            hi = mid;
+            cx = c;
+            if (!exact && c <= K + K / 2) {
+                loose = true;
+                break;
+            }
         }
-        wr += __popcll(mb);
-        eq += __popcll(me);
     }
-    if (lane == 0) {
-        B.st[0] = K;
-        B.st[1] = (int32_t)__float_as_uint(ord_value(vk));
+    const uint32_t vk = hi;
+    if (!exact && !loose) {
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < R; ++i) c += __popcll(__ballot((uint32_t)(k[i] >> 32) <= vk));
+        cx = c;
+        loose = c <= K + K / 2;
+    }
+    list_sync();
+    const uint64_t lt = (1ull << lane) - 1;
+    if (loose) {
+        // keep every entry <= vk; a dropped entry is above vk
+        int wr = 0;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const bool keep = (uint32_t)(k[i] >> 32) <= vk;
+            const uint64_t mk = __ballot(keep);
+            if (keep) B.key[wr + __popcll(mk & lt)] = k[i];
+            wr += __popcll(mk);
+        }
+        if (lane == 0) {
+            B.st[0] = cx;
+            B.st[1] = (int32_t)__float_as_uint(ord_value(vk + 1u));
+        }
+    } else {
+        // entries below vk, then entries equal to vk up to K in all
+        int below = 0;
+#pragma unroll
+        for (int i = 0; i < R; ++i) below += __popcll(__ballot((uint32_t)(k[i] >> 32) < vk));
+        int wr = 0, eq = 0;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const uint32_t v = (uint32_t)(k[i] >> 32);
+            const uint64_t mb = __ballot(v < vk);
+            const uint64_t me = __ballot(v == vk);
+            if (v < vk) B.key[wr + __popcll(mb & lt)] = k[i];
+            if (v == vk) {
+                const int pos = below + eq + __popcll(me & lt);
+                if (pos < K) B.key[pos] = k[i];
+            }
+            wr += __popcll(mb);
+            eq += __popcll(me);
+        }
+        if (lane == 0) {
+            B.st[0] = K;
+            B.st[1] = (int32_t)__float_as_uint(ord_value(vk));
+        }
     }
     list_sync();
 }
@@ -188,8 +239,12 @@ __device__ __forceinline__ void buf_offer(const BufList& B, uint64_t gm, float a
     const int lane = __lane_id();
     int f = __builtin_amdgcn_readfirstlane(B.st[0]);
     if (f + __popcll(gm) > 2 * K) {
-        buf_cut<K>(B);
+        buf_cut<K>(B, false);
         f = __builtin_amdgcn_readfirstlane(B.st[0]);
+        if (f + __popcll(gm) > 2 * K) {   // a loose cut can leave 3K/2: make room for 64
+            buf_cut<K>(B, true);
+            f = __builtin_amdgcn_readfirstlane(B.st[0]);
+        }
         const float thr = __int_as_float(__builtin_amdgcn_readfirstlane(B.st[1]));
         gm &= __ballot(a < thr);
     }
