@@ -1,7 +1,8 @@
 """Full-size parity on the benchmark workload (n = 1,000,000, d = 128, 10,000
-mixed-selectivity queries) in the launch configurations bench.py times
-(L = 32, entry points min(cnt, 2560), budget 24, LDS table 2^10, the fastest
-setting reaching recall 0.9, and its neighbours on the frontier).
+mixed-selectivity queries) in the launch configurations bench.py times: the
+fastest settings reaching recall 0.9 of both entry modes (shared sample:
+L = 24, entry points min(cnt, 3072), budget 24; stratified: L = 24, 2560,
+budget 32) and their neighbours on the frontier, LDS table 2^10.
 
 The index is built by the library's host construction, whose equality with
 the oracle's construction is established entry by entry on smaller inputs in
@@ -20,9 +21,12 @@ from tests.parity import assert_parity
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-SETTING = dict(epn=16, epn_frac=1.0, epn_max=2560, budget=24, hash_log2=10)
-FRONTIER = [(32, 2560, 24), (32, 2560, 28), (32, 3072, 16)]   # (L, epn_max, budget)
-L, K = 32, 10
+SETTINGS = {1: dict(epn=16, epn_frac=1.0, epn_max=3072, budget=24, entry_mode=1, hash_log2=10),
+            0: dict(epn=16, epn_frac=1.0, epn_max=2560, budget=32, entry_mode=0, hash_log2=10)}
+# (L, epn_max, budget, entry_mode)
+FRONTIER = [(24, 3072, 24, 1), (24, 2560, 32, 1), (32, 3072, 16, 1), (24, 2560, 32, 0), (32, 2560, 24, 0),
+            (32, 3072, 16, 0)]
+L, K = 24, 10
 
 
 @pytest.fixture(scope="module")
@@ -40,17 +44,17 @@ def c2():
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("Lp,emax,B", FRONTIER)
-def test_full_size_sampled_rows_match_oracle(c2, Lp, emax, B):
+@pytest.mark.parametrize("Lp,emax,B,mode", FRONTIER)
+def test_full_size_sampled_rows_match_oracle(c2, Lp, emax, B, mode):
     w, ix, ox, d = c2
     ids, ds, st = F.search(ix, d["Q"], d["lo"], d["hi"], K, Lp, stats=True, epn=16, epn_frac=1.0,
-                           epn_max=emax, budget=B, hash_log2=10)
+                           epn_max=emax, budget=B, entry_mode=mode, hash_log2=10)
     torch.cuda.synchronize()
     ids, ds, st = ids.cpu().numpy(), ds.cpu().numpy(), st.cpu().numpy()
     rng = np.random.default_rng(0)
     sample = np.sort(rng.choice(w.nq, 400, replace=False))
     o_ids, o_d, o_st = oracle.search(ox, w.Q[sample], w.lo[sample], w.hi[sample], K, Lp, qidx=sample,
-                                     epn=16, epn_frac=1.0, epn_max=emax, B=B)
+                                     epn=16, epn_frac=1.0, epn_max=emax, B=B, entry_mode=mode)
     res = assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
     ok = np.setdiff1d(np.arange(len(sample)), res)
     # the search took the same path: expansions, |EN| sums, ENC entries, hotspot
@@ -62,9 +66,10 @@ def test_full_size_sampled_rows_match_oracle(c2, Lp, emax, B):
 
 
 @pytest.mark.timeout(900)
-def test_full_size_properties_every_row(c2):
+@pytest.mark.parametrize("mode", [1, 0])
+def test_full_size_properties_every_row(c2, mode):
     w, ix, ox, d = c2
-    ids, ds = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTING)
+    ids, ds = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTINGS[mode])
     torch.cuda.synchronize()
     ids, ds = ids.cpu().numpy(), ds.cpu().numpy()
     cnt = (w.hi - w.lo + 1).astype(np.int64)
@@ -84,7 +89,7 @@ def test_full_size_properties_every_row(c2):
     got = ds[qi, kj]
     assert (np.abs(got - ref) <= np.spacing(ref)).all()
     # determinism of the timed launch
-    ids2, ds2 = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTING)
+    ids2, ds2 = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTINGS[mode])
     torch.cuda.synchronize()
     assert (ids2.cpu().numpy() == ids).all()
 
