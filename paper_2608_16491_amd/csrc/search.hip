@@ -58,6 +58,9 @@ typedef float floatx4_t __attribute__((ext_vector_type(4)));
 #ifndef FROG_WAVES_PER_EU
 #define FROG_WAVES_PER_EU 3
 #endif
+#ifndef FROG_SEARCH_WAVES_PER_EU
+#define FROG_SEARCH_WAVES_PER_EU FROG_WAVES_PER_EU
+#endif
 // Entry points per work unit (a chunk of a query's entry phase).
 #ifndef FROG_CHUNK
 #define FROG_CHUNK 768
@@ -1064,16 +1067,32 @@ __global__ void s_plan_kernel(SParams P) {
 // Bucket offsets: level by level, each level's run of places padded to a
 // multiple of 16; inside a level, buckets in order of l.  The empty ranges'
 // bucket comes last.  One thread per level.
-__global__ __launch_bounds__(64) void s_offsets_kernel(SParams P) {
+__global__ __launch_bounds__(1024) void s_offsets_kernel(SParams P) {
+    // thread t owns buckets [8t, 8t + 8); the 32 threads of a half-wave own
+    // one level (256 buckets)
+    constexpr int kPer = kSBins / 32;
     __shared__ uint32_t start[34];
-    const int j = threadIdx.x;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
     const int nlev = P.a.lv.nlev;
-    uint32_t tot = 0;
-    if (j <= nlev)
-        for (int b = 0; b < kSBins; ++b) tot += P.hist[j * kSBins + b];
-    if (j <= nlev) start[j + 1] = (tot + kSQ - 1) / kSQ * kSQ;
+    const int j = t / 32;
+    uint32_t h[kPer];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        h[i] = j <= nlev ? P.hist[t * kPer + i] : 0u;
+        sum += h[i];
+    }
+    // inclusive scan over the 32 threads of the level
+    uint32_t inc = sum;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+        const uint32_t v = __shfl_up(inc, o, 32);
+        if ((lane & 31) >= o) inc += v;
+    }
+    if ((t & 31) == 31 && j <= nlev) start[j + 1] = (inc + kSQ - 1) / kSQ * kSQ;
     __syncthreads();
-    if (j == 0) {
+    if (t == 0) {
         start[0] = 0;
         for (int i = 1; i <= nlev + 1; ++i) start[i] += start[i - 1];
         P.bstart[P.nbins - 1] = start[nlev + 1];
@@ -1082,10 +1101,11 @@ __global__ __launch_bounds__(64) void s_offsets_kernel(SParams P) {
     }
     __syncthreads();
     if (j <= nlev) {
-        uint32_t run = start[j];
-        for (int b = 0; b < kSBins; ++b) {
-            P.bstart[j * kSBins + b] = run;
-            run += P.hist[j * kSBins + b];
+        uint32_t run = start[j] + inc - sum;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            P.bstart[t * kPer + i] = run;
+            run += h[i];
         }
     }
 }
@@ -1097,41 +1117,58 @@ __global__ void s_order_kernel(SParams P) {
     P.order[P.bstart[p.bin] + p.pos] = (int32_t)q;
 }
 
-__global__ void s_tile_kernel(SParams P) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// one wavefront per tile: lanes 0..15 take its slots
+__global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
+    const int lane = lane_id();
+    const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (t >= P.tmax) return;
     const int64_t places = P.meta[0];
-    STile T{};
-    T.nq = 0;
-    int lev = 64;
-    int32_t ul = 0x7FFFFFFF, ur = -1;
-    for (int s = 0; s < kSQ; ++s) {
-        const int64_t i = t * kSQ + s;
-        T.q[s] = -1;
-        T.l[s] = 0;
-        T.r[s] = -1;
-        T.T[s] = 0u;
-        if (i >= places) continue;
-        const int32_t q = P.order[i];
-        if (q < 0) continue;
+    STile* T = P.tiles + t;
+    const int64_t i = t * kSQ + lane;
+    int32_t q = -1;
+    if (lane < kSQ && i < places) q = P.order[i];
+    int32_t l = 0, r = -1, lev = 64, all = 0;
+    uint32_t thr = 0u;
+    if (q >= 0) {
         SPlan& p = P.plan[q];
-        T.q[s] = q;
-        T.l[s] = p.l;
-        T.r[s] = p.r;
-        T.T[s] = p.T;
-        if (p.all) T.allmask |= 1u << s;
-        lev = p.lev < lev ? p.lev : lev;
-        ul = p.l < ul ? p.l : ul;
-        ur = p.r > ur ? p.r : ur;
-        p.tslot = (int32_t)(t * kSQ + s);
-        ++T.nq;
+        l = p.l;
+        r = p.r;
+        thr = p.T;
+        lev = p.lev;
+        all = p.all;
+        p.tslot = (int32_t)(t * kSQ + lane);
     }
-    if (T.nq > 0) {
-        T.lev = lev;
-        T.ua = (int32_t)level_lower(P.a.lv, P.ix.n, lev, ul);
-        T.ub = (int32_t)level_lower(P.a.lv, P.ix.n, lev, (int64_t)ur + 1);
+    if (lane < kSQ) {
+        T->q[lane] = q;
+        T->l[lane] = l;
+        T->r[lane] = r;
+        T->T[lane] = thr;
     }
-    P.tiles[t] = T;
+    const uint64_t valid = __ballot(q >= 0);
+    const uint64_t allm = __ballot(q >= 0 && all);
+    int32_t ul = q >= 0 ? l : 0x7FFFFFFF, ur = q >= 0 ? r : -1, lv = lev;
+#pragma unroll
+    for (int o = 1; o < kSQ; o <<= 1) {
+        ul = min(ul, __shfl_xor(ul, o));
+        ur = max(ur, __shfl_xor(ur, o));
+        lv = min(lv, __shfl_xor(lv, o));
+    }
+    ul = uniform(ul);
+    ur = uniform(ur);
+    lv = uniform(lv);
+    const int nq = __popcll(valid);
+    // lane 0: the union's first position, lane 1: its end
+    int64_t pos = 0;
+    if (nq > 0 && lane < 2) pos = level_lower(P.a.lv, P.ix.n, lv, lane == 0 ? (int64_t)ul : (int64_t)ur + 1);
+    const int32_t ua = __builtin_amdgcn_readlane((int32_t)pos, 0);
+    const int32_t ub = __builtin_amdgcn_readlane((int32_t)pos, 1);
+    if (lane == 0) {
+        T->allmask = (uint32_t)allm;
+        T->lev = nq > 0 ? lv : 0;
+        T->ua = nq > 0 ? ua : 0;
+        T->ub = nq > 0 ? ub : 0;
+        T->nq = nq;
+    }
 }
 
 // per wave: 16 buffers of 2 kkeep keys, |q|^2 of the 16 queries, 16 list states
@@ -1386,7 +1423,7 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
 }
 
 template <int C, int LP, int KK>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_SEARCH_WAVES_PER_EU)))
 void s_search_kernel(SParams P) {
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1431,19 +1468,44 @@ void s_search_kernel(SParams P) {
         const int64_t t = p.tslot / kSQ;
         const int slot = p.tslot % kSQ;
         float texcl = __int_as_float(0x7f800000);   // every row left out is at or above this
+        // the chunks' fill, threshold and sample count in lanes 0..7, then
+        // all their entries at once (no round trip between chunks)
+        int mf = 0, mc = 0;
+        float mt = __int_as_float(0x7f800000);
+        if (lane < kSChunks) {
+            const int64_t base = (t * kSChunks + lane) * kSQ + slot;
+            mf = P.pfill[base];
+            mt = P.pthr[base];
+            mc = P.pcnt[base];
+        }
         int64_t ne = 0;
+#pragma unroll
+        for (int o = 1; o < kSChunks; o <<= 1) {
+            mc += __shfl_xor(mc, o);
+            mt = fminf(mt, __shfl_xor(mt, o));
+        }
+        ne = uniform(mc);
+        texcl = __int_as_float(uniform(__float_as_int(mt)));
+        constexpr int kR = kkeep / 64;   // entries per lane and chunk
+        float av[kSChunks][kR];
+        int32_t rw[kSChunks][kR];
+#pragma unroll
         for (int c = 0; c < kSChunks; ++c) {
+            const int fi = __builtin_amdgcn_readlane(mf, c);
             const int64_t base = (t * kSChunks + c) * kSQ + slot;
-            ne += P.pcnt[base];
-            texcl = fminf(texcl, P.pthr[base]);
-            const int fi = P.pfill[base];
-            for (int j0 = 0; j0 < fi; j0 += 64) {
-                const int j = j0 + lane;
-                const bool have = j < fi;
-                const float av = have ? P.pv[base * kkeep + j] : 0.f;
-                const int32_t rw = have ? P.pr[base * kkeep + j] : -1;
-                const uint64_t gm = ballot(have && av < __int_as_float(Lst.st[1]));
-                if (gm) buf_offer<kkeep>(Lst, gm, av, rw);
+#pragma unroll
+            for (int r = 0; r < kR; ++r) {
+                const int j = r * 64 + lane;
+                av[c][r] = j < fi ? P.pv[base * kkeep + j] : __int_as_float(0x7f800000);
+                rw[c][r] = j < fi ? P.pr[base * kkeep + j] : -1;
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < kSChunks; ++c) {
+#pragma unroll
+            for (int r = 0; r < kR; ++r) {
+                const uint64_t gm = ballot(rw[c][r] >= 0 && av[c][r] < __int_as_float(Lst.st[1]));
+                if (gm) buf_offer<kkeep>(Lst, gm, av[c][r], rw[c][r]);
             }
         }
         buf_cut<kkeep>(Lst);
@@ -1677,9 +1739,10 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     const int64_t rb_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
     hipLaunchKernelGGL(s_plan_kernel, dim3(qb), dim3(256), 0, stream, P);
-    hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(64), 0, stream, P);
+    hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(1024), 0, stream, P);
     hipLaunchKernelGGL(s_order_kernel, dim3(qb), dim3(256), 0, stream, P);
-    hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + 255) / 256)), dim3(256), 0, stream, P);
+    hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + kWavesPerBlock - 1) / kWavesPerBlock)), dim3(kBlock),
+                       0, stream, P);
     if (ev) (void)hipEventRecord(ev[0], stream);
     hipLaunchKernelGGL(scan, dim3((unsigned)((items + scan_waves - 1) / scan_waves)), dim3(64 * scan_waves), smem_scan,
                        stream, P);
