@@ -75,9 +75,9 @@ typedef struct {
                            used to count distinct evaluations) */
     void** phase_events;/* NULL, or 3 caller-created hipEvent_t recorded on `stream`:
                            entry_mode 0: before and after the search kernel (the
-                           second and third together); entry_mode 1: before the
-                           matrix-core entry scan, between it and the search
-                           kernel, and after the search kernel */
+                           second and third together); entry_mode 1: before and
+                           after the matrix-core entry scan, and after the
+                           search kernels (pool and traversal) */
     int entry_mode;     /* how the entry points of Alg. 2 are drawn uniformly from
                            the range: 0 (default) one per stratum, jittered per
                            query; 1 every rank whose priority, a hash of (seed,

@@ -58,8 +58,9 @@ typedef float floatx4_t __attribute__((ext_vector_type(4)));
 #ifndef FROG_WAVES_PER_EU
 #define FROG_WAVES_PER_EU 3
 #endif
+// The shared-sample traversal kernel needs about 100 VGPRs: 5 wavefronts per SIMD.
 #ifndef FROG_SEARCH_WAVES_PER_EU
-#define FROG_SEARCH_WAVES_PER_EU FROG_WAVES_PER_EU
+#define FROG_SEARCH_WAVES_PER_EU 5
 #endif
 // Entry points per work unit (a chunk of a query's entry phase).
 #ifndef FROG_CHUNK
@@ -934,13 +935,15 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
 //                     blocks of q.x on the matrix cores, the approximate
 //                     squared distance |q|^2 + |x|^2 - 2 q.x of each query's
 //                     sample rows, the kkeep smallest per query kept in LDS
-//   s_search_kernel   one wavefront per query (persistent grid): the kkeep
-//                     smallest of its tile's lists, re-ranked with the exact
-//                     canonical distance into the pool (the L nearest entry
-//                     points); a margin test proves that no row left out
-//                     could enter the pool, else the whole sample is
-//                     evaluated exactly; then the traversal, where the
-//                     sample's ranks count as visited by their priority.
+//   s_pool_kernel     one wavefront per query: the kkeep smallest of its
+//                     tile's lists, re-ranked with the exact canonical
+//                     distance into the pool (the L nearest entry points); a
+//                     margin test proves that no row left out could enter the
+//                     pool, else the whole sample is evaluated exactly
+//   s_search_kernel   one wavefront per query (persistent grid, ~100 VGPRs,
+//                     5 wavefronts per SIMD): the traversal from that pool,
+//                     where the sample's ranks count as visited by their
+//                     priority.
 // Bucket order inside a bucket follows atomic arrival, so tiles differ from
 // run to run; results do not, since every pool is the exact L nearest of the
 // sample.
@@ -991,10 +994,13 @@ struct SParams {
     float* pthr;        // [tmax * kSChunks][16] threshold of a full list, else +inf
     int32_t* pfill;     // [tmax * kSChunks][16] entries kept
     int32_t* pcnt;      // [tmax * kSChunks][16] sample rows seen
+    uint64_t* pools;    // [nq][64 LP] the L nearest sample points per query (sorted keys)
+    int32_t* pne;       // [nq] sample size
     uint32_t* gvis;
     int64_t gvis_words;
-    int lds_per_wave;   // s_search_kernel, bytes
-    int lds_list;       // offset of the re-rank list inside a wave's LDS
+    int lds_per_wave;   // s_pool_kernel, bytes
+    int lds_list;       // offset of the re-rank list inside its wave's LDS
+    int lds_search;     // s_search_kernel, bytes per wave
 };
 
 __device__ __forceinline__ int32_t level_rank(const SharedLevels& lv, int j, int64_t pos) {
@@ -1422,40 +1428,26 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
     }
 }
 
+// The pool of each query: one wavefront per query.
 template <int C, int LP, int KK>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_SEARCH_WAVES_PER_EU)))
-void s_search_kernel(SParams P) {
+__global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const DevIndex& ix = P.ix;
     const SearchLaunch& A = P.a;
     const int lane = lane_id();
     const int wave = threadIdx.x >> 6;
-    WaveLds<LP> W(smem, P.lds_per_wave, A.hash_log2);
+    WaveLds<LP> W(smem, P.lds_per_wave, 0);
     char* lbase = smem + (size_t)wave * P.lds_per_wave + P.lds_list;
     constexpr int kkeep = KK;
     const BufList Lst{reinterpret_cast<uint64_t*>(lbase), reinterpret_cast<int32_t*>(lbase + (size_t)2 * kkeep * 8)};
-    Visited vis;
-    vis.tab = W.tab;
-    vis.shift = 32 - A.hash_log2;
-    const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + wave;
-    vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
     const double u_round = 5.9604644775390625e-08;   // 2^-24
 
-    for (;;) {
-        uint32_t qq = 0;
-        if (lane == 0) qq = atomicAdd(P.meta + 2, 1u);
-        const int64_t qi = (int64_t)(uint32_t)uniform((int)__shfl((int)qq, 0));
-        if (qi >= A.nq) break;
+    {
+        const int64_t qi = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+        if (qi >= A.nq) return;   // wave-uniform; no workgroup barrier follows
         const SPlan p = P.plan[qi];
-        if (p.l > p.r) {
-            for (int j = lane; j < A.k; j += 64) {
-                A.ids[qi * A.k + j] = -1;
-                A.dists[qi * A.k + j] = __int_as_float(0x7f800000);
-            }
-            if (A.stats && lane < FROG_STAT_N) A.stats[qi * FROG_STAT_N + lane] = 0;
-            continue;
-        }
+        if (p.l > p.r) return;
         QueryCtx<C> Q;
         Q.load(ix, A, P.lr, qi);
         Q.load_vector(ix);
@@ -1517,11 +1509,31 @@ void s_search_kernel(SParams P) {
 #pragma unroll
         for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
         pool.np = 0;
-        for (int j0 = 0; j0 < f; j0 += 64) {
-            const int nb = f - j0 < 64 ? f - j0 : 64;
-            const int32_t id = lane < nb ? (int32_t)(uint32_t)Lst.key[j0 + lane] : 0;
-            const float dd = Q.eval_batch(ix, nb, id);
-            merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
+        if (f <= 64) {
+            // one key per lane: a bitonic sort over the wavefront, the first L are the pool
+            const int32_t id = lane < f ? (int32_t)(uint32_t)Lst.key[lane] : 0;
+            const float dd = Q.eval_batch(ix, f, id);
+            uint64_t key = lane < f ? make_key(dd, id) : kEmpty;
+#pragma unroll
+            for (int kb = 2; kb <= 64; kb <<= 1) {
+#pragma unroll
+                for (int jb = kb >> 1; jb > 0; jb >>= 1) {
+                    const uint64_t other = (uint64_t)__shfl_xor((long long)key, jb);
+                    const bool up = (lane & kb) == 0;
+                    const bool low = (lane & jb) == 0;
+                    key = (low == up) ? (other < key ? other : key) : (other > key ? other : key);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < LP; ++s) pool.key[s] = (s == 0 && lane < A.L) ? key : kEmpty;
+            pool.np = f < A.L ? f : A.L;
+        } else {
+            for (int j0 = 0; j0 < f; j0 += 64) {
+                const int nb = f - j0 < 64 ? f - j0 : 64;
+                const int32_t id = lane < nb ? (int32_t)(uint32_t)Lst.key[j0 + lane] : 0;
+                const float dd = Q.eval_batch(ix, nb, id);
+                merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
+            }
         }
         // margin test: a row left out has exact distance >= texcl - eps
         bool certified = true;
@@ -1564,10 +1576,61 @@ void s_search_kernel(SParams P) {
                 merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
             }
         }
-        Q.ne = ne;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) P.pools[qi * 64 * LP + s * 64 + lane] = pool.key[s];
+        if (lane == 0) P.pne[qi] = (int32_t)ne;
+    }
+}
+
+// Traversal: persistent, one wavefront per query, from the pool s_pool_kernel wrote.
+template <int C, int LP>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_SEARCH_WAVES_PER_EU)))
+void s_search_kernel(SParams P) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const DevIndex& ix = P.ix;
+    const SearchLaunch& A = P.a;
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    WaveLds<LP> W(smem, P.lds_search, A.hash_log2);
+    Visited vis;
+    vis.tab = W.tab;
+    vis.shift = 32 - A.hash_log2;
+    const int64_t gwave = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+    vis.bits = A.hash_log2 > 0 ? nullptr : P.gvis + gwave * P.gvis_words;
+    for (;;) {
+        uint32_t qq = 0;
+        if (lane == 0) qq = atomicAdd(P.meta + 2, 1u);
+        const int64_t qi = (int64_t)(uint32_t)uniform((int)__shfl((int)qq, 0));
+        if (qi >= A.nq) break;
+        const SPlan p = P.plan[qi];
+        if (p.l > p.r) {
+            for (int j = lane; j < A.k; j += 64) {
+                A.ids[qi * A.k + j] = -1;
+                A.dists[qi * A.k + j] = __int_as_float(0x7f800000);
+            }
+            if (A.stats && lane < FROG_STAT_N) A.stats[qi * FROG_STAT_N + lane] = 0;
+            continue;
+        }
+        QueryCtx<C> Q;
+        Q.load(ix, A, P.lr, qi);
+        Q.load_vector(ix);
+        Q.shared = true;
+        Q.T = p.T;
+        Q.pkey = A.lv.key;
+        Q.ne = P.pne[qi];
+        Pool<LP> pool;
+        int np = 0;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) {
+            pool.key[s] = P.pools[qi * 64 * LP + s * 64 + lane];
+            pool.flag[s] = 0u;
+            np += __popcll(ballot(pool.key[s] != kEmpty));
+        }
+        pool.np = np;
         traverse<C, LP>(ix, A, P.gvis_words, Q, pool, W, vis);
     }
 }
+
 
 // ------------------------------------------------------------------ dispatch
 
@@ -1620,20 +1683,37 @@ int max_blocks(KernelFn fn, int smem) {
 int shared_kkeep(int L) { return L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256); }
 
 template <int C>
-void (*pick_s_lp(int L))(SParams) {
+void (*pick_s_pool_c(int L))(SParams) {
     const int kk = shared_kkeep(L);
-    if (L <= 64) return kk == 64 ? s_search_kernel<C, 1, 64> : s_search_kernel<C, 1, 128>;
-    if (L <= 128) return kk == 128 ? s_search_kernel<C, 2, 128> : s_search_kernel<C, 2, 256>;
-    return s_search_kernel<C, 4, 256>;
+    if (L <= 64) return kk == 64 ? s_pool_kernel<C, 1, 64> : s_pool_kernel<C, 1, 128>;
+    if (L <= 128) return kk == 128 ? s_pool_kernel<C, 2, 128> : s_pool_kernel<C, 2, 256>;
+    return s_pool_kernel<C, 4, 256>;
+}
+
+template <int C>
+void (*pick_s_search_c(int L))(SParams) {
+    if (L <= 64) return s_search_kernel<C, 1>;
+    if (L <= 128) return s_search_kernel<C, 2>;
+    return s_search_kernel<C, 4>;
+}
+
+void (*pick_s_pool(int dp, int L))(SParams) {
+    switch (dp) {
+        case 32: return pick_s_pool_c<1>(L);
+        case 64: return pick_s_pool_c<2>(L);
+        case 96: return pick_s_pool_c<3>(L);
+        case 128: return pick_s_pool_c<4>(L);
+        default: return pick_s_pool_c<0>(L);
+    }
 }
 
 void (*pick_s_search(int dp, int L))(SParams) {
     switch (dp) {
-        case 32: return pick_s_lp<1>(L);
-        case 64: return pick_s_lp<2>(L);
-        case 96: return pick_s_lp<3>(L);
-        case 128: return pick_s_lp<4>(L);
-        default: return pick_s_lp<0>(L);
+        case 32: return pick_s_search_c<1>(L);
+        case 64: return pick_s_search_c<2>(L);
+        case 96: return pick_s_search_c<3>(L);
+        case 128: return pick_s_search_c<4>(L);
+        default: return pick_s_search_c<0>(L);
     }
 }
 
@@ -1658,12 +1738,22 @@ void (*pick_s_scan(int dp, int kkeep))(SParams) {
 int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream) {
     const int kkeep = shared_kkeep(a.L);
     auto sfn = pick_s_search(ix.dp, a.L);
-    const int base_lds = lds_per_wave(a.L, a.hash_log2);
+    auto pfn = pick_s_pool(ix.dp, a.L);
+    // search kernel: pool staging, EN list and visited table per wave
+    const int lps = lds_per_wave(a.L, a.hash_log2);
+    const int smem = lps * kWavesPerBlock;
+    // pool kernel: pool staging and EN list, then the re-rank list
+    const int base_lds = lds_per_wave(a.L, 0);
     const int lpw = base_lds + 2 * kkeep * 8 + 16;
-    const int smem = lpw * kWavesPerBlock;
-    if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);
+    const int smem_pool = lpw * kWavesPerBlock;
+    if (smem > 160 * 1024 || smem_pool > 160 * 1024)
+        return fail(FROG_EUNSUPPORTED, "LDS per block %d / %d too large", smem, smem_pool);
     if (smem > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)sfn, hipFuncAttributeMaxDynamicSharedMemorySize, smem);
+        if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
+    }
+    if (smem_pool > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute((const void*)pfn, hipFuncAttributeMaxDynamicSharedMemorySize, smem_pool);
         if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
     auto scan = pick_s_scan(ix.dp, kkeep);
@@ -1685,6 +1775,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     P.kkeep = kkeep;
     P.lds_per_wave = lpw;
     P.lds_list = base_lds;
+    P.lds_search = lps;
     int blocks = max_blocks((KernelFn)sfn, smem);
     const int64_t need = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     if (need < blocks) blocks = (int)need;
@@ -1704,6 +1795,9 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     const size_t o_pthr = take((size_t)items * kSQ * 4);
     const size_t o_pfill = take((size_t)items * kSQ * 4);
     const size_t o_pcnt = take((size_t)items * kSQ * 4);
+    const int lp = lp_of(a.L);
+    const size_t o_pools = take((size_t)a.nq * 64 * lp * 8);
+    const size_t o_pne = take((size_t)a.nq * 4);
     const size_t o_gvis = off;
     if (a.hash_log2 == 0) {
         P.gvis_words = (ix.n + 31) / 32;
@@ -1728,11 +1822,14 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     P.pthr = reinterpret_cast<float*>(base + o_pthr);
     P.pfill = reinterpret_cast<int32_t*>(base + o_pfill);
     P.pcnt = reinterpret_cast<int32_t*>(base + o_pcnt);
+    P.pools = reinterpret_cast<uint64_t*>(base + o_pools);
+    P.pne = reinterpret_cast<int32_t*>(base + o_pne);
     P.gvis = reinterpret_cast<uint32_t*>(base + o_gvis);
     hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(a.events);
     const unsigned qb = (unsigned)((a.nq + 255) / 256);
-    // events: before the matrix-core scan, between it and the search kernel,
-    // after the search kernel (the planning kernels come before the first)
+    // events: before the matrix-core scan, after it, after the search kernel
+    // (the planning kernels come before the first, the pool kernel after the
+    // second)
     const int64_t ninit = norder > P.nbins ? norder : P.nbins;
     hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.hist,
                        P.nbins, P.order, norder);
@@ -1747,6 +1844,8 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     hipLaunchKernelGGL(scan, dim3((unsigned)((items + scan_waves - 1) / scan_waves)), dim3(64 * scan_waves), smem_scan,
                        stream, P);
     if (ev) (void)hipEventRecord(ev[1], stream);
+    hipLaunchKernelGGL(pfn, dim3((unsigned)((a.nq + kWavesPerBlock - 1) / kWavesPerBlock)), dim3(kBlock), smem_pool,
+                       stream, P);
     hipLaunchKernelGGL(sfn, dim3(blocks), dim3(kBlock), smem, stream, P);
     if (ev) (void)hipEventRecord(ev[2], stream);
     e = hipGetLastError();
