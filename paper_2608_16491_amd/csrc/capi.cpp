@@ -54,10 +54,14 @@ void release_device(frog_index* ix) {
         hipFree(ix->dperm);
         if (ix->dshared) hipFree(ix->dshared);
         if (ix->dshared_x) hipFree(ix->dshared_x);
+        if (ix->dshared_p) hipFree(ix->dshared_p);
+        if (ix->dshared_nrm) hipFree(ix->dshared_nrm);
         hipSetDevice(prev);
     }
     ix->dshared = nullptr;
     ix->dshared_x = nullptr;
+    ix->dshared_p = nullptr;
+    ix->dshared_nrm = nullptr;
     ix->shared_valid = false;
     ix->dX = nullptr;
     ix->dENC = nullptr;
@@ -481,8 +485,10 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         const int nlev = std::max(1, std::min(31, 32 - cl + 1));
         std::vector<uint8_t> depth((size_t)n);
         std::vector<int64_t> cnt((size_t)nlev + 2, 0);
+        std::vector<uint32_t> prio_rank((size_t)n);
         for (int64_t i = 0; i < n; ++i) {
             const uint32_t p = (uint32_t)(mix64(key ^ (uint64_t)i) >> 32);
+            prio_rank[(size_t)i] = p;
             const int z = p == 0 ? 32 : __builtin_clz(p);
             depth[(size_t)i] = (uint8_t)std::min(z, nlev);
             for (int j = 1; j <= depth[(size_t)i]; ++j) ++cnt[(size_t)j];
@@ -494,16 +500,36 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         std::vector<int64_t> fill(off, off + nlev + 2);
         for (int64_t i = 0; i < n; ++i)
             for (int j = 1; j <= depth[(size_t)i]; ++j) ranks[(size_t)fill[(size_t)j]++] = (int32_t)i;
+        // priorities and squared norms, by rank and then in list order
+        const int64_t total = off[nlev + 1];
+        std::vector<uint32_t> prio((size_t)(n + total));
+        std::vector<float> nrm((size_t)(n + total));
+        for (int64_t i = 0; i < n; ++i) {
+            const float* x = ix->X.data() + (size_t)i * ix->d;
+            float sq = 0.f;
+            for (int c = 0; c < ix->d; ++c) sq += x[c] * x[c];
+            prio[(size_t)i] = prio_rank[(size_t)i];
+            nrm[(size_t)i] = sq;
+        }
+        for (int64_t p = 0; p < total; ++p) {
+            prio[(size_t)(n + p)] = prio_rank[(size_t)ranks[(size_t)p]];
+            nrm[(size_t)(n + p)] = nrm[(size_t)ranks[(size_t)p]];
+        }
         int prev = 0;
         if (hipGetDevice(&prev) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
         if (hipSetDevice(ix->device) != hipSuccess) return fail(FROG_EHIP, "hipSetDevice failed");
         if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
         if (ix->dshared_x) { (void)hipFree(ix->dshared_x); ix->dshared_x = nullptr; }
+        if (ix->dshared_p) { (void)hipFree(ix->dshared_p); ix->dshared_p = nullptr; }
+        if (ix->dshared_nrm) { (void)hipFree(ix->dshared_nrm); ix->dshared_nrm = nullptr; }
         ix->shared_valid = false;
-        const int64_t total = off[nlev + 1];
         hipError_t e = hipMalloc(&ix->dshared, ranks.size() * sizeof(int32_t));
         if (e == hipSuccess)
             e = hipMemcpy(ix->dshared, ranks.data(), ranks.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMalloc(&ix->dshared_p, prio.size() * sizeof(uint32_t));
+        if (e == hipSuccess) e = hipMemcpy(ix->dshared_p, prio.data(), prio.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMalloc(&ix->dshared_nrm, nrm.size() * sizeof(float));
+        if (e == hipSuccess) e = hipMemcpy(ix->dshared_nrm, nrm.data(), nrm.size() * sizeof(float), hipMemcpyHostToDevice);
         // the listed rows of X, so that a scan over a list reads contiguous rows
         if (e == hipSuccess) e = hipMalloc(&ix->dshared_x, (size_t)std::max<int64_t>(total, 1) * ix->dp * sizeof(float));
         int rc = FROG_OK;
@@ -515,6 +541,8 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         if (e != hipSuccess || rc != FROG_OK) {
             if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
             if (ix->dshared_x) { (void)hipFree(ix->dshared_x); ix->dshared_x = nullptr; }
+            if (ix->dshared_p) { (void)hipFree(ix->dshared_p); ix->dshared_p = nullptr; }
+            if (ix->dshared_nrm) { (void)hipFree(ix->dshared_nrm); ix->dshared_nrm = nullptr; }
             if (rc != FROG_OK) return rc;
             return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "shared sample levels: %s",
                         hipGetErrorString(e));
@@ -526,6 +554,8 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
     }
     out->ranks = ix->dshared;
     out->xrows = ix->dshared_x;
+    out->prio = ix->dshared_p;
+    out->norm = ix->dshared_nrm;
     std::copy(ix->shared_off, ix->shared_off + 34, out->off);
     out->nlev = ix->shared_nlev;
     out->key = key;

@@ -35,6 +35,8 @@ struct frog_index {
     int64_t shared_off[34] = {};
     int32_t* dshared = nullptr;
     float* dshared_x = nullptr;  // the levels' rows of X, in list order, dp floats each
+    uint32_t* dshared_p = nullptr;  // priorities: rank order [0, n), then the levels' lists
+    float* dshared_nrm = nullptr;   // squared row norms, same layout
 };
 
 namespace frog {
@@ -63,6 +65,8 @@ struct DevIndex {
 struct SharedLevels {
     const int32_t* ranks;
     const float* xrows;  // row p of level j's list at xrows + (off[j] + p) * dp
+    const uint32_t* prio;  // priority of rank i at [i]; of level j's position p at [n + off[j] + p]
+    const float* norm;     // squared norm of the row, same indexing (fp32, any order of summation)
     int64_t off[34];
     int nlev;
     uint64_t key;      // splitmix64(seed): priority(i) = hi32(splitmix64(key ^ i))

@@ -1265,6 +1265,10 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
     const int32_t* lranks = lev == 0 ? nullptr : lv.ranks + lv.off[lev];
     const float4* X4 = reinterpret_cast<const float4*>(P.ix.X);
     const float4* R4 = lev == 0 ? X4 : reinterpret_cast<const float4*>(lv.xrows + lv.off[lev] * dp);
+    // the level's priorities and squared row norms, in list order
+    const int64_t pbase = lev == 0 ? 0 : P.ix.n + lv.off[lev];
+    const uint32_t* lprio = lv.prio + pbase;
+    const float* lnorm = lv.norm + pbase;
     auto pos_at = [&](int64_t blk) -> int64_t {
         const int64_t pos = c0 + blk * 16 + ii;
         return pos < c1 ? pos : c1 - 1;   // in bounds past the end
@@ -1312,11 +1316,10 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
     };
     // one 16-row block: q.x on the matrix cores (four independent
     // accumulation chains), then the candidates
-    auto process = [&](const float4 (&x)[KT > 0 ? KT : 1], int32_t rk, int64_t blk) {
+    auto process = [&](const float4 (&x)[KT > 0 ? KT : 1], int32_t rk, uint32_t pri, float xn, int64_t blk) {
         const bool inrun = c0 + blk * 16 + ii < c1;
         make_room();
         floatx4_t acc;
-        float xn = 0.f;
         if constexpr (KT > 0) {
             floatx4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0, a2 = a0, a3 = a0;
 #pragma unroll
@@ -1325,7 +1328,6 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
                 a1 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].y, x[u].y, a1, 0, 0, 0);
                 a2 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].z, x[u].z, a2, 0, 0, 0);
                 a3 = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[u].w, x[u].w, a3, 0, 0, 0);
-                xn += x[u].x * x[u].x + x[u].y * x[u].y + x[u].z * x[u].z + x[u].w * x[u].w;
             }
             acc = (a0 + a1) + (a2 + a3);
         } else {
@@ -1337,12 +1339,8 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, xv.y, acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.z, xv.z, acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, xv.w, acc, 0, 0, 0);
-                xn += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
             }
         }
-        xn += __shfl_xor(xn, 16);
-        xn += __shfl_xor(xn, 32);
-        const uint32_t pri = s_priority(P.a.lv.key, rk);
         const uint64_t below = (1ull << lane) - 1;
         // lane holds D[4kk + e][ii]: query slot 4kk + e, the block's row ii
 #pragma unroll
@@ -1374,15 +1372,23 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
         float4 xa[KT > 0 ? KT : 1], xb[KT > 0 ? KT : 1];
         load_rows(0, xa);
         int32_t ra = rank_at(0);
+        uint32_t pa = lprio[pos_at(0)];
+        float na = lnorm[pos_at(0)];
         load_rows(1, xb);
         int32_t rb = rank_at(1);
+        uint32_t pb = lprio[pos_at(1)];
+        float nb = lnorm[pos_at(1)];
         for (int64_t blk = 0; blk < nblk; blk += 2) {
-            process(xa, ra, blk);
+            process(xa, ra, pa, na, blk);
             load_rows(blk + 2, xa);
             ra = rank_at(blk + 2);
-            if (blk + 1 < nblk) process(xb, rb, blk + 1);
+            pa = lprio[pos_at(blk + 2)];
+            na = lnorm[pos_at(blk + 2)];
+            if (blk + 1 < nblk) process(xb, rb, pb, nb, blk + 1);
             load_rows(blk + 3, xb);
             rb = rank_at(blk + 3);
+            pb = lprio[pos_at(blk + 3)];
+            nb = lnorm[pos_at(blk + 3)];
         }
     }
     // the item's lists: entries kept, threshold, sample rows seen
