@@ -269,9 +269,9 @@ def main():
             f"whole step {alg_bytes / per_step / 1e9:.0f} GB/s; forgetful-table evaluations x{overhead:.3f}")
     else:
         # entry scan: the rows of every tile's run, once per tile (row data
-        # and, above level 0, its rank); search kernel: the kept candidates
-        # re-ranked, the traversal's distinct evaluations, the ENC entries,
-        # the query, its rank search and the output
+        # and, above level 0, its rank); pool and search kernels: the kept
+        # candidates re-ranked, the traversal's distinct evaluations, the ENC
+        # entries, the query, its rank search and the output
         scan_rows = int(st_f[:, F.STAT_SCANROWS].sum())
         kkeep = 64 if L + 8 <= 64 else (128 if L + 8 <= 128 else 256)
         rerank = int(np.minimum(st_e[:, F.STAT_ENTRY], kkeep).sum())
@@ -282,12 +282,13 @@ def main():
         phases = {"entry_scan": {"kernel": "s_scan_kernel", "ms": t_a * 1e3, "rows": scan_rows,
                                  "alg_bytes": scan_bytes, "GB_s": a_scan,
                                  "matrix_TFLOP_s": scan_flops / t_a / 1e12},
-                  "search": {"kernel": "s_search_kernel", "ms": t_b * 1e3, "alg_bytes": search_bytes,
-                             "GB_s": a_search}}
+                  "search": {"kernel": "s_pool_kernel+s_search_kernel", "ms": t_b * 1e3,
+                             "alg_bytes": search_bytes, "GB_s": a_search}}
         if t_a >= t_b:
             dominant, t_kernel, alg_bytes, achieved = "s_scan_kernel", t_a, scan_bytes, a_scan
         else:
-            dominant, t_kernel, alg_bytes, achieved = "s_search_kernel", t_b, search_bytes, a_search
+            dominant, t_kernel, alg_bytes, achieved = ("s_pool_kernel+s_search_kernel", t_b, search_bytes,
+                                                       a_search)
         log(f"entry scan: {scan_rows} tile rows, {scan_bytes / 1e6:.1f} MB, {a_scan:.0f} GB/s, "
             f"{scan_flops / t_a / 1e12:.1f} TFLOP/s on the matrix cores; search kernel: "
             f"{search_bytes / 1e6:.1f} MB (re-ranked {rerank}, traversal evaluations {D - NE}, ENC entries {S}), "
@@ -302,10 +303,11 @@ def main():
         tf = json.load(open(TRAFFIC_FILE))
         if tf.get("source_sha") == sha and tf.get("n") == n and tf.get("nq") == w.nq:
             for ent in tf.get("settings", []):
-                if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode) and dominant in ent["kernels"]:
-                    kc = ent["kernels"][dominant]
-                    traffic = 1024.0 * (kc["fetch_kib"] * tf["fetch_factor"]
-                                        + kc["write_kib"] * tf["write_factor"])
+                names = dominant.split("+")
+                if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode) and all(
+                        x in ent["kernels"] for x in names):
+                    traffic = sum(1024.0 * (ent["kernels"][x]["fetch_kib"] * tf["fetch_factor"]
+                                            + ent["kernels"][x]["write_kib"] * tf["write_factor"]) for x in names)
 
     # per selectivity band: each octave of the mixed batch re-run as a batch of
     # its own (smaller batches, so lower QPS than the mixed batch)
