@@ -91,7 +91,7 @@ def configure(lib):
     lib.fo_en_ident.argtypes = [P, i32, i32, i64, i64, i64, i32, i32, i32, P, P]
     lib.fo_search_batch.restype = i32
     lib.fo_search_batch.argtypes = [P, P, P, P, i64, i32, i32, i32, P, P, P, i64, P,
-                                    i32, i32, i32, f64, i32, i32, u64, i32, P, P, P, i32]
+                                    i32, i32, i32, f64, i32, i32, u64, i32, i32, i32, P, P, P, i32]
     lib.fo_entry_priority.restype = C.c_uint32
     lib.fo_entry_priority.argtypes = [u64, i64]
     lib.fo_entry_threshold.restype = u64
@@ -269,13 +269,15 @@ def entry_count(cnt: int, epn: int, epn_frac: float = 0.0, epn_max: int = 0) -> 
 
 
 def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, epn_frac: float = 0.0,
-           epn_max: int = 0, B: int = 16, seed: int = 0, entry_mode: int = 0, qidx=None, threads=None,
-           rank_ids: bool = False):
+           epn_max: int = 0, B: int = 16, seed: int = 0, entry_mode: int = 0, hot_mode: int = 0,
+           eager: bool = False, qidx=None, threads=None, rank_ids: bool = False):
     """FROGSearch for every query.  Returns (ids int32 [nq,k] original ids or
     ranks, dists float32 [nq,k], stats int64 [nq,8]).  The entry-point count
     is epn, or clamp(ceil(epn_frac * cnt), epn, epn_max) when epn_frac > 0;
     entry_mode 0 draws them stratified per query, 1 from the shared-priority
-    sample (that count is then the expected size)."""
+    sample (that count is then the expected size).  Ablations (Sec 8.4):
+    hot_mode 1 scans layers L_start..H-1, 2 all layers; eager moves the
+    visited check into ENIdentification."""
     Q = _c(Q, np.float32)
     lo = _c(lo, np.float64)
     hi = _c(hi, np.float64)
@@ -289,7 +291,8 @@ def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, epn_fra
     rc = _load().fo_search_batch(
         _p(ix.X_rank), _p(ENC), _p(ix.attr_sorted), None if rank_ids else _p(ix.perm),
         ix.n, ix.d, ix.H, ix.m, _p(Q), _p(lo), _p(hi), nq,
-        None if qi is None else _p(qi), k, L, epn, epn_frac, epn_max, B, seed, entry_mode, _p(ids), _p(ds), _p(st),
+        None if qi is None else _p(qi), k, L, epn, epn_frac, epn_max, B, seed, entry_mode, hot_mode, int(eager),
+        _p(ids), _p(ds), _p(st),
         threads or default_threads())
     if rc:
         raise MemoryError("oracle search: allocation failed")

@@ -22,7 +22,9 @@
  *                      shared by all queries (second reading, below)
  *   fo_en_ident        ENIdentification (Alg. 4): scan hotspot layers in stored
  *                      order, keep in-range candidates, stop at budget B
- *   fo_search_batch    FROGSearch (Alg. 2) with an exact visited set
+ *   fo_search_batch    FROGSearch (Alg. 2) with an exact visited set, and the
+ *                      ablation variants of Sec 8.4 (hotspot without its end
+ *                      condition or without localisation; eager visited check)
  *   fo_exact_batch     exhaustive filtered k-NN (Def. 2, RFANNS), the ground
  *                      truth the search approximates
  *   fo_build           index construction (Sec 6: leaf brute force, then per
@@ -249,6 +251,10 @@ int fo_en_ident(const int32_t* ENC, int H, int m, int64_t u, int64_t l, int64_t 
 /* Candidate lists                                                           */
 /* ------------------------------------------------------------------------ */
 
+/* forward declarations of the visited set (below) */
+typedef struct fo_visited_s fo_visited;
+static int fo_visited_insert(fo_visited* s, int32_t v);
+
 typedef struct { float dist; int32_t id; int32_t flag; } fo_cand;
 
 static int fo_cand_cmp(const void* pa, const void* pb) {
@@ -263,7 +269,7 @@ static int fo_cand_cmp(const void* pa, const void* pb) {
 
 /* A visited set over 0..n-1: one byte per vertex plus the list of marks, so it
  * can be cleared in time proportional to its content. */
-typedef struct { uint8_t* mark; int32_t* list; int64_t size; } fo_visited;
+struct fo_visited_s { uint8_t* mark; int32_t* list; int64_t size; };
 
 static int fo_visited_init(fo_visited* v, int64_t n) {
     v->mark = (uint8_t*)calloc((size_t)(n > 0 ? n : 1), 1);
@@ -288,6 +294,27 @@ static int fo_visited_insert(fo_visited* s, int32_t v) {
 /* FROGSearch (Alg. 2)                                                       */
 /* ------------------------------------------------------------------------ */
 
+/* ENIdentification with an eager visited check (the ablation of the lazy
+ * check): an in-range candidate already visited is skipped and does not count
+ * against B; an admitted one is marked visited at once. */
+static int fo_en_ident_eager(const int32_t* ENC, int H, int m, int64_t u, int64_t l, int64_t r,
+                             int Ls, int Le, int B, fo_visited* vis, int32_t* EN, int64_t* scanned) {
+    int cnt = 0;
+    for (int h = Ls; h <= Le; ++h) {
+        const int32_t* row = ENC + ((int64_t)u * H + h) * m;
+        *scanned += m;
+        for (int t = 0; t < m; ++t) {
+            int32_t v = row[t];
+            if (v != FO_NONE && v >= l && v <= r && fo_visited_insert(vis, v)) {
+                EN[cnt] = v;
+                cnt = cnt + 1;
+                if (cnt == B) return cnt;
+            }
+        }
+    }
+    return cnt;
+}
+
 /* Per-query statistics written by fo_search_batch (int64 each). */
 enum { FO_ST_EXPANSIONS = 0, FO_ST_EN = 1, FO_ST_DIST = 2, FO_ST_SCANNED = 3,
        FO_ST_ENTRY = 4, FO_ST_LS = 5, FO_ST_LE = 6, FO_ST_N = 8 };
@@ -303,7 +330,7 @@ typedef struct {
 
 static void fo_search_one(const fo_index* ix, const float* q, double lo, double hi,
                           int k, int L, int epn, double epn_frac, int epn_max, int B,
-                          uint64_t seed, int entry_mode, uint64_t qi,
+                          uint64_t seed, int entry_mode, int hot_mode, int eager, uint64_t qi,
                           int32_t* out_ids, float* out_d, int64_t* st,
                           fo_visited* vis, fo_cand* pool, fo_cand* work,
                           int32_t* ep, int32_t* EN) {
@@ -315,6 +342,8 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
 
     int Ls, Le;
     fo_hotspot(l, r, ix->H, ix->n, &Ls, &Le);
+    if (hot_mode == 1) Le = ix->H - 1;                  /* no end condition */
+    if (hot_mode == 2) { Ls = 0; Le = ix->H - 1; }      /* no localisation */
     st[FO_ST_LS] = Ls;
     st[FO_ST_LE] = Le;
 
@@ -346,7 +375,8 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
         int32_t u = pool[i].id;
         st[FO_ST_EXPANSIONS] += 1;
 
-        int nen = fo_en_ident(ix->ENC, ix->H, ix->m, u, l, r, Ls, Le, B, EN, &st[FO_ST_SCANNED]);
+        int nen = eager ? fo_en_ident_eager(ix->ENC, ix->H, ix->m, u, l, r, Ls, Le, B, vis, EN, &st[FO_ST_SCANNED])
+                        : fo_en_ident(ix->ENC, ix->H, ix->m, u, l, r, Ls, Le, B, EN, &st[FO_ST_SCANNED]);
         st[FO_ST_EN] += nen;
 
         /* lazy visited check just before the distance; new candidates */
@@ -354,7 +384,7 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
         for (int t = 0; t < np; ++t) work[t] = pool[t];
         for (int t = 0; t < nen; ++t) {
             int32_t v = EN[t];
-            if (fo_visited_insert(vis, v)) {
+            if (eager || fo_visited_insert(vis, v)) {
                 work[np + nnew].dist = fo_dist(q, ix->X + (int64_t)v * ix->d, ix->d);
                 work[np + nnew].id = v;
                 work[np + nnew].flag = 0;
@@ -378,14 +408,17 @@ static void fo_search_one(const fo_index* ix, const float* q, double lo, double 
 /* Batch driver.  qidx (may be NULL) gives each query's index in its batch,
  * which keys its entry-point jitter (entry_mode 0); NULL means 0..nq-1.
  * entry_mode 0: stratified per-query sample; 1: shared-priority sample.
+ * hot_mode 0: HotspotLocalization (Alg. 3); 1: layers L_start..H-1 (no end
+ * condition); 2: all layers 0..H-1.  eager: visited check inside
+ * ENIdentification instead of after it.
  * Returns 0 or -1 on allocation failure.  stats (may be NULL) is [nq][8]
  * int64. */
 int fo_search_batch(const float* X, const int32_t* ENC, const double* attr_sorted,
                     const int32_t* perm, int64_t n, int d, int H, int m,
                     const float* Q, const double* lo, const double* hi, int64_t nq,
                     const int64_t* qidx, int k, int L, int epn, double epn_frac, int epn_max,
-                    int B, uint64_t seed, int entry_mode, int32_t* out_ids, float* out_d,
-                    int64_t* stats, int nthreads) {
+                    int B, uint64_t seed, int entry_mode, int hot_mode, int eager, int32_t* out_ids,
+                    float* out_d, int64_t* stats, int nthreads) {
     fo_index ix = { X, ENC, attr_sorted, perm, n, d, H, m };
     int fail = 0;
     if (nthreads <= 0) nthreads = 1;
@@ -406,7 +439,7 @@ int fo_search_batch(const float* X, const int32_t* ENC, const double* attr_sorte
             for (int64_t i = 0; i < nq; ++i) {
                 int64_t st_local[FO_ST_N];
                 fo_search_one(&ix, Q + i * d, lo[i], hi[i], k, L, epn, epn_frac, epn_max, B, seed,
-                              entry_mode, (uint64_t)(qidx ? qidx[i] : i),
+                              entry_mode, hot_mode, eager, (uint64_t)(qidx ? qidx[i] : i),
                               out_ids + i * k, out_d + i * k,
                               stats ? stats + i * FO_ST_N : st_local,
                               &vis, pool, work, ep, EN);

@@ -39,13 +39,19 @@ MUTANTS = [
      "return (uint32_t)fo_splitmix64(fo_splitmix64(seed) ^ (uint64_t)i);", ["test_entry_priority_is_splitmix_high_word"]),
     ("shared priority seed unmixed", "return (uint32_t)(fo_splitmix64(fo_splitmix64(seed) ^ (uint64_t)i) >> 32);",
      "return (uint32_t)(fo_splitmix64(seed ^ (uint64_t)i) >> 32);", ["test_entry_points_shared_size_nesting_and_sharing"]),
+    ("eager check does not skip visited",
+     "if (v != FO_NONE && v >= l && v <= r && fo_visited_insert(vis, v)) {",
+     "if (v != FO_NONE && v >= l && v <= r && (fo_visited_insert(vis, v) || 1)) {",
+     [("test_search_ablations_equal_textbook", dict(hot_mode=0, eager=True))]),
+    ("hotspot ablation keeps one layer less", "if (hot_mode == 1) Le = ix->H - 1;", "if (hot_mode == 1) Le = ix->H - 2;",
+     [("test_search_ablations_equal_textbook", dict(hot_mode=1, eager=False))]),
     ("tie order reversed", "if (a->id < b->id) return -1;\n    if (a->id > b->id) return 1;\n    return 0;\n}\n\n/* A visited",
      "if (a->id < b->id) return 1;\n    if (a->id > b->id) return -1;\n    return 0;\n}\n\n/* A visited",
      ["test_exact_breaks_distance_ties_by_rank"]),
     ("pool truncation", "np = np + nnew < L ? np + nnew : L;", "np = np + nnew < L ? np + nnew : L - 1;",
      ["test_search_full_range_equals_textbook_greedy"]),
-    ("visited check skipped", "            if (fo_visited_insert(vis, v)) {\n                work[np + nnew].dist = fo_dist(q,",
-     "            if (fo_visited_insert(vis, v) || 1) {\n                work[np + nnew].dist = fo_dist(q,",
+    ("visited check skipped", "            if (eager || fo_visited_insert(vis, v)) {\n                work[np + nnew].dist = fo_dist(q,",
+     "            if (eager || fo_visited_insert(vis, v) || 1) {\n                work[np + nnew].dist = fo_dist(q,",
      ["test_search_invariants_tiny_workload"]),
     ("fusion weight", "double w = 1.0 - beta * (1.0 - pow(da, gamma));", "double w = 1.0 - beta * pow(da, gamma);",
      ["test_fusion_special_values"]),
@@ -70,8 +76,10 @@ def test_pins_catch_planted_mistake(name, old, new, tests, tmp_path, monkeypatch
     mutant = oracle.configure(C.CDLL(str(so_path)))
     monkeypatch.setattr(oracle, "_lib", mutant)
     for tname in tests:
-        fn = getattr(pins, tname)
         kwargs = {}
+        if isinstance(tname, tuple):
+            tname, kwargs = tname[0], dict(tname[1])
+        fn = getattr(pins, tname)
         if "tiny_index" in fn.__code__.co_varnames[:fn.__code__.co_argcount]:
             import workloads
             w = workloads.make("tiny", n=3000, nq=200)

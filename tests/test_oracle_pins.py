@@ -646,3 +646,68 @@ def test_search_shared_small_range_is_exact(tiny_index):
     ids, ds, _ = oracle.search(ix, w.Q[:nq], lo, hi, 10, 32, epn=64, entry_mode=1, rank_ids=True)
     gi, gd = oracle.exact(ix.X_rank, ix.attr_sorted, None, w.Q[:nq], lo, hi, 10, rank_ids=True)
     assert (ids == gi).all() and (ds == gd).all()
+
+
+# ------------------------------------------------------------------ ablations (Sec 8.4)
+
+def _textbook_frog(ix, q, l, r, layers, B, entries, L, eager):
+    """Alg. 2 written independently for the ablations: EN(u) = the in-range
+    entries of u's rows over `layers` in stored order, at most B of them --
+    counted before the visited check (lazy) or skipping visited ones (eager)."""
+    qd = q.astype(np.float64)
+    dist = lambda v: np.float32(((ix.X_rank[v].astype(np.float64) - qd) ** 2).sum())
+    computed = set()
+    pool = []
+    for e in entries:
+        if e not in computed:
+            computed.add(e)
+            pool.append((dist(e), e))
+    pool = sorted(pool)[:L]
+    expanded = set()
+    while True:
+        nxt = [p for p in pool if p[1] not in expanded]
+        if not nxt:
+            break
+        u = nxt[0][1]
+        expanded.add(u)
+        en = []
+        for h in layers:
+            for v in ix.ENC[u, h].tolist():
+                if v == -1 or not (l <= v <= r):
+                    continue
+                if eager:
+                    if v in computed:
+                        continue
+                    computed.add(v)
+                en.append(v)
+                if len(en) == B:
+                    break
+            if len(en) == B:
+                break
+        for v in en:
+            if eager:
+                pool.append((dist(v), v))
+            elif v not in computed:
+                computed.add(v)
+                pool.append((dist(v), v))
+        pool = sorted(pool)[:L]
+    return [p[1] for p in pool]
+
+
+@pytest.mark.parametrize("hot_mode,eager", [(0, False), (1, False), (2, False), (0, True), (2, True)])
+def test_search_ablations_equal_textbook(tiny_index, hot_mode, eager):
+    w, ix = tiny_index
+    n, H = ix.n, ix.H
+    rng = np.random.default_rng(13)
+    for i in range(10):
+        cnt = int(rng.integers(60, n // 2))
+        l = int(rng.integers(0, n - cnt))
+        r = l + cnt - 1
+        Ls, Le = oracle.hotspot(l, r, H, n)
+        layers = {0: range(Ls, Le + 1), 1: range(Ls, H), 2: range(0, H)}[hot_mode]
+        ep = oracle.entry_points(l, r, 16, 0, i)
+        ref = _textbook_frog(ix, w.Q[i], l, r, list(layers), 8, ep.tolist(), 24, eager)
+        ids, _, st = oracle.search(ix, w.Q[i][None], [float(l)], [float(r)], 24, 24, B=8, qidx=[i],
+                                   hot_mode=hot_mode, eager=eager, rank_ids=True)
+        assert ids[0][:len(ref)].tolist() == ref, (hot_mode, eager, i)
+        assert (st[0, oracle.STAT_LS], st[0, oracle.STAT_LE]) == (min(layers), max(layers))
