@@ -87,6 +87,13 @@ typedef struct {
                            cores in tiles of 16 queries.  Mode 1 builds and
                            uploads the seed's rank lists on its first call
                            (synchronously; about n int32 of device memory) */
+    int hotspot_mode;   /* ablation of HotspotLocalization (Sec 8.4): 0 (default)
+                           layers L_start..L_end of Alg. 3; 1 layers
+                           L_start..H-1 (no end condition); 2 all layers */
+    int eager_check;    /* ablation of the lazy visited check: 1 checks (and
+                           marks) visited candidates inside ENIdentification,
+                           so visited ones do not count against the budget;
+                           needs the exact visited set (hash_log2 = 0) */
 } frog_search_params_t;
 
 /* Per-query statistics written by frog_search_ex (int32, FROG_STAT_N per query). */

@@ -46,7 +46,8 @@ class BuildParams(C.Structure):
 class SearchParams(C.Structure):
     _fields_ = [("epn", C.c_int), ("epn_frac", C.c_double), ("epn_max", C.c_int), ("budget", C.c_int),
                 ("seed", C.c_uint64), ("query_base", C.c_int64), ("hash_log2", C.c_int),
-                ("phase_events", C.c_void_p), ("entry_mode", C.c_int)]
+                ("phase_events", C.c_void_p), ("entry_mode", C.c_int), ("hotspot_mode", C.c_int),
+                ("eager_check", C.c_int)]
 
 
 _lib = None
@@ -233,7 +234,7 @@ def search(index: Index, Q, lo, hi, k: int, L: int, *, stats: bool = False, stre
     the index's device.  Returns (ids int32 [nq, k], dists float32 [nq, k]) and,
     with stats=True, the per-query statistics int32 [nq, 8].  Keyword params:
     epn, epn_frac, epn_max, budget, seed, query_base, hash_log2, entry_mode,
-    and events (three torch.cuda.Event recorded before the search kernels,
+    hotspot_mode, eager_check, and events (three torch.cuda.Event recorded before the search kernels,
     after the entry-point kernels and after the last kernel)."""
     import torch
     nq = Q.shape[0]

@@ -157,6 +157,8 @@ void frog_search_params_default(frog_search_params_t* p) {
     p->hash_log2 = 10;
     p->phase_events = nullptr;
     p->entry_mode = 0;
+    p->hotspot_mode = 0;
+    p->eager_check = 0;
 }
 
 int frog_build_index(const float* X, const double* attr, int64_t n, int d,
@@ -408,6 +410,10 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
         return fail(FROG_EINVAL, "hash_log2=%d: 0 or 6..13", q.hash_log2);
     if (q.query_base < 0) return fail(FROG_EINVAL, "query_base < 0");
     if (q.entry_mode != 0 && q.entry_mode != 1) return fail(FROG_EINVAL, "entry_mode=%d: 0 or 1", q.entry_mode);
+    if (q.hotspot_mode < 0 || q.hotspot_mode > 2) return fail(FROG_EINVAL, "hotspot_mode=%d: 0, 1 or 2", q.hotspot_mode);
+    if (q.eager_check != 0 && q.eager_check != 1) return fail(FROG_EINVAL, "eager_check=%d: 0 or 1", q.eager_check);
+    if (q.eager_check && q.hash_log2 != 0)
+        return fail(FROG_EINVAL, "eager_check needs the exact visited set (hash_log2 = 0)");
     if (!frog::search_shape_supported(ix->dp, ix->m, L))
         return fail(FROG_EUNSUPPORTED, "no search kernel for padded d=%d, m=%d, L=%d", ix->dp, ix->m, L);
     if (nq == 0) return FROG_OK;
@@ -418,6 +424,8 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
     a.B = q.budget; a.hash_log2 = q.hash_log2; a.seed = q.seed; a.qbase = q.query_base;
     a.ids = d_ids; a.dists = d_dists; a.stats = d_stats; a.events = q.phase_events;
     a.entry_mode = q.entry_mode;
+    a.hotspot_mode = q.hotspot_mode;
+    a.eager = q.eager_check;
     if (q.entry_mode == 1) {
         frog_index* mix = const_cast<frog_index*>(ix);
         a.maxnorm = frog::index_maxnorm(mix);

@@ -86,6 +86,8 @@ struct SearchLaunch {
     int32_t* stats;
     void** events;   // NULL or 3 hipEvent_t
     int entry_mode;  // 0 stratified per query, 1 shared sample
+    int hotspot_mode;  // 0 Alg. 3, 1 no end condition, 2 all layers
+    int eager;         // visited check inside ENIdentification (exact set only)
     SharedLevels lv; // entry_mode 1
     float maxnorm;   // entry_mode 1: largest squared row norm of the index
 };

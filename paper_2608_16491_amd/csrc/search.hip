@@ -448,6 +448,11 @@ struct Visited {
         const uint32_t bit = 1u << (v & 31);
         return (atomicOr(bits + (v >> 5), bit) & bit) == 0;
     }
+    // membership without inserting (exact set)
+    __device__ __forceinline__ bool contains(int32_t v) const {
+        if (tab) return tab[slot(v)] == v;
+        return (atomicOr(bits + (v >> 5), 0u) >> (v & 31)) & 1u;
+    }
     __device__ __forceinline__ void insert(int32_t v) const {
         if (tab) tab[slot(v)] = v;
         else atomicOr(bits + (v >> 5), 1u << (v & 31));
@@ -593,6 +598,8 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
     hotspot(l, r, H, ix.n, Ls, Le);
     Ls = uniform(Ls);
     Le = uniform(Le);
+    if (A.hotspot_mode == 1) Le = H - 1;                   // ablation: no end condition
+    if (A.hotspot_mode == 2) { Ls = 0; Le = H - 1; }       // ablation: no localisation
     st[FROG_STAT_LSTART] = Ls;
     st[FROG_STAT_LEND] = Le;
 
@@ -673,12 +680,25 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         for (int64_t off = 0; off < nent && nen < B; off += 64) {
             const int64_t e = off + lane;
             const int32_t v = (off == 0 && hit) ? cur_pre : (e < nent ? row[e] : -1);
-            const bool pred = v >= l && v <= r;
+            bool pred = v >= l && v <= r;
+            if (A.eager) {
+                // ablation: visited candidates are skipped here and do not
+                // count against the budget; a repeat of an earlier lane's
+                // candidate in this load is visited by then (exact set only)
+                pred = pred && !Q.is_entry(v) && !vis.contains(v);
+                for (uint64_t mm = ballot(pred); mm; mm &= mm - 1) {
+                    const int j = __builtin_ctzll(mm);
+                    if (lane > j && v == __builtin_amdgcn_readlane(v, j)) pred = false;
+                }
+            }
             const uint64_t pm = ballot(pred);
             const int rk = mbcnt(pm);
             const int tot = __popcll(pm);
             const int admit = tot < B - nen ? tot : B - nen;
-            if (pred && rk < admit) enbuf[nen + rk] = v;
+            if (pred && rk < admit) {
+                enbuf[nen + rk] = v;
+                if (A.eager) vis.insert(v);
+            }
             if (!(off == 0 && hit)) st[FROG_STAT_LOADED] += (int32_t)(nent - off < 64 ? nent - off : 64);
             if (admit == B - nen && admit > 0) {
                 // budget reached: Alg. 4 examined every layer up to the
@@ -696,7 +716,7 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         // a7: lazy visited check on the compacted list
         int32_t v = lane < nen ? enbuf[lane] : -1;
         bool fresh = false;
-        if (lane < nen) fresh = !Q.is_entry(v) && vis.check_insert(v);
+        if (lane < nen) fresh = A.eager || (!Q.is_entry(v) && vis.check_insert(v));
         const uint64_t fm = ballot(fresh);
         const int ns = __popcll(fm);
         wave_sync();

@@ -36,6 +36,8 @@ def test_param_defaults_follow_the_paper():
     assert (p.m, p.ef_c, p.n_inv) == (32, 256, 6)
     s = F.search_params()
     assert (s.epn, s.budget, s.epn_frac) == (16, 16, 0.0)
+    # the struct's tail fields as the library fills them (layout check)
+    assert (s.hash_log2, s.entry_mode, s.hotspot_mode, s.eager_check) == (10, 0, 0, 0)
 
 
 def _small_index(n=400, d=8):

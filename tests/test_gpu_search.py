@@ -34,7 +34,8 @@ class Case:
 
     def cpu(self, k, L, **p):
         kw = dict(epn=p.get("epn", 16), epn_frac=p.get("epn_frac", 0.0), epn_max=p.get("epn_max", 0),
-                  B=p.get("budget", 16), seed=p.get("seed", 0), entry_mode=p.get("entry_mode", 0))
+                  B=p.get("budget", 16), seed=p.get("seed", 0), entry_mode=p.get("entry_mode", 0),
+                  hot_mode=p.get("hotspot_mode", 0), eager=bool(p.get("eager_check", 0)))
         qidx = np.arange(self.Q.shape[0]) + p.get("query_base", 0)
         return oracle.search(self.ox, self.Q, self.lo, self.hi, k, L, qidx=qidx, **kw)
 
@@ -175,3 +176,29 @@ def test_other_dimensions(d):
     g_ids, g_d = c.gpu(10, 64)
     o_ids, o_d, _ = c.cpu(10, 64)
     assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+@pytest.mark.parametrize("entry_mode", [0, 1])
+@pytest.mark.parametrize("hotspot_mode,eager", [(1, 0), (2, 0), (0, 1), (2, 1)])
+def test_ablation_switches_match_oracle(tiny, entry_mode, hotspot_mode, eager):
+    # Sec 8.4 ablations: hotspot without end condition / without localisation,
+    # eager visited check (exact visited set); every statistic as the oracle's
+    p = dict(entry_mode=entry_mode, epn=16, epn_frac=0.2, epn_max=600, hotspot_mode=hotspot_mode,
+             eager_check=eager, hash_log2=0)
+    g_ids, g_d, g_st = tiny.gpu(10, 64, stats=True, **p)
+    o_ids, o_d, o_st = tiny.cpu(10, 64, **p)
+    res = assert_parity(g_ids, g_d, o_ids, o_d)
+    ok = np.setdiff1d(np.arange(len(g_ids)), res)
+    cols = [(F.STAT_EXPANSIONS, oracle.STAT_EXPANSIONS), (F.STAT_EN, oracle.STAT_EN),
+            (F.STAT_DIST, oracle.STAT_DIST), (F.STAT_SCANNED, oracle.STAT_SCANNED),
+            (F.STAT_ENTRY, oracle.STAT_ENTRY), (F.STAT_LSTART, oracle.STAT_LS), (F.STAT_LEND, oracle.STAT_LE)]
+    for gc, oc in cols:
+        assert (g_st[ok, gc] == o_st[ok, oc]).all(), (gc, g_st[ok, gc][:8], o_st[ok, oc][:8])
+
+
+def test_ablation_hotspot_modes_forgetful_table(tiny):
+    # the hotspot ablations also hold with the forgetful LDS table
+    for hm in (1, 2):
+        g_ids, g_d = tiny.gpu(10, 64, hotspot_mode=hm)
+        o_ids, o_d, _ = tiny.cpu(10, 64, hotspot_mode=hm)
+        assert_parity(g_ids, g_d, o_ids, o_d)
