@@ -104,6 +104,10 @@ def main():
                          "for rocprofv3 counters")
     ap.add_argument("--details", default=None, help="write sweep details (JSON) here")
     ap.add_argument("--index-cache", default=None, help="load the index from / save it to this file")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also measure the ablations of Sec 8.4 at the chosen setting: hotspot without its end "
+                         "condition / without localisation, eager visited check, and (rebuilding the index) "
+                         "beta = 0; reported under 'ablation' in --details")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -327,6 +331,42 @@ def main():
                              recall_in_mixed_batch=chosen["recall_band"][b]))
     log("per band (own batch): " + ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M" for r in per_band))
 
+    # ablations (Sec 8.4) at the chosen setting
+    ablation = None
+    if args.ablation:
+        ablation = []
+
+        def abl(name, hm=0, eager=0, hl2=args.hash_log2, index=ix):
+            f = lambda: F.search(index, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
+                                 entry_mode=mode, hash_log2=hl2, hotspot_mode=hm, eager_check=eager)
+            ids_a, _ = f()
+            torch.cuda.synchronize()
+            rec_a = recall_at_k(ids_a.cpu().numpy(), gt_ids)
+            ta = timed(f, 5)
+            _, _, st_a = F.search(index, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
+                                  entry_mode=mode, hash_log2=0, hotspot_mode=hm, eager_check=eager, stats=True)
+            st_a = st_a.cpu().numpy().astype(np.int64)
+            row = dict(variant=name, hash_log2=hl2, recall=float(rec_a.mean()), qps=w.nq / ta, ms=ta * 1e3,
+                       expansions=float(st_a[:, F.STAT_EXPANSIONS].mean()),
+                       evaluations=float(st_a[:, F.STAT_DIST].mean()),
+                       enc_entries=float(st_a[:, F.STAT_SCANNED].mean()))
+            ablation.append(row)
+            log(f"ablation {name:32s} recall={row['recall']:.4f} {row['ms']:7.3f} ms {row['qps']:10.0f} QPS "
+                f"expansions={row['expansions']:.1f} evaluations={row['evaluations']:.0f} "
+                f"ENC entries={row['enc_entries']:.0f}")
+
+        abl("FROG (hotspot, lazy check)")
+        abl("no hotspot end condition", hm=1)
+        abl("no hotspot localisation", hm=2)
+        abl("lazy check, exact visited set", hl2=0)
+        abl("eager check, exact visited set", eager=1, hl2=0)
+        t0 = time.time()
+        ix0 = F.Index.build(w.X, w.attr, beta=0.0)
+        ix0.upload(0)
+        log(f"beta = 0 index built in {time.time() - t0:.1f}s")
+        abl("beta = 0 (no attribute fusion)", index=ix0)
+        ix0.free()
+
     # CPU oracle on a bounded sample (same index arrays, same parameters)
     cpu = None
     try:
@@ -396,7 +436,8 @@ def main():
     }
     if args.details:
         with open(args.details, "w") as f:
-            json.dump(dict(result=result, sweep=rows, per_band=per_band, alg_bytes=alg_bytes, source_sha=sha,
+            json.dump(dict(result=result, sweep=rows, per_band=per_band, ablation=ablation, alg_bytes=alg_bytes,
+                           source_sha=sha,
                            eval_overhead=float(overhead),
                            mean_stats_exact=st_e.mean(0).tolist(),
                            mean_stats_timed=st_f.mean(0).tolist()), f, indent=1, default=_plain)
