@@ -108,6 +108,11 @@ def main():
                     help="also measure the ablations of Sec 8.4 at the chosen setting: hotspot without its end "
                          "condition / without localisation, eager visited check, and (rebuilding the index) "
                          "beta = 0; reported under 'ablation' in --details")
+    ap.add_argument("--no-fp16", action="store_true",
+                    help="skip the secondary measurement with the rows stored in fp16")
+    ap.add_argument("--storage", default="fp32", choices=("fp32", "fp16"),
+                    help="row storage of the sweep and the timed steps (the ground truth always uses fp32 "
+                         "rows); fp16 is for profiling that path, the metric is quoted on fp32")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -169,11 +174,14 @@ def main():
 
     if args.profile_pass:
         settings = [parse_setting(t) for t in args.setting.split(";")]
+        if args.storage == "fp16":
+            ix.upload(0, storage="fp16")
         for (L, epn, frac, emax, B, mode) in settings:
             run(L, epn, frac, emax, B, mode)
             torch.cuda.synchronize()
-        F.bruteforce(ix, Q, lo, hi, k)
-        torch.cuda.synchronize()
+        if args.storage == "fp32":
+            F.bruteforce(ix, Q, lo, hi, k)
+            torch.cuda.synchronize()
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
         b = torch.empty_like(a)
         b.copy_(a)
@@ -190,6 +198,10 @@ def main():
     bf_time = timed(lambda: F.bruteforce(ix, Q, lo, hi, k), 1)
     gt_ids = gt_ids.cpu().numpy()
     cert = cert.cpu().numpy()
+    # bytes per stored value of the searched rows
+    eb = 2 if args.storage == "fp16" else 4
+    if args.storage == "fp16":
+        ix.upload(0, storage="fp16")
     cnt = (w.hi - w.lo + 1).astype(np.int64)
     bf_flops = 2.0 * d * float(cnt.sum())
     log(f"ground truth: {t_gt:.2f}s first call, {bf_time * 1e3:.1f} ms timed, certified "
@@ -265,7 +277,7 @@ def main():
         # one kernel reads every distinct evaluated vector (entry points and
         # traversal), the ENC entries Alg. 4 examines, the query, its rank
         # search, and writes the output through the id map
-        alg_bytes = 4.0 * d * D + 4.0 * S + per_query
+        alg_bytes = eb * d * D + 4.0 * S + per_query
         dominant, t_kernel = "coop_kernel", t_a
         achieved = alg_bytes / t_kernel / 1e9
         log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, entry points {NE}, "
@@ -279,8 +291,8 @@ def main():
         scan_rows = int(st_f[:, F.STAT_SCANROWS].sum())
         kkeep = 64 if L + 8 <= 64 else (128 if L + 8 <= 128 else 256)
         rerank = int(np.minimum(st_e[:, F.STAT_ENTRY], kkeep).sum())
-        scan_bytes = (4.0 * d + 4.0) * scan_rows
-        search_bytes = 4.0 * d * (rerank + D - NE) + 4.0 * S + per_query
+        scan_bytes = (eb * d + 4.0) * scan_rows
+        search_bytes = eb * d * (rerank + D - NE) + 4.0 * S + per_query
         scan_flops = 2.0 * d * 16 * scan_rows
         a_scan, a_search = scan_bytes / t_a / 1e9, search_bytes / t_b / 1e9
         phases = {"entry_scan": {"kernel": "s_scan_kernel", "ms": t_a * 1e3, "rows": scan_rows,
@@ -305,7 +317,8 @@ def main():
     sha = source_sha()
     if os.path.exists(TRAFFIC_FILE):
         tf = json.load(open(TRAFFIC_FILE))
-        if tf.get("source_sha") == sha and tf.get("n") == n and tf.get("nq") == w.nq:
+        if (tf.get("source_sha") == sha and tf.get("n") == n and tf.get("nq") == w.nq
+                and tf.get("storage", "fp32") == args.storage):
             for ent in tf.get("settings", []):
                 names = dominant.split("+")
                 if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode) and all(
@@ -330,6 +343,51 @@ def main():
         per_band.append(dict(band=f"[2^-{b + 1}, 2^-{b}]", nq=int(len(sel)), qps=len(sel) / tb, ms=tb * 1e3,
                              recall_in_mixed_batch=chosen["recall_band"][b]))
     log("per band (own batch): " + ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M" for r in per_band))
+
+    # fp16 rows (the paper keeps the vectors in half precision, Sec 8.1): the
+    # same host index uploaded with its rows rounded to binary16, the sweep's
+    # shared-sample settings, recall against the fp32 ground truth
+    fp16 = None
+    if not args.no_fp16 and args.storage == "fp32":
+        ix.upload(0, storage="fp16")
+        hrows = []
+        for (Lh, eh, fh, mh, Bh, modeh) in [norm_setting(x) for x in SWEEP]:
+            if modeh != 1 or Lh < k:
+                continue
+            fh_run = lambda: F.search(ix, Q, lo, hi, k, Lh, epn=eh, epn_frac=fh, epn_max=mh, budget=Bh,
+                                      entry_mode=1, hash_log2=args.hash_log2)
+            ids_h, _ = fh_run()
+            torch.cuda.synchronize()
+            rec_h = recall_at_k(ids_h.cpu().numpy(), gt_ids)
+            fh_run()
+            th = timed(fh_run, 5)
+            hrows.append(dict(L=Lh, epn=eh, epn_frac=fh, epn_max=mh, budget=Bh, entry_mode=1,
+                              recall=float(rec_h.mean()), qps=w.nq / th, ms=th * 1e3))
+            log(f"fp16 rows: L={Lh:4d} max={mh:5d} B={Bh:2d}  recall={rec_h.mean():.4f}  {th * 1e3:8.3f} ms  "
+                f"{w.nq / th:12.0f} QPS")
+        okh = [r for r in hrows if r["recall"] >= 0.9]
+        best = max(okh, key=lambda r: r["qps"]) if okh else max(hrows, key=lambda r: r["recall"])
+        # phase split of the best setting: entry scan, then pool + search
+        reps = 10
+        ph = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+        for trio in ph:
+            for ev in trio:
+                ev.record(stream)
+        torch.cuda.synchronize()
+        for i in range(reps):
+            F.search(ix, Q, lo, hi, k, best["L"], epn=best["epn"], epn_frac=best["epn_frac"],
+                     epn_max=best["epn_max"], budget=best["budget"], entry_mode=1, hash_log2=args.hash_log2,
+                     events=ph[i])
+        torch.cuda.synchronize()
+        ha = sum(t[0].elapsed_time(t[1]) for t in ph) / 1000.0 / reps
+        hb = sum(t[1].elapsed_time(t[2]) for t in ph) / 1000.0 / reps
+        fp16 = {"storage": "fp16 rows (binary16, nearest even), fp32 queries, fp64-accumulated distances",
+                "best": best, "recall_target_met": bool(okh), "vs_fp32_value": best["qps"] / qps,
+                "entry_scan_ms": ha * 1e3, "search_ms": hb * 1e3, "sweep": hrows}
+        log(f"fp16 rows: best L={best['L']} max={best['epn_max']} B={best['budget']} recall={best['recall']:.4f} "
+            f"{best['qps']:.0f} QPS (x{best['qps'] / qps:.2f} of fp32); entry scan {ha * 1e3:.3f} ms, "
+            f"search {hb * 1e3:.3f} ms")
+        ix.upload(0)
 
     # ablations (Sec 8.4) at the chosen setting
     ablation = None
@@ -362,7 +420,7 @@ def main():
         abl("eager check, exact visited set", eager=1, hl2=0)
         t0 = time.time()
         ix0 = F.Index.build(w.X, w.attr, beta=0.0)
-        ix0.upload(0)
+        ix0.upload(0, storage=args.storage)
         log(f"beta = 0 index built in {time.time() - t0:.1f}s")
         abl("beta = 0 (no attribute fusion)", index=ix0)
         ix0.free()
@@ -372,7 +430,10 @@ def main():
     try:
         import oracle
         arrs = ix.export()
-        ox = oracle.OracleIndex(arrs["perm"], arrs["attr_sorted"], arrs["X_rank"], arrs["ENC"])
+        Xr = arrs["X_rank"]
+        if args.storage == "fp16":
+            Xr = Xr.astype(np.float16).astype(np.float32)
+        ox = oracle.OracleIndex(arrs["perm"], arrs["attr_sorted"], Xr, arrs["ENC"])
         threads = oracle.default_threads()
         probe = min(200, w.nq)
         t0 = time.time()
@@ -414,7 +475,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32" if args.storage == "fp32" else "f16 rows, f32 queries, f64 accumulation",
         "data": "synthetic",
         "config": {
             "workload": f"{w.name}: n={n} d={d} Gaussian mixture (1000 centres, noise 0.3), "
@@ -432,6 +493,9 @@ def main():
         "cpu_baseline": cpu,
         # the exhaustive filtered search as the pre-filter baseline: recall 1
         # (certified), queries per second of the same batch
+        # the same search with the rows stored in fp16 (secondary; the
+        # metric above is fp32)
+        "fp16_storage": fp16,
         "bruteforce": {"ms": bf_time * 1e3, "qps": w.nq / bf_time, "recall@10": 1.0,
                        "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,

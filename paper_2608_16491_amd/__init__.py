@@ -22,11 +22,13 @@ ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "EBADINDEX", -5: "ENOTUPLO
 (STAT_EXPANSIONS, STAT_EN, STAT_DIST, STAT_SCANNED, STAT_ENTRY, STAT_LSTART, STAT_LEND, STAT_LOADED,
  STAT_SCANROWS) = range(9)
 STAT_N = 9
+STORAGE_F32, STORAGE_F16 = 0, 1
+STORAGE = {"fp32": STORAGE_F32, "fp16": STORAGE_F16}
 
 SYMBOLS = (
     "frog_build_params_default", "frog_search_params_default", "frog_build_index",
     "frog_index_from_arrays", "frog_index_export", "frog_index_info", "frog_index_save",
-    "frog_index_load", "frog_index_upload", "frog_index_free", "frog_rank_bounds", "frog_search",
+    "frog_index_load", "frog_index_upload", "frog_index_upload_ex", "frog_index_free", "frog_rank_bounds", "frog_search",
     "frog_search_ex", "frog_bruteforce_filtered", "frog_last_error",
 )
 
@@ -84,6 +86,8 @@ def lib() -> C.CDLL:
     L.frog_index_load.argtypes = [C.c_char_p, C.POINTER(P)]
     L.frog_index_upload.restype = i32
     L.frog_index_upload.argtypes = [P, i32]
+    L.frog_index_upload_ex.restype = i32
+    L.frog_index_upload_ex.argtypes = [P, i32, i32]
     L.frog_index_free.restype = None
     L.frog_index_free.argtypes = [P]
     L.frog_rank_bounds.restype = i32
@@ -185,8 +189,16 @@ class Index:
         _check(lib().frog_index_export(self._h, _ptr(X), _ptr(a), _ptr(p), _ptr(E)))
         return dict(X_rank=X, attr_sorted=a, perm=p, ENC=E)
 
-    def upload(self, device: int = 0) -> "Index":
-        _check(lib().frog_index_upload(self._h, device))
+    def upload(self, device: int = 0, storage: str = "fp32") -> "Index":
+        """Copy to `device` with rows stored as "fp32" or "fp16" (rounded to
+        nearest even; the search is then exact over the rounded rows)."""
+        if storage not in STORAGE:
+            raise ValueError(f"storage {storage!r}: one of {sorted(STORAGE)}")
+        if storage == "fp32":
+            _check(lib().frog_index_upload(self._h, device))
+        else:
+            _check(lib().frog_index_upload_ex(self._h, device, STORAGE[storage]))
+        self.storage = storage
         return self
 
     def free(self):

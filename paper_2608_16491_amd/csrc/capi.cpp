@@ -48,7 +48,8 @@ void release_device(frog_index* ix) {
         int prev = 0;
         hipGetDevice(&prev);
         hipSetDevice(ix->device);
-        hipFree(ix->dX);
+        if (ix->dX) hipFree(ix->dX);
+        if (ix->dXh) hipFree(ix->dXh);
         hipFree(ix->dENC);
         hipFree(ix->dattr);
         hipFree(ix->dperm);
@@ -64,6 +65,8 @@ void release_device(frog_index* ix) {
     ix->dshared_nrm = nullptr;
     ix->shared_valid = false;
     ix->dX = nullptr;
+    ix->dXh = nullptr;
+    ix->maxnorm = -1.f;
     ix->dENC = nullptr;
     ix->dattr = nullptr;
     ix->dperm = nullptr;
@@ -313,8 +316,30 @@ int frog_index_load(const char* path, frog_index_t** out) {
 }
 
 int frog_index_upload(frog_index_t* ix, int device) {
+    return frog_index_upload_ex(ix, device, FROG_STORAGE_F32);
+}
+
+int frog_index_upload_ex(frog_index_t* ix, int device, int storage) {
     frog::clear_error();
     if (!ix) return fail(FROG_EINVAL, "index is NULL");
+    if (storage != FROG_STORAGE_F32 && storage != FROG_STORAGE_F16)
+        return fail(FROG_EINVAL, "storage=%d: FROG_STORAGE_F32 or FROG_STORAGE_F16", storage);
+    const bool half = storage == FROG_STORAGE_F16;
+    if (half && ix->d > 128) return fail(FROG_EUNSUPPORTED, "fp16 storage needs d <= 128 (d=%d)", ix->d);
+    // fp16 rows: round every value once (nearest even) and pad to dp halves
+    const int dp = half ? (ix->d + 63) / 64 * 64 : (ix->d + 31) / 32 * 32;
+    std::vector<uint16_t> hx;
+    if (half) {
+        hx.assign((size_t)ix->n * dp, 0);
+        for (int64_t i = 0; i < ix->n; ++i)
+            for (int c = 0; c < ix->d; ++c) {
+                const _Float16 h = (_Float16)ix->X[(size_t)i * ix->d + c];
+                if (!(h == h) || h > (_Float16)65504.f || h < (_Float16)-65504.f)
+                    return fail(FROG_EUNSUPPORTED, "row %lld: value %g outside the fp16 range", (long long)i,
+                                (double)ix->X[(size_t)i * ix->d + c]);
+                std::memcpy(&hx[(size_t)i * dp + c], &h, 2);
+            }
+    }
     int ndev = 0;
     HIP_TRY(hipGetDeviceCount(&ndev));
     if (device < 0 || device >= ndev) return fail(FROG_EINVAL, "device %d not in [0, %d)", device, ndev);
@@ -322,19 +347,21 @@ int frog_index_upload(frog_index_t* ix, int device) {
     int prev = 0;
     HIP_TRY(hipGetDevice(&prev));
     HIP_TRY(hipSetDevice(device));
-    const int dp = (ix->d + 31) / 32 * 32;
     const size_t nX = (size_t)ix->n * dp, nE = (size_t)ix->n * ix->H * ix->m;
     ix->device = device;
     ix->dp = dp;
+    ix->storage = storage;
     auto bail = [&](int rc) { release_device(ix); hipSetDevice(prev); return rc; };
-    hipError_t e = hipMalloc(&ix->dX, nX * sizeof(float));
+    hipError_t e = half ? hipMalloc(&ix->dXh, nX * sizeof(uint16_t)) : hipMalloc(&ix->dX, nX * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(&ix->dENC, nE * sizeof(int32_t));
     if (e == hipSuccess) e = hipMalloc(&ix->dattr, (size_t)ix->n * sizeof(double));
     if (e == hipSuccess) e = hipMalloc(&ix->dperm, (size_t)ix->n * sizeof(int32_t));
     if (e != hipSuccess)
         return bail(fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "device allocation: %s",
                          hipGetErrorString(e)));
-    if (dp == ix->d) {
+    if (half) {
+        e = hipMemcpy(ix->dXh, hx.data(), nX * sizeof(uint16_t), hipMemcpyHostToDevice);
+    } else if (dp == ix->d) {
         e = hipMemcpy(ix->dX, ix->X.data(), nX * sizeof(float), hipMemcpyHostToDevice);
     } else {
         e = hipMemset(ix->dX, 0, nX * sizeof(float));
@@ -361,14 +388,15 @@ void frog_index_free(frog_index_t* ix) {
 namespace {
 
 frog::DevIndex view(const frog_index* ix) {
-    return frog::DevIndex{ix->dX, ix->dENC, ix->dattr, ix->dperm, ix->n, ix->d, ix->dp, ix->H, ix->m};
+    return frog::DevIndex{ix->dX, ix->dXh, ix->dENC, ix->dattr, ix->dperm, ix->n, ix->d, ix->dp, ix->H, ix->m,
+                          ix->storage};
 }
 
 // Device entry points run on the index's device; the caller's stream must
 // belong to it.
 int check_device_index(const frog_index_t* ix) {
     if (!ix) return fail(FROG_EINVAL, "index is NULL");
-    if (ix->device < 0 || !ix->dX) return fail(FROG_ENOTUPLOADED, "index has not been uploaded");
+    if (ix->device < 0 || (!ix->dX && !ix->dXh)) return fail(FROG_ENOTUPLOADED, "index has not been uploaded");
     int cur = -1;
     if (hipGetDevice(&cur) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
     if (cur != ix->device)
@@ -448,6 +476,8 @@ int frog_bruteforce_filtered(const frog_index_t* ix, const float* d_queries, int
     if (rc) return rc;
     if (nq < 0) return fail(FROG_EINVAL, "nq < 0");
     if (k < 1 || k > 256) return fail(FROG_EINVAL, "k=%d outside [1, 256]", k);
+    if (ix->storage != FROG_STORAGE_F32)
+        return fail(FROG_EUNSUPPORTED, "exhaustive search needs an index uploaded with fp32 rows");
     if (nq == 0) return FROG_OK;
     if (!d_queries || !d_lo || !d_hi || !d_ids || !d_dists) return fail(FROG_EINVAL, "NULL device pointer");
     return frog::launch_bruteforce(ix, d_queries, nq, d_lo, d_hi, k, d_ids, d_dists, d_certified, stream);
@@ -464,14 +494,22 @@ static uint64_t mix64(uint64_t x) {
     return z ^ (z >> 31);
 }
 
+// value c of row i as the device stores it (fp32, or rounded to binary16)
+static inline float stored_value(const frog_index* ix, int64_t i, int c) {
+    const float v = ix->X[(size_t)i * ix->d + c];
+    return ix->storage == FROG_STORAGE_F16 ? (float)(_Float16)v : v;
+}
+
 float index_maxnorm(frog_index* ix) {
     std::lock_guard<std::mutex> g(ix->shared_mu);
     if (ix->maxnorm < 0.f) {
         double mx = 0.0;
         for (int64_t i = 0; i < ix->n; ++i) {
-            const float* x = ix->X.data() + (size_t)i * ix->d;
             double s = 0.0;
-            for (int c = 0; c < ix->d; ++c) s += (double)x[c] * x[c];
+            for (int c = 0; c < ix->d; ++c) {
+                const double v = stored_value(ix, i, c);
+                s += v * v;
+            }
             mx = std::max(mx, s);
         }
         ix->maxnorm = (float)(mx * (1.0 + 1e-6));
@@ -513,9 +551,11 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         std::vector<uint32_t> prio((size_t)(n + total));
         std::vector<float> nrm((size_t)(n + total));
         for (int64_t i = 0; i < n; ++i) {
-            const float* x = ix->X.data() + (size_t)i * ix->d;
             float sq = 0.f;
-            for (int c = 0; c < ix->d; ++c) sq += x[c] * x[c];
+            for (int c = 0; c < ix->d; ++c) {
+                const float v = stored_value(ix, i, c);
+                sq += v * v;
+            }
             prio[(size_t)i] = prio_rank[(size_t)i];
             nrm[(size_t)i] = sq;
         }
@@ -538,11 +578,13 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         if (e == hipSuccess) e = hipMemcpy(ix->dshared_p, prio.data(), prio.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
         if (e == hipSuccess) e = hipMalloc(&ix->dshared_nrm, nrm.size() * sizeof(float));
         if (e == hipSuccess) e = hipMemcpy(ix->dshared_nrm, nrm.data(), nrm.size() * sizeof(float), hipMemcpyHostToDevice);
-        // the listed rows of X, so that a scan over a list reads contiguous rows
-        if (e == hipSuccess) e = hipMalloc(&ix->dshared_x, (size_t)std::max<int64_t>(total, 1) * ix->dp * sizeof(float));
+        // the listed stored rows, so that a scan over a list reads contiguous rows
+        const int row_bytes = ix->dp * (ix->storage == FROG_STORAGE_F16 ? 2 : 4);
+        if (e == hipSuccess) e = hipMalloc(&ix->dshared_x, (size_t)std::max<int64_t>(total, 1) * row_bytes);
         int rc = FROG_OK;
         if (e == hipSuccess && total > 0) {
-            rc = launch_gather_rows(ix->dX, ix->dp, ix->dshared, total, ix->dshared_x, nullptr);
+            const void* rows = ix->storage == FROG_STORAGE_F16 ? (const void*)ix->dXh : (const void*)ix->dX;
+            rc = launch_gather_rows(rows, row_bytes, ix->dshared, total, ix->dshared_x, nullptr);
             if (rc == FROG_OK) e = hipDeviceSynchronize();
         }
         (void)hipSetDevice(prev);
@@ -561,7 +603,8 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         ix->shared_valid = true;
     }
     out->ranks = ix->dshared;
-    out->xrows = ix->dshared_x;
+    out->xrows = ix->storage == FROG_STORAGE_F32 ? static_cast<const float*>(ix->dshared_x) : nullptr;
+    out->xrowsh = ix->storage == FROG_STORAGE_F16 ? static_cast<const uint16_t*>(ix->dshared_x) : nullptr;
     out->prio = ix->dshared_p;
     out->norm = ix->dshared_nrm;
     std::copy(ix->shared_off, ix->shared_off + 34, out->off);

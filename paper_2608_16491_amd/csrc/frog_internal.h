@@ -17,14 +17,17 @@ struct frog_index {
     std::vector<double> attr;    // n, ascending
     std::vector<int32_t> perm;   // n, rank -> original index
     std::vector<int32_t> ENC;    // n * H * m
-    // device copy (HBM): X rows padded to dp floats
+    // device copy (HBM): X rows padded to dp values of the storage type
+    // (fp32 in dX, or binary16 bit patterns in dXh)
     int device = -1;
     int dp = 0;
+    int storage = FROG_STORAGE_F32;
     float* dX = nullptr;
+    uint16_t* dXh = nullptr;
     int32_t* dENC = nullptr;
     double* dattr = nullptr;
     int32_t* dperm = nullptr;
-    float maxnorm = -1.f;        // largest squared row norm, computed on first use
+    float maxnorm = -1.f;        // largest squared norm of the stored rows, computed on first use
     // shared entry sample (entry_mode 1): for one seed, the ascending rank
     // lists of levels 1..nlev (level j: ranks whose priority is below
     // 2^(32-j)), concatenated on the device; built on first use
@@ -34,9 +37,9 @@ struct frog_index {
     int shared_nlev = 0;
     int64_t shared_off[34] = {};
     int32_t* dshared = nullptr;
-    float* dshared_x = nullptr;  // the levels' rows of X, in list order, dp floats each
+    void* dshared_x = nullptr;   // the levels' stored rows, in list order, dp values each
     uint32_t* dshared_p = nullptr;  // priorities: rank order [0, n), then the levels' lists
-    float* dshared_nrm = nullptr;   // squared row norms, same layout
+    float* dshared_nrm = nullptr;   // squared norms of the stored rows, same layout
 };
 
 namespace frog {
@@ -52,19 +55,22 @@ int layers_for(int64_t n, int n_inv);
 
 // device index view passed to the kernels
 struct DevIndex {
-    const float* X;
+    const float* X;       // fp32 rows (storage FROG_STORAGE_F32), else NULL
+    const uint16_t* Xh;   // binary16 rows (storage FROG_STORAGE_F16), else NULL
     const int32_t* ENC;
     const double* attr;
     const int32_t* perm;
     int64_t n;
     int d, dp, H, m;
+    int storage;
 };
 
 // Levels of the shared entry sample, as the kernels see them: level j's list
 // is ranks[off[j], off[j + 1]) for 1 <= j <= nlev; level 0 is every rank.
 struct SharedLevels {
     const int32_t* ranks;
-    const float* xrows;  // row p of level j's list at xrows + (off[j] + p) * dp
+    const float* xrows;  // row p of level j's list at xrows + (off[j] + p) * dp (fp32 storage)
+    const uint16_t* xrowsh;  // the same for binary16 storage
     const uint32_t* prio;  // priority of rank i at [i]; of level j's position p at [n + off[j] + p]
     const float* norm;     // squared norm of the row, same indexing (fp32, any order of summation)
     int64_t off[34];
@@ -102,8 +108,9 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream);
 int launch_rank_bounds(const DevIndex& ix, const double* lo, const double* hi, int64_t nq,
                        int32_t* lr, void* stream);
 bool search_shape_supported(int dp, int m, int L);
-// copy the rows of the listed ranks: out[i] = X[ranks[i]] (dp floats each)
-int launch_gather_rows(const float* X, int dp, const int32_t* ranks, int64_t count, float* out, void* stream);
+// copy the rows of the listed ranks: out[i] = X[ranks[i]] (row_bytes each, a
+// multiple of 16)
+int launch_gather_rows(const void* X, int row_bytes, const int32_t* ranks, int64_t count, void* out, void* stream);
 // bruteforce.hip
 int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const double* lo,
                       const double* hi, int k, int32_t* ids, float* dists, int32_t* cert,

@@ -36,6 +36,7 @@
 //     plus (# new keys below it); entries scatter through LDS.  Keys are
 //     unique once duplicates are dropped, so this equals sorting the union.
 
+#include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -212,17 +213,38 @@ __device__ void hotspot(int64_t l, int64_t r, int H, int64_t n, int& Ls, int& Le
 
 // ------------------------------------------------------------------ a8: distances
 
+// Chunk c (of C = dp/32) of row `id` that lane `sub` (of 8) reads, as 4
+// floats.  fp32 rows: float4 number sub + 8c of the row.  fp16 rows (dp a
+// multiple of 64): the lane's 16-byte piece sub + 8(c/2) holds 8 halves, of
+// which chunk c is the first or second 4, converted exactly to float.
+template <typename XT>
+__device__ __forceinline__ float4 row_chunk(const XT* __restrict__ X, int dp, int64_t id, int sub, int c) {
+    if constexpr (sizeof(XT) == 4) {
+        return reinterpret_cast<const float4*>(X)[id * (dp >> 2) + sub + 8 * c];
+    } else {
+        const uint2 h = *reinterpret_cast<const uint2*>(X + id * dp + 8 * (sub + 8 * (c >> 1)) + 4 * (c & 1));
+        const float2 a = __half22float2(__builtin_bit_cast(__half2, h.x));
+        const float2 b = __half22float2(__builtin_bit_cast(__half2, h.y));
+        return make_float4(a.x, a.y, b.x, b.y);
+    }
+}
+
+// The query dimensions a lane pairs with chunk c (same layout as row_chunk).
+template <typename XT>
+__device__ __forceinline__ int chunk_dim(int sub, int c) {
+    if constexpr (sizeof(XT) == 4) return 4 * (sub + 8 * c);
+    else return 8 * (sub + 8 * (c >> 1)) + 4 * (c & 1);
+}
+
 // Squared L2 of up to `cnt` (<= 64) candidates; lane j holds candidate j's
 // rank in `myid` and receives its distance in the return value.  The query's
 // float4 chunks this lane needs are in qv.
-template <int C>
-__device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
+template <int C, typename XT = float>
+__device__ float eval_small(const XT* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
     // G = 8 lanes per vector: lane reads float4 chunks (lane % 8) + 8c; one
     // group of 8 vectors per step (an expansion rarely yields more than 8)
     const int lane = lane_id();
     const int sub = lane & 7;
-    const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
-    const int dp4 = dp >> 2;
     const int src = (lane & 7) << 3;
     float mine = 0.f;
     for (int sb0 = 0; sb0 < cnt; sb0 += 8) {
@@ -232,7 +254,7 @@ __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&
         float4 x[C];
 #pragma unroll
         for (int c = 0; c < C; ++c)
-            x[c] = v ? X4[(int64_t)id * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
+            x[c] = v ? row_chunk<XT>(X, dp, id, sub, c) : make_float4(0.f, 0.f, 0.f, 0.f);
         double s = 0.0;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
@@ -257,10 +279,10 @@ __device__ float eval_small(const float* __restrict__ X, int dp, const float4 (&
 // Same result as eval_small for the entry-point batches (up to 64 candidates),
 // with two steps of 16 vectors in flight: the loads of step i+1 are issued
 // before step i is reduced, so the arithmetic overlaps the memory latency.
-template <int C>
+template <int C, typename XT = float>
 struct Gather16 {
     float4 x[2][C];
-    __device__ __forceinline__ void issue(const float4* __restrict__ X4, int dp4, int cnt, int32_t myid, int sb0) {
+    __device__ __forceinline__ void issue(const XT* __restrict__ X, int dp, int cnt, int32_t myid, int sb0) {
         const int lane = lane_id();
         const int sub = lane & 7;
 #pragma unroll
@@ -270,7 +292,7 @@ struct Gather16 {
             const bool v = j < cnt;
 #pragma unroll
             for (int c = 0; c < C; ++c)
-                x[g][c] = v ? X4[(int64_t)id * dp4 + sub + 8 * c] : make_float4(0.f, 0.f, 0.f, 0.f);
+                x[g][c] = v ? row_chunk<XT>(X, dp, id, sub, c) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
     __device__ __forceinline__ void consume(const float4 (&qv)[C], int sb0, float& mine) const {
@@ -300,17 +322,15 @@ struct Gather16 {
     }
 };
 
-template <int C>
-__device__ float eval_pipelined(const float* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
-    const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
-    const int dp4 = dp >> 2;
+template <int C, typename XT = float>
+__device__ float eval_pipelined(const XT* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
     float mine = 0.f;
-    Gather16<C> a, b;
-    a.issue(X4, dp4, cnt, myid, 0);
+    Gather16<C, XT> a, b;
+    a.issue(X, dp, cnt, myid, 0);
     for (int sb0 = 0; sb0 < cnt; sb0 += 32) {
-        if (sb0 + 16 < cnt) b.issue(X4, dp4, cnt, myid, sb0 + 16);
+        if (sb0 + 16 < cnt) b.issue(X, dp, cnt, myid, sb0 + 16);
         a.consume(qv, sb0, mine);
-        if (sb0 + 32 < cnt) a.issue(X4, dp4, cnt, myid, sb0 + 32);
+        if (sb0 + 32 < cnt) a.issue(X, dp, cnt, myid, sb0 + 32);
         if (sb0 + 16 < cnt) b.consume(qv, sb0 + 16, mine);
     }
     return mine;
@@ -489,7 +509,20 @@ __device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b, double rb) {
     return f;
 }
 
-template <int C>
+// The index's rows, and the shared sample's level rows, in storage type T
+// (fp32 or fp16).
+template <typename XT>
+__device__ __forceinline__ const XT* rows_of(const DevIndex& ix) {
+    if constexpr (sizeof(XT) == 4) return ix.X;
+    else return reinterpret_cast<const __half*>(ix.Xh);
+}
+template <typename XT>
+__device__ __forceinline__ const XT* lev_rows(const SharedLevels& lv) {
+    if constexpr (sizeof(XT) == 4) return lv.xrows;
+    else return reinterpret_cast<const __half*>(lv.xrowsh);
+}
+
+template <int C, typename XT = float>
 struct QueryCtx {
     float4 qv[C > 0 ? C : 1];
     const float* qrow;
@@ -525,7 +558,7 @@ struct QueryCtx {
             const int lane = lane_id();
 #pragma unroll
             for (int c = 0; c < C; ++c) {
-                const int b = 4 * ((lane & 7) + 8 * c);
+                const int b = chunk_dim<XT>(lane & 7, c);
                 qv[c].x = b < ix.d ? qrow[b] : 0.f;
                 qv[c].y = b + 1 < ix.d ? qrow[b + 1] : 0.f;
                 qv[c].z = b + 2 < ix.d ? qrow[b + 2] : 0.f;
@@ -549,19 +582,19 @@ struct QueryCtx {
         return shared && (uint32_t)(splitmix64(pkey ^ (uint64_t)(uint32_t)v) >> 32) < T;
     }
     __device__ float eval(const DevIndex& ix, int nb, int32_t myid) const {
-        if constexpr (C > 0) return eval_small<C>(ix.X, ix.dp, qv, nb, myid);
+        if constexpr (C > 0) return eval_small<C, XT>(rows_of<XT>(ix), ix.dp, qv, nb, myid);
         else return eval_large(ix.X, ix.dp, qrow, ix.d, nb, myid);
     }
     __device__ float eval_batch(const DevIndex& ix, int nb, int32_t myid) const {
-        if constexpr (C > 0) return eval_pipelined<C>(ix.X, ix.dp, qv, nb, myid);
+        if constexpr (C > 0) return eval_pipelined<C, XT>(rows_of<XT>(ix), ix.dp, qv, nb, myid);
         else return eval_large(ix.X, ix.dp, qrow, ix.d, nb, myid);
     }
 };
 
 // a3 (entry points, Alg. 2): evaluate entry points [e0, e1) of a query into
 // a pool holding their L nearest.
-template <int C, int LP>
-__device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const QueryCtx<C>& Q, int64_t e0,
+template <int C, int LP, typename XT>
+__device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const QueryCtx<C, XT>& Q, int64_t e0,
                             int64_t e1, Pool<LP>& pool, const WaveLds<LP>& W) {
     const int lane = lane_id();
 #pragma unroll
@@ -579,8 +612,8 @@ __device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const Que
 
 // a2, a4-a11 for one query whose pool holds the L nearest entry points:
 // HotspotLocalization, the best-first loop of Alg. 2, output and statistics.
-template <int C, int LP>
-__device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis_words, const QueryCtx<C>& Q,
+template <int C, int LP, typename XT>
+__device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis_words, const QueryCtx<C, XT>& Q,
                          Pool<LP>& pool, const WaveLds<LP>& W, const Visited& vis) {
     const int lane = lane_id();
     const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
@@ -780,7 +813,7 @@ __device__ __forceinline__ uint64_t ctl_word(uint32_t q, uint32_t next, uint32_t
     return ((uint64_t)q << 32) | ((uint64_t)next << 16) | nch;
 }
 
-template <int C, int LP>
+template <int C, int LP, typename XT = float>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
 void coop_kernel(KParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -870,13 +903,13 @@ void coop_kernel(KParams P) {
         // ---- the chunk's entry points
         const int64_t qi = cq;
         const int ci = (int)cc, nch = (int)cn;
-        QueryCtx<C> Q;
+        QueryCtx<C, XT> Q;
         Q.load(ix, A, P.lr, qi);
         Q.load_vector(ix);
         Pool<LP> pool;
         const int64_t e0 = (int64_t)ci * P.chunk;
         const int64_t e1 = e0 + P.chunk < Q.ne ? e0 + P.chunk : Q.ne;
-        entry_chunk<C, LP>(ix, A, Q, e0, e1, pool, W);
+        entry_chunk<C, LP, XT>(ix, A, Q, e0, e1, pool, W);
 
         if (nch > 1) {
             uint64_t* mine = P.part + ((uint64_t)qi * P.cpq + ci) * slots;
@@ -909,7 +942,7 @@ void coop_kernel(KParams P) {
                 }
             }
         }
-        traverse<C, LP>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
+        traverse<C, LP, XT>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
         if (A.stats && lane == 0) A.stats[qi * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
     }
 }
@@ -1203,9 +1236,11 @@ __host__ __device__ constexpr size_t s_scan_lds_per_wave(int kkeep) {
 }
 
 // KT = dp / 16 float4 chunks of the query operand in registers (d <= 128);
-// KT = 0 reloads it for every block.
-template <int KT, int KK>
+// KT = 0 reloads it for every block (fp32 rows only).  T is the rows'
+// storage type: fp16 rows are converted exactly to fp32 on load.
+template <int KT, int KK, typename XT = float>
 __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
+    static_assert(sizeof(XT) == 4 || (KT > 0 && KT % 2 == 0), "fp16 rows need dp a multiple of 32 held in registers");
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int lane = lane_id();
@@ -1231,13 +1266,15 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
 
     // MFMA operand mapping (16x16x4 f32): A[i][kk] in lane i + 16 kk, B[kk][j]
     // in lane j + 16 kk, D[4 (lane/16) + e][lane % 16] in element e.  Lane
-    // group kk takes dimensions 16 u + 4 kk + {0..3} of K step u.
+    // group kk takes dimensions 16 u + 4 kk + {0..3} of K step u (fp32 rows),
+    // or 32 (u/2) + 8 kk + 4 (u%2) + {0..3} (fp16 rows: one 16-byte load
+    // feeds two K steps).
     const int ii = lane & 15;
     const int kk = lane >> 4;
     const int qrow = T.q[ii];
     const float* Qr = P.a.Q + (int64_t)(qrow >= 0 ? qrow : 0) * d;
     auto qchunk = [&](int u) -> float4 {
-        const int b = 16 * u + 4 * kk;
+        const int b = sizeof(XT) == 4 ? 16 * u + 4 * kk : 32 * (u >> 1) + 8 * kk + 4 * (u & 1);
         float4 v;
         v.x = (qrow >= 0 && b < d) ? Qr[b] : 0.f;
         v.y = (qrow >= 0 && b + 1 < d) ? Qr[b + 1] : 0.f;
@@ -1283,8 +1320,9 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
     const int64_t nblk = (c1 - c0 + 15) / 16;
     // the level's list and its rows (level 0: every rank, rows of X)
     const int32_t* lranks = lev == 0 ? nullptr : lv.ranks + lv.off[lev];
-    const float4* X4 = reinterpret_cast<const float4*>(P.ix.X);
-    const float4* R4 = lev == 0 ? X4 : reinterpret_cast<const float4*>(lv.xrows + lv.off[lev] * dp);
+    const XT* X0 = rows_of<XT>(P.ix);
+    const XT* Rl = lev == 0 ? X0 : lev_rows<XT>(lv) + lv.off[lev] * dp;
+    const float4* R4 = reinterpret_cast<const float4*>(Rl);
     // the level's priorities and squared row norms, in list order
     const int64_t pbase = lev == 0 ? 0 : P.ix.n + lv.off[lev];
     const uint32_t* lprio = lv.prio + pbase;
@@ -1300,8 +1338,23 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
     auto load_rows = [&](int64_t blk, float4 (&x)[KT > 0 ? KT : 1]) {
         if constexpr (KT > 0) {
             const int64_t pos = pos_at(blk);
+            if constexpr (sizeof(XT) == 4) {
 #pragma unroll
-            for (int u = 0; u < KT; ++u) x[u] = R4[pos * dp4 + 4 * u + kk];
+                for (int u = 0; u < KT; ++u) x[u] = R4[pos * dp4 + 4 * u + kk];
+            } else {
+                // dp halves per row: 16-byte piece 4 v + kk holds K steps 2v, 2v + 1
+                const int dp8 = dp >> 3;
+#pragma unroll
+                for (int v = 0; v < KT / 2; ++v) {
+                    const uint4 h = reinterpret_cast<const uint4*>(Rl)[pos * dp8 + 4 * v + kk];
+                    const float2 a = __half22float2(__builtin_bit_cast(__half2, h.x));
+                    const float2 b = __half22float2(__builtin_bit_cast(__half2, h.y));
+                    const float2 c = __half22float2(__builtin_bit_cast(__half2, h.z));
+                    const float2 e = __half22float2(__builtin_bit_cast(__half2, h.w));
+                    x[2 * v] = make_float4(a.x, a.y, b.x, b.y);
+                    x[2 * v + 1] = make_float4(c.x, c.y, e.x, e.y);
+                }
+            }
         }
     };
     // list state in registers: entries per slot (uniform) and the threshold
@@ -1455,7 +1508,7 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
 }
 
 // The pool of each query: one wavefront per query.
-template <int C, int LP, int KK>
+template <int C, int LP, int KK, typename XT = float>
 __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1474,7 +1527,7 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
         if (qi >= A.nq) return;   // wave-uniform; no workgroup barrier follows
         const SPlan p = P.plan[qi];
         if (p.l > p.r) return;
-        QueryCtx<C> Q;
+        QueryCtx<C, XT> Q;
         Q.load(ix, A, P.lr, qi);
         Q.load_vector(ix);
         Q.shared = true;
@@ -1609,7 +1662,7 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
 }
 
 // Traversal: persistent, one wavefront per query, from the pool s_pool_kernel wrote.
-template <int C, int LP>
+template <int C, int LP, typename XT = float>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_SEARCH_WAVES_PER_EU)))
 void s_search_kernel(SParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1637,7 +1690,7 @@ void s_search_kernel(SParams P) {
             if (A.stats && lane < FROG_STAT_N) A.stats[qi * FROG_STAT_N + lane] = 0;
             continue;
         }
-        QueryCtx<C> Q;
+        QueryCtx<C, XT> Q;
         Q.load(ix, A, P.lr, qi);
         Q.load_vector(ix);
         Q.shared = true;
@@ -1653,7 +1706,7 @@ void s_search_kernel(SParams P) {
             np += __popcll(ballot(pool.key[s] != kEmpty));
         }
         pool.np = np;
-        traverse<C, LP>(ix, A, P.gvis_words, Q, pool, W, vis);
+        traverse<C, LP, XT>(ix, A, P.gvis_words, Q, pool, W, vis);
     }
 }
 
@@ -1662,14 +1715,16 @@ void s_search_kernel(SParams P) {
 
 using KernelFn = void (*)(KParams);
 
-template <int C>
+template <int C, typename XT = float>
 KernelFn pick_lp(int L) {
-    if (L <= 64) return coop_kernel<C, 1>;
-    if (L <= 128) return coop_kernel<C, 2>;
-    return coop_kernel<C, 4>;
+    if (L <= 64) return coop_kernel<C, 1, XT>;
+    if (L <= 128) return coop_kernel<C, 2, XT>;
+    return coop_kernel<C, 4, XT>;
 }
 
-KernelFn pick_kernel(int dp, int L) {
+// fp16 rows come with dp = 64 or 128 (the upload checks it)
+KernelFn pick_kernel(int dp, int L, int storage) {
+    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_lp<2, __half>(L) : pick_lp<4, __half>(L);
     switch (dp) {
         case 32: return pick_lp<1>(L);
         case 64: return pick_lp<2>(L);
@@ -1708,22 +1763,23 @@ int max_blocks(KernelFn fn, int smem) {
 // candidates kept per query and work item: K > L with room for the margin
 int shared_kkeep(int L) { return L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256); }
 
-template <int C>
+template <int C, typename XT = float>
 void (*pick_s_pool_c(int L))(SParams) {
     const int kk = shared_kkeep(L);
-    if (L <= 64) return kk == 64 ? s_pool_kernel<C, 1, 64> : s_pool_kernel<C, 1, 128>;
-    if (L <= 128) return kk == 128 ? s_pool_kernel<C, 2, 128> : s_pool_kernel<C, 2, 256>;
-    return s_pool_kernel<C, 4, 256>;
+    if (L <= 64) return kk == 64 ? s_pool_kernel<C, 1, 64, XT> : s_pool_kernel<C, 1, 128, XT>;
+    if (L <= 128) return kk == 128 ? s_pool_kernel<C, 2, 128, XT> : s_pool_kernel<C, 2, 256, XT>;
+    return s_pool_kernel<C, 4, 256, XT>;
 }
 
-template <int C>
+template <int C, typename XT = float>
 void (*pick_s_search_c(int L))(SParams) {
-    if (L <= 64) return s_search_kernel<C, 1>;
-    if (L <= 128) return s_search_kernel<C, 2>;
-    return s_search_kernel<C, 4>;
+    if (L <= 64) return s_search_kernel<C, 1, XT>;
+    if (L <= 128) return s_search_kernel<C, 2, XT>;
+    return s_search_kernel<C, 4, XT>;
 }
 
-void (*pick_s_pool(int dp, int L))(SParams) {
+void (*pick_s_pool(int dp, int L, int storage))(SParams) {
+    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_s_pool_c<2, __half>(L) : pick_s_pool_c<4, __half>(L);
     switch (dp) {
         case 32: return pick_s_pool_c<1>(L);
         case 64: return pick_s_pool_c<2>(L);
@@ -1733,7 +1789,8 @@ void (*pick_s_pool(int dp, int L))(SParams) {
     }
 }
 
-void (*pick_s_search(int dp, int L))(SParams) {
+void (*pick_s_search(int dp, int L, int storage))(SParams) {
+    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_s_search_c<2, __half>(L) : pick_s_search_c<4, __half>(L);
     switch (dp) {
         case 32: return pick_s_search_c<1>(L);
         case 64: return pick_s_search_c<2>(L);
@@ -1744,7 +1801,8 @@ void (*pick_s_search(int dp, int L))(SParams) {
 }
 
 template <int KK>
-void (*pick_s_scan_k(int dp))(SParams) {
+void (*pick_s_scan_k(int dp, int storage))(SParams) {
+    if (storage == FROG_STORAGE_F16) return dp == 64 ? s_scan_kernel<4, KK, __half> : s_scan_kernel<8, KK, __half>;
     switch (dp) {
         case 32: return s_scan_kernel<2, KK>;
         case 64: return s_scan_kernel<4, KK>;
@@ -1754,17 +1812,17 @@ void (*pick_s_scan_k(int dp))(SParams) {
     }
 }
 
-void (*pick_s_scan(int dp, int kkeep))(SParams) {
-    if (kkeep == 64) return pick_s_scan_k<64>(dp);
-    if (kkeep == 128) return pick_s_scan_k<128>(dp);
-    return pick_s_scan_k<256>(dp);
+void (*pick_s_scan(int dp, int kkeep, int storage))(SParams) {
+    if (kkeep == 64) return pick_s_scan_k<64>(dp, storage);
+    if (kkeep == 128) return pick_s_scan_k<128>(dp, storage);
+    return pick_s_scan_k<256>(dp, storage);
 }
 
 // entry_mode 1: plan, group, scan on the matrix cores, then search
 int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream) {
     const int kkeep = shared_kkeep(a.L);
-    auto sfn = pick_s_search(ix.dp, a.L);
-    auto pfn = pick_s_pool(ix.dp, a.L);
+    auto sfn = pick_s_search(ix.dp, a.L, ix.storage);
+    auto pfn = pick_s_pool(ix.dp, a.L, ix.storage);
     // search kernel: pool staging, EN list and visited table per wave
     const int lps = lds_per_wave(a.L, a.hash_log2);
     const int smem = lps * kWavesPerBlock;
@@ -1782,7 +1840,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
         hipError_t e = hipFuncSetAttribute((const void*)pfn, hipFuncAttributeMaxDynamicSharedMemorySize, smem_pool);
         if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
-    auto scan = pick_s_scan(ix.dp, kkeep);
+    auto scan = pick_s_scan(ix.dp, kkeep, ix.storage);
     // wavefronts per scan workgroup: as many as 160 KB of LDS hold (at most 4)
     int scan_waves = (int)((160 * 1024) / s_scan_lds_per_wave(kkeep));
     if (scan_waves > kWavesPerBlock) scan_waves = kWavesPerBlock;
@@ -1880,23 +1938,27 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     return FROG_OK;
 }
 
-__global__ void gather_rows_kernel(const float4* __restrict__ X, int dp4, const int32_t* __restrict__ ranks,
-                                   int64_t count, float4* __restrict__ out) {
+// one 16-byte piece per thread: piece c of row i of out is piece c of row
+// ranks[i] of X (w pieces per row)
+__global__ void gather_rows_kernel(const uint4* __restrict__ X, int w, const int32_t* __restrict__ ranks,
+                                   int64_t count, uint4* __restrict__ out) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t row = i / dp4;
+    const int64_t row = i / w;
     if (row >= count) return;
-    const int c = (int)(i % dp4);
-    out[i] = X[(int64_t)ranks[row] * dp4 + c];
+    const int c = (int)(i % w);
+    out[i] = X[(int64_t)ranks[row] * w + c];
 }
 
 }  // namespace
 
-int launch_gather_rows(const float* X, int dp, const int32_t* ranks, int64_t count, float* out, void* stream_v) {
+int launch_gather_rows(const void* X, int row_bytes, const int32_t* ranks, int64_t count, void* out,
+                       void* stream_v) {
     hipStream_t stream = (hipStream_t)stream_v;
-    const int dp4 = dp / 4;
-    const int64_t total = count * dp4;
+    if (row_bytes <= 0 || row_bytes % 16 != 0) return fail(FROG_EINVAL, "gather rows: row of %d bytes", row_bytes);
+    const int w = row_bytes / 16;
+    const int64_t total = count * w;
     hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<const float4*>(X), dp4, ranks, count, reinterpret_cast<float4*>(out));
+                       reinterpret_cast<const uint4*>(X), w, ranks, count, reinterpret_cast<uint4*>(out));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(FROG_EHIP, "gather rows: %s", hipGetErrorString(e));
     return FROG_OK;
@@ -1909,7 +1971,7 @@ bool search_shape_supported(int dp, int m, int L) {
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
     hipStream_t stream = (hipStream_t)stream_v;
     if (a.entry_mode == 1) return launch_shared(ix, a, stream);
-    const KernelFn fn = pick_kernel(ix.dp, a.L);
+    const KernelFn fn = pick_kernel(ix.dp, a.L, ix.storage);
     const int lpw = lds_per_wave(a.L, a.hash_log2);
     const int smem = lpw * kWavesPerBlock + 16;
     if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);

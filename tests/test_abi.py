@@ -91,6 +91,27 @@ def test_device_calls_need_an_uploaded_index():
     assert rc == -1
 
 
+def test_fp16_upload_rejects_on_the_host():
+    # checked before any device is touched: unknown storage, d > 128, a
+    # value that rounds past the largest binary16 (65504)
+    L = F.lib()
+    X, attr = _small_index(64, 4)
+    ix = F.Index.from_arrays(X, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
+    assert L.frog_index_upload_ex(ix.handle, 0, 7) == -1
+    assert b"storage" in L.frog_last_error()
+    with pytest.raises(ValueError):
+        ix.upload(0, storage="bf16")
+    X2 = X.copy()
+    X2[10, 2] = 65520.0          # rounds to infinity
+    ix2 = F.Index.from_arrays(X2, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
+    assert L.frog_index_upload_ex(ix2.handle, 0, F.STORAGE_F16) == -7
+    assert b"fp16 range" in L.frog_last_error()
+    Xw = np.zeros((64, 130), np.float32)
+    ix3 = F.Index.from_arrays(Xw, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
+    assert L.frog_index_upload_ex(ix3.handle, 0, F.STORAGE_F16) == -7
+    assert b"d <= 128" in L.frog_last_error()
+
+
 def test_save_load_roundtrip_and_corruption(tmp_path):
     w = workloads.make("tiny", n=1500, nq=1)
     ix = F.Index.build(w.X, w.attr)

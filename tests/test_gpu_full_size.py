@@ -127,3 +127,33 @@ def test_full_size_k100_pool256_sampled(c2):
     o_ids, o_d, _ = oracle.search(ox, Q[sample], lo[sample], hi[sample], 100, 256, qidx=sample,
                                   epn=16, epn_frac=1.0, epn_max=3072, B=16)
     assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("mode", [1, 0])
+def test_full_size_fp16_rows_sampled(c2, mode):
+    """The same 1M index uploaded with fp16 rows at the timed setting: sampled
+    rows equal the oracle's search over the rows rounded to binary16 (numpy's
+    rounding), and every distance is the squared L2 to the rounded row."""
+    w, ix, ox, d = c2
+    oh = oracle.OracleIndex(ox.perm, ox.attr_sorted, ox.X_rank.astype(np.float16).astype(np.float32), ox.ENC)
+    p = SETTINGS[mode]
+    try:
+        ix.upload(0, storage="fp16")
+        ids, ds = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **p)
+        torch.cuda.synchronize()
+    finally:
+        ix.upload(0)
+    ids, ds = ids.cpu().numpy(), ds.cpu().numpy()
+    rng = np.random.default_rng(7)
+    sample = np.sort(rng.choice(w.nq, 300, replace=False))
+    o_ids, o_d, _ = oracle.search(oh, w.Q[sample], w.lo[sample], w.hi[sample], K, L, qidx=sample,
+                                  epn=p["epn"], epn_frac=p["epn_frac"], epn_max=p["epn_max"], B=p["budget"],
+                                  entry_mode=mode)
+    assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
+    valid = ids >= 0
+    qi, kj = np.nonzero(valid)
+    Xh = w.X.astype(np.float16).astype(np.float64)
+    ref = ((Xh[ids[qi, kj]] - w.Q[qi].astype(np.float64)) ** 2).sum(1).astype(np.float32)
+    got = ds[qi, kj]
+    assert (np.abs(got - ref) <= np.spacing(ref)).all()
