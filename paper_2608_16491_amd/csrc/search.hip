@@ -213,23 +213,39 @@ __device__ void hotspot(int64_t l, int64_t r, int H, int64_t n, int& Ls, int& Le
 
 // ------------------------------------------------------------------ a8: distances
 
-// Chunk c (of C = dp/32) of row `id` that lane `sub` (of 8) reads, as 4
-// floats.  fp32 rows: float4 number sub + 8c of the row.  fp16 rows (dp a
-// multiple of 64): the lane's 16-byte piece sub + 8(c/2) holds 8 halves, of
-// which chunk c is the first or second 4, converted exactly to float.
-template <typename XT>
-__device__ __forceinline__ float4 row_chunk(const XT* __restrict__ X, int dp, int64_t id, int sub, int c) {
+// Row layout a lane reads (C = dp / 32 float4 chunks per lane, 8 lanes per
+// row).  fp32 rows: chunk c of lane `sub` is float4 number sub + 8c of the
+// row.  fp16 rows (dp a multiple of 64): the lane's 16-byte piece sub + 8(c/2)
+// holds 8 halves, of which chunk c is the first or second 4, widened exactly
+// to float.
+// All C chunks of row `id` for lane `sub` (zeros when !v).  fp16 rows take
+// one 16-byte load per pair of chunks, so that the 8 lanes of a row read
+// 128 contiguous bytes per instruction, as for fp32 rows.
+template <int C, typename XT>
+__device__ __forceinline__ void load_row(const XT* __restrict__ X, int dp, int64_t id, int sub, bool v,
+                                         float4 (&x)[C]) {
     if constexpr (sizeof(XT) == 4) {
-        return reinterpret_cast<const float4*>(X)[id * (dp >> 2) + sub + 8 * c];
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+            x[c] = v ? reinterpret_cast<const float4*>(X)[id * (dp >> 2) + sub + 8 * c]
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
     } else {
-        const uint2 h = *reinterpret_cast<const uint2*>(X + id * dp + 8 * (sub + 8 * (c >> 1)) + 4 * (c & 1));
-        const float2 a = __half22float2(__builtin_bit_cast(__half2, h.x));
-        const float2 b = __half22float2(__builtin_bit_cast(__half2, h.y));
-        return make_float4(a.x, a.y, b.x, b.y);
+        static_assert(C % 2 == 0, "fp16 rows come in pairs of chunks");
+#pragma unroll
+        for (int p = 0; p < C / 2; ++p) {
+            const uint4 h = v ? reinterpret_cast<const uint4*>(X)[id * (dp >> 3) + sub + 8 * p]
+                              : make_uint4(0u, 0u, 0u, 0u);
+            const float2 a = __half22float2(__builtin_bit_cast(__half2, h.x));
+            const float2 b = __half22float2(__builtin_bit_cast(__half2, h.y));
+            const float2 c2 = __half22float2(__builtin_bit_cast(__half2, h.z));
+            const float2 e = __half22float2(__builtin_bit_cast(__half2, h.w));
+            x[2 * p] = make_float4(a.x, a.y, b.x, b.y);
+            x[2 * p + 1] = make_float4(c2.x, c2.y, e.x, e.y);
+        }
     }
 }
 
-// The query dimensions a lane pairs with chunk c (same layout as row_chunk).
+// The query dimensions a lane pairs with chunk c (the layout of load_row).
 template <typename XT>
 __device__ __forceinline__ int chunk_dim(int sub, int c) {
     if constexpr (sizeof(XT) == 4) return 4 * (sub + 8 * c);
@@ -252,9 +268,7 @@ __device__ float eval_small(const XT* __restrict__ X, int dp, const float4 (&qv)
         const int id = __shfl(myid, j & 63);
         const bool v = j < cnt;
         float4 x[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c)
-            x[c] = v ? row_chunk<XT>(X, dp, id, sub, c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        load_row<C, XT>(X, dp, id, sub, v, x);
         double s = 0.0;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
@@ -290,9 +304,7 @@ struct Gather16 {
             const int j = sb0 + 8 * g + (lane >> 3);
             const int id = __shfl(myid, j & 63);
             const bool v = j < cnt;
-#pragma unroll
-            for (int c = 0; c < C; ++c)
-                x[g][c] = v ? row_chunk<XT>(X, dp, id, sub, c) : make_float4(0.f, 0.f, 0.f, 0.f);
+            load_row<C, XT>(X, dp, id, sub, v, x[g]);
         }
     }
     __device__ __forceinline__ void consume(const float4 (&qv)[C], int sb0, float& mine) const {
