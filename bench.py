@@ -108,6 +108,8 @@ def main():
                     help="also measure the ablations of Sec 8.4 at the chosen setting: hotspot without its end "
                          "condition / without localisation, eager visited check, and (rebuilding the index) "
                          "beta = 0; reported under 'ablation' in --details")
+    ap.add_argument("--no-gpu-build", action="store_true",
+                    help="skip timing the GPU construction against the host one")
     ap.add_argument("--no-fp16", action="store_true",
                     help="skip the secondary measurement with the rows stored in fp16")
     ap.add_argument("--storage", default="fp32", choices=("fp32", "fp16"),
@@ -140,6 +142,24 @@ def main():
     t_build = time.time() - t0
     n, d, H, m = ix.info()
     log(f"host build: {t_build:.1f}s  H={H} m={m}")
+    # the same construction on the GPU (Sec 6): timed, and checked equal to
+    # the host's entry for entry
+    gpu_build = None
+    if not args.no_gpu_build and not args.profile_pass:
+        torch.cuda.synchronize()
+        t0 = time.time()
+        gix = F.Index.build(w.X, w.attr, device=0)
+        t_gb = time.time() - t0
+        g_enc = gix.export()["ENC"]
+        same = bool((g_enc == ix.export()["ENC"]).all())
+        gd, ge = gix.build_stats()
+        gix.free()
+        del g_enc
+        host_ref = None if (args.index_cache and os.path.exists(args.index_cache)) else t_build
+        gpu_build = {"s": t_gb, "host_s": host_ref, "speedup": (host_ref / t_gb) if host_ref else None,
+                     "equal_to_host": same, "distances": gd, "expansions": ge}
+        log(f"GPU build: {t_gb:.2f}s (host {t_build:.1f}s{' loaded from cache' if host_ref is None else ''}), "
+            f"ENC equal to the host build: {same}, {gd} distances, {ge} sibling-search expansions")
     ix.upload(0)
     Q = torch.as_tensor(w.Q, device=dev)
     lo = torch.as_tensor(w.lo, device=dev)
@@ -496,6 +516,9 @@ def main():
         # the same search with the rows stored in fp16 (secondary; the
         # metric above is fp32)
         "fp16_storage": fp16,
+        # index construction (Sec 6) on the GPU, wall time including the host
+        # sort and the copies, against the host construction
+        "gpu_build": gpu_build,
         "bruteforce": {"ms": bf_time * 1e3, "qps": w.nq / bf_time, "recall@10": 1.0,
                        "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,

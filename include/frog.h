@@ -125,6 +125,24 @@ void frog_search_params_default(frog_search_params_t* p);
 int frog_build_index(const float* X, const double* attr, int64_t n, int d,
                      const frog_build_params_t* p, frog_index_t** out);
 
+/* The same construction on HIP device `device`: the host sorts by attribute
+ * and tabulates the fusion-distance factors; the leaf brute force and every
+ * layer (child m-ANN, sibling greedy search with patience, RNG prune, fusion
+ * re-rank; Sec 6, Alg. 1) run as kernels, one wavefront per vertex, with the
+ * construction's distances (dimension order, double accumulation, one
+ * rounding), so the candidate array equals frog_build_index's entry for
+ * entry.  X, attr: host arrays as for frog_build_index.  On success *out owns
+ * a host index whose device copy (fp32 rows) is already uploaded on `device`.
+ * Errors: as frog_build_index; FROG_EUNSUPPORTED unless d <= 1024, m <= 32,
+ * ef_c <= 256 and sib_seeds <= 64; FROG_EHIP / FROG_ENOMEM from the device.
+ * p->num_threads only sizes the host part. */
+int frog_build_index_gpu(const float* X, const double* attr, int64_t n, int d,
+                         const frog_build_params_t* p, int device, frog_index_t** out);
+
+/* Work of the last GPU construction of idx: distances evaluated and
+ * sibling-search expansions (both 0 for a host-built index). */
+int frog_index_build_stats(const frog_index_t* idx, int64_t* distances, int64_t* expansions);
+
 /* Wrap already-built arrays (copied): X_rank n x d floats in rank order,
  * attr_sorted n ascending doubles, perm n ints (rank -> original index, a
  * permutation), ENC n x H x m ints (each entry -1 or a rank).  Validates sizes,

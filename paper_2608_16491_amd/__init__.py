@@ -28,7 +28,8 @@ STORAGE = {"fp32": STORAGE_F32, "fp16": STORAGE_F16}
 SYMBOLS = (
     "frog_build_params_default", "frog_search_params_default", "frog_build_index",
     "frog_index_from_arrays", "frog_index_export", "frog_index_info", "frog_index_save",
-    "frog_index_load", "frog_index_upload", "frog_index_upload_ex", "frog_index_free", "frog_rank_bounds", "frog_search",
+    "frog_index_load", "frog_index_upload", "frog_index_upload_ex", "frog_index_free",
+    "frog_build_index_gpu", "frog_index_build_stats", "frog_rank_bounds", "frog_search",
     "frog_search_ex", "frog_bruteforce_filtered", "frog_last_error",
 )
 
@@ -87,6 +88,10 @@ def lib() -> C.CDLL:
     L.frog_index_upload.restype = i32
     L.frog_index_upload.argtypes = [P, i32]
     L.frog_index_upload_ex.restype = i32
+    L.frog_build_index_gpu.restype = i32
+    L.frog_build_index_gpu.argtypes = [P, P, i64, i32, C.POINTER(BuildParams), i32, C.POINTER(P)]
+    L.frog_index_build_stats.restype = i32
+    L.frog_index_build_stats.argtypes = [P, C.POINTER(i64), C.POINTER(i64)]
     L.frog_index_upload_ex.argtypes = [P, i32, i32]
     L.frog_index_free.restype = None
     L.frog_index_free.argtypes = [P]
@@ -142,15 +147,28 @@ class Index:
 
     # -- construction
     @classmethod
-    def build(cls, X, attr, **params) -> "Index":
+    def build(cls, X, attr, device=None, **params) -> "Index":
+        """Construct the index (Sec 6) on the host, or with device=k on HIP
+        device k (same result; the device copy is then already uploaded)."""
         X = _np(X, np.float32)
         attr = _np(attr, np.float64)
         n, d = X.shape
         assert attr.shape == (n,)
         p = build_params(d, **params)
         h = C.c_void_p()
-        _check(lib().frog_build_index(_ptr(X), _ptr(attr), n, d, C.byref(p), C.byref(h)))
-        return cls(h.value)
+        if device is None:
+            _check(lib().frog_build_index(_ptr(X), _ptr(attr), n, d, C.byref(p), C.byref(h)))
+            return cls(h.value)
+        _check(lib().frog_build_index_gpu(_ptr(X), _ptr(attr), n, d, C.byref(p), int(device), C.byref(h)))
+        ix = cls(h.value)
+        ix.storage = "fp32"
+        return ix
+
+    def build_stats(self):
+        """(distances, sibling-search expansions) of a GPU construction."""
+        a, b = C.c_int64(), C.c_int64()
+        _check(lib().frog_index_build_stats(self._h, C.byref(a), C.byref(b)))
+        return a.value, b.value
 
     @classmethod
     def from_arrays(cls, X_rank, attr_sorted, perm, ENC) -> "Index":

@@ -23,7 +23,7 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["build_index.cpp"]
-HIP_SOURCES = ["capi.cpp", "search.hip", "bruteforce.hip"]
+HIP_SOURCES = ["capi.cpp", "search.hip", "bruteforce.hip", "build_gpu.hip"]
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

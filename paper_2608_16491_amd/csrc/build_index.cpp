@@ -289,15 +289,7 @@ int layers_for(int64_t n, int n_inv) {
     return H < 1 ? 1 : H;
 }
 
-int build_host(const float* X, const double* attr, int64_t n, int d,
-               const frog_build_params_t& p, frog_index* out) {
-    const int m = p.m, ef = p.ef_c, ns = p.sib_seeds;
-    int threads = p.num_threads;
-    if (threads <= 0) {
-        unsigned hw = std::thread::hardware_concurrency();
-        threads = hw ? (int)hw : 1;
-    }
-
+int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int n_inv, frog_index* out) {
     // attribute-rank domain (Sec 4): stable sort by (value, original index)
     for (int64_t i = 0; i < n; ++i)
         if (std::isnan(attr[i])) return fail(FROG_EINVAL, "attribute %lld is NaN", (long long)i);
@@ -306,7 +298,7 @@ int build_host(const float* X, const double* attr, int64_t n, int d,
     std::sort(perm.begin(), perm.end(), [&](int32_t a, int32_t b) {
         return attr[a] < attr[b] || (attr[a] == attr[b] && a < b);
     });
-    const int H = layers_for(n, p.n_inv);
+    const int H = layers_for(n, n_inv);
     out->n = n;
     out->d = d;
     out->H = H;
@@ -323,6 +315,72 @@ int build_host(const float* X, const double* attr, int64_t n, int d,
         out->attr[(size_t)i] = attr[perm[(size_t)i]];
         std::memcpy(&out->X[(size_t)i * d], X + (int64_t)perm[(size_t)i] * d, sizeof(float) * (size_t)d);
     }
+    return FROG_OK;
+}
+
+int host_threads(int requested) {
+    if (requested > 0) return requested;
+    unsigned hw = std::thread::hardware_concurrency();
+    return hw ? (int)hw : 1;
+}
+
+int fusion_weights(int64_t n, int H, double beta, double gamma, int threads, std::vector<double>& tab,
+                   std::vector<int64_t>& meta) {
+    // segment lengths at depth h take at most two consecutive values: a
+    // segment of length l splits into ceil(l/2) and floor(l/2)
+    meta.assign((size_t)4 * H, 0);
+    int64_t lo = n, hi = n, total = 0;
+    for (int h = 0; h < H; ++h) {
+        meta[(size_t)4 * h + 0] = lo;
+        meta[(size_t)4 * h + 1] = total;
+        total += lo;
+        meta[(size_t)4 * h + 2] = hi;
+        meta[(size_t)4 * h + 3] = hi == lo ? meta[(size_t)4 * h + 1] : total;
+        if (hi != lo) total += hi;
+        const int64_t nlo = lo / 2, nhi = (hi + 1) / 2;
+        lo = nlo > 0 ? nlo : 1;
+        hi = nhi > 0 ? nhi : 1;
+    }
+    try {
+        tab.assign((size_t)std::max<int64_t>(total, 1), 0.0);
+    } catch (const std::bad_alloc&) {
+        return fail(FROG_ENOMEM, "fusion weight table of %lld entries", (long long)total);
+    }
+    // the factor fusion() applies to the L2 distance, term by term the same
+    // expression, for every offset |ru - rv| of a segment of each length
+    std::vector<std::pair<int64_t, int64_t>> lens;
+    for (int h = 0; h < H; ++h)
+        for (int k = 0; k < 2; ++k) {
+            const int64_t len = meta[(size_t)4 * h + 2 * k], off = meta[(size_t)4 * h + 2 * k + 1];
+            if (k == 1 && off == meta[(size_t)4 * h + 1]) continue;
+            lens.emplace_back(len, off);
+        }
+    const int64_t chunk = 1 << 16;
+    int64_t units = 0;
+    std::vector<std::pair<size_t, int64_t>> work;   // (length index, first offset)
+    for (size_t i = 0; i < lens.size(); ++i)
+        for (int64_t b = 0; b < lens[i].first; b += chunk) { work.emplace_back(i, b); ++units; }
+    parallel_for(units, threads, 1, [&](int64_t wi, int) {
+        const int64_t len = lens[(size_t)work[(size_t)wi].first].first;
+        const int64_t off = lens[(size_t)work[(size_t)wi].first].second;
+        const int64_t b = work[(size_t)wi].second, e = std::min(len, b + chunk);
+        if (len < 2) return;
+        for (int64_t diff = b; diff < e; ++diff) {
+            double da = (double)diff / (double)(len - 1);
+            double w = 1.0 - beta * (1.0 - std::pow(da, gamma));
+            tab[(size_t)(off + diff)] = w;
+        }
+    });
+    return FROG_OK;
+}
+
+int build_host(const float* X, const double* attr, int64_t n, int d,
+               const frog_build_params_t& p, frog_index* out) {
+    const int m = p.m, ef = p.ef_c, ns = p.sib_seeds;
+    const int threads = host_threads(p.num_threads);
+    int rc = rank_order(X, attr, n, d, m, p.n_inv, out);
+    if (rc != FROG_OK) return rc;
+    const int H = out->H;
     const float* Xr = out->X.data();
     int32_t* ENC = out->ENC.data();
     const double beta = p.beta, gamma = p.gamma;

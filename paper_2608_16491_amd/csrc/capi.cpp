@@ -164,6 +164,49 @@ void frog_search_params_default(frog_search_params_t* p) {
     p->eager_check = 0;
 }
 
+static int check_build_args(const float* X, const double* attr, int64_t n, int d, const frog_build_params_t* p,
+                            frog_index_t** out, frog_build_params_t* q) {
+    if (!out) return fail(FROG_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!X || !attr) return fail(FROG_EINVAL, "X or attr is NULL");
+    if (n < 1 || n > INT32_MAX - 1) return fail(FROG_EINVAL, "n=%lld outside [1, 2^31-2]", (long long)n);
+    if (d < 1 || d > 65536) return fail(FROG_EINVAL, "d=%d outside [1, 65536]", d);
+    if (p) *q = *p; else frog_build_params_default(d, q);
+    if (q->m < 1 || q->m > 64) return fail(FROG_EINVAL, "m=%d outside [1, 64]", q->m);
+    if (q->ef_c < q->m || q->ef_c > 4096) return fail(FROG_EINVAL, "ef_c=%d outside [m, 4096]", q->ef_c);
+    if (q->n_inv < 0 || q->n_inv > 40) return fail(FROG_EINVAL, "n_inv=%d outside [0, 40]", q->n_inv);
+    if (q->patience < 1) return fail(FROG_EINVAL, "patience=%d < 1", q->patience);
+    if (q->sib_seeds < 1 || q->sib_seeds > 4096)
+        return fail(FROG_EINVAL, "sib_seeds=%d outside [1, 4096]", q->sib_seeds);
+    if (!(q->beta >= 0.0 && q->beta < 1.0) || !(q->gamma > 0.0))
+        return fail(FROG_EINVAL, "beta=%g must be in [0,1), gamma=%g > 0", q->beta, q->gamma);
+    return FROG_OK;
+}
+
+int frog_build_index_gpu(const float* X, const double* attr, int64_t n, int d, const frog_build_params_t* p,
+                         int device, frog_index_t** out) {
+    frog::clear_error();
+    frog_build_params_t q;
+    int rc = check_build_args(X, attr, n, d, p, out, &q);
+    if (rc) return rc;
+    if (!frog::device_build_supported(d, q))
+        return fail(FROG_EUNSUPPORTED, "GPU construction needs d <= 1024, m <= 32, ef_c <= 256, sib_seeds <= 64");
+    frog_index* ix = new (std::nothrow) frog_index;
+    if (!ix) return fail(FROG_ENOMEM, "allocation failed");
+    rc = frog::build_device(X, attr, n, d, q, device, ix);
+    if (rc != FROG_OK) { delete ix; return rc; }
+    *out = ix;
+    return FROG_OK;
+}
+
+int frog_index_build_stats(const frog_index_t* ix, int64_t* distances, int64_t* expansions) {
+    frog::clear_error();
+    if (!ix) return fail(FROG_EINVAL, "index is NULL");
+    if (distances) *distances = ix->build_distances;
+    if (expansions) *expansions = ix->build_expansions;
+    return FROG_OK;
+}
+
 int frog_build_index(const float* X, const double* attr, int64_t n, int d,
                      const frog_build_params_t* p, frog_index_t** out) {
     frog::clear_error();

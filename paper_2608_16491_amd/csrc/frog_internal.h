@@ -28,6 +28,8 @@ struct frog_index {
     double* dattr = nullptr;
     int32_t* dperm = nullptr;
     float maxnorm = -1.f;        // largest squared norm of the stored rows, computed on first use
+    // work of the GPU construction: distances evaluated, sibling-search expansions
+    int64_t build_distances = 0, build_expansions = 0;
     // shared entry sample (entry_mode 1): for one seed, the ascending rank
     // lists of levels 1..nlev (level j: ranks whose priority is below
     // 2^(32-j)), concatenated on the device; built on first use
@@ -52,6 +54,21 @@ void clear_error();
 int build_host(const float* X, const double* attr, int64_t n, int d,
                const frog_build_params_t& p, frog_index* out);
 int layers_for(int64_t n, int n_inv);
+// the attribute-rank order (Sec 4) of the input: out's n, d, H, m, perm,
+// attr, X (rank order) and ENC (all -1)
+int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int n_inv, frog_index* out);
+int host_threads(int requested);
+// The fusion-distance factor 1 - beta (1 - (|ru - rv| / (len - 1))^gamma) of
+// every offset of every segment length, as the host construction computes
+// it: depth h's lengths are meta[4h] and meta[4h + 2], their offsets' factors
+// start at tab[meta[4h + 1]] and tab[meta[4h + 3]].
+int fusion_weights(int64_t n, int H, double beta, double gamma, int threads, std::vector<double>& tab,
+                   std::vector<int64_t>& meta);
+// GPU construction (build_gpu.hip): the same index as build_host, with the
+// device copy (fp32 rows) left uploaded on `device`
+int build_device(const float* X, const double* attr, int64_t n, int d, const frog_build_params_t& p,
+                 int device, frog_index* out);
+bool device_build_supported(int d, const frog_build_params_t& p);
 
 // device index view passed to the kernels
 struct DevIndex {

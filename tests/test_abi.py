@@ -91,6 +91,20 @@ def test_device_calls_need_an_uploaded_index():
     assert rc == -1
 
 
+def test_gpu_build_rejects_unsupported_shapes_on_the_host():
+    # checked before any device is touched
+    X, attr = _small_index(64, 4)
+    with pytest.raises(F.FrogError) as e:
+        F.Index.build(X, attr, device=0, m=64, ef_c=128)
+    assert e.value.code == -7
+    with pytest.raises(F.FrogError) as e:
+        F.Index.build(X, attr, device=0, m=16, ef_c=512)
+    assert e.value.code == -7
+    with pytest.raises(F.FrogError) as e:
+        F.Index.build(X, attr, device=0, beta=1.5)
+    assert e.value.code == -1
+
+
 def test_fp16_upload_rejects_on_the_host():
     # checked before any device is touched: unknown storage, d > 128, a
     # value that rounds past the largest binary16 (65504)

@@ -157,3 +157,21 @@ def test_full_size_fp16_rows_sampled(c2, mode):
     ref = ((Xh[ids[qi, kj]] - w.Q[qi].astype(np.float64)) ** 2).sum(1).astype(np.float32)
     got = ds[qi, kj]
     assert (np.abs(got - ref) <= np.spacing(ref)).all()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_gpu_construction_equals_host(c2):
+    """The 1M x 128 index built on the GPU equals the host construction (whose
+    equality with the oracle's is established on smaller inputs) entry for
+    entry: rank order, rows and all n x H x m candidates."""
+    import time
+    w, ix, ox, d = c2
+    t0 = time.time()
+    g = F.Index.build(w.X, w.attr, device=0)
+    print(f"[gpu] full-size construction on the GPU: {time.time() - t0:.2f}s", flush=True)
+    e = g.export()
+    assert (e["perm"] == ox.perm).all()
+    assert (e["X_rank"] == ox.X_rank).all()
+    diff = np.argwhere(e["ENC"] != ox.ENC)
+    assert len(diff) == 0, f"{len(diff)} entries differ, first at {diff[:3].tolist()}"
+    g.free()
