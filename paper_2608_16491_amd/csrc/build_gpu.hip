@@ -100,7 +100,7 @@ __device__ __forceinline__ void segment_of(int64_t n, int h, int64_t p, int64_t&
 // padding adds +0 and changes nothing).
 __device__ __forceinline__ float dist_seq(const float* __restrict__ a, const float* __restrict__ b, int dp) {
     double s = 0.0;
-#pragma unroll 2
+#pragma unroll 8
     for (int i = 0; i < dp; i += 4) {
         const float4 x = *reinterpret_cast<const float4*>(a + i);
         const float4 y = *reinterpret_cast<const float4*>(b + i);
@@ -111,6 +111,27 @@ __device__ __forceinline__ float dist_seq(const float* __restrict__ a, const flo
         t = (double)x.z - (double)y.z;
         s = s + t * t;
         t = (double)x.w - (double)y.w;
+        s = s + t * t;
+    }
+    return (float)s;
+}
+
+// The same distance with the first row already widened to double (the
+// vertex's own row, kept in LDS): t = a_i - (double)b_i as above.
+__device__ __forceinline__ float dist_seq_q(const double* __restrict__ a, const float* __restrict__ b, int dp) {
+    double s = 0.0;
+#pragma unroll 8
+    for (int i = 0; i < dp; i += 4) {
+        const double2 x0 = *reinterpret_cast<const double2*>(a + i);
+        const double2 x1 = *reinterpret_cast<const double2*>(a + i + 2);
+        const float4 y = *reinterpret_cast<const float4*>(b + i);
+        double t = x0.x - (double)y.x;
+        s = s + t * t;
+        t = x0.y - (double)y.y;
+        s = s + t * t;
+        t = x1.x - (double)y.z;
+        s = s + t * t;
+        t = x1.y - (double)y.w;
         s = s + t * t;
     }
     return (float)s;
@@ -309,11 +330,11 @@ __device__ bool bpool_merge(BPool<LP>& P, uint64_t nkey, bool cand, int cap, int
 // LDS per wavefront of the layer kernel
 __host__ __device__ inline size_t layer_region_bytes(int m, int hash_log2) {
     const size_t tab = (size_t)4 << hash_log2;
-    const size_t pairs = (size_t)4 * (2 * m) * (2 * m);
+    const size_t pairs = (size_t)16 * (m + 3);   // the prune's distances of a round
     return tab > pairs ? tab : pairs;
 }
 __host__ __device__ inline size_t layer_lds_per_wave(int dp, int m, int hash_log2, int lp) {
-    return (size_t)dp * 4 + layer_region_bytes(m, hash_log2) + (size_t)64 * lp * 12 + (size_t)64 * 12;
+    return (size_t)dp * 8 + layer_region_bytes(m, hash_log2) + (size_t)64 * lp * 12 + (size_t)64 * 12;
 }
 
 template <int LP>
@@ -325,10 +346,10 @@ __global__ __launch_bounds__(kBBlock) void layer_kernel(BArgs A) {
     if (u >= A.n) return;   // wave-uniform; no workgroup barrier follows
     const int h = A.h, m = A.m, dp = A.dp, ef = A.ef;
     char* wb = smem + (size_t)wave * A.lds_per_wave;
-    float* xu = reinterpret_cast<float*>(wb);
-    char* region = wb + (size_t)dp * 4;
-    int32_t* tab = reinterpret_cast<int32_t*>(region);        // visited table, then the pair distances
-    float* pd = reinterpret_cast<float*>(region);
+    double* xu = reinterpret_cast<double*>(wb);   // u's row, widened
+    char* region = wb + (size_t)dp * 8;
+    int32_t* tab = reinterpret_cast<int32_t*>(region);        // visited table, then the prune's distances
+    float* gd = reinterpret_cast<float*>(region);
     uint64_t* st_key = reinterpret_cast<uint64_t*>(region + layer_region_bytes(m, A.hash_log2));
     uint32_t* st_flag = reinterpret_cast<uint32_t*>(st_key + 64 * LP);
     int32_t* sid = reinterpret_cast<int32_t*>(st_flag + 64 * LP);  // up to 64 ids in sorted order
@@ -342,8 +363,7 @@ __global__ __launch_bounds__(kBBlock) void layer_kernel(BArgs A) {
     const int64_t mid = s + (e - s) / 2;
     int64_t ts, te;
     if (u <= mid) { ts = mid + 1; te = e; } else { ts = s; te = mid; }
-    const float4* xr = reinterpret_cast<const float4*>(A.X + u * dp);
-    for (int i = lane; i < dp / 4; i += 64) reinterpret_cast<float4*>(xu)[i] = xr[i];
+    for (int i = lane; i < dp; i += 64) xu[i] = (double)A.X[u * dp + i];
     for (int i = lane; i <= (int)tmask; i += 64) tab[i] = -1;
     wave_sync();
     unsigned long long nd = 0, nexp = 0;
@@ -351,7 +371,7 @@ __global__ __launch_bounds__(kBBlock) void layer_kernel(BArgs A) {
     // the child layer's row: m-ANN of u inside its own child segment
     const int32_t va = lane < m ? A.PGc[u * m + lane] : kNone;
     float da = 0.f;
-    if (va != kNone) da = dist_seq(xu, A.X + (int64_t)va * dp, dp);
+    if (va != kNone) da = dist_seq_q(xu, A.X + (int64_t)va * dp, dp);
     nd += __popcll(ballot(va != kNone));
 
     // greedy search of Alg. 1 over the sibling's temporary graph
@@ -380,7 +400,7 @@ __global__ __launch_bounds__(kBBlock) void layer_kernel(BArgs A) {
         const bool isv = lane < ns;
         if (isv) tab[((uint32_t)sv * 0x9E3779B1u) >> (32 - A.hash_log2)] = sv;
         float ds = 0.f;
-        if (isv) ds = dist_seq(xu, A.X + (int64_t)sv * dp, dp);
+        if (isv) ds = dist_seq_q(xu, A.X + (int64_t)sv * dp, dp);
         nd += (unsigned long long)ns;
         bpool_merge<LP>(P, isv ? dkey(ds, sv) : kEmptyKey, isv, ef, m, st_key, st_flag);
         int left = A.patience;
@@ -411,7 +431,7 @@ __global__ __launch_bounds__(kBBlock) void layer_kernel(BArgs A) {
                 else tab[slot] = v;
             }
             float dv = 0.f;
-            if (fresh) dv = dist_seq(xu, A.X + (int64_t)v * dp, dp);
+            if (fresh) dv = dist_seq_q(xu, A.X + (int64_t)v * dp, dp);
             nd += __popcll(ballot(fresh));
             const bool improved = bpool_merge<LP>(P, fresh ? dkey(dv, v) : kEmptyKey, fresh, ef, m, st_key, st_flag);
             if (improved) {
@@ -444,32 +464,48 @@ __global__ __launch_bounds__(kBBlock) void layer_kernel(BArgs A) {
     if (cv) { sid[rank] = key_id(ck); sdist[rank] = key_dist(ck); }
     wave_sync();
 
-    // RNG prune: the distances between candidates, then the sequential test
-    const int S = 2 * m;
-    const int npair = nc * (nc - 1) / 2;
-    for (int p0 = 0; p0 < npair; p0 += 64) {
-        const int p = p0 + lane;
-        if (p < npair) {
-            // p = i (i - 1) / 2 + j with 0 <= j < i
-            int i = (int)((1.0 + sqrt(1.0 + 8.0 * (double)p)) * 0.5);
-            while (i * (i - 1) / 2 > p) --i;
-            while ((i + 1) * i / 2 <= p) ++i;
-            const int j = p - i * (i - 1) / 2;
-            pd[i * S + j] = dist_seq(A.X + (int64_t)sid[i] * dp, A.X + (int64_t)sid[j] * dp, dp);
-        }
-    }
-    nd += (unsigned long long)npair;
-    wave_sync();
+    // RNG prune (alpha = 1) in candidate order, four candidates per round:
+    // each is tested against the rows kept before the round and against the
+    // round's earlier candidates, and kept unless one of the kept rows is
+    // closer to it than u is.  These are the decisions of the one-by-one
+    // test (its early exit only skips distances).
+    const int G = m + 3;   // member gi's distances at gd[gi G + slot]
     uint64_t kept = 0;
     int nk = 0;
-    for (int i = 0; i < nc && nk < m; ++i) {
-        const float di = sdist[i];
-        const bool viol = lane < i && ((kept >> lane) & 1ull) && pd[i * S + lane] < di;
-        if (ballot(viol) == 0) {
-            kept |= 1ull << i;
-            if (lane == 0) outp[nk] = sid[i];
-            ++nk;
+    for (int i0 = 0; i0 < nc && nk < m; i0 += 4) {
+        const int g = nc - i0 < 4 ? nc - i0 : 4;
+        const int nk0 = nk;
+        // member gi: slots [0, nk0) the rows kept so far, then the round's
+        // members before it; its pairs start at gi nk0 + gi (gi - 1) / 2
+        const int npair = g * nk0 + g * (g - 1) / 2;
+        for (int p0 = 0; p0 < npair; p0 += 64) {
+            const int p = p0 + lane;
+            if (p < npair) {
+                int gi = 0;
+                while (gi + 1 < g && (gi + 1) * nk0 + (gi + 1) * gi / 2 <= p) ++gi;
+                const int slot = p - (gi * nk0 + gi * (gi - 1) / 2);
+                const int32_t other = slot < nk0 ? outp[slot] : sid[i0 + slot - nk0];
+                gd[gi * G + slot] = dist_seq(A.X + (int64_t)sid[i0 + gi] * dp, A.X + (int64_t)other * dp, dp);
+            }
         }
+        nd += (unsigned long long)npair;
+        wave_sync();
+        uint32_t acc = 0;   // members kept in this round
+        for (int gi = 0; gi < g && nk < m; ++gi) {
+            const float di = sdist[i0 + gi];
+            bool viol = false;
+            if (lane < nk0 + gi) {
+                const bool live = lane < nk0 || ((acc >> (lane - nk0)) & 1u);
+                viol = live && gd[gi * G + lane] < di;
+            }
+            if (ballot(viol) == 0) {
+                acc |= 1u << gi;
+                kept |= 1ull << (i0 + gi);
+                if (lane == 0) outp[nk] = sid[i0 + gi];
+                ++nk;
+            }
+        }
+        wave_sync();
     }
     for (int i = 0; i < nc && nk < m; ++i)
         if (!((kept >> i) & 1ull)) {
@@ -549,7 +585,7 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
     if (rc != FROG_OK) return rc;
     const int dp = (d + 31) / 32 * 32;
     const int lp = p.ef_c <= 64 ? 1 : (p.ef_c <= 128 ? 2 : 4);
-    const int hash_log2 = 11;
+    const int hash_log2 = 9;
 
     int prev = 0;
     if (hipGetDevice(&prev) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
