@@ -91,7 +91,7 @@ def lib() -> C.CDLL:
     L.frog_build_index_gpu.restype = i32
     L.frog_build_index_gpu.argtypes = [P, P, i64, i32, C.POINTER(BuildParams), i32, C.POINTER(P)]
     L.frog_index_build_stats.restype = i32
-    L.frog_index_build_stats.argtypes = [P, C.POINTER(i64), C.POINTER(i64)]
+    L.frog_index_build_stats.argtypes = [P, C.POINTER(i64), C.POINTER(i64), C.POINTER(C.c_double)]
     L.frog_index_upload_ex.argtypes = [P, i32, i32]
     L.frog_index_free.restype = None
     L.frog_index_free.argtypes = [P]
@@ -165,10 +165,11 @@ class Index:
         return ix
 
     def build_stats(self):
-        """(distances, sibling-search expansions) of a GPU construction."""
-        a, b = C.c_int64(), C.c_int64()
-        _check(lib().frog_index_build_stats(self._h, C.byref(a), C.byref(b)))
-        return a.value, b.value
+        """(distances, sibling-search expansions, kernel milliseconds) of a
+        GPU construction."""
+        a, b, t = C.c_int64(), C.c_int64(), C.c_double()
+        _check(lib().frog_index_build_stats(self._h, C.byref(a), C.byref(b), C.byref(t)))
+        return a.value, b.value, t.value
 
     @classmethod
     def from_arrays(cls, X_rank, attr_sorted, perm, ENC) -> "Index":

@@ -640,6 +640,13 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
         cleanup();
         return fail(FROG_EHIP, "construction upload: %s", hipGetErrorString(e));
     }
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    if (hipEventCreate(&ev0) != hipSuccess || hipEventCreate(&ev1) != hipSuccess) {
+        if (ev0) (void)hipEventDestroy(ev0);
+        cleanup();
+        return fail(FROG_EHIP, "hipEventCreate failed");
+    }
+    (void)hipEventRecord(ev0, stream);
     hipLaunchKernelGGL(fill_kernel, dim3((unsigned)((nE + 255) / 256)), dim3(256), 0, stream, dENC, (int64_t)nE, kNone);
 
     BArgs A{};
@@ -666,6 +673,9 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
     hipLaunchKernelGGL(leaf_kernel, dim3((unsigned)blocks), dim3(kBBlock), (size_t)A.lds_per_wave * kBW, stream, A);
     e = hipGetLastError();
     if (e != hipSuccess) {
+        (void)hipDeviceSynchronize();
+        (void)hipEventDestroy(ev0);
+        (void)hipEventDestroy(ev1);
         cleanup();
         return fail(FROG_EHIP, "leaf kernel: %s", hipGetErrorString(e));
     }
@@ -678,12 +688,19 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
         rc = lp == 1 ? launch_layer<1>(A, stream) : (lp == 2 ? launch_layer<2>(A, stream) : launch_layer<4>(A, stream));
         if (rc != FROG_OK) {
             (void)hipDeviceSynchronize();
+            (void)hipEventDestroy(ev0);
+            (void)hipEventDestroy(ev1);
             cleanup();
             return rc;
         }
         std::swap(cur, nxt);
     }
+    (void)hipEventRecord(ev1, stream);
     e = hipDeviceSynchronize();
+    float kms = 0.f;
+    if (e == hipSuccess) (void)hipEventElapsedTime(&kms, ev0, ev1);
+    (void)hipEventDestroy(ev0);
+    (void)hipEventDestroy(ev1);
     unsigned long long st[4] = {0, 0, 0, 0};
     if (e == hipSuccess) e = hipMemcpy(st, dStats, sizeof(st), hipMemcpyDeviceToHost);
     if (e == hipSuccess) e = hipMemcpy(out->ENC.data(), dENC, nE * sizeof(int32_t), hipMemcpyDeviceToHost);
@@ -697,6 +714,7 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
     }
     out->build_distances = (int64_t)st[0];
     out->build_expansions = (int64_t)st[1];
+    out->build_kernel_ms = kms;
     // keep the construction's rows, candidate array, attributes and id map
     // as the device copy
     (void)hipFree(dPG0);

@@ -199,11 +199,12 @@ int frog_build_index_gpu(const float* X, const double* attr, int64_t n, int d, c
     return FROG_OK;
 }
 
-int frog_index_build_stats(const frog_index_t* ix, int64_t* distances, int64_t* expansions) {
+int frog_index_build_stats(const frog_index_t* ix, int64_t* distances, int64_t* expansions, double* kernel_ms) {
     frog::clear_error();
     if (!ix) return fail(FROG_EINVAL, "index is NULL");
     if (distances) *distances = ix->build_distances;
     if (expansions) *expansions = ix->build_expansions;
+    if (kernel_ms) *kernel_ms = ix->build_kernel_ms;
     return FROG_OK;
 }
 

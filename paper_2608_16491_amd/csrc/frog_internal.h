@@ -30,6 +30,7 @@ struct frog_index {
     float maxnorm = -1.f;        // largest squared norm of the stored rows, computed on first use
     // work of the GPU construction: distances evaluated, sibling-search expansions
     int64_t build_distances = 0, build_expansions = 0;
+    double build_kernel_ms = 0.0;   // from the first kernel's start to the last one's end
     // shared entry sample (entry_mode 1): for one seed, the ascending rank
     // lists of levels 1..nlev (level j: ranks whose priority is below
     // 2^(32-j)), concatenated on the device; built on first use

@@ -1530,7 +1530,9 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
     const int wave = threadIdx.x >> 6;
     WaveLds<LP> W(smem, P.lds_per_wave, 0);
     char* lbase = smem + (size_t)wave * P.lds_per_wave + P.lds_list;
-    constexpr int kkeep = KK;
+    // KK: entries of each chunk list the scan left (their stride); the merged
+    // list keeps kkeep >= 64 of them (an offer of 64 fits after a cut)
+    constexpr int kkeep = KK > 64 ? KK : 64;
     const BufList Lst{reinterpret_cast<uint64_t*>(lbase), reinterpret_cast<int32_t*>(lbase + (size_t)2 * kkeep * 8)};
     const double u_round = 5.9604644775390625e-08;   // 2^-24
 
@@ -1569,7 +1571,7 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
         }
         ne = uniform(mc);
         texcl = __int_as_float(uniform(__float_as_int(mt)));
-        constexpr int kR = kkeep / 64;   // entries per lane and chunk
+        constexpr int kR = KK > 64 ? KK / 64 : 1;   // entries per lane and chunk
         float av[kSChunks][kR];
         int32_t rw[kSChunks][kR];
 #pragma unroll
@@ -1579,8 +1581,8 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
 #pragma unroll
             for (int r = 0; r < kR; ++r) {
                 const int j = r * 64 + lane;
-                av[c][r] = j < fi ? P.pv[base * kkeep + j] : __int_as_float(0x7f800000);
-                rw[c][r] = j < fi ? P.pr[base * kkeep + j] : -1;
+                av[c][r] = j < fi ? P.pv[base * KK + j] : __int_as_float(0x7f800000);
+                rw[c][r] = j < fi ? P.pr[base * KK + j] : -1;
             }
         }
 #pragma unroll
@@ -1774,6 +1776,8 @@ int max_blocks(KernelFn fn, int smem) {
 
 // candidates kept per query and work item: K > L with room for the margin
 int shared_kkeep(int L) { return L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256); }
+// the pool kernel's merged list: at least 64
+int pool_kkeep(int kkeep) { return kkeep > 64 ? kkeep : 64; }
 
 template <int C, typename XT = float>
 void (*pick_s_pool_c(int L))(SParams) {
@@ -1840,7 +1844,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     const int smem = lps * kWavesPerBlock;
     // pool kernel: pool staging and EN list, then the re-rank list
     const int base_lds = lds_per_wave(a.L, 0);
-    const int lpw = base_lds + 2 * kkeep * 8 + 16;
+    const int lpw = base_lds + 2 * pool_kkeep(kkeep) * 8 + 16;
     const int smem_pool = lpw * kWavesPerBlock;
     if (smem > 160 * 1024 || smem_pool > 160 * 1024)
         return fail(FROG_EUNSUPPORTED, "LDS per block %d / %d too large", smem, smem_pool);

@@ -133,9 +133,9 @@ __device__ __forceinline__ void buf_init(const BufList& B) {
 
 // Cut the buffer: with exact = true keep its K smallest entries (all if
 // there are at most K); with exact = false keep every entry at or below some
-// value x with K <= #kept <= 3K/2 (a cheaper search; the exact cut when ties
+// value x with K <= #kept <= 5K/4 (a cheaper search; the exact cut when ties
 // leave no such x).  The new threshold is the smallest value a dropped entry
-// can have.  K is 64, 128 or 256.
+// can have.  K is 32, 64, 128 or 256.
 template <int K>
 __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
     constexpr int R = 2 * K / 64;   // entries per lane
@@ -160,7 +160,7 @@ __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
         vmax = b > vmax ? b : vmax;
     }
     // smallest x in [vmin, vmax] with #(entries <= x) >= K, or (loose) any x
-    // with K <= #(entries <= x) <= 3K/2
+    // with K <= #(entries <= x) <= 5K/4
     uint32_t lo = __builtin_amdgcn_readfirstlane(vmin), hi = __builtin_amdgcn_readfirstlane(vmax);
     int cx = f;
     bool loose = false;
@@ -174,7 +174,7 @@ __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
         } else {
             hi = mid;
             cx = c;
-            if (!exact && c <= K + K / 2) {
+            if (!exact && c <= K + K / 4) {
                 loose = true;
                 break;
             }
@@ -186,7 +186,7 @@ __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
 #pragma unroll
         for (int i = 0; i < R; ++i) c += __popcll(__ballot((uint32_t)(k[i] >> 32) <= vk));
         cx = c;
-        loose = c <= K + K / 2;
+        loose = c <= K + K / 4;
     }
     list_sync();
     const uint64_t lt = (1ull << lane) - 1;
@@ -241,7 +241,7 @@ __device__ __forceinline__ void buf_offer(const BufList& B, uint64_t gm, float a
     if (f + __popcll(gm) > 2 * K) {
         buf_cut<K>(B, false);
         f = __builtin_amdgcn_readfirstlane(B.st[0]);
-        if (f + __popcll(gm) > 2 * K) {   // a loose cut can leave 3K/2: make room for 64
+        if (f + __popcll(gm) > 2 * K) {   // a loose cut can leave 5K/4: make room for 64
             buf_cut<K>(B, true);
             f = __builtin_amdgcn_readfirstlane(B.st[0]);
         }

@@ -31,8 +31,8 @@ def _compare(X, attr, **params):
 def test_gpu_build_iid():
     w = workloads.make("tiny", n=4000, nq=1)
     ix, _ = _compare(w.X, w.attr)
-    dists, exps = ix.build_stats()
-    assert dists > 0 and exps > 0
+    dists, exps, kms = ix.build_stats()
+    assert dists > 0 and exps > 0 and kms > 0
 
 
 def test_gpu_build_mixture_d128():

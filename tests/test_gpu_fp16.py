@@ -50,7 +50,7 @@ def mix128():
 
 
 @pytest.mark.parametrize("mode", [0, 1])
-@pytest.mark.parametrize("L", [32, 64, 128, 256])
+@pytest.mark.parametrize("L", [16, 24, 32, 64, 128, 256])
 def test_fp16_tiny_parity(tiny, mode, L):
     p = dict(SH, entry_mode=mode)
     g_ids, g_d = tiny.gpu(10, L, **p)
