@@ -576,12 +576,15 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
     if (hipGetDeviceCount(&ndev) != hipSuccess) return fail(FROG_EHIP, "hipGetDeviceCount failed");
     if (device < 0 || device >= ndev) return fail(FROG_EINVAL, "device %d not in [0, %d)", device, ndev);
     const int m = p.m;
-    int rc = rank_order(X, attr, n, d, m, p.n_inv, out);
+    const int threads = host_threads(p.num_threads);
+    // ENC is left unset on the host: the device array is filled with -1 and
+    // copied back whole
+    int rc = rank_order(X, attr, n, d, m, p.n_inv, threads, false, out);
     if (rc != FROG_OK) return rc;
     const int H = out->H;
     std::vector<double> wtab;
     std::vector<int64_t> wmeta;
-    rc = fusion_weights(n, H, p.beta, p.gamma, host_threads(p.num_threads), wtab, wmeta);
+    rc = fusion_weights(n, H, p.beta, p.gamma, threads, wtab, wmeta);
     if (rc != FROG_OK) return rc;
     const int dp = (d + 31) / 32 * 32;
     const int lp = p.ef_c <= 64 ? 1 : (p.ef_c <= 128 ? 2 : 4);

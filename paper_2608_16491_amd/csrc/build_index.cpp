@@ -289,15 +289,33 @@ int layers_for(int64_t n, int n_inv) {
     return H < 1 ? 1 : H;
 }
 
-int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int n_inv, frog_index* out) {
-    // attribute-rank domain (Sec 4): stable sort by (value, original index)
+int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int n_inv, int threads,
+               bool fill_enc, frog_index* out) {
+    // attribute-rank domain (Sec 4): sort by (value, original index), a strict
+    // order, so chunks sorted apart and merged give the one sorted sequence
     for (int64_t i = 0; i < n; ++i)
         if (std::isnan(attr[i])) return fail(FROG_EINVAL, "attribute %lld is NaN", (long long)i);
-    std::vector<int32_t> perm((size_t)n);
+    auto less = [&](int32_t a, int32_t b) { return attr[a] < attr[b] || (attr[a] == attr[b] && a < b); };
+    std::vector<int32_t> perm((size_t)n), tmp;
     for (int64_t i = 0; i < n; ++i) perm[(size_t)i] = (int32_t)i;
-    std::sort(perm.begin(), perm.end(), [&](int32_t a, int32_t b) {
-        return attr[a] < attr[b] || (attr[a] == attr[b] && a < b);
-    });
+    int parts = 1;
+    while (parts * 2 <= threads && (int64_t)parts * 2 * 65536 <= n) parts *= 2;
+    if (parts == 1) {
+        std::sort(perm.begin(), perm.end(), less);
+    } else {
+        tmp.resize((size_t)n);
+        auto cut = [&](int k) { return (size_t)((int64_t)k * n / parts); };
+        parallel_for(parts, parts, 1, [&](int64_t k, int) {
+            std::sort(perm.begin() + cut((int)k), perm.begin() + cut((int)k + 1), less);
+        });
+        for (int w = 1; w < parts; w *= 2) {
+            parallel_for(parts / (2 * w), parts / (2 * w), 1, [&](int64_t k, int) {
+                const size_t a = cut((int)(2 * w * k)), b = cut((int)(2 * w * k + w)), c = cut((int)(2 * w * k + 2 * w));
+                std::merge(perm.begin() + a, perm.begin() + b, perm.begin() + b, perm.begin() + c, tmp.begin() + a, less);
+            });
+            perm.swap(tmp);
+        }
+    }
     const int H = layers_for(n, n_inv);
     out->n = n;
     out->d = d;
@@ -307,13 +325,19 @@ int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int 
         out->perm = perm;
         out->attr.resize((size_t)n);
         out->X.resize((size_t)n * d);
-        out->ENC.assign((size_t)n * H * m, kNone);
+        out->ENC.resize((size_t)n * H * m);
     } catch (const std::bad_alloc&) {
         return fail(FROG_ENOMEM, "host allocation of the index failed");
     }
-    for (int64_t i = 0; i < n; ++i) {
+    parallel_for(n, threads, 4096, [&](int64_t i, int) {
         out->attr[(size_t)i] = attr[perm[(size_t)i]];
         std::memcpy(&out->X[(size_t)i * d], X + (int64_t)perm[(size_t)i] * d, sizeof(float) * (size_t)d);
+    });
+    if (fill_enc) {
+        const int64_t per = (int64_t)H * m;
+        parallel_for(n, threads, 4096, [&](int64_t i, int) {
+            std::fill(out->ENC.begin() + i * per, out->ENC.begin() + (i + 1) * per, kNone);
+        });
     }
     return FROG_OK;
 }
@@ -378,7 +402,7 @@ int build_host(const float* X, const double* attr, int64_t n, int d,
                const frog_build_params_t& p, frog_index* out) {
     const int m = p.m, ef = p.ef_c, ns = p.sib_seeds;
     const int threads = host_threads(p.num_threads);
-    int rc = rank_order(X, attr, n, d, m, p.n_inv, out);
+    int rc = rank_order(X, attr, n, d, m, p.n_inv, threads, true, out);
     if (rc != FROG_OK) return rc;
     const int H = out->H;
     const float* Xr = out->X.data();

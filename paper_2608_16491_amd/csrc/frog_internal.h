@@ -3,20 +3,45 @@
 #pragma once
 
 #include <cstdint>
+#include <memory>
 #include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "frog.h"
+
+// An allocator whose value-initialisation of a new element is default-
+// initialisation: resize() leaves ints and floats unset, so that a large
+// array written right after (in parallel, or by a device copy) is not
+// cleared first on one thread.
+template <class T>
+struct uninit_alloc : std::allocator<T> {
+    template <class U>
+    struct rebind {
+        using other = uninit_alloc<U>;
+    };
+    uninit_alloc() = default;
+    template <class U>
+    uninit_alloc(const uninit_alloc<U>&) noexcept {}
+    template <class U>
+    void construct(U* p) noexcept {
+        ::new ((void*)p) U;
+    }
+    template <class U, class... Args>
+    void construct(U* p, Args&&... args) {
+        ::new ((void*)p) U(std::forward<Args>(args)...);
+    }
+};
 
 struct frog_index {
     int64_t n = 0;
     int d = 0, H = 0, m = 0;
     // host copy, rank order
-    std::vector<float> X;        // n * d
+    std::vector<float, uninit_alloc<float>> X;        // n * d
     std::vector<double> attr;    // n, ascending
     std::vector<int32_t> perm;   // n, rank -> original index
-    std::vector<int32_t> ENC;    // n * H * m
+    std::vector<int32_t, uninit_alloc<int32_t>> ENC;  // n * H * m
     // device copy (HBM): X rows padded to dp values of the storage type
     // (fp32 in dX, or binary16 bit patterns in dXh)
     int device = -1;
@@ -55,9 +80,11 @@ void clear_error();
 int build_host(const float* X, const double* attr, int64_t n, int d,
                const frog_build_params_t& p, frog_index* out);
 int layers_for(int64_t n, int n_inv);
-// the attribute-rank order (Sec 4) of the input: out's n, d, H, m, perm,
-// attr, X (rank order) and ENC (all -1)
-int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int n_inv, frog_index* out);
+// the attribute-rank order (Sec 4) of the input on `threads` host threads:
+// out's n, d, H, m, perm, attr, X (rank order) and ENC (n x H x m, all -1
+// when fill_enc, else left unset for the caller to write)
+int rank_order(const float* X, const double* attr, int64_t n, int d, int m, int n_inv, int threads,
+               bool fill_enc, frog_index* out);
 int host_threads(int requested);
 // The fusion-distance factor 1 - beta (1 - (|ru - rv| / (len - 1))^gamma) of
 // every offset of every segment length, as the host construction computes
