@@ -33,25 +33,34 @@ if ROOT not in sys.path:
 METRIC = "filtered QPS at recall@10≥0.9, mixed selectivity, n=1M d=128 fp32"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+FP64_VECTOR_PEAK_TFLOPS = 78.6
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "search_c2_traffic.json")
+# the pool sizes the 1M x 128 workload is quoted on
+HEADLINE_L = (32, 64, 128)
 
-# (L, epn, epn_frac, epn_max, budget[, entry_mode]): the paper's fixed 16
+# (L, epn, epn_frac, epn_max, budget[, entry_mode[, n_inv]]): the paper's fixed 16
 # entry points, then the per-query count min(cnt, epn_max) -- on the clustered
 # mixture a query must start inside its own cluster, which takes a few
 # thousand uniform samples.  entry_mode 0 draws them per query (stratified),
 # 1 from the rank priority shared by all queries (matrix-core entry scan).
 SWEEP = [
+    # entry mode 0 (per-query stratified sample)
     (32, 16, 0.0, 0, 16), (64, 16, 0.0, 0, 16),
-    (32, 16, 1.0, 2048, 16), (64, 16, 1.0, 2048, 16),
-    (32, 16, 1.0, 2560, 16), (48, 16, 1.0, 2560, 16), (64, 16, 1.0, 2560, 16), (48, 16, 1.0, 2560, 32),
-    (32, 16, 1.0, 2816, 16), (40, 16, 1.0, 2816, 16), (48, 16, 1.0, 2816, 16), (32, 16, 1.0, 2816, 32),
-    (32, 16, 1.0, 3072, 16), (64, 16, 1.0, 3072, 16),
-    (32, 16, 1.0, 4096, 16), (64, 16, 1.0, 4096, 16),
-    (32, 16, 1.0, 2304, 32), (32, 16, 1.0, 2560, 32), (40, 16, 1.0, 2560, 32), (32, 16, 1.0, 2560, 24),
-    (32, 16, 1.0, 2560, 28), (24, 16, 1.0, 2560, 32),
+    (32, 16, 1.0, 2560, 32), (64, 16, 1.0, 2560, 16), (32, 16, 1.0, 3072, 16), (64, 16, 1.0, 3072, 16),
+    (32, 16, 1.0, 2304, 32), (24, 16, 1.0, 2560, 32), (32, 16, 1.0, 2560, 24), (32, 16, 1.0, 2560, 28),
+    (40, 16, 1.0, 2560, 32), (48, 16, 1.0, 2560, 16), (64, 16, 1.0, 4096, 16),
+    # entry mode 1 (shared sample) on the paper's default index
     (32, 16, 1.0, 2560, 24, 1), (24, 16, 1.0, 2560, 32, 1), (32, 16, 1.0, 2048, 32, 1),
     (24, 16, 1.0, 2304, 32, 1), (32, 16, 1.0, 3072, 16, 1), (24, 16, 1.0, 3072, 24, 1),
-    (16, 16, 1.0, 3072, 32, 1), (32, 16, 1.0, 4096, 16, 1),
+    (16, 16, 1.0, 3072, 32, 1), (32, 16, 1.0, 4096, 16, 1), (64, 16, 1.0, 2560, 16, 1),
+    (64, 16, 1.0, 3072, 16, 1), (128, 16, 1.0, 2048, 16, 1),
+    # entry mode 1 on indexes with one or two more layers (n_inv 6 and 5,
+    # built on the GPU)
+    (32, 16, 1.0, 2048, 24, 1, 6), (32, 16, 1.0, 2304, 24, 1, 6), (32, 16, 1.0, 2560, 16, 1, 6),
+    (32, 16, 1.0, 2560, 24, 1, 6), (24, 16, 1.0, 2048, 32, 1, 6), (64, 16, 1.0, 2048, 16, 1, 6),
+    (32, 16, 1.0, 2304, 16, 1, 6), (32, 16, 1.0, 2304, 20, 1, 6), (32, 16, 1.0, 2432, 16, 1, 6),
+    (32, 16, 1.0, 2048, 24, 1, 5), (32, 16, 1.0, 2048, 16, 1, 5), (32, 16, 1.0, 2560, 16, 1, 5),
+    (32, 16, 1.0, 2304, 16, 1, 5),
 ]
 
 
@@ -108,6 +117,9 @@ def main():
                     help="also measure the ablations of Sec 8.4 at the chosen setting: hotspot without its end "
                          "condition / without localisation, eager visited check, and (rebuilding the index) "
                          "beta = 0; reported under 'ablation' in --details")
+    ap.add_argument("--sweep-params", action="store_true",
+                    help="also measure recall and QPS against beta, gamma, n_inv (GPU rebuilds), the budget and "
+                         "the entry-point cap; reported under 'sensitivity' in --details")
     ap.add_argument("--no-gpu-build", action="store_true",
                     help="skip timing the GPU construction against the host one")
     ap.add_argument("--no-fp16", action="store_true",
@@ -152,14 +164,21 @@ def main():
         t_gb = time.time() - t0
         g_enc = gix.export()["ENC"]
         same = bool((g_enc == ix.export()["ENC"]).all())
-        gd, ge = gix.build_stats()
+        gd, ge, gkms = gix.build_stats()
         gix.free()
         del g_enc
         host_ref = None if (args.index_cache and os.path.exists(args.index_cache)) else t_build
+        # the distances are fp64 arithmetic in dimension order: 3 flops (sub,
+        # mul, add) per dimension, against the fp64 vector peak
+        gflop = 3.0 * d * gd / 1e9
         gpu_build = {"s": t_gb, "host_s": host_ref, "speedup": (host_ref / t_gb) if host_ref else None,
-                     "equal_to_host": same, "distances": gd, "expansions": ge}
-        log(f"GPU build: {t_gb:.2f}s (host {t_build:.1f}s{' loaded from cache' if host_ref is None else ''}), "
-            f"ENC equal to the host build: {same}, {gd} distances, {ge} sibling-search expansions")
+                     "equal_to_host": same, "distances": gd, "expansions": ge, "kernel_s": gkms / 1e3,
+                     "fp64_tflops": gflop / (gkms / 1e3) / 1e3 if gkms > 0 else None,
+                     "fp64_frac": gflop / (gkms / 1e3) / 1e3 / FP64_VECTOR_PEAK_TFLOPS if gkms > 0 else None}
+        log(f"GPU build: {t_gb:.2f}s wall, kernels {gkms / 1e3:.2f}s (host build {t_build:.1f}s"
+            f"{', loaded from cache' if host_ref is None else ''}), ENC equal to the host build: {same}, "
+            f"{gd} distances, {ge} sibling-search expansions, "
+            f"{gflop / max(gkms, 1e-9):.2f} TFLOP/s fp64 in the distance loops")
     ix.upload(0)
     Q = torch.as_tensor(w.Q, device=dev)
     lo = torch.as_tensor(w.lo, device=dev)
@@ -167,8 +186,23 @@ def main():
     k = w.k
     stream = torch.cuda.current_stream()
 
-    def run(L, epn, frac, emax, B=16, mode=0, hl2=args.hash_log2, stats=False, events=None):
-        return F.search(ix, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
+    # indexes by n_inv (the number of deepest segment-tree layers left out,
+    # Sec 6): the paper's default is the host build above; others are built
+    # on the GPU on first use (same construction, same result as the host's)
+    default_ninv = F.build_params(d).n_inv
+    indexes = {default_ninv: ix}
+    cur = {"ni": default_ninv}   # the index run() uses when no n_inv is given
+
+    def index_for(ni):
+        if ni not in indexes:
+            t0 = time.time()
+            indexes[ni] = F.Index.build(w.X, w.attr, device=0, n_inv=ni)
+            log(f"index with n_inv={ni} built on the GPU in {time.time() - t0:.2f}s (H={indexes[ni].info()[2]})")
+        return indexes[ni]
+
+    def run(L, epn, frac, emax, B=16, mode=0, ni=None, hl2=args.hash_log2, stats=False, events=None):
+        index = index_for(cur["ni"] if ni is None else ni)
+        return F.search(index, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
                         entry_mode=mode, hash_log2=hl2, stats=stats, events=events)
 
     def norm_setting(v):
@@ -177,7 +211,9 @@ def main():
             v.append(16)
         if len(v) == 5:
             v.append(0)
-        return int(v[0]), int(v[1]), float(v[2]), int(v[3]), int(v[4]), int(v[5])
+        if len(v) == 6:
+            v.append(default_ninv)
+        return int(v[0]), int(v[1]), float(v[2]), int(v[3]), int(v[4]), int(v[5]), int(v[6])
 
     def parse_setting(text):
         return norm_setting([float(x) for x in text.split(",")])
@@ -194,10 +230,13 @@ def main():
 
     if args.profile_pass:
         settings = [parse_setting(t) for t in args.setting.split(";")]
+        for (L, epn, frac, emax, B, mode, ni) in settings:
+            index_for(ni)
         if args.storage == "fp16":
-            ix.upload(0, storage="fp16")
-        for (L, epn, frac, emax, B, mode) in settings:
-            run(L, epn, frac, emax, B, mode)
+            for index in indexes.values():
+                index.upload(0, storage="fp16")
+        for (L, epn, frac, emax, B, mode, ni) in settings:
+            run(L, epn, frac, emax, B, mode, ni)
             torch.cuda.synchronize()
         if args.storage == "fp32":
             F.bruteforce(ix, Q, lo, hi, k)
@@ -231,27 +270,43 @@ def main():
     # sweep
     rows = []
     settings = [norm_setting(x) for x in SWEEP] if args.setting is None else [parse_setting(args.setting)]
-    for (L, epn, frac, emax, B, mode) in settings:
+    for (L, epn, frac, emax, B, mode, ni) in settings:
+        index_for(ni)
+    if args.storage == "fp16":
+        for index in indexes.values():
+            index.upload(0, storage="fp16")
+    for (L, epn, frac, emax, B, mode, ni) in settings:
         if L < k:
             continue
-        ids, _ = run(L, epn, frac, emax, B, mode)
+        ids, _ = run(L, epn, frac, emax, B, mode, ni)
         torch.cuda.synchronize()
         rec = recall_at_k(ids.cpu().numpy(), gt_ids)
-        run(L, epn, frac, emax, B, mode)
-        t = timed(lambda: run(L, epn, frac, emax, B, mode), 3)
-        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, entry_mode=mode,
+        run(L, epn, frac, emax, B, mode, ni)
+        t = timed(lambda: run(L, epn, frac, emax, B, mode, ni), 3)
+        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, entry_mode=mode, n_inv=ni,
                          recall=float(rec.mean()), qps=w.nq / t, ms=t * 1e3,
                          recall_band=[float(rec[band == b].mean()) if (band == b).any() else None
                                       for b in range(10)]))
         log(f"L={L:4d} epn={epn} frac={frac:<6} max={emax:5d} B={B:2d} mode={mode}  recall={rec.mean():.4f}  "
             f"{t * 1e3:8.3f} ms  {w.nq / t:12.0f} QPS")
-    ok = [r for r in rows if r["recall"] >= 0.9]
+    # the headline takes the pool sizes the workload names; the fastest
+    # setting of any pool size is reported beside it
+    ok_any = [r for r in rows if r["recall"] >= 0.9]
+    ok = [r for r in ok_any if r["L"] in HEADLINE_L] if args.setting is None else ok_any
     chosen = max(ok, key=lambda r: r["qps"]) if ok else max(rows, key=lambda r: r["recall"])
+    fastest_any = max(ok_any, key=lambda r: r["qps"]) if ok_any else None
     met = bool(ok)
-    L, epn, frac, emax, B, mode = (chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"],
-                                   chosen["budget"], chosen["entry_mode"])
-    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} entry_mode={mode} "
+    L, epn, frac, emax, B, mode, ni = (chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"],
+                                       chosen["budget"], chosen["entry_mode"], chosen["n_inv"])
+    cur["ni"] = ni
+    ix = indexes[ni]
+    n, d, H, m = ix.info()
+    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} entry_mode={mode} n_inv={ni} "
         f"recall={chosen['recall']:.4f}" + ("" if met else "  (recall target NOT met)"))
+    if fastest_any is not None and fastest_any is not chosen:
+        log(f"fastest of any pool size: L={fastest_any['L']} max={fastest_any['epn_max']} B={fastest_any['budget']} "
+            f"mode={fastest_any['entry_mode']} n_inv={fastest_any['n_inv']} recall={fastest_any['recall']:.4f} "
+            f"{fastest_any['qps']:.0f} QPS")
 
     # timed steps; each step also records events around the library's kernels
     # on the same stream (entry_mode 0: the search kernel; entry_mode 1: the
@@ -341,7 +396,7 @@ def main():
                 and tf.get("storage", "fp32") == args.storage):
             for ent in tf.get("settings", []):
                 names = dominant.split("+")
-                if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode) and all(
+                if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode, ni) and all(
                         x in ent["kernels"] for x in names):
                     traffic = sum(1024.0 * (ent["kernels"][x]["fetch_kib"] * tf["fetch_factor"]
                                             + ent["kernels"][x]["write_kib"] * tf["write_factor"]) for x in names)
@@ -360,9 +415,16 @@ def main():
         idb, _ = fb()
         torch.cuda.synchronize()
         tb = timed(fb, 5)
+        # the exhaustive filtered search of the same batch: the pre-filter
+        # baseline at recall 1
+        fbf = lambda: F.bruteforce(ix, Qb, lob, hib, k)
+        fbf()
+        tbf = timed(fbf, 2)
         per_band.append(dict(band=f"[2^-{b + 1}, 2^-{b}]", nq=int(len(sel)), qps=len(sel) / tb, ms=tb * 1e3,
-                             recall_in_mixed_batch=chosen["recall_band"][b]))
-    log("per band (own batch): " + ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M" for r in per_band))
+                             recall_in_mixed_batch=chosen["recall_band"][b],
+                             bruteforce_qps=len(sel) / tbf, bruteforce_ms=tbf * 1e3))
+    log("per band (own batch), FROG / brute force: " +
+        ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M/{r['bruteforce_qps'] / 1e6:.3f}M" for r in per_band))
 
     # fp16 rows (the paper keeps the vectors in half precision, Sec 8.1): the
     # same host index uploaded with its rows rounded to binary16, the sweep's
@@ -371,8 +433,8 @@ def main():
     if not args.no_fp16 and args.storage == "fp32":
         ix.upload(0, storage="fp16")
         hrows = []
-        for (Lh, eh, fh, mh, Bh, modeh) in [norm_setting(x) for x in SWEEP]:
-            if modeh != 1 or Lh < k:
+        for (Lh, eh, fh, mh, Bh, modeh, nih) in [norm_setting(x) for x in SWEEP]:
+            if modeh != 1 or Lh < k or nih != ni:
                 continue
             fh_run = lambda: F.search(ix, Q, lo, hi, k, Lh, epn=eh, epn_frac=fh, epn_max=mh, budget=Bh,
                                       entry_mode=1, hash_log2=args.hash_log2)
@@ -439,11 +501,52 @@ def main():
         abl("lazy check, exact visited set", hl2=0)
         abl("eager check, exact visited set", eager=1, hl2=0)
         t0 = time.time()
-        ix0 = F.Index.build(w.X, w.attr, beta=0.0)
-        ix0.upload(0, storage=args.storage)
+        ix0 = F.Index.build(w.X, w.attr, device=0, beta=0.0, n_inv=ni)
+        if args.storage != "fp32":
+            ix0.upload(0, storage=args.storage)
         log(f"beta = 0 index built in {time.time() - t0:.1f}s")
         abl("beta = 0 (no attribute fusion)", index=ix0)
         ix0.free()
+
+    # sensitivity (Sec 8.4): construction parameters through GPU rebuilds, the
+    # expansion budget and the entry-point cap at query time, each around the
+    # chosen setting with the others at their defaults
+    sensitivity = None
+    if args.sweep_params:
+        sensitivity = []
+
+        base_ix = indexes[default_ninv]
+
+        def measure(index, Lx=L, Bx=B, emx=emax):
+            f = lambda: F.search(index, Q, lo, hi, k, Lx, epn=epn, epn_frac=frac, epn_max=emx, budget=Bx,
+                                 entry_mode=mode, hash_log2=args.hash_log2)
+            ids_s, _ = f()
+            torch.cuda.synchronize()
+            rec_s = float(recall_at_k(ids_s.cpu().numpy(), gt_ids).mean())
+            return rec_s, w.nq / timed(f, 5)
+
+        defaults = dict(beta=0.2, gamma=0.5, n_inv=7)
+        grid = [("default", None)] + [("beta", v) for v in (0.0, 0.1, 0.3, 0.5)] + \
+               [("gamma", v) for v in (0.25, 1.0, 2.0)] + [("n_inv", v) for v in (5, 6, 8, 9)]
+        for name, v in grid:
+            prm = dict(defaults)
+            if v is not None:
+                prm[name] = v
+            t0 = time.time()
+            ixv = F.Index.build(w.X, w.attr, device=0, **prm)
+            tbv = time.time() - t0
+            rec_s, qps_s = measure(ixv)
+            ixv.free()
+            sensitivity.append(dict(param=name, value=v, build_s=tbv, recall=rec_s, qps=qps_s, **prm))
+            log(f"sensitivity {name}={v}: GPU build {tbv:.2f}s, recall={rec_s:.4f}, {qps_s:.0f} QPS")
+        for Bx in (8, 16, 24, 32, 48):
+            rec_s, qps_s = measure(base_ix, Bx=Bx)
+            sensitivity.append(dict(param="budget", value=Bx, recall=rec_s, qps=qps_s))
+            log(f"sensitivity budget={Bx}: recall={rec_s:.4f}, {qps_s:.0f} QPS")
+        for emx in (1024, 2048, 3072, 4096, 6144):
+            rec_s, qps_s = measure(base_ix, emx=emx)
+            sensitivity.append(dict(param="epn_max", value=emx, recall=rec_s, qps=qps_s))
+            log(f"sensitivity epn_max={emx}: recall={rec_s:.4f}, {qps_s:.0f} QPS")
 
     # CPU oracle on a bounded sample (same index arrays, same parameters)
     cpu = None
@@ -503,7 +606,11 @@ def main():
                         f"[2^-10,1], k={k}",
             "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": B, "entry_mode": mode,
             "hash_log2": args.hash_log2, "recall@10": chosen["recall"], "recall_target_met": met,
-            "index": {"H": H, "m": m, "build_s": round(t_build, 1)},
+            "index": {"n_inv": ni, "H": H, "m": m, "paper_default_n_inv": default_ninv,
+                      "built": "host" if ni == default_ninv else "GPU (frog_build_index_gpu)",
+                      "host_build_s": round(t_build, 1)},
+            "pool_sizes_named": sorted(HEADLINE_L),
+            "fastest_any_pool_size": fastest_any,
         },
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
@@ -522,11 +629,16 @@ def main():
         "bruteforce": {"ms": bf_time * 1e3, "qps": w.nq / bf_time, "recall@10": 1.0,
                        "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,
-                       "certified": float(cert.mean())},
+                       "certified": float(cert.mean()),
+                       # each selectivity band as its own batch: FROG at the
+                       # chosen setting against the brute force (recall 1)
+                       "per_band": [{"band": r["band"], "frog_qps": r["qps"], "bruteforce_qps": r["bruteforce_qps"]}
+                                    for r in per_band]},
     }
     if args.details:
         with open(args.details, "w") as f:
-            json.dump(dict(result=result, sweep=rows, per_band=per_band, ablation=ablation, alg_bytes=alg_bytes,
+            json.dump(dict(result=result, sweep=rows, per_band=per_band, ablation=ablation, sensitivity=sensitivity,
+                           alg_bytes=alg_bytes,
                            source_sha=sha,
                            eval_overhead=float(overhead),
                            mean_stats_exact=st_e.mean(0).tolist(),
