@@ -1,8 +1,9 @@
 """Full-size parity on the benchmark workload (n = 1,000,000, d = 128, 10,000
 mixed-selectivity queries) in the launch configurations bench.py times: the
-fastest settings reaching recall 0.9 of both entry modes (shared sample:
-L = 24, entry points min(cnt, 3072), budget 24; stratified: L = 24, 2560,
-budget 32) and their neighbours on the frontier, LDS table 2^10.
+headline setting (shared sample, L = 32, entry points min(cnt, 2560), budget
+16, on the index with n_inv = 6 built on the GPU), its neighbours, and the
+frontier on the paper's default index (both entry modes, L = 24 and 32), LDS
+table 2^10.
 
 The index is built by the library's host construction, whose equality with
 the oracle's construction is established entry by entry on smaller inputs in
@@ -92,6 +93,46 @@ def test_full_size_properties_every_row(c2, mode):
     ids2, ds2 = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **SETTINGS[mode])
     torch.cuda.synchronize()
     assert (ids2.cpu().numpy() == ids).all()
+
+
+@pytest.fixture(scope="module")
+def c2_ninv6(c2):
+    """The same workload's index with one more segment-tree layer (n_inv = 6),
+    built on the GPU: the index bench.py's headline setting searches."""
+    w, _, _, d = c2
+    print("[gpu] full-size c2: building the n_inv = 6 index on the GPU", flush=True)
+    ix6 = F.Index.build(w.X, w.attr, device=0, n_inv=6)
+    arr = ix6.export()
+    ox6 = oracle.OracleIndex(arr["perm"], arr["attr_sorted"], arr["X_rank"], arr["ENC"])
+    yield w, ix6, ox6, d
+    ix6.free()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("Lp,emax,B,mode", [(32, 2560, 16, 1), (32, 2304, 20, 1), (32, 2560, 24, 0)])
+def test_full_size_ninv6_sampled_rows_match_oracle(c2_ninv6, Lp, emax, B, mode):
+    w, ix6, ox6, d = c2_ninv6
+    ids, ds, st = F.search(ix6, d["Q"], d["lo"], d["hi"], K, Lp, stats=True, epn=16, epn_frac=1.0,
+                           epn_max=emax, budget=B, entry_mode=mode, hash_log2=10)
+    torch.cuda.synchronize()
+    ids, ds, st = ids.cpu().numpy(), ds.cpu().numpy(), st.cpu().numpy()
+    rng = np.random.default_rng(11)
+    sample = np.sort(rng.choice(w.nq, 400, replace=False))
+    o_ids, o_d, o_st = oracle.search(ox6, w.Q[sample], w.lo[sample], w.hi[sample], K, Lp, qidx=sample,
+                                     epn=16, epn_frac=1.0, epn_max=emax, B=B, entry_mode=mode)
+    res = assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
+    ok = np.setdiff1d(np.arange(len(sample)), res)
+    for gc, oc in [(F.STAT_EXPANSIONS, oracle.STAT_EXPANSIONS), (F.STAT_EN, oracle.STAT_EN),
+                   (F.STAT_SCANNED, oracle.STAT_SCANNED), (F.STAT_ENTRY, oracle.STAT_ENTRY),
+                   (F.STAT_LSTART, oracle.STAT_LS), (F.STAT_LEND, oracle.STAT_LE)]:
+        assert (st[sample][ok, gc] == o_st[ok, oc]).all(), gc
+    # every row: in range, distinct, ascending, min(k, cnt) results
+    cnt = (w.hi - w.lo + 1).astype(np.int64)
+    valid = ids >= 0
+    assert (valid.sum(1) == np.minimum(K, cnt)).all()
+    a = w.attr[np.where(valid, ids, 0)]
+    assert ((a >= w.lo[:, None]) & (a <= w.hi[:, None]) | ~valid).all()
+    assert (np.diff(np.where(valid, ds, np.inf), axis=1) >= 0).all()
 
 
 @pytest.mark.timeout(900)
