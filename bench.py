@@ -417,14 +417,19 @@ def main():
         tb = timed(fb, 5)
         # the exhaustive filtered search of the same batch: the pre-filter
         # baseline at recall 1
-        fbf = lambda: F.bruteforce(ix, Qb, lob, hib, k)
-        fbf()
-        tbf = timed(fbf, 2)
+        # (fp32 rows only: with --storage fp16 every index holds fp16 rows)
+        tbf = None
+        if args.storage == "fp32":
+            fbf = lambda: F.bruteforce(ix, Qb, lob, hib, k)
+            fbf()
+            tbf = timed(fbf, 2)
         per_band.append(dict(band=f"[2^-{b + 1}, 2^-{b}]", nq=int(len(sel)), qps=len(sel) / tb, ms=tb * 1e3,
                              recall_in_mixed_batch=chosen["recall_band"][b],
-                             bruteforce_qps=len(sel) / tbf, bruteforce_ms=tbf * 1e3))
+                             bruteforce_qps=len(sel) / tbf if tbf else None,
+                             bruteforce_ms=tbf * 1e3 if tbf else None))
     log("per band (own batch), FROG / brute force: " +
-        ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M/{r['bruteforce_qps'] / 1e6:.3f}M" for r in per_band))
+        ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M/" +
+                  (f"{r['bruteforce_qps'] / 1e6:.3f}M" if r['bruteforce_qps'] else "-") for r in per_band))
 
     # fp16 rows (the paper keeps the vectors in half precision, Sec 8.1): the
     # same host index uploaded with its rows rounded to binary16, the sweep's

@@ -139,9 +139,12 @@ int frog_build_index(const float* X, const double* attr, int64_t n, int d,
 int frog_build_index_gpu(const float* X, const double* attr, int64_t n, int d,
                          const frog_build_params_t* p, int device, frog_index_t** out);
 
-/* Work of the last GPU construction of idx: distances evaluated and
- * sibling-search expansions (both 0 for a host-built index). */
-int frog_index_build_stats(const frog_index_t* idx, int64_t* distances, int64_t* expansions);
+/* Work of the GPU construction that made idx: distances evaluated,
+ * sibling-search expansions, and the time from its first kernel's start to
+ * its last one's end in milliseconds (all 0 for a host-built index; any
+ * pointer may be NULL). */
+int frog_index_build_stats(const frog_index_t* idx, int64_t* distances, int64_t* expansions,
+                           double* kernel_ms);
 
 /* Wrap already-built arrays (copied): X_rank n x d floats in rank order,
  * attr_sorted n ascending doubles, perm n ints (rank -> original index, a
