@@ -120,6 +120,9 @@ def main():
     ap.add_argument("--sweep-params", action="store_true",
                     help="also measure recall and QPS against beta, gamma, n_inv (GPU rebuilds), the budget and "
                          "the entry-point cap; reported under 'sensitivity' in --details")
+    ap.add_argument("--oracle-pg", action="store_true",
+                    help="also compare FROG's recall with a per-query index over the in-range objects only "
+                         "(a ceiling, on the first 200k objects); reported under 'oracle_pg' in --details")
     ap.add_argument("--no-gpu-build", action="store_true",
                     help="skip timing the GPU construction against the host one")
     ap.add_argument("--no-fp16", action="store_true",
@@ -282,7 +285,7 @@ def main():
         torch.cuda.synchronize()
         rec = recall_at_k(ids.cpu().numpy(), gt_ids)
         run(L, epn, frac, emax, B, mode, ni)
-        t = timed(lambda: run(L, epn, frac, emax, B, mode, ni), 3)
+        t = timed(lambda: run(L, epn, frac, emax, B, mode, ni), 10)
         rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, entry_mode=mode, n_inv=ni,
                          recall=float(rec.mean()), qps=w.nq / t, ms=t * 1e3,
                          recall_band=[float(rec[band == b].mean()) if (band == b).any() else None
@@ -553,6 +556,50 @@ def main():
             sensitivity.append(dict(param="epn_max", value=emx, recall=rec_s, qps=qps_s))
             log(f"sensitivity epn_max={emx}: recall={rec_s:.4f}, {qps_s:.0f} QPS")
 
+    # the ceiling of Sec 8's comparison: per query, an index built over the
+    # in-range objects only (an "oracle" proximity graph for that range),
+    # searched over its whole domain with the same pool size and budget,
+    # against FROG's one index; a sample of queries per selectivity
+    oracle_pg = None
+    if args.oracle_pg:
+        oracle_pg = []
+        rng_pg = np.random.default_rng(5)
+        n_pg = 200_000
+        sub = w.X[:n_pg]
+        order = np.argsort(w.attr[:n_pg], kind="stable")
+        Xs, As = sub[order], w.attr[:n_pg][order]
+        ixf = F.Index.build(Xs, As, device=0)
+        for sig in (0.001, 0.01, 0.1, 0.5):
+            cnt_pg = max(int(round(sig * n_pg)), 1)
+            rec_f, rec_o = [], []
+            for qn in rng_pg.choice(w.nq, 64, replace=False):
+                st = int(rng_pg.integers(0, n_pg - cnt_pg + 1))
+                lo_v, hi_v = float(As[st]), float(As[st + cnt_pg - 1])
+                q1 = torch.as_tensor(w.Q[qn:qn + 1], device=dev)
+                lo1 = torch.tensor([lo_v], dtype=torch.float64, device=dev)
+                hi1 = torch.tensor([hi_v], dtype=torch.float64, device=dev)
+                gt1, _, _ = F.bruteforce(ixf, q1, lo1, hi1, k)
+                f1, _ = F.search(ixf, q1, lo1, hi1, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
+                                 entry_mode=1)
+                ixo = F.Index.build(Xs[st:st + cnt_pg], As[st:st + cnt_pg], device=0)
+                o1, _ = F.search(ixo, q1, lo1, hi1, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
+                                 entry_mode=1)
+                torch.cuda.synchronize()
+                ixo.free()
+                gt_set = set(gt1.cpu().numpy()[0].tolist()) - {-1}
+                # both indexes number objects by their position in Xs (the
+                # slice's from st)
+                o_ids = [st + i for i in o1.cpu().numpy()[0].tolist() if i >= 0]
+                f_ids = [i for i in f1.cpu().numpy()[0].tolist() if i >= 0]
+                den = max(1, len(gt_set))
+                rec_f.append(len(gt_set & set(f_ids)) / den)
+                rec_o.append(len(gt_set & set(o_ids)) / den)
+            oracle_pg.append(dict(sigma=sig, n=n_pg, queries=64, frog_recall=float(np.mean(rec_f)),
+                                  oracle_pg_recall=float(np.mean(rec_o))))
+            log(f"oracle-PG ceiling sigma={sig}: FROG recall {np.mean(rec_f):.4f}, per-range index "
+                f"{np.mean(rec_o):.4f} (n={n_pg}, 64 queries, L={L})")
+        ixf.free()
+
     # CPU oracle on a bounded sample (same index arrays, same parameters)
     cpu = None
     try:
@@ -643,6 +690,7 @@ def main():
     if args.details:
         with open(args.details, "w") as f:
             json.dump(dict(result=result, sweep=rows, per_band=per_band, ablation=ablation, sensitivity=sensitivity,
+                           oracle_pg=oracle_pg,
                            alg_bytes=alg_bytes,
                            source_sha=sha,
                            eval_overhead=float(overhead),
