@@ -263,7 +263,7 @@ def search(index: Index, Q, lo, hi, k: int, L: int, *, stats: bool = False, stre
            **params):
     """FROGSearch for a batch: Q [nq, d] float32, lo/hi [nq] float64, all on
     the index's device.  Returns (ids int32 [nq, k], dists float32 [nq, k]) and,
-    with stats=True, the per-query statistics int32 [nq, 8].  Keyword params:
+    with stats=True, the per-query statistics int32 [nq, STAT_N].  Keyword params:
     epn, epn_frac, epn_max, budget, seed, query_base, hash_log2, entry_mode,
     hotspot_mode, eager_check, and events (three torch.cuda.Event recorded before the search kernels,
     after the entry-point kernels and after the last kernel)."""
