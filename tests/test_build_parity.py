@@ -50,3 +50,19 @@ def test_build_parity_tiny_n():
         X = rng.standard_normal((n, 4)).astype(np.float32)
         attr = rng.permutation(n).astype(np.float64)
         _compare(X, attr, m=4, ef_c=8, n_inv=0)
+
+
+def test_rank_order_large_with_ties_matches_a_stable_sort():
+    # 300k objects: the rank sort runs as chunks sorted on several threads and
+    # merged; with 1000 distinct values the (value, index) tie-break decides
+    # most places.  Cheap construction parameters keep the build short.
+    rng = np.random.default_rng(8)
+    n = 300_000
+    X = rng.standard_normal((n, 2)).astype(np.float32)
+    attr = rng.integers(0, 1000, n).astype(np.float64)
+    ix = F.Index.build(X, attr, m=4, ef_c=8, patience=2, sib_seeds=2, num_threads=8)
+    e = ix.export()
+    order = np.lexsort((np.arange(n), attr))
+    assert (e["perm"] == order).all()
+    assert (e["attr_sorted"] == attr[order]).all()
+    assert (e["X_rank"] == X[order]).all()
