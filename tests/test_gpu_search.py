@@ -202,3 +202,24 @@ def test_ablation_hotspot_modes_forgetful_table(tiny):
         g_ids, g_d = tiny.gpu(10, 64, hotspot_mode=hm)
         o_ids, o_d, _ = tiny.cpu(10, 64, hotspot_mode=hm)
         assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_empty_and_single_query_batches(tiny, mode):
+    # nq = 0 returns empty outputs without launching; nq = 1 matches the oracle
+    p = dict(entry_mode=mode, epn=16, epn_frac=1.0, epn_max=2000)
+    d = tiny.dQ.shape[1]
+    dev = tiny.dQ.device
+    Q0 = torch.empty((0, d), dtype=torch.float32, device=dev)
+    lo0 = torch.empty((0,), dtype=torch.float64, device=dev)
+    ids, ds = F.search(tiny.ix, Q0, lo0, lo0.clone(), 10, 64, **p)
+    torch.cuda.synchronize()
+    assert tuple(ids.shape) == (0, 10) and tuple(ds.shape) == (0, 10)
+    gt, gd, cert = F.bruteforce(tiny.ix, Q0, lo0, lo0.clone(), 10)
+    assert tuple(gt.shape) == (0, 10)
+    ids, ds = F.search(tiny.ix, tiny.dQ[3:4].contiguous(), tiny.dlo[3:4].contiguous(), tiny.dhi[3:4].contiguous(),
+                       10, 64, **p)
+    torch.cuda.synchronize()
+    o_ids, o_d, _ = oracle.search(tiny.ox, tiny.Q[3:4], tiny.lo[3:4], tiny.hi[3:4], 10, 64, qidx=np.array([0]),
+                                  epn=16, epn_frac=1.0, epn_max=2000, entry_mode=mode)
+    assert_parity(ids.cpu().numpy(), ds.cpu().numpy(), o_ids, o_d)
