@@ -638,6 +638,29 @@ def main():
         log(f"cpu oracle: {ns} queries x {reps} in {tp * reps:.1f}s on {threads} threads = {ns / tp:.0f} QPS")
     except Exception as ex:  # the oracle is optional on the timing path
         log(f"cpu oracle skipped: {ex}")
+    # the oracle's exhaustive filtered k-NN on a bounded sample of the same
+    # batch (about a tenth of the CPU time above), beside the GPU brute force
+    cpu_exact = None
+    try:
+        import oracle
+        arrs = ix.export()
+        threads = oracle.default_threads()
+        ns, tp = 16, 0.0
+        while True:
+            t0 = time.time()
+            oracle.exact(arrs["X_rank"], arrs["attr_sorted"], arrs["perm"], w.Q[:ns], w.lo[:ns], w.hi[:ns], k,
+                         threads=threads)
+            tp = time.time() - t0
+            if tp > args.cpu_seconds / 10 or ns >= w.nq:
+                break
+            ns = min(w.nq, ns * 4)
+        cpu_exact = {"value": ns / tp, "unit": "queries/s", "cores": threads, "kind": "oracle exhaustive",
+                     "sample": f"first {ns} of the {w.nq} queries, {tp:.1f}s",
+                     "gpu_bruteforce_qps": w.nq / bf_time}
+        log(f"cpu oracle, exhaustive: {ns} queries in {tp:.1f}s on {threads} threads = {ns / tp:.0f} QPS "
+            f"(GPU brute force {w.nq / bf_time:.0f} QPS)")
+    except Exception as ex:
+        log(f"cpu exhaustive oracle skipped: {ex}")
 
     result = {
         "metric": METRIC,
@@ -670,6 +693,7 @@ def main():
                      "step_achieved": alg_bytes / per_step / 1e9},
         "phases": phases,
         "cpu_baseline": cpu,
+        "cpu_exact": cpu_exact,
         # the exhaustive filtered search as the pre-filter baseline: recall 1
         # (certified), queries per second of the same batch
         # the same search with the rows stored in fp16 (secondary; the
