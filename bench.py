@@ -125,11 +125,11 @@ def main():
                          "(a ceiling, on the first 200k objects); reported under 'oracle_pg' in --details")
     ap.add_argument("--no-gpu-build", action="store_true",
                     help="skip timing the GPU construction against the host one")
-    ap.add_argument("--no-fp16", action="store_true",
-                    help="skip the secondary measurement with the rows stored in fp16")
-    ap.add_argument("--storage", default="fp32", choices=("fp32", "fp16"),
+    ap.add_argument("--no-16bit", "--no-fp16", dest="no_16bit", action="store_true",
+                    help="skip the secondary measurements with the rows stored in fp16 and bf16")
+    ap.add_argument("--storage", default="fp32", choices=("fp32", "fp16", "bf16"),
                     help="row storage of the sweep and the timed steps (the ground truth always uses fp32 "
-                         "rows); fp16 is for profiling that path, the metric is quoted on fp32")
+                         "rows); fp16 and bf16 are for profiling those paths, the metric is quoted on fp32")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -235,9 +235,9 @@ def main():
         settings = [parse_setting(t) for t in args.setting.split(";")]
         for (L, epn, frac, emax, B, mode, ni) in settings:
             index_for(ni)
-        if args.storage == "fp16":
+        if args.storage != "fp32":
             for index in indexes.values():
-                index.upload(0, storage="fp16")
+                index.upload(0, storage=args.storage)
         for (L, epn, frac, emax, B, mode, ni) in settings:
             run(L, epn, frac, emax, B, mode, ni)
             torch.cuda.synchronize()
@@ -261,9 +261,9 @@ def main():
     gt_ids = gt_ids.cpu().numpy()
     cert = cert.cpu().numpy()
     # bytes per stored value of the searched rows
-    eb = 2 if args.storage == "fp16" else 4
-    if args.storage == "fp16":
-        ix.upload(0, storage="fp16")
+    eb = 4 if args.storage == "fp32" else 2
+    if args.storage != "fp32":
+        ix.upload(0, storage=args.storage)
     cnt = (w.hi - w.lo + 1).astype(np.int64)
     bf_flops = 2.0 * d * float(cnt.sum())
     log(f"ground truth: {t_gt:.2f}s first call, {bf_time * 1e3:.1f} ms timed, certified "
@@ -275,9 +275,9 @@ def main():
     settings = [norm_setting(x) for x in SWEEP] if args.setting is None else [parse_setting(args.setting)]
     for (L, epn, frac, emax, B, mode, ni) in settings:
         index_for(ni)
-    if args.storage == "fp16":
+    if args.storage != "fp32":
         for index in indexes.values():
-            index.upload(0, storage="fp16")
+            index.upload(0, storage=args.storage)
     for (L, epn, frac, emax, B, mode, ni) in settings:
         if L < k:
             continue
@@ -420,7 +420,7 @@ def main():
         tb = timed(fb, 5)
         # the exhaustive filtered search of the same batch: the pre-filter
         # baseline at recall 1
-        # (fp32 rows only: with --storage fp16 every index holds fp16 rows)
+        # (fp32 rows only: with a 16-bit --storage every index holds 16-bit rows)
         tbf = None
         if args.storage == "fp32":
             fbf = lambda: F.bruteforce(ix, Qb, lob, hib, k)
@@ -434,12 +434,15 @@ def main():
         ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M/" +
                   (f"{r['bruteforce_qps'] / 1e6:.3f}M" if r['bruteforce_qps'] else "-") for r in per_band))
 
-    # fp16 rows (the paper keeps the vectors in half precision, Sec 8.1): the
-    # same host index uploaded with its rows rounded to binary16, the sweep's
-    # shared-sample settings, recall against the fp32 ground truth
-    fp16 = None
-    if not args.no_fp16 and args.storage == "fp32":
-        ix.upload(0, storage="fp16")
+    # 16-bit rows (the paper keeps the vectors in half precision, Sec 8.1):
+    # the same host index uploaded with its rows rounded to binary16, then to
+    # bfloat16, the sweep's shared-sample settings, recall against the fp32
+    # ground truth
+    half = {"fp16": None, "bf16": None}
+    for sto, desc in (("fp16", "fp16 rows (binary16, nearest even)"), ("bf16", "bf16 rows (bfloat16, nearest even)")):
+        if args.no_16bit or args.storage != "fp32":
+            break
+        ix.upload(0, storage=sto)
         hrows = []
         for (Lh, eh, fh, mh, Bh, modeh, nih) in [norm_setting(x) for x in SWEEP]:
             if modeh != 1 or Lh < k or nih != ni:
@@ -453,7 +456,7 @@ def main():
             th = timed(fh_run, 5)
             hrows.append(dict(L=Lh, epn=eh, epn_frac=fh, epn_max=mh, budget=Bh, entry_mode=1,
                               recall=float(rec_h.mean()), qps=w.nq / th, ms=th * 1e3))
-            log(f"fp16 rows: L={Lh:4d} max={mh:5d} B={Bh:2d}  recall={rec_h.mean():.4f}  {th * 1e3:8.3f} ms  "
+            log(f"{sto} rows: L={Lh:4d} max={mh:5d} B={Bh:2d}  recall={rec_h.mean():.4f}  {th * 1e3:8.3f} ms  "
                 f"{w.nq / th:12.0f} QPS")
         okh = [r for r in hrows if r["recall"] >= 0.9]
         best = max(okh, key=lambda r: r["qps"]) if okh else max(hrows, key=lambda r: r["recall"])
@@ -471,10 +474,10 @@ def main():
         torch.cuda.synchronize()
         ha = sum(t[0].elapsed_time(t[1]) for t in ph) / 1000.0 / reps
         hb = sum(t[1].elapsed_time(t[2]) for t in ph) / 1000.0 / reps
-        fp16 = {"storage": "fp16 rows (binary16, nearest even), fp32 queries, fp64-accumulated distances",
-                "best": best, "recall_target_met": bool(okh), "vs_fp32_value": best["qps"] / qps,
-                "entry_scan_ms": ha * 1e3, "search_ms": hb * 1e3, "sweep": hrows}
-        log(f"fp16 rows: best L={best['L']} max={best['epn_max']} B={best['budget']} recall={best['recall']:.4f} "
+        half[sto] = {"storage": desc + ", fp32 queries, fp64-accumulated distances",
+                     "best": best, "recall_target_met": bool(okh), "vs_fp32_value": best["qps"] / qps,
+                     "entry_scan_ms": ha * 1e3, "search_ms": hb * 1e3, "sweep": hrows}
+        log(f"{sto} rows: best L={best['L']} max={best['epn_max']} B={best['budget']} recall={best['recall']:.4f} "
             f"{best['qps']:.0f} QPS (x{best['qps'] / qps:.2f} of fp32); entry scan {ha * 1e3:.3f} ms, "
             f"search {hb * 1e3:.3f} ms")
         ix.upload(0)
@@ -608,6 +611,9 @@ def main():
         Xr = arrs["X_rank"]
         if args.storage == "fp16":
             Xr = Xr.astype(np.float16).astype(np.float32)
+        elif args.storage == "bf16":
+            mant, ex = np.frexp(Xr.astype(np.float64))       # nearest bfloat16, ties to even
+            Xr = np.ldexp(np.rint(mant * 256.0) / 256.0, ex).astype(np.float32)
         ox = oracle.OracleIndex(arrs["perm"], arrs["attr_sorted"], Xr, arrs["ENC"])
         threads = oracle.default_threads()
         probe = min(200, w.nq)
@@ -673,7 +679,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if args.storage == "fp32" else "f16 rows, f32 queries, f64 accumulation",
+        "dtype": "f32" if args.storage == "fp32" else f"{args.storage} rows, f32 queries, f64 accumulation",
         "data": "synthetic",
         "config": {
             "workload": f"{w.name}: n={n} d={d} Gaussian mixture (1000 centres, noise 0.3), "
@@ -696,9 +702,10 @@ def main():
         "cpu_exact": cpu_exact,
         # the exhaustive filtered search as the pre-filter baseline: recall 1
         # (certified), queries per second of the same batch
-        # the same search with the rows stored in fp16 (secondary; the
-        # metric above is fp32)
-        "fp16_storage": fp16,
+        # the same search with the rows stored in fp16 and in bf16
+        # (secondary; the metric above is fp32)
+        "fp16_storage": half["fp16"],
+        "bf16_storage": half["bf16"],
         # index construction (Sec 6) on the GPU, wall time including the host
         # sort and the copies, against the host construction
         "gpu_build": gpu_build,

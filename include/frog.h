@@ -173,21 +173,24 @@ int frog_index_upload(frog_index_t* idx, int device);
 /* Storage type of the device copy's rows. */
 enum {
     FROG_STORAGE_F32 = 0,  /* fp32 rows, dp = d rounded up to a multiple of 32 */
-    FROG_STORAGE_F16 = 1   /* IEEE binary16 rows (round to nearest even), dp = d
+    FROG_STORAGE_F16 = 1,  /* IEEE binary16 rows (round to nearest even), dp = d
                               rounded up to a multiple of 64, d <= 128 */
+    FROG_STORAGE_BF16 = 2  /* bfloat16 rows (the upper half of the fp32 value,
+                              round to nearest even), same padding and limit */
 };
 
 /* As frog_index_upload, with the rows stored as `storage` (FROG_STORAGE_*).
- * The paper keeps the vectors in half precision on the device (Sec 8.1); the
- * search then returns the exact FROGSearch result over the rounded vectors:
+ * The paper keeps the vectors in half precision on the device (Sec 8.1); with
+ * fp16 or bf16 rows the search returns the exact FROGSearch result over the
+ * rounded vectors:
  * each row is rounded once on the host, converted exactly to fp32 in the
  * kernels, and distances are accumulated as for fp32 rows.  Queries stay
  * fp32.  The host copy keeps the fp32 rows (export and save are unchanged).
  * Errors: FROG_EINVAL for an unknown storage value, FROG_EUNSUPPORTED for
- * fp16 with d > 128 or a value whose rounding overflows binary16.  An fp16
- * device copy serves frog_search / frog_search_ex (both entry modes) and
- * frog_rank_bounds; frog_bruteforce_filtered needs fp32 rows and returns
- * FROG_EUNSUPPORTED. */
+ * 16-bit rows with d > 128 or a value whose rounding overflows the format
+ * (or is not finite).  A 16-bit device copy serves frog_search /
+ * frog_search_ex (both entry modes) and frog_rank_bounds;
+ * frog_bruteforce_filtered needs fp32 rows and returns FROG_EUNSUPPORTED. */
 int frog_index_upload_ex(frog_index_t* idx, int device, int storage);
 /* Release host and device memory.  NULL is a no-op. */
 void frog_index_free(frog_index_t* idx);

@@ -22,8 +22,8 @@ ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "EBADINDEX", -5: "ENOTUPLO
 (STAT_EXPANSIONS, STAT_EN, STAT_DIST, STAT_SCANNED, STAT_ENTRY, STAT_LSTART, STAT_LEND, STAT_LOADED,
  STAT_SCANROWS) = range(9)
 STAT_N = 9
-STORAGE_F32, STORAGE_F16 = 0, 1
-STORAGE = {"fp32": STORAGE_F32, "fp16": STORAGE_F16}
+STORAGE_F32, STORAGE_F16, STORAGE_BF16 = 0, 1, 2
+STORAGE = {"fp32": STORAGE_F32, "fp16": STORAGE_F16, "bf16": STORAGE_BF16}
 
 SYMBOLS = (
     "frog_build_params_default", "frog_search_params_default", "frog_build_index",
@@ -209,8 +209,9 @@ class Index:
         return dict(X_rank=X, attr_sorted=a, perm=p, ENC=E)
 
     def upload(self, device: int = 0, storage: str = "fp32") -> "Index":
-        """Copy to `device` with rows stored as "fp32" or "fp16" (rounded to
-        nearest even; the search is then exact over the rounded rows)."""
+        """Copy to `device` with rows stored as "fp32", "fp16" or "bf16" (16-bit
+        rows rounded to nearest even; the search is then exact over the
+        rounded rows)."""
         if storage not in STORAGE:
             raise ValueError(f"storage {storage!r}: one of {sorted(STORAGE)}")
         if storage == "fp32":

@@ -363,25 +363,70 @@ int frog_index_upload(frog_index_t* ix, int device) {
     return frog_index_upload_ex(ix, device, FROG_STORAGE_F32);
 }
 
+}  // extern "C"
+
+namespace frog {
+
+// The 16-bit pattern of v rounded to nearest even in `storage` (fp16: the
+// compiler's binary16 conversion; bf16: the upper half of the fp32 bits after
+// adding half an ulp, ties to even); false if v or its rounding is not
+// finite.
+bool half_bits(float v, int storage, uint16_t* out) {
+    if (!std::isfinite(v)) return false;
+    if (storage == FROG_STORAGE_F16) {
+        const _Float16 h = (_Float16)v;
+        if (!(h == h) || h > (_Float16)65504.f || h < (_Float16)-65504.f) return false;
+        std::memcpy(out, &h, 2);
+        return true;
+    }
+    uint32_t b;
+    std::memcpy(&b, &v, 4);
+    const uint32_t r = b + 0x7FFFu + ((b >> 16) & 1u);
+    const uint16_t h = (uint16_t)(r >> 16);
+    if ((h & 0x7F80u) == 0x7F80u) return false;   // rounded to infinity
+    *out = h;
+    return true;
+}
+
+// value c of row i as the device stores it
+float stored_value(const frog_index* ix, int64_t i, int c) {
+    const float v = ix->X[(size_t)i * ix->d + c];
+    if (ix->storage == FROG_STORAGE_F16) return (float)(_Float16)v;
+    if (ix->storage == FROG_STORAGE_BF16) {
+        uint16_t h = 0;
+        half_bits(v, FROG_STORAGE_BF16, &h);
+        const uint32_t w = (uint32_t)h << 16;
+        float f;
+        std::memcpy(&f, &w, 4);
+        return f;
+    }
+    return v;
+}
+
+}  // namespace frog
+
+extern "C" {
+
 int frog_index_upload_ex(frog_index_t* ix, int device, int storage) {
     frog::clear_error();
     if (!ix) return fail(FROG_EINVAL, "index is NULL");
-    if (storage != FROG_STORAGE_F32 && storage != FROG_STORAGE_F16)
-        return fail(FROG_EINVAL, "storage=%d: FROG_STORAGE_F32 or FROG_STORAGE_F16", storage);
-    const bool half = storage == FROG_STORAGE_F16;
-    if (half && ix->d > 128) return fail(FROG_EUNSUPPORTED, "fp16 storage needs d <= 128 (d=%d)", ix->d);
-    // fp16 rows: round every value once (nearest even) and pad to dp halves
+    if (storage != FROG_STORAGE_F32 && storage != FROG_STORAGE_F16 && storage != FROG_STORAGE_BF16)
+        return fail(FROG_EINVAL, "storage=%d: FROG_STORAGE_F32, FROG_STORAGE_F16 or FROG_STORAGE_BF16", storage);
+    const bool half = storage != FROG_STORAGE_F32;
+    if (half && ix->d > 128) return fail(FROG_EUNSUPPORTED, "16-bit storage needs d <= 128 (d=%d)", ix->d);
+    // 16-bit rows: round every value once (nearest even) and pad to dp values
     const int dp = half ? (ix->d + 63) / 64 * 64 : (ix->d + 31) / 32 * 32;
     std::vector<uint16_t> hx;
     if (half) {
         hx.assign((size_t)ix->n * dp, 0);
         for (int64_t i = 0; i < ix->n; ++i)
             for (int c = 0; c < ix->d; ++c) {
-                const _Float16 h = (_Float16)ix->X[(size_t)i * ix->d + c];
-                if (!(h == h) || h > (_Float16)65504.f || h < (_Float16)-65504.f)
-                    return fail(FROG_EUNSUPPORTED, "row %lld: value %g outside the fp16 range", (long long)i,
-                                (double)ix->X[(size_t)i * ix->d + c]);
-                std::memcpy(&hx[(size_t)i * dp + c], &h, 2);
+                const float v = ix->X[(size_t)i * ix->d + c];
+                uint16_t bits;
+                if (!frog::half_bits(v, storage, &bits))
+                    return fail(FROG_EUNSUPPORTED, "row %lld: value %g outside the %s range", (long long)i, (double)v,
+                                storage == FROG_STORAGE_F16 ? "fp16" : "bf16");
+                hx[(size_t)i * dp + c] = bits;
             }
     }
     int ndev = 0;
@@ -538,12 +583,6 @@ static uint64_t mix64(uint64_t x) {
     return z ^ (z >> 31);
 }
 
-// value c of row i as the device stores it (fp32, or rounded to binary16)
-static inline float stored_value(const frog_index* ix, int64_t i, int c) {
-    const float v = ix->X[(size_t)i * ix->d + c];
-    return ix->storage == FROG_STORAGE_F16 ? (float)(_Float16)v : v;
-}
-
 float index_maxnorm(frog_index* ix) {
     std::lock_guard<std::mutex> g(ix->shared_mu);
     if (ix->maxnorm < 0.f) {
@@ -623,11 +662,11 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
         if (e == hipSuccess) e = hipMalloc(&ix->dshared_nrm, nrm.size() * sizeof(float));
         if (e == hipSuccess) e = hipMemcpy(ix->dshared_nrm, nrm.data(), nrm.size() * sizeof(float), hipMemcpyHostToDevice);
         // the listed stored rows, so that a scan over a list reads contiguous rows
-        const int row_bytes = ix->dp * (ix->storage == FROG_STORAGE_F16 ? 2 : 4);
+        const int row_bytes = ix->dp * (ix->storage == FROG_STORAGE_F32 ? 4 : 2);
         if (e == hipSuccess) e = hipMalloc(&ix->dshared_x, (size_t)std::max<int64_t>(total, 1) * row_bytes);
         int rc = FROG_OK;
         if (e == hipSuccess && total > 0) {
-            const void* rows = ix->storage == FROG_STORAGE_F16 ? (const void*)ix->dXh : (const void*)ix->dX;
+            const void* rows = ix->storage == FROG_STORAGE_F32 ? (const void*)ix->dX : (const void*)ix->dXh;
             rc = launch_gather_rows(rows, row_bytes, ix->dshared, total, ix->dshared_x, nullptr);
             if (rc == FROG_OK) e = hipDeviceSynchronize();
         }
@@ -648,7 +687,7 @@ int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
     }
     out->ranks = ix->dshared;
     out->xrows = ix->storage == FROG_STORAGE_F32 ? static_cast<const float*>(ix->dshared_x) : nullptr;
-    out->xrowsh = ix->storage == FROG_STORAGE_F16 ? static_cast<const uint16_t*>(ix->dshared_x) : nullptr;
+    out->xrowsh = ix->storage != FROG_STORAGE_F32 ? static_cast<const uint16_t*>(ix->dshared_x) : nullptr;
     out->prio = ix->dshared_p;
     out->norm = ix->dshared_nrm;
     std::copy(ix->shared_off, ix->shared_off + 34, out->off);

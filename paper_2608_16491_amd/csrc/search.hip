@@ -40,8 +40,9 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
-#include <mutex>
 #include <map>
+#include <mutex>
+#include <type_traits>
 
 #include "frog_internal.h"
 #include "wave_topk.h"
@@ -215,9 +216,31 @@ __device__ void hotspot(int64_t l, int64_t r, int H, int64_t n, int& Ls, int& Le
 
 // Row layout a lane reads (C = dp / 32 float4 chunks per lane, 8 lanes per
 // row).  fp32 rows: chunk c of lane `sub` is float4 number sub + 8c of the
-// row.  fp16 rows (dp a multiple of 64): the lane's 16-byte piece sub + 8(c/2)
-// holds 8 halves, of which chunk c is the first or second 4, widened exactly
-// to float.
+// row.  16-bit rows (fp16 or bf16, dp a multiple of 64): the lane's 16-byte
+// piece sub + 8(c/2) holds 8 values, of which chunk c is the first or second
+// 4, widened exactly to float.
+
+// bfloat16 storage: the upper 16 bits of an fp32 value (a tag type; the
+// rows hold the bit patterns).
+struct bf16x {
+    uint16_t bits;
+};
+
+// Four stored 16-bit values (two 32-bit words, first value in the low half)
+// widened exactly to float.
+template <typename XT>
+__device__ __forceinline__ float4 widen4(uint32_t w0, uint32_t w1) {
+    if constexpr (std::is_same<XT, __half>::value) {
+        const float2 a = __half22float2(__builtin_bit_cast(__half2, w0));
+        const float2 b = __half22float2(__builtin_bit_cast(__half2, w1));
+        return make_float4(a.x, a.y, b.x, b.y);
+    } else {
+        static_assert(std::is_same<XT, bf16x>::value, "16-bit storage is fp16 or bf16");
+        return make_float4(__uint_as_float(w0 << 16), __uint_as_float(w0 & 0xFFFF0000u), __uint_as_float(w1 << 16),
+                           __uint_as_float(w1 & 0xFFFF0000u));
+    }
+}
+
 // All C chunks of row `id` for lane `sub` (zeros when !v).  fp16 rows take
 // one 16-byte load per pair of chunks, so that the 8 lanes of a row read
 // 128 contiguous bytes per instruction, as for fp32 rows.
@@ -235,12 +258,8 @@ __device__ __forceinline__ void load_row(const XT* __restrict__ X, int dp, int64
         for (int p = 0; p < C / 2; ++p) {
             const uint4 h = v ? reinterpret_cast<const uint4*>(X)[id * (dp >> 3) + sub + 8 * p]
                               : make_uint4(0u, 0u, 0u, 0u);
-            const float2 a = __half22float2(__builtin_bit_cast(__half2, h.x));
-            const float2 b = __half22float2(__builtin_bit_cast(__half2, h.y));
-            const float2 c2 = __half22float2(__builtin_bit_cast(__half2, h.z));
-            const float2 e = __half22float2(__builtin_bit_cast(__half2, h.w));
-            x[2 * p] = make_float4(a.x, a.y, b.x, b.y);
-            x[2 * p + 1] = make_float4(c2.x, c2.y, e.x, e.y);
+            x[2 * p] = widen4<XT>(h.x, h.y);
+            x[2 * p + 1] = widen4<XT>(h.z, h.w);
         }
     }
 }
@@ -526,12 +545,12 @@ __device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b, double rb) {
 template <typename XT>
 __device__ __forceinline__ const XT* rows_of(const DevIndex& ix) {
     if constexpr (sizeof(XT) == 4) return ix.X;
-    else return reinterpret_cast<const __half*>(ix.Xh);
+    else return reinterpret_cast<const XT*>(ix.Xh);
 }
 template <typename XT>
 __device__ __forceinline__ const XT* lev_rows(const SharedLevels& lv) {
     if constexpr (sizeof(XT) == 4) return lv.xrows;
-    else return reinterpret_cast<const __half*>(lv.xrowsh);
+    else return reinterpret_cast<const XT*>(lv.xrowsh);
 }
 
 template <int C, typename XT = float>
@@ -1248,11 +1267,11 @@ __host__ __device__ constexpr size_t s_scan_lds_per_wave(int kkeep) {
 }
 
 // KT = dp / 16 float4 chunks of the query operand in registers (d <= 128);
-// KT = 0 reloads it for every block (fp32 rows only).  T is the rows'
-// storage type: fp16 rows are converted exactly to fp32 on load.
+// KT = 0 reloads it for every block (fp32 rows only).  XT is the rows'
+// storage type: 16-bit rows are widened exactly to fp32 on load.
 template <int KT, int KK, typename XT = float>
 __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
-    static_assert(sizeof(XT) == 4 || (KT > 0 && KT % 2 == 0), "fp16 rows need dp a multiple of 32 held in registers");
+    static_assert(sizeof(XT) == 4 || (KT > 0 && KT % 2 == 0), "16-bit rows need dp a multiple of 32 held in registers");
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int lane = lane_id();
@@ -1359,12 +1378,8 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
 #pragma unroll
                 for (int v = 0; v < KT / 2; ++v) {
                     const uint4 h = reinterpret_cast<const uint4*>(Rl)[pos * dp8 + 4 * v + kk];
-                    const float2 a = __half22float2(__builtin_bit_cast(__half2, h.x));
-                    const float2 b = __half22float2(__builtin_bit_cast(__half2, h.y));
-                    const float2 c = __half22float2(__builtin_bit_cast(__half2, h.z));
-                    const float2 e = __half22float2(__builtin_bit_cast(__half2, h.w));
-                    x[2 * v] = make_float4(a.x, a.y, b.x, b.y);
-                    x[2 * v + 1] = make_float4(c.x, c.y, e.x, e.y);
+                    x[2 * v] = widen4<XT>(h.x, h.y);
+                    x[2 * v + 1] = widen4<XT>(h.z, h.w);
                 }
             }
         }
@@ -1739,6 +1754,7 @@ KernelFn pick_lp(int L) {
 // fp16 rows come with dp = 64 or 128 (the upload checks it)
 KernelFn pick_kernel(int dp, int L, int storage) {
     if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_lp<2, __half>(L) : pick_lp<4, __half>(L);
+    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_lp<2, bf16x>(L) : pick_lp<4, bf16x>(L);
     switch (dp) {
         case 32: return pick_lp<1>(L);
         case 64: return pick_lp<2>(L);
@@ -1796,6 +1812,7 @@ void (*pick_s_search_c(int L))(SParams) {
 
 void (*pick_s_pool(int dp, int L, int storage))(SParams) {
     if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_s_pool_c<2, __half>(L) : pick_s_pool_c<4, __half>(L);
+    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_s_pool_c<2, bf16x>(L) : pick_s_pool_c<4, bf16x>(L);
     switch (dp) {
         case 32: return pick_s_pool_c<1>(L);
         case 64: return pick_s_pool_c<2>(L);
@@ -1807,6 +1824,7 @@ void (*pick_s_pool(int dp, int L, int storage))(SParams) {
 
 void (*pick_s_search(int dp, int L, int storage))(SParams) {
     if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_s_search_c<2, __half>(L) : pick_s_search_c<4, __half>(L);
+    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_s_search_c<2, bf16x>(L) : pick_s_search_c<4, bf16x>(L);
     switch (dp) {
         case 32: return pick_s_search_c<1>(L);
         case 64: return pick_s_search_c<2>(L);
@@ -1819,6 +1837,7 @@ void (*pick_s_search(int dp, int L, int storage))(SParams) {
 template <int KK>
 void (*pick_s_scan_k(int dp, int storage))(SParams) {
     if (storage == FROG_STORAGE_F16) return dp == 64 ? s_scan_kernel<4, KK, __half> : s_scan_kernel<8, KK, __half>;
+    if (storage == FROG_STORAGE_BF16) return dp == 64 ? s_scan_kernel<4, KK, bf16x> : s_scan_kernel<8, KK, bf16x>;
     switch (dp) {
         case 32: return s_scan_kernel<2, KK>;
         case 64: return s_scan_kernel<4, KK>;

@@ -105,7 +105,7 @@ def test_gpu_build_rejects_unsupported_shapes_on_the_host():
     assert e.value.code == -1
 
 
-def test_fp16_upload_rejects_on_the_host():
+def test_16bit_upload_rejects_on_the_host():
     # checked before any device is touched: unknown storage, d > 128, a
     # value that rounds past the largest binary16 (65504)
     L = F.lib()
@@ -114,7 +114,7 @@ def test_fp16_upload_rejects_on_the_host():
     assert L.frog_index_upload_ex(ix.handle, 0, 7) == -1
     assert b"storage" in L.frog_last_error()
     with pytest.raises(ValueError):
-        ix.upload(0, storage="bf16")
+        ix.upload(0, storage="fp8")
     X2 = X.copy()
     X2[10, 2] = 65520.0          # rounds to infinity
     ix2 = F.Index.from_arrays(X2, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
@@ -124,6 +124,17 @@ def test_fp16_upload_rejects_on_the_host():
     ix3 = F.Index.from_arrays(Xw, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
     assert L.frog_index_upload_ex(ix3.handle, 0, F.STORAGE_F16) == -7
     assert b"d <= 128" in L.frog_last_error()
+    # bf16: a value that rounds to infinity (above the largest bf16,
+    # (2 - 2^-7) 2^127) and a non-finite value
+    X4 = X.copy()
+    X4[3, 1] = np.float32(3.4028235e38)
+    ix4 = F.Index.from_arrays(X4, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
+    assert L.frog_index_upload_ex(ix4.handle, 0, F.STORAGE_BF16) == -7
+    assert b"bf16 range" in L.frog_last_error()
+    X5 = X.copy()
+    X5[7, 0] = np.inf
+    ix5 = F.Index.from_arrays(X5, np.sort(attr), np.arange(64, dtype=np.int32), -np.ones((64, 2, 4), np.int32))
+    assert L.frog_index_upload_ex(ix5.handle, 0, F.STORAGE_BF16) == -7
 
 
 def test_save_load_roundtrip_and_corruption(tmp_path):
