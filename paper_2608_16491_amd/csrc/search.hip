@@ -1010,7 +1010,7 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
 // a dense product (16 queries x a run of rows) for the fp32 matrix cores in
 // place of per-query gathers:
 //   s_plan_kernel     per query: threshold, level, run in the level's list,
-//                     and a bucket (level, position of l) for grouping
+//                     and a bucket (level, range midpoint) for grouping
 //   s_offsets_kernel  bucket offsets (one workgroup)
 //   s_order_kernel    the queries in bucket order
 //   s_tile_kernel     tiles of 16 consecutive queries: the union of their
@@ -1034,7 +1034,7 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
 
 constexpr int kSQ = 16;        // queries per tile
 constexpr int kSChunks = 8;    // work items per tile
-constexpr int kSBins = 256;    // buckets of l per level
+constexpr int kSBins = 2048;   // buckets of the range midpoint per level
 
 struct SPlan {
     int32_t l, r;
@@ -1147,7 +1147,9 @@ __global__ void s_plan_kernel(SParams P) {
         }
         p.a = (int32_t)level_lower(lv, n, p.lev, p.l);
         p.b = (int32_t)level_lower(lv, n, p.lev, (int64_t)p.r + 1);
-        p.bin = p.lev * kSBins + (int)(((int64_t)p.l * kSBins) / n);
+        // queries sorted by the midpoint of their range share most of their
+        // runs, so a tile's union stays close to one run
+        p.bin = p.lev * kSBins + (int)((((int64_t)p.l + p.r) * kSBins) / (2 * n));
     }
     p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
     P.plan[q] = p;
@@ -1155,32 +1157,44 @@ __global__ void s_plan_kernel(SParams P) {
 }
 
 // Bucket offsets: level by level, each level's run of places padded to a
-// multiple of 16; inside a level, buckets in order of l.  The empty ranges'
-// bucket comes last.  One thread per level.
+// multiple of 16; inside a level, buckets in order of the range midpoint.
+// The empty ranges' bucket comes last.  Wavefront w owns levels w and w + 16
+// (nlev <= 31); lane i owns buckets [32 i, 32 i + 32) of a level, read and
+// written as 16-byte vectors.
 __global__ __launch_bounds__(1024) void s_offsets_kernel(SParams P) {
-    // thread t owns buckets [8t, 8t + 8); the 32 threads of a half-wave own
-    // one level (256 buckets)
-    constexpr int kPer = kSBins / 32;
+    static_assert(kSBins == 64 * 32, "32 buckets per lane");
+    constexpr int kWaves = 1024 / 64;
     __shared__ uint32_t start[34];
     const int t = threadIdx.x;
     const int lane = t & 63;
+    const int w = t >> 6;
     const int nlev = P.a.lv.nlev;
-    const int j = t / 32;
-    uint32_t h[kPer];
-    uint32_t sum = 0;
+    uint4 h[2][8];
+    uint32_t excl[2] = {0u, 0u};
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        h[i] = j <= nlev ? P.hist[t * kPer + i] : 0u;
-        sum += h[i];
-    }
-    // inclusive scan over the 32 threads of the level
-    uint32_t inc = sum;
+    for (int s = 0; s < 2; ++s) {
+        const int j = w + kWaves * s;   // wave-uniform
+        uint32_t sum = 0;
 #pragma unroll
-    for (int o = 1; o < 32; o <<= 1) {
-        const uint32_t v = __shfl_up(inc, o, 32);
-        if ((lane & 31) >= o) inc += v;
+        for (int i = 0; i < 8; ++i) h[s][i] = make_uint4(0u, 0u, 0u, 0u);
+        if (j <= nlev) {
+            const uint4* src = reinterpret_cast<const uint4*>(P.hist + (size_t)j * kSBins + lane * 32);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                h[s][i] = src[i];
+                sum += h[s][i].x + h[s][i].y + h[s][i].z + h[s][i].w;
+            }
+        }
+        // exclusive scan of the lanes' sums
+        uint32_t inc = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t v = __shfl_up(inc, o);
+            if (lane >= o) inc += v;
+        }
+        excl[s] = inc - sum;
+        if (lane == 63 && j <= nlev) start[j + 1] = (inc + kSQ - 1) / kSQ * kSQ;
     }
-    if ((t & 31) == 31 && j <= nlev) start[j + 1] = (inc + kSQ - 1) / kSQ * kSQ;
     __syncthreads();
     if (t == 0) {
         start[0] = 0;
@@ -1190,12 +1204,24 @@ __global__ __launch_bounds__(1024) void s_offsets_kernel(SParams P) {
         P.meta[1] = start[nlev + 1] / kSQ;
     }
     __syncthreads();
-    if (j <= nlev) {
-        uint32_t run = start[j] + inc - sum;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-            P.bstart[t * kPer + i] = run;
-            run += h[i];
+    for (int s = 0; s < 2; ++s) {
+        const int j = w + kWaves * s;
+        if (j > nlev) continue;
+        uint32_t run = start[j] + excl[s];
+        uint4* dst = reinterpret_cast<uint4*>(P.bstart + (size_t)j * kSBins + lane * 32);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint4 o;
+            o.x = run;
+            run += h[s][i].x;
+            o.y = run;
+            run += h[s][i].y;
+            o.z = run;
+            run += h[s][i].z;
+            o.w = run;
+            run += h[s][i].w;
+            dst[i] = o;
         }
     }
 }
