@@ -134,8 +134,10 @@ __device__ __forceinline__ void buf_init(const BufList& B) {
 // Cut the buffer: with exact = true keep its K smallest entries (all if
 // there are at most K); with exact = false keep every entry at or below some
 // value x with K <= #kept <= 5K/4 (a cheaper search; the exact cut when ties
-// leave no such x).  The new threshold is the smallest value a dropped entry
-// can have.  K is 32, 64, 128 or 256.
+// leave no such x).  The bisection over the value bits stops at the first x
+// that qualifies (for the exact cut: exactly K entries at or below x), so it
+// rarely runs to a single value.  The new threshold is at or below the value
+// of every dropped entry.  K is 32, 64, 128 or 256.
 template <int K>
 __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
     constexpr int R = 2 * K / 64;   // entries per lane
@@ -159,8 +161,8 @@ __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
         vmin = a < vmin ? a : vmin;
         vmax = b > vmax ? b : vmax;
     }
-    // smallest x in [vmin, vmax] with #(entries <= x) >= K, or (loose) any x
-    // with K <= #(entries <= x) <= 5K/4
+    // an x in [vmin, vmax] with #(entries <= x) equal to K (exact) or in
+    // [K, 5K/4] (loose); failing that, the smallest x with #(entries <= x) >= K
     uint32_t lo = __builtin_amdgcn_readfirstlane(vmin), hi = __builtin_amdgcn_readfirstlane(vmax);
     int cx = f;
     bool loose = false;
@@ -174,7 +176,8 @@ __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
         } else {
             hi = mid;
             cx = c;
-            if (!exact && c <= K + K / 4) {
+            // keeping every entry <= mid is the cut asked for
+            if (c <= (exact ? K : K + K / 4)) {
                 loose = true;
                 break;
             }

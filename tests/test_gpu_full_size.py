@@ -171,6 +171,46 @@ def test_full_size_k100_pool256_sampled(c2):
 
 
 @pytest.mark.timeout(900)
+@pytest.mark.parametrize("epn", [4, 16])
+def test_full_size_deep_sample_levels(c2, epn):
+    """A fixed number of entry points (epn = 4 or 16, no scaling with the
+    range) over ranges of selectivity 2^-8 .. 1: the shared sample then lies
+    in the deep levels of the priority lists (up to level 17 of 20 at n = 1M),
+    whose buckets the planning kernels handle in a second pass.  Sampled rows
+    vs the oracle, every row checked for its properties."""
+    w, ix, ox, d = c2
+    rng = np.random.default_rng(11 + epn)
+    nq = 3000
+    sigma = 2.0 ** rng.uniform(-8, 0, nq)
+    lo, hi = workloads.ranges_for_selectivity(rng, sigma, w.n)
+    dev = torch.device("cuda:0")
+    p = dict(epn=epn, epn_frac=0.0, budget=16, entry_mode=1, hash_log2=10)
+    ids, ds = F.search(ix, d["Q"][:nq].contiguous(), torch.as_tensor(lo, device=dev),
+                       torch.as_tensor(hi, device=dev), K, 32, **p)
+    torch.cuda.synchronize()
+    ids, ds = ids.cpu().numpy(), ds.cpu().numpy()
+    sample = np.sort(rng.choice(nq, 200, replace=False))
+    o_ids, o_d, _ = oracle.search(ox, w.Q[:nq][sample], lo[sample], hi[sample], K, 32, qidx=sample,
+                                  epn=epn, epn_frac=0.0, epn_max=0, B=16, entry_mode=1)
+    assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
+    a = np.sort(w.attr)
+    cnt = np.searchsorted(a, hi, "right") - np.searchsorted(a, lo, "left")
+    valid = ids >= 0
+    # the shared sample's size is binomial with mean epn (empty with
+    # probability about e^-epn), and from so few entry points a traversal
+    # can end with fewer than k in-range results; the sampled rows' counts
+    # are part of the parity above
+    assert (valid.sum(1) <= np.minimum(K, cnt)).all()
+    print(f"[gpu] deep levels, epn={epn}: rows with fewer than k results: {(valid.sum(1) < np.minimum(K, cnt)).sum()}",
+          flush=True)
+    av = w.attr[np.where(valid, ids, 0)]
+    assert ((av >= lo[:, None]) & (av <= hi[:, None]) | ~valid).all()
+    # results first (ascending), padding after
+    assert (np.diff(valid.astype(np.int8), axis=1) <= 0).all()
+    assert (np.diff(np.where(valid, ds, np.finfo(np.float32).max), axis=1) >= 0).all()
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("mode", [1, 0])
 def test_full_size_fp16_rows_sampled(c2, mode):
     """The same 1M index uploaded with fp16 rows at the timed setting: sampled
