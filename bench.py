@@ -54,13 +54,15 @@ SWEEP = [
     (24, 16, 1.0, 2304, 32, 1), (32, 16, 1.0, 3072, 16, 1), (24, 16, 1.0, 3072, 24, 1),
     (16, 16, 1.0, 3072, 32, 1), (32, 16, 1.0, 4096, 16, 1), (64, 16, 1.0, 2560, 16, 1),
     (64, 16, 1.0, 3072, 16, 1), (128, 16, 1.0, 2048, 16, 1),
-    # entry mode 1 on indexes with one or two more layers (n_inv 6 and 5,
-    # built on the GPU)
+    # entry mode 1 on indexes with one, two or three more layers (n_inv 6,
+    # 5 and 4, built on the GPU)
     (32, 16, 1.0, 2048, 24, 1, 6), (32, 16, 1.0, 2304, 24, 1, 6), (32, 16, 1.0, 2560, 16, 1, 6),
     (32, 16, 1.0, 2560, 24, 1, 6), (24, 16, 1.0, 2048, 32, 1, 6), (64, 16, 1.0, 2048, 16, 1, 6),
     (32, 16, 1.0, 2304, 16, 1, 6), (32, 16, 1.0, 2304, 20, 1, 6), (32, 16, 1.0, 2432, 16, 1, 6),
     (32, 16, 1.0, 2048, 24, 1, 5), (32, 16, 1.0, 2048, 16, 1, 5), (32, 16, 1.0, 2560, 16, 1, 5),
-    (32, 16, 1.0, 2304, 16, 1, 5),
+    (32, 16, 1.0, 2304, 16, 1, 5), (32, 16, 1.0, 2432, 16, 1, 5), (24, 16, 1.0, 2304, 32, 1, 5),
+    (24, 16, 1.0, 2560, 24, 1, 5), (24, 16, 1.0, 2048, 32, 1, 5), (16, 16, 1.0, 3072, 32, 1, 5),
+    (32, 16, 1.0, 2304, 16, 1, 4), (32, 16, 1.0, 2560, 16, 1, 4), (24, 16, 1.0, 2304, 32, 1, 4),
 ]
 
 
