@@ -1091,11 +1091,25 @@ __device__ __forceinline__ int32_t level_rank(const SharedLevels& lv, int j, int
     return j == 0 ? (int32_t)pos : lv.ranks[lv.off[j] + pos];
 }
 
-// first position of level j's list whose rank is >= x
+// first position of level j's list whose rank is >= x.  One thread: a
+// 16-ary search whose 15 probes per round are independent loads (about 5
+// dependent rounds at n = 1M instead of 20 binary steps), then a binary
+// search over the last 16 positions.
 __device__ int64_t level_lower(const SharedLevels& lv, int64_t n, int j, int64_t x) {
     if (j == 0) return x < 0 ? 0 : (x > n ? n : x);
     const int32_t* a = lv.ranks + lv.off[j];
+    // the answer lies in [lo, hi]: a[i] < x for i < lo, a[hi] >= x or hi = end
     int64_t lo = 0, hi = lv.off[j + 1] - lv.off[j];
+    while (hi - lo > 16) {
+        const int64_t step = (hi - lo) / 16;   // probes lo + t step, t = 1..15, all < hi
+        int c = 0;
+#pragma unroll
+        for (int t = 1; t < 16; ++t) c += a[lo + t * step] < x ? 1 : 0;
+        // the ranks ascend: probes 1..c are below x, c + 1 .. 15 are not
+        const int64_t nlo = c > 0 ? lo + c * step + 1 : lo;
+        if (c < 15) hi = lo + (c + 1) * step;
+        lo = nlo;
+    }
     while (lo < hi) {
         const int64_t mid = (lo + hi) >> 1;
         if (a[mid] < x) lo = mid + 1;
