@@ -223,7 +223,11 @@ def main():
     def parse_setting(text):
         return norm_setting([float(x) for x in text.split(",")])
 
-    def timed(fn, reps):
+    def timed(fn, reps, warm=2):
+        # untimed calls first: the first calls after an index upload or a
+        # rebuild also grow the allocator's pool
+        for _ in range(warm):
+            fn()
         s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         s.record(stream)
