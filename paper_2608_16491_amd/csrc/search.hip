@@ -1009,8 +1009,9 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
 // at the same level draw from the same rows, and their entry distances form
 // a dense product (16 queries x a run of rows) for the fp32 matrix cores in
 // place of per-query gathers:
-//   s_plan_kernel     per query: threshold, level, run in the level's list,
-//                     and a bucket (level, range midpoint) for grouping
+//   s_plan_kernel     per query (one wavefront): rank interval, threshold,
+//                     level, run in the level's list, and a bucket (level,
+//                     range midpoint) for grouping
 //   s_offsets_kernel  bucket offsets (one workgroup)
 //   s_order_kernel    the queries in bucket order
 //   s_tile_kernel     tiles of 16 consecutive queries: the union of their
@@ -1062,7 +1063,7 @@ struct STile {
 struct SParams {
     DevIndex ix;
     SearchLaunch a;
-    const int32_t* lr;
+    int32_t* lr;        // [nq][2] rank intervals (written by s_plan_kernel)
     SPlan* plan;
     uint32_t* hist;     // [nbins] queries per bucket
     uint32_t* bstart;   // [nbins] first place of each bucket
@@ -1129,15 +1130,56 @@ __global__ void s_init_kernel(uint32_t* meta, uint32_t* hist, int nbins, int32_t
     if (i < norder) order[i] = -1;
 }
 
-__global__ void s_plan_kernel(SParams P) {
-    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (q >= P.a.nq) return;
+// Half-wave searches over an ascending array a[0, n): each half counts the
+// leading entries for which its predicate holds (lanes 0..31 call
+// below(v, false), lanes 32..63 below(v, true); each predicate holds on a
+// prefix).  A 32-ary search: every round each lane of a half probes one
+// position and the half's ballot narrows its interval 32-fold; the two
+// halves run in the same rounds (4 for n = 1M).  Every lane returns its
+// half's count.
+template <typename TA, typename F>
+__device__ int64_t half_count(const TA* __restrict__ a, int64_t n, F below) {
+    const int lane = lane_id();
+    const int hl = lane & 31;
+    const bool upper = lane >= 32;
+    int64_t lo = 0, hi = n;   // the count lies in [lo, hi]
+    for (;;) {
+        const bool live = hi > lo;
+        if (ballot(live) == 0) break;
+        const int64_t step = (hi - lo + 31) / 32;
+        const int64_t p = lo + (int64_t)(hl + 1) * step - 1;
+        const bool b = live && p < hi && below(a[p], upper);
+        const uint64_t m = ballot(b);
+        const int c = __popc((uint32_t)(upper ? (m >> 32) : m));
+        if (live) {
+            const int64_t nhi = lo + (int64_t)(c + 1) * step - 1;
+            lo += (int64_t)c * step;
+            hi = nhi < hi ? nhi : hi;
+        }
+    }
+    return lo;
+}
+
+// One wavefront per query: the rank interval of its range (the two bounds
+// searched side by side, one per half-wave), the threshold, the level, the
+// run of the level's list (again one bound per half-wave) and a bucket.
+__global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
+    const int64_t q = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (q >= P.a.nq) return;   // wave-uniform
     const SharedLevels& lv = P.a.lv;
     const int64_t n = P.ix.n;
+    const double lo_v = P.a.lo[q], hi_v = P.a.hi[q];
     SPlan p{};
-    p.l = P.lr[2 * q];
-    p.r = P.lr[2 * q + 1];
     p.tslot = -1;
+    if (isnan(lo_v) || isnan(hi_v)) {
+        p.l = 0;
+        p.r = -1;
+    } else {
+        // l = #{attr < lo}, r = #{attr <= hi} - 1
+        const int64_t c = half_count(P.ix.attr, n, [&](double v, bool upper) { return upper ? v <= hi_v : v < lo_v; });
+        p.l = __builtin_amdgcn_readlane((int32_t)c, 0);
+        p.r = __builtin_amdgcn_readlane((int32_t)c, 32) - 1;
+    }
     if (p.l > p.r) {
         p.bin = P.nbins - 1;
     } else {
@@ -1159,15 +1201,29 @@ __global__ void s_plan_kernel(SParams P) {
             const int cl = t <= 1 ? 0 : 64 - __builtin_clzll(t - 1);   // ceil(log2 t)
             p.lev = 32 - cl < lv.nlev ? 32 - cl : lv.nlev;
         }
-        p.a = (int32_t)level_lower(lv, n, p.lev, p.l);
-        p.b = (int32_t)level_lower(lv, n, p.lev, (int64_t)p.r + 1);
+        if (p.lev == 0) {
+            p.a = p.l;
+            p.b = p.r + 1;
+        } else {
+            // first positions of the level's list with rank >= l and >= r + 1
+            const int32_t* ar = lv.ranks + lv.off[p.lev];
+            const int64_t len = lv.off[p.lev + 1] - lv.off[p.lev];
+            const int32_t x0 = p.l, x1 = p.r + 1;
+            const int64_t c = half_count(ar, len, [&](int32_t v, bool upper) { return v < (upper ? x1 : x0); });
+            p.a = __builtin_amdgcn_readlane((int32_t)c, 0);
+            p.b = __builtin_amdgcn_readlane((int32_t)c, 32);
+        }
         // queries sorted by the midpoint of their range share most of their
         // runs, so a tile's union stays close to one run
         p.bin = p.lev * kSBins + (int)((((int64_t)p.l + p.r) * kSBins) / (2 * n));
     }
-    p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
-    P.plan[q] = p;
-    if (P.a.stats) P.a.stats[q * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
+    if (lane_id() == 0) {
+        p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
+        P.plan[q] = p;
+        P.lr[2 * q] = p.l;
+        P.lr[2 * q + 1] = p.r;
+        if (P.a.stats) P.a.stats[q * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
+    }
 }
 
 // Bucket offsets: level by level, each level's run of places padded to a
@@ -1992,9 +2048,8 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     const int64_t ninit = norder > P.nbins ? norder : P.nbins;
     hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.hist,
                        P.nbins, P.order, norder);
-    const int64_t rb_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
-    hipLaunchKernelGGL(rank_bounds_kernel, dim3((unsigned)rb_blocks), dim3(kBlock), 0, stream, ix, a.lo, a.hi, a.nq, lr);
-    hipLaunchKernelGGL(s_plan_kernel, dim3(qb), dim3(256), 0, stream, P);
+    const int64_t plan_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL(s_plan_kernel, dim3((unsigned)plan_blocks), dim3(kBlock), 0, stream, P);
     hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(1024), 0, stream, P);
     hipLaunchKernelGGL(s_order_kernel, dim3(qb), dim3(256), 0, stream, P);
     hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + kWavesPerBlock - 1) / kWavesPerBlock)), dim3(kBlock),
