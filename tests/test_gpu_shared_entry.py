@@ -136,3 +136,28 @@ def test_shared_other_dimensions(d):
     g_ids, g_d = c.gpu(10, 32, **p)
     o_ids, o_d, _ = c.cpu(10, 32, **p)
     assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_duplicate_attribute_values(mode):
+    # 8,000 objects on 200 distinct attribute values (40 per value): the rank
+    # domain breaks ties by original index, and a range's bounds count
+    # attr < lo and attr <= hi, so integer bounds fall on runs of ties and
+    # half-integer bounds between them
+    print(f"[gpu] duplicate attribute values, entry mode {mode}", flush=True)
+    rng = np.random.default_rng(17)
+    w = workloads.make("tiny", n=8000, nq=120)
+    attr = rng.integers(0, 200, 8000).astype(np.float64)
+    a0 = rng.integers(0, 200, 120).astype(np.float64)
+    span = rng.integers(0, 60, 120).astype(np.float64)
+    lo = np.where(np.arange(120) % 2 == 0, a0, a0 - 0.5)
+    hi = np.where(np.arange(120) % 3 == 0, a0 + span, a0 + span + 0.5)
+    c = Case(w.X, attr, w.Q, lo, hi)
+    p = dict(entry_mode=mode, epn=16, epn_frac=0.5, epn_max=600)
+    g_ids, g_d = c.gpu(10, 32, **p)
+    o_ids, o_d, _ = c.cpu(10, 32, **p)
+    assert_parity(g_ids, g_d, o_ids, o_d)
+    # every result lies in its range
+    valid = g_ids >= 0
+    av = attr[np.where(valid, g_ids, 0)]
+    assert ((av >= lo[:, None]) & (av <= hi[:, None]) | ~valid).all()
