@@ -1012,7 +1012,7 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
 //   s_plan_kernel     per query (one wavefront): rank interval, threshold,
 //                     level, run in the level's list, and a bucket (level,
 //                     range midpoint) for grouping
-//   s_offsets_kernel  bucket offsets (one wavefront per level)
+//   s_offsets_kernel  bucket offsets (one workgroup)
 //   s_order_kernel    the queries in bucket order
 //   s_tile_kernel     tiles of 16 consecutive queries: the union of their
 //                     runs in the finest level among them
@@ -1066,7 +1066,6 @@ struct SParams {
     int32_t* lr;        // [nq][2] rank intervals (written by s_plan_kernel)
     SPlan* plan;
     uint32_t* hist;     // [nbins] queries per bucket
-    uint32_t* levcnt;   // [nlev + 1] queries with a non-empty range per level
     uint32_t* bstart;   // [nbins] first place of each bucket
     uint32_t* meta;     // [0] places used in `order`, [1] tiles, [2] query counter
     int32_t* order;     // [nq + 16 (nlev + 1)] queries by bucket, each level's run
@@ -1220,7 +1219,6 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
     }
     if (lane_id() == 0) {
         p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
-        if (p.l <= p.r) atomicAdd(P.levcnt + p.lev, 1u);
         P.plan[q] = p;
         P.lr[2 * q] = p.l;
         P.lr[2 * q + 1] = p.r;
@@ -1228,58 +1226,73 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
     }
 }
 
-// Bucket offsets: one wavefront per level j.  Each level's run of places is
-// padded to a multiple of 16 and starts after the runs of the levels before
-// it, whose sizes s_plan_kernel counted; inside the level, buckets in order
-// of the range midpoint, lane i owning buckets [32 i, 32 i + 32) of it, read
-// and written as 16-byte vectors.  The empty ranges' bucket comes last.
-__global__ __launch_bounds__(64) void s_offsets_kernel(SParams P) {
+// Bucket offsets: level by level, each level's run of places padded to a
+// multiple of 16; inside a level, buckets in order of the range midpoint.
+// The empty ranges' bucket comes last.  Wavefront w owns levels w and w + 16
+// (nlev <= 31); lane i owns buckets [32 i, 32 i + 32) of a level, read and
+// written as 16-byte vectors.
+__global__ __launch_bounds__(1024) void s_offsets_kernel(SParams P) {
     static_assert(kSBins == 64 * 32, "32 buckets per lane");
-    const int lane = lane_id();
-    const int j = blockIdx.x;
-    const int nlev = P.a.lv.nlev;   // <= 31: one lane per level
-    const uint32_t run = lane <= nlev ? (P.levcnt[lane] + kSQ - 1) / kSQ * kSQ : 0u;
-    uint32_t before = lane < j ? run : 0u;
-    uint32_t all = run;
+    constexpr int kWaves = 1024 / 64;
+    __shared__ uint32_t start[34];
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int nlev = P.a.lv.nlev;
+    uint4 h[2][8];
+    uint32_t excl[2] = {0u, 0u};
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        before += __shfl_xor(before, o);
-        all += __shfl_xor(all, o);
-    }
-    if (j == 0 && lane == 0) {
-        P.bstart[P.nbins - 1] = all;
-        P.meta[0] = all;
-        P.meta[1] = all / kSQ;
-    }
-    const uint4* src = reinterpret_cast<const uint4*>(P.hist + (size_t)j * kSBins + lane * 32);
-    uint4 h[8];
-    uint32_t sum = 0;
+    for (int s = 0; s < 2; ++s) {
+        const int j = w + kWaves * s;   // wave-uniform
+        uint32_t sum = 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        h[i] = src[i];
-        sum += h[i].x + h[i].y + h[i].z + h[i].w;
-    }
-    // exclusive scan of the lanes' sums
-    uint32_t inc = sum;
+        for (int i = 0; i < 8; ++i) h[s][i] = make_uint4(0u, 0u, 0u, 0u);
+        if (j <= nlev) {
+            const uint4* src = reinterpret_cast<const uint4*>(P.hist + (size_t)j * kSBins + lane * 32);
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t v = __shfl_up(inc, o);
-        if (lane >= o) inc += v;
-    }
-    uint32_t r = before + inc - sum;
-    uint4* dst = reinterpret_cast<uint4*>(P.bstart + (size_t)j * kSBins + lane * 32);
+            for (int i = 0; i < 8; ++i) {
+                h[s][i] = src[i];
+                sum += h[s][i].x + h[s][i].y + h[s][i].z + h[s][i].w;
+            }
+        }
+        // exclusive scan of the lanes' sums
+        uint32_t inc = sum;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        uint4 o;
-        o.x = r;
-        r += h[i].x;
-        o.y = r;
-        r += h[i].y;
-        o.z = r;
-        r += h[i].z;
-        o.w = r;
-        r += h[i].w;
-        dst[i] = o;
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t v = __shfl_up(inc, o);
+            if (lane >= o) inc += v;
+        }
+        excl[s] = inc - sum;
+        if (lane == 63 && j <= nlev) start[j + 1] = (inc + kSQ - 1) / kSQ * kSQ;
+    }
+    __syncthreads();
+    if (t == 0) {
+        start[0] = 0;
+        for (int i = 1; i <= nlev + 1; ++i) start[i] += start[i - 1];
+        P.bstart[P.nbins - 1] = start[nlev + 1];
+        P.meta[0] = start[nlev + 1];
+        P.meta[1] = start[nlev + 1] / kSQ;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        const int j = w + kWaves * s;
+        if (j > nlev) continue;
+        uint32_t run = start[j] + excl[s];
+        uint4* dst = reinterpret_cast<uint4*>(P.bstart + (size_t)j * kSBins + lane * 32);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint4 o;
+            o.x = run;
+            run += h[s][i].x;
+            o.y = run;
+            run += h[s][i].y;
+            o.z = run;
+            run += h[s][i].z;
+            o.w = run;
+            run += h[s][i].w;
+            dst[i] = o;
+        }
     }
 }
 
@@ -1988,7 +2001,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     const size_t o_meta = take(16);
     const size_t o_lr = take((size_t)a.nq * 8);
     const size_t o_plan = take((size_t)a.nq * sizeof(SPlan));
-    const size_t o_hist = take((size_t)(P.nbins + 64) * 4);   // then levcnt[64]
+    const size_t o_hist = take((size_t)P.nbins * 4);
     const size_t o_bstart = take((size_t)P.nbins * 4);
     const size_t o_order = take((size_t)norder * 4);
     const size_t o_tiles = take((size_t)P.tmax * sizeof(STile));
@@ -2016,7 +2029,6 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     P.lr = lr;
     P.plan = reinterpret_cast<SPlan*>(base + o_plan);
     P.hist = reinterpret_cast<uint32_t*>(base + o_hist);
-    P.levcnt = P.hist + P.nbins;
     P.bstart = reinterpret_cast<uint32_t*>(base + o_bstart);
     P.order = reinterpret_cast<int32_t*>(base + o_order);
     P.tiles = reinterpret_cast<STile*>(base + o_tiles);
@@ -2033,13 +2045,12 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     // events: before the matrix-core scan, after it, after the search kernel
     // (the planning kernels come before the first, the pool kernel after the
     // second)
-    const int nhist = P.nbins + 64;   // the buckets and the per-level counts
-    const int64_t ninit = norder > nhist ? norder : nhist;
+    const int64_t ninit = norder > P.nbins ? norder : P.nbins;
     hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.hist,
-                       nhist, P.order, norder);
+                       P.nbins, P.order, norder);
     const int64_t plan_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL(s_plan_kernel, dim3((unsigned)plan_blocks), dim3(kBlock), 0, stream, P);
-    hipLaunchKernelGGL(s_offsets_kernel, dim3((unsigned)(a.lv.nlev + 1)), dim3(64), 0, stream, P);
+    hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(1024), 0, stream, P);
     hipLaunchKernelGGL(s_order_kernel, dim3(qb), dim3(256), 0, stream, P);
     hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + kWavesPerBlock - 1) / kWavesPerBlock)), dim3(kBlock),
                        0, stream, P);
