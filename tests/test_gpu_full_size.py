@@ -257,6 +257,43 @@ def test_full_size_fp16_rows_sampled(c2, mode):
     assert (np.abs(got - ref) <= np.spacing(ref)).all()
 
 
+def _to_bf16(x):
+    """x rounded to the nearest bfloat16 (ties to even), as fp64: with
+    x = m 2^e, 0.5 <= |m| < 1, bf16 keeps 8 bits of m (normal numbers)."""
+    m, e = np.frexp(np.asarray(x, np.float64))
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("mode", [1, 0])
+def test_full_size_bf16_rows_sampled(c2, mode):
+    """The same 1M index uploaded with bf16 rows at the timed setting: sampled
+    rows equal the oracle's search over the rows rounded to bfloat16 (frexp
+    and ties-to-even rint), and every distance is the squared L2 to the
+    rounded row."""
+    w, ix, ox, d = c2
+    ob = oracle.OracleIndex(ox.perm, ox.attr_sorted, _to_bf16(ox.X_rank).astype(np.float32), ox.ENC)
+    p = SETTINGS[mode]
+    try:
+        ix.upload(0, storage="bf16")
+        ids, ds = F.search(ix, d["Q"], d["lo"], d["hi"], K, L, **p)
+        torch.cuda.synchronize()
+    finally:
+        ix.upload(0)
+    ids, ds = ids.cpu().numpy(), ds.cpu().numpy()
+    rng = np.random.default_rng(9)
+    sample = np.sort(rng.choice(w.nq, 300, replace=False))
+    o_ids, o_d, _ = oracle.search(ob, w.Q[sample], w.lo[sample], w.hi[sample], K, L, qidx=sample,
+                                  epn=p["epn"], epn_frac=p["epn_frac"], epn_max=p["epn_max"], B=p["budget"],
+                                  entry_mode=mode)
+    assert_parity(ids[sample], ds[sample], o_ids, o_d, max_residual=1)
+    valid = ids >= 0
+    qi, kj = np.nonzero(valid)
+    ref = ((_to_bf16(w.X[ids[qi, kj]]) - w.Q[qi].astype(np.float64)) ** 2).sum(1).astype(np.float32)
+    got = ds[qi, kj]
+    assert (np.abs(got - ref) <= np.spacing(ref)).all()
+
+
 @pytest.mark.timeout(900)
 def test_full_size_gpu_construction_equals_host(c2):
     """The 1M x 128 index built on the GPU equals the host construction (whose
