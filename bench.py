@@ -116,7 +116,7 @@ def main():
     ap.add_argument("--details", default=None, help="write sweep details (JSON) here")
     ap.add_argument("--index-cache", default=None, help="load the index from / save it to this file")
     ap.add_argument("--ablation", action="store_true",
-                    help="also measure the ablations of Sec 8.4 at the chosen setting: hotspot without its end "
+                    help="also measure the ablations of Sec 8.2.3 at the chosen setting: hotspot without its end "
                          "condition / without localisation, eager visited check, and (rebuilding the index) "
                          "beta = 0; reported under 'ablation' in --details")
     ap.add_argument("--sweep-params", action="store_true",
@@ -488,7 +488,7 @@ def main():
             f"search {hb * 1e3:.3f} ms")
         ix.upload(0)
 
-    # ablations (Sec 8.4) at the chosen setting
+    # ablations (Sec 8.2.3) at the chosen setting
     ablation = None
     if args.ablation:
         ablation = []
@@ -525,7 +525,7 @@ def main():
         abl("beta = 0 (no attribute fusion)", index=ix0)
         ix0.free()
 
-    # sensitivity (Sec 8.4): construction parameters through GPU rebuilds, the
+    # sensitivity (Sec 8.2.5 for beta and gamma; n_inv, B and the entry cap likewise): construction parameters through GPU rebuilds, the
     # expansion budget and the entry-point cap at query time, each around the
     # chosen setting with the others at their defaults
     sensitivity = None

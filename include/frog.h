@@ -87,7 +87,7 @@ typedef struct {
                            cores in tiles of 16 queries.  Mode 1 builds and
                            uploads the seed's rank lists on its first call
                            (synchronously; about n int32 of device memory) */
-    int hotspot_mode;   /* ablation of HotspotLocalization (Sec 8.4): 0 (default)
+    int hotspot_mode;   /* ablation of HotspotLocalization (Sec 8.2.3): 0 (default)
                            layers L_start..L_end of Alg. 3; 1 layers
                            L_start..H-1 (no end condition); 2 all layers */
     int eager_check;    /* ablation of the lazy visited check: 1 checks (and

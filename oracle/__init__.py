@@ -107,6 +107,10 @@ def configure(lib):
     lib.fo_build.restype = i32
     lib.fo_build.argtypes = [P, P, i64, i32, i32, i32, i32, i32, i32, f64, f64, u64, i32,
                              P, P, P, P]
+    lib.fo_rng_prune_list.restype = i32
+    lib.fo_rng_prune_list.argtypes = [P, i32, P, P, i32, i32, P]
+    lib.fo_sibling_search_list.restype = i32
+    lib.fo_sibling_search_list.argtypes = [P, i64, i32, P, i32, P, i64, i64, P, i32, i32, i32, P, P, P]
     lib.fo_closure.restype = i64
     lib.fo_closure.argtypes = [P, i32, i32, i64, i64, i64, i32, i32, i32, P, i64, P]
     return lib
@@ -262,6 +266,41 @@ def build(X, attr, *, m=None, ef_c=None, n_inv=None, patience=None, sib_seeds=No
     return OracleIndex(perm, attr_sorted, X_rank, ENC)
 
 
+def rng_prune(X, ids, dists, m: int) -> np.ndarray:
+    """The construction's RNG prune (Sec 6.1, alpha = 1) of candidates given
+    by rank `ids` (rows of X) with their squared distances to the vertex,
+    ascending by (distance, id).  Returns the m-entry temporary-PG row (-1
+    padded)."""
+    X = _c(X, np.float32)
+    ids = _c(ids, np.int32)
+    dists = _c(dists, np.float32)
+    out = np.full(m, -1, np.int32)
+    rc = _load().fo_rng_prune_list(_p(X), X.shape[1], _p(ids), _p(dists), ids.shape[0], m, _p(out))
+    if rc < 0:
+        raise MemoryError("oracle rng_prune: allocation failed")
+    return out
+
+
+def sibling_search(X, PG, xq, ts: int, te: int, seeds, ef: int, patience: int):
+    """The construction's greedy search (Alg 1 with the patience stop of Sec
+    6.2.2) for the vector xq over the temporary PG (int32 [n, m], -1 empty)
+    restricted to ranks [ts, te], from the given seed ranks.  Returns (the m
+    nearest found, their squared distances, expansions)."""
+    X = _c(X, np.float32)
+    PG = _c(PG, np.int32)
+    xq = _c(xq, np.float32)
+    seeds = _c(seeds, np.int32)
+    n, m = PG.shape
+    res = np.full(m, -1, np.int32)
+    resd = np.full(m, np.inf, np.float32)
+    nexp = C.c_int64(0)
+    rc = _load().fo_sibling_search_list(_p(X), n, X.shape[1], _p(PG), m, _p(xq), ts, te, _p(seeds),
+                                        seeds.shape[0], ef, patience, _p(res), _p(resd), C.byref(nexp))
+    if rc < 0:
+        raise MemoryError("oracle sibling_search: allocation failed")
+    return res[:rc].copy(), resd[:rc].copy(), nexp.value
+
+
 # ---------------------------------------------------------------- search
 
 def entry_count(cnt: int, epn: int, epn_frac: float = 0.0, epn_max: int = 0) -> int:
@@ -275,7 +314,7 @@ def search(ix: OracleIndex, Q, lo, hi, k: int, L: int, *, epn: int = 16, epn_fra
     ranks, dists float32 [nq,k], stats int64 [nq,8]).  The entry-point count
     is epn, or clamp(ceil(epn_frac * cnt), epn, epn_max) when epn_frac > 0;
     entry_mode 0 draws them stratified per query, 1 from the shared-priority
-    sample (that count is then the expected size).  Ablations (Sec 8.4):
+    sample (that count is then the expected size).  Ablations (Sec 8.2.3):
     hot_mode 1 scans layers L_start..H-1, 2 all layers; eager moves the
     visited check into ENIdentification."""
     Q = _c(Q, np.float32)

@@ -23,7 +23,7 @@
  *   fo_en_ident        ENIdentification (Alg. 4): scan hotspot layers in stored
  *                      order, keep in-range candidates, stop at budget B
  *   fo_search_batch    FROGSearch (Alg. 2) with an exact visited set, and the
- *                      ablation variants of Sec 8.4 (hotspot without its end
+ *                      ablation variants of Sec 8.2.3 (hotspot without its end
  *                      condition or without localisation; eager visited check)
  *   fo_exact_batch     exhaustive filtered k-NN (Def. 2, RFANNS), the ground
  *                      truth the search approximates
@@ -31,6 +31,10 @@
  *                      layer child m-ANN + sibling greedy search (Alg. 1 with
  *                      patience), RNG prune -> temporary PG, fusion re-rank
  *                      (Eq. fusion-distance) -> ENC row)
+ *   fo_rng_prune_list, fo_sibling_search_list
+ *                      the construction's RNG prune (Sec 6.1) and sibling
+ *                      search with the patience stop (Sec 6.2.2) on their own,
+ *                      so that the tests can pin them on hand-built inputs
  *
  * Readings where the paper is silent (the same readings bind the library):
  *   - distances are SQUARED L2, accumulated in double from float inputs in
@@ -555,13 +559,14 @@ int fo_rank_order(const double* attr, int64_t n, int32_t* perm, double* attr_sor
 /* Greedy best-first search (Alg. 1) for the vertex xq over the temporary PG
  * restricted to segment [ts, te], pool width ef, several seeds, stopping
  * early after `patience` consecutive expansions that change nothing in the
- * top-m.  Writes the m nearest found (ascending (dist, id)) to res/resd and
- * returns how many were found. */
+ * top-m (Sec 6.2.2).  Writes the m nearest found (ascending (dist, id)) to
+ * res/resd and returns how many were found; *expansions (may be NULL)
+ * receives the number of pool entries expanded. */
 static int fo_sibling_search(const float* X, int d, const int32_t* PG, int m,
                              const float* xq, int64_t ts, int64_t te,
                              const int32_t* seeds, int nseeds, int ef, int patience,
                              fo_visited* vis, fo_cand* pool, fo_cand* work,
-                             int32_t* res, float* resd) {
+                             int32_t* res, float* resd, int64_t* expansions) {
     fo_visited_clear(vis);
     int np = 0;
     int nw = 0;
@@ -577,11 +582,13 @@ static int fo_sibling_search(const float* X, int d, const int32_t* PG, int m,
     np = nw < ef ? nw : ef;
     for (int i = 0; i < np; ++i) pool[i] = work[i];
     int left = patience;
+    int64_t nexp = 0;
     for (;;) {
         int i = -1;
         for (int t = 0; t < np; ++t) if (pool[t].flag == 0) { i = t; break; }
         if (i < 0) break;
         pool[i].flag = 1;
+        nexp = nexp + 1;
         int32_t w = pool[i].id;
         for (int t = 0; t < np; ++t) work[t] = pool[t];
         int nnew = 0;
@@ -616,6 +623,7 @@ static int fo_sibling_search(const float* X, int d, const int32_t* PG, int m,
     }
     int nr = np < m ? np : m;
     for (int t = 0; t < nr; ++t) { res[t] = pool[t].id; resd[t] = pool[t].dist; }
+    if (expansions) *expansions = nexp;
     return nr;
 }
 
@@ -638,6 +646,41 @@ static int fo_rng_prune(const float* X, int d, const fo_ranked* cand, int nc, in
     free(kept);
     for (int i = nk; i < m; ++i) out[i] = FO_NONE;
     return nk;
+}
+
+/* The two construction steps above on their own, for the tests: the RNG
+ * prune of nc candidates given as (id, squared distance to u) ascending by
+ * (distance, id); and the sibling search over a temporary PG of n vertices
+ * (PG [n][m], -1 for empty slots) with the given seeds.  Each returns what the
+ * step returns, or -2 if memory runs out. */
+int fo_rng_prune_list(const float* X, int d, const int32_t* ids, const float* dists, int nc, int m,
+                      int32_t* out) {
+    fo_ranked* cand = (fo_ranked*)malloc(sizeof(fo_ranked) * (size_t)(nc > 0 ? nc : 1));
+    if (!cand) return -2;
+    for (int i = 0; i < nc; ++i) {
+        cand[i].key = (double)dists[i];
+        cand[i].dist = dists[i];
+        cand[i].id = ids[i];
+    }
+    int nk = fo_rng_prune(X, d, cand, nc, m, out);
+    free(cand);
+    return nk;
+}
+
+int fo_sibling_search_list(const float* X, int64_t n, int d, const int32_t* PG, int m, const float* xq,
+                           int64_t ts, int64_t te, const int32_t* seeds, int nseeds, int ef, int patience,
+                           int32_t* res, float* resd, int64_t* expansions) {
+    fo_visited vis;
+    fo_cand* pool = (fo_cand*)malloc(sizeof(fo_cand) * (size_t)(ef + 1));
+    fo_cand* work = (fo_cand*)malloc(sizeof(fo_cand) * (size_t)(ef + m + nseeds + 1));
+    int rc = -2;
+    if (fo_visited_init(&vis, n) == 0 && pool && work)
+        rc = fo_sibling_search(X, d, PG, m, xq, ts, te, seeds, nseeds, ef, patience, &vis, pool, work,
+                               res, resd, expansions);
+    fo_visited_free(&vis);
+    free(pool);
+    free(work);
+    return rc;
 }
 
 /* Build the index.  X is [n][d] in ORIGINAL object order, attr [n].  Outputs:
@@ -753,7 +796,7 @@ int fo_build(const float* X, const double* attr, int64_t n, int d,
                             }
                         }
                         int nr = fo_sibling_search(X_rank, d, PG, m, xu, ts, te, seeds, ns, ef_c,
-                                                   patience, &vis, pool, work, res, resd);
+                                                   patience, &vis, pool, work, res, resd, NULL);
                         for (int t = 0; t < nr; ++t) {
                             cand[nc].dist = resd[t];
                             cand[nc].key = (double)resd[t];

@@ -181,7 +181,7 @@ def test_other_dimensions(d):
 @pytest.mark.parametrize("entry_mode", [0, 1])
 @pytest.mark.parametrize("hotspot_mode,eager", [(1, 0), (2, 0), (0, 1), (2, 1)])
 def test_ablation_switches_match_oracle(tiny, entry_mode, hotspot_mode, eager):
-    # Sec 8.4 ablations: hotspot without end condition / without localisation,
+    # Sec 8.2.3 ablations: hotspot without end condition / without localisation,
     # eager visited check (exact visited set); every statistic as the oracle's
     p = dict(entry_mode=entry_mode, epn=16, epn_frac=0.2, epn_max=600, hotspot_mode=hotspot_mode,
              eager_check=eager, hash_log2=0)

@@ -60,6 +60,32 @@ MUTANTS = [
     ("leaf keeps farthest", "qsort(fu, (size_t)c, sizeof(fo_ranked), fo_ranked_cmp);\n                    qsort(ve",
      "qsort(fu, (size_t)c, sizeof(fo_ranked), fo_ranked_cmp);\n                    for (int z = 0; z < c / 2; ++z) { fo_ranked tz = fu[z]; fu[z] = fu[c - 1 - z]; fu[c - 1 - z] = tz; }\n                    qsort(ve",
      ["test_build_leaf_layer_is_exact_fusion_topm"]),
+    # construction's inductive step (Sec 6.1) and patience (Sec 6.2.2)
+    ("rng comparison reversed", "if (dck < cand[i].dist) { ok = 0; break; }",
+     "if (dck > cand[i].dist) { ok = 0; break; }", ["test_rng_prune_hand_1d", "test_rng_prune_hand_2d"]),
+    ("rng prunes ties", "if (dck < cand[i].dist) { ok = 0; break; }",
+     "if (dck <= cand[i].dist) { ok = 0; break; }", ["test_rng_prune_tie_keeps_candidate"]),
+    ("rng tops up with the farthest", "for (int i = 0; i < nc && nk < m; ++i) {\n        if (!kept[i])",
+     "for (int i = nc - 1; i >= 0 && nk < m; --i) {\n        if (!kept[i])", ["test_rng_prune_hand_1d"]),
+    ("patience stops late", "if (left <= 0) break;", "if (left < 0) break;",
+     [("test_sibling_search_patience_chain", dict(patience=4))]),
+    ("patience stops early", "int left = patience;\n    int64_t nexp", "int left = patience - 1;\n    int64_t nexp",
+     ["test_sibling_search_all_seeded_is_exact_topm"]),
+    ("improved tested over the whole pool", "int top = nnp < m ? nnp : m;", "int top = nnp;",
+     [("test_sibling_search_patience_chain", dict(patience=4))]),
+    ("patience never reset", "if (improved) left = patience;", "if (improved) left = left + 0;",
+     ["test_sibling_search_patience_resets_on_improvement"]),
+    ("sibling is the own child", "if (u <= mid) { ts = mid + 1; te = e; } else { ts = s; te = mid; }",
+     "if (u <= mid) { ts = s; te = mid; } else { ts = mid + 1; te = e; }", ["test_build_all_seeded_equals_restatement"]),
+    ("child m-ANN dropped", "int32_t v = PG[u * m + t];\n                        if (v == FO_NONE) continue;",
+     "int32_t v = PG[u * m + t];\n                        if (v == FO_NONE || 1) continue;",
+     ["test_build_all_seeded_equals_restatement"]),
+    ("fusion re-rank on the child length", "fus[t].key = fo_fusion(cand[t].dist, u, cand[t].id, len, beta, gamma);",
+     "fus[t].key = fo_fusion(cand[t].dist, u, cand[t].id, len / 2 + 1, beta, gamma);",
+     ["test_build_all_seeded_equals_restatement"]),
+    ("parent graph keeps the unpruned list", "fo_rng_prune(X_rank, d, cand, nc, m, PGn + u * m);",
+     "for (int t = 0; t < m; ++t) PGn[u * m + t] = t < nc ? cand[t].id : FO_NONE;",
+     ["test_build_all_seeded_equals_restatement"]),
 ]
 
 

@@ -8,6 +8,7 @@ FROGSearch (Alg 2), ENIdentification (Alg 4), KANNSearch (Alg 1), RFANNS
 (Def. 2), fusion distance (Eq. fusion-distance), boundary effect (Eq.
 naive_attr_dist), construction (Sec 6).
 """
+import math
 import os
 
 import numpy as np
@@ -466,6 +467,228 @@ def test_boundary_effect_closed_form():
     assert np.abs(u - ix2.ENC[:, H - 1, 0]).mean() < dist.mean()
 
 
+
+# ------------------------------------------------------------------ construction: inductive step
+#
+# Sec 6.1 builds a parent layer from (i) the vertex's m-ANN in its own child
+# (the child's temporary PG row), (ii) its m-ANN in the sibling child, found
+# by the greedy search of Alg 1 over the sibling's temporary PG with the
+# patience stop of Sec 6.2.2; the 2m set is RNG-pruned into the parent's
+# temporary PG row and re-ranked by fusion distance into the ENC row.  The
+# expected rows below are worked out by hand from the RNG rule (keep a
+# candidate c, taken in ascending distance to u, unless an already kept k has
+# delta(c, k) < delta(u, c); stop at m kept; top up with the nearest pruned).
+
+def _sq(a, b):
+    return oracle.dist(np.asarray(a, np.float32), np.asarray(b, np.float32))
+
+
+def test_rng_prune_hand_1d():
+    # u = 0 on a line; candidates (id: position, squared distance to u):
+    # 1: 1 (1), 4: -1.5 (2.25), 2: 2 (4), 3: 3 (9), 5: -4 (16)
+    X = np.array([[0.0], [1.0], [2.0], [3.0], [-1.5], [-4.0]], np.float32)
+    ids = np.array([1, 4, 2, 3, 5], np.int32)
+    dd = np.array([_sq(X[0], X[i]) for i in ids], np.float32)
+    assert dd.tolist() == [1.0, 2.25, 4.0, 9.0, 16.0]
+    # 1 kept; 4: delta(4,1) = 6.25 >= 2.25 kept; 2: delta(2,1) = 1 < 4 pruned;
+    # 3: delta(3,1) = 4 < 9 pruned; 5: delta(5,4) = 6.25 < 16 pruned.
+    # kept [1, 4]; the pruned in ascending distance: 2, 3, 5
+    assert oracle.rng_prune(X, ids, dd, 1).tolist() == [1]
+    assert oracle.rng_prune(X, ids, dd, 2).tolist() == [1, 4]
+    assert oracle.rng_prune(X, ids, dd, 3).tolist() == [1, 4, 2]
+    assert oracle.rng_prune(X, ids, dd, 4).tolist() == [1, 4, 2, 3]
+    assert oracle.rng_prune(X, ids, dd, 5).tolist() == [1, 4, 2, 3, 5]
+    assert oracle.rng_prune(X, ids, dd, 7).tolist() == [1, 4, 2, 3, 5, -1, -1]
+
+
+def test_rng_prune_hand_2d():
+    # u = (0,0); a = (1,0) d 1, c = (1.2,0.3) d 1.53, b = (0,1.5) d 2.25,
+    # e = (-2,0) d 4, f = (2,2) d 8  (ids 1, 3, 2, 4, 5 in that order)
+    X = np.array([[0, 0], [1, 0], [0, 1.5], [1.2, 0.3], [-2, 0], [2, 2]], np.float32)
+    ids = np.array([1, 3, 2, 4, 5], np.int32)
+    dd = np.array([_sq(X[0], X[i]) for i in ids], np.float32)
+    assert (np.diff(dd) > 0).all()
+    # a kept; c: delta(c,a) = 0.13 < 1.53 pruned; b: delta(b,a) = 3.25 >= 2.25
+    # kept; e: delta(e,a) = 9, delta(e,b) = 6.25, both >= 4, kept;
+    # f: delta(f,a) = 5 < 8 pruned.  Kept [a, b, e]; pruned c, f.
+    assert oracle.rng_prune(X, ids, dd, 2).tolist() == [1, 2]
+    assert oracle.rng_prune(X, ids, dd, 3).tolist() == [1, 2, 4]
+    assert oracle.rng_prune(X, ids, dd, 4).tolist() == [1, 2, 4, 3]
+    assert oracle.rng_prune(X, ids, dd, 5).tolist() == [1, 2, 4, 3, 5]
+
+
+def test_rng_prune_tie_keeps_candidate():
+    # c2 = (0.5, 1) lies on the bisector of u = (0,0) and c1 = (1,0):
+    # delta(c2, c1) = delta(u, c2) = 1.25 exactly.  The rule prunes only on a
+    # strictly closer kept neighbour, so c2 stays; c3 = (-3, 0) is kept too
+    # (delta(c3,c1) = 16, delta(c3,c2) = 13.25, both >= 9).
+    X = np.array([[0, 0], [1, 0], [0.5, 1], [-3, 0]], np.float32)
+    ids = np.array([1, 2, 3], np.int32)
+    dd = np.array([_sq(X[0], X[i]) for i in ids], np.float32)
+    assert dd.tolist() == [1.0, 1.25, 9.0] and _sq(X[2], X[1]) == dd[1]
+    assert oracle.rng_prune(X, ids, dd, 3).tolist() == [1, 2, 3]
+
+
+def _seq_sqdist(A, b):
+    """Squared L2 of every row of A to b, summed dimension by dimension in
+    float64 (one rounding to float32 at the end)."""
+    A = np.asarray(A, np.float64)
+    b = np.asarray(b, np.float64)
+    s = np.zeros(A.shape[0])
+    for i in range(A.shape[1]):
+        t = A[:, i] - b[i]
+        s = s + t * t
+    return s.astype(np.float32)
+
+
+def test_sibling_search_all_seeded_is_exact_topm():
+    # every vertex of the segment seeded: the pool starts with the ef nearest
+    # of them, so its top m is the exact top m whatever the graph, and no
+    # expansion adds anything (each is non-improving: the search stops after
+    # `patience` expansions, or when the pool has none left)
+    rng = np.random.default_rng(11)
+    n, d, m = 200, 8, 8
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    ts, te = 50, 149
+    PG = rng.integers(ts, te + 1, size=(n, m)).astype(np.int32)
+    for trial in range(5):
+        xq = rng.standard_normal(d).astype(np.float32)
+        seeds = np.arange(ts, te + 1, dtype=np.int32)
+        rng.shuffle(seeds)
+        res, resd, nexp = oracle.sibling_search(X, PG, xq, ts, te, seeds, ef=32, patience=5)
+        cand = np.arange(ts, te + 1)
+        D = _seq_sqdist(X[cand], xq)
+        order = np.lexsort((cand, D))[:m]
+        assert res.tolist() == cand[order].tolist()
+        assert resd.tolist() == D[order].tolist()
+        assert nexp == 5
+    res, _, nexp = oracle.sibling_search(X, PG, xq, ts, te, seeds[:3], ef=32, patience=50)
+    assert nexp <= 100
+
+
+def _chain_pg(n, rows):
+    PG = np.full((n, 1), -1, np.int32)
+    for u, v in rows.items():
+        PG[u, 0] = v
+    return PG
+
+
+@pytest.mark.parametrize("patience", [2, 4, 7])
+def test_sibling_search_patience_chain(patience):
+    # Points on a line, query at 3.2, m = 1, one seed (vertex 0 at 0).  Chain
+    # i -> i+1 with vertex i at position i (0..K), then K -> h, a vertex at
+    # 3.25 (nearer to the query than 3).  Best-first follows the chain (each
+    # expansion adds exactly one new vertex, the only unexpanded one):
+    # expanding 0, 1, 2 adds 1, 2, 3, each a new nearest (improving);
+    # expanding 3, 4, ... adds 4, 5, ..., never a new nearest.  After
+    # `patience` such expansions in a row (of 3 .. patience+2) the search
+    # stops.  So with K = patience + 2 the last of them adds h (improving)
+    # and h is found; with K = patience + 3 the search stops after expanding
+    # patience + 2 and never reaches h.
+    p = patience
+    for K, found in ((p + 2, True), (p + 3, False)):
+        h = K + 1
+        X = np.array([[float(i)] for i in range(K + 1)] + [[3.25]], np.float32)
+        PG = _chain_pg(K + 2, {**{i: i + 1 for i in range(K)}, K: h})
+        xq = np.array([3.2], np.float32)
+        res, _, nexp = oracle.sibling_search(X, PG, xq, 0, K + 1, np.array([0], np.int32), ef=64,
+                                            patience=p)
+        if found:
+            # 0..K expanded, then h (which adds nothing)
+            assert res.tolist() == [h] and nexp == K + 2
+        else:
+            # 0 .. p+2 expanded
+            assert res.tolist() == [3] and nexp == p + 3
+
+
+def test_sibling_search_patience_resets_on_improvement():
+    # Query at 0, m = 1, patience 3, seed vertex 0.  Chain v0 -> v1 -> ... ->
+    # v7 with positions 5, 4, 4.5, 4.6, 3, 3.5, 3.6, 1 (squared 25, 16,
+    # 20.25, 21.16, 9, 12.25, 12.96, 1).  Expansion (adds; new nearest?;
+    # patience left): v0 (v1; yes; 3), v1 (v2; no; 2), v2 (v3; no; 1),
+    # v3 (v4; yes; 3), v4 (v5; no; 2), v5 (v6; no; 1), v6 (v7; yes; 3),
+    # v7 (nothing; no; 2), then no unexpanded vertex is left.  The nearest
+    # is v7 after 8 expansions; without the reset the search would stop
+    # after expanding v4 with v4 as the nearest.
+    pos = [5, 4, 4.5, 4.6, 3, 3.5, 3.6, 1]
+    X = np.array([[x] for x in pos], np.float32)
+    PG = _chain_pg(8, {i: i + 1 for i in range(7)})
+    res, resd, nexp = oracle.sibling_search(X, PG, np.array([0.0], np.float32), 0, 7,
+                                            np.array([0], np.int32), ef=64, patience=3)
+    assert res.tolist() == [7] and resd.tolist() == [1.0] and nexp == 8
+
+
+def _restated_build_all_seeded(X, attr, m, H, beta, gamma):
+    """The construction of Sec 6 for the case where every sibling vertex is a
+    seed of the sibling search, so that search returns the sibling's exact
+    m-ANN: leaf rows by brute force, then per layer the child's temporary-PG
+    row plus the sibling's exact top m, RNG prune, fusion re-rank."""
+    n, d = X.shape
+    order = np.argsort(attr, kind="stable")
+    Xr = X[order]
+    # segments per depth by explicit halving: left [L, mid], right [mid+1, R]
+    segs = [[(0, n - 1)]]
+    for _ in range(H - 1):
+        nxt = []
+        for (a, b) in segs[-1]:
+            mid = a + (b - a) // 2
+            nxt += [(a, mid), (mid + 1, b)]
+        segs.append(nxt)
+    seg_of = []
+    for lay in segs:
+        t = np.empty(n, np.int64)
+        for i, (a, b) in enumerate(lay):
+            t[a:b + 1] = i
+        seg_of.append(t)
+    D = np.stack([_seq_sqdist(Xr, Xr[u]) for u in range(n)])   # D[u, v]
+
+    def fusion_key(u, v, seglen):
+        da = abs(u - v) / (seglen - 1)
+        return math.sqrt(float(D[u, v])) * (1.0 - beta * (1.0 - da ** gamma))
+
+    ENC = np.full((n, H, m), -1, np.int32)
+    PG = [[] for _ in range(n)]
+    h = H - 1
+    for u in range(n):
+        a, b = segs[h][seg_of[h][u]]
+        cand = [v for v in range(a, b + 1) if v != u]
+        ENC[u, h, :min(m, len(cand))] = sorted(cand, key=lambda v: (fusion_key(u, v, b - a + 1), v))[:m]
+        PG[u] = sorted(cand, key=lambda v: (D[u, v], v))[:m]
+    for h in range(H - 2, -1, -1):
+        newPG = [None] * n
+        for u in range(n):
+            a, b = segs[h][seg_of[h][u]]
+            mid = a + (b - a) // 2
+            sib = range(mid + 1, b + 1) if u <= mid else range(a, mid + 1)
+            cand = list(PG[u]) + sorted(sib, key=lambda v: (D[u, v], v))[:m]
+            cand.sort(key=lambda v: (D[u, v], v))
+            kept = []
+            for c in cand:
+                if len(kept) == m:
+                    break
+                if all(not (D[c, k] < D[u, c]) for k in kept):
+                    kept.append(c)
+            kept += [c for c in cand if c not in kept][:m - len(kept)]
+            newPG[u] = kept
+            fus = sorted(cand, key=lambda v: (fusion_key(u, v, b - a + 1), v))[:m]
+            ENC[u, h, :len(fus)] = fus
+        PG = newPG
+    return ENC
+
+
+def test_build_all_seeded_equals_restatement():
+    # n = 100: the root's children hold 50 ranks, so 64 seeds cover every
+    # sibling at every layer
+    rng = np.random.default_rng(12)
+    n, d, m = 100, 8, 4
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    attr = rng.permutation(n).astype(np.float64)
+    for beta, gamma in ((0.2, 0.5), (0.0, 0.5), (0.5, 2.0)):
+        ix = oracle.build(X, attr, m=m, ef_c=16, n_inv=3, patience=30, sib_seeds=64, beta=beta, gamma=gamma)
+        assert ix.H == 5
+        ref = _restated_build_all_seeded(X, attr, m, ix.H, beta, gamma)
+        assert (ix.ENC == ref).all(), np.argwhere(ix.ENC != ref)[:5]
+
 # ------------------------------------------------------------------ search
 
 def _bruteforce_rank_space(ix, q, l, r, k):
@@ -648,7 +871,7 @@ def test_search_shared_small_range_is_exact(tiny_index):
     assert (ids == gi).all() and (ds == gd).all()
 
 
-# ------------------------------------------------------------------ ablations (Sec 8.4)
+# ------------------------------------------------------------------ ablations (Sec 8.2.3)
 
 def _textbook_frog(ix, q, l, r, layers, B, entries, L, eager):
     """Alg. 2 written independently for the ablations: EN(u) = the in-range
