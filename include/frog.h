@@ -44,7 +44,8 @@ enum {
     FROG_EBADINDEX = -4,     /* index file: bad magic, version, size or checksum */
     FROG_ENOTUPLOADED = -5,  /* device entry point called before frog_index_upload */
     FROG_EIO = -6,           /* file could not be opened, read or written */
-    FROG_EUNSUPPORTED = -7   /* shape outside what the kernels are built for */
+    FROG_EUNSUPPORTED = -7,  /* shape outside what the kernels are built for */
+    FROG_ENOTPREPARED = -8   /* entry_mode 1 with a seed frog_index_prepare_sample has not built */
 };
 
 typedef struct frog_index frog_index_t; /* opaque; owns host and device copies */
@@ -84,9 +85,9 @@ typedef struct {
                            rank) shared by all queries, is below count/cnt of
                            its range: a sample of expected size count that
                            overlapping queries share, evaluated on matrix
-                           cores in tiles of 16 queries.  Mode 1 builds and
-                           uploads the seed's rank lists on its first call
-                           (synchronously; about n int32 of device memory) */
+                           cores in tiles of 16 queries.  Mode 1 reads the
+                           seed's level lists, which frog_index_prepare_sample
+                           must have built (else FROG_ENOTPREPARED) */
     int hotspot_mode;   /* ablation of HotspotLocalization (Sec 8.2.3): 0 (default)
                            layers L_start..L_end of Alg. 3; 1 layers
                            L_start..H-1 (no end condition); 2 all layers */
@@ -167,8 +168,23 @@ int frog_index_load(const char* path, frog_index_t** out);
 /* Copy the index to HIP device `device` (the HBM layout: X rows in rank order,
  * padded to a multiple of 32 floats; ENC n x H x m; attr_sorted; perm).  The
  * device copy is read-only afterwards, so concurrent searches on different
- * streams are safe.  Calling it again replaces the previous device copy. */
+ * streams are safe.  Calling it again replaces the previous device copy and
+ * drops every prepared sample (no search may be running then). */
 int frog_index_upload(frog_index_t* idx, int device);
+
+/* The shared entry sample of `seed` for entry_mode 1 (the second reading of
+ * Alg. 2's uniform sampling: rank i is drawn when its priority
+ * hi32(splitmix64(splitmix64(seed) ^ i)) is below the query's threshold).
+ * Builds, on the index's device, for levels j = 1..~log2(n) the ascending
+ * ranks whose priority is below 2^(32-j), a copy of their stored rows in the
+ * same order, and every rank's priority and squared row norm: about
+ * n * (4 dp + 20) bytes of device memory for fp32 rows (n * (2 dp + 20) for
+ * 16-bit rows), 0.53 GB at n = 1M, d = 128.  Synchronous (it waits for the
+ * device); idempotent (a prepared seed returns at once); safe to call while
+ * other threads search with other seeds.  The lists are immutable once built
+ * and freed with the device copy (frog_index_upload again, or
+ * frog_index_free).  Errors: FROG_ENOTUPLOADED, FROG_ENOMEM, FROG_EHIP. */
+int frog_index_prepare_sample(frog_index_t* idx, uint64_t seed);
 
 /* Storage type of the device copy's rows. */
 enum {
@@ -202,27 +218,35 @@ int frog_rank_bounds(const frog_index_t* idx, const double* d_lo, const double* 
 
 /* FROGSearch (Alg. 2 with HotspotLocalization, Alg. 3, and ENIdentification,
  * Alg. 4) for nq queries with default parameters.  d_queries: nq x d floats
- * row-major; d_lo/d_hi: nq doubles; k >= 1, L in [k, 256] (pool size ef_s);
- * outputs d_ids (int32) and d_dists (float), nq x k each. */
+ * row-major; d_lo/d_hi: nq doubles; k >= 1, L in [k, 256] (pool size ef_s;
+ * at most 248 with entry_mode 1, else FROG_EUNSUPPORTED); outputs d_ids
+ * (int32) and d_dists (float), nq x k each. */
 int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
                 const double* d_lo, const double* d_hi, int k, int L,
                 int32_t* d_ids, float* d_dists, void* stream);
 
 /* As frog_search with explicit parameters (p = NULL: defaults) and optional
- * per-query statistics d_stats (NULL or nq x FROG_STAT_N int32). */
+ * per-query statistics d_stats (NULL or nq x FROG_STAT_N int32).  With
+ * p->entry_mode == 1 the seed's sample must be prepared
+ * (frog_index_prepare_sample), else FROG_ENOTPREPARED; nothing is built or
+ * freed here, so searches on several streams or threads may share an index
+ * whatever their seeds.  The per-call workspace comes from hipMallocAsync on
+ * `stream` and is released on it (stream-ordered). */
 int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
                    const double* d_lo, const double* d_hi, int k, int L,
                    const frog_search_params_t* p, int32_t* d_ids, float* d_dists,
                    int32_t* d_stats, void* stream);
 
 /* Exhaustive filtered k-NN (Def. 2, RFANNS): the exact k nearest objects whose
- * attribute lies in [lo, hi].  The dot products q.x run on fp32 matrix cores;
- * a per-query certified margin selects candidates that are re-ranked with the
- * exact squared distance.  1 <= k <= 256.  d_certified (NULL or nq int32) is
- * set to 1 where the margin proves the result exact, else 0 (the row then
- * holds the best candidates found).  The ranges are read back to the host to
- * group queries into tiles, so this call synchronises `stream`; it is a
- * ground-truth tool, not the search path. */
+ * attribute lies in [lo, hi], by (distance, rank), padded with (-1, +inf).
+ * The dot products q.x run on fp32 matrix cores; a per-query margin test
+ * proves that the candidates re-ranked with the exact squared distance hold
+ * the result; a query the test cannot certify is recomputed over every rank
+ * of its range with the exact distance.  Every row is exact.  1 <= k <= 256.
+ * d_certified (NULL or nq int32) tells how each row was obtained: 1 = by the
+ * margin test (or an empty range), 2 = by the exhaustive exact pass.  The
+ * ranges and the certification are read back to the host, so this call
+ * synchronises `stream`; it is a ground-truth tool, not the search path. */
 int frog_bruteforce_filtered(const frog_index_t* idx, const float* d_queries, int64_t nq,
                              const double* d_lo, const double* d_hi, int k,
                              int32_t* d_ids, float* d_dists, int32_t* d_certified,

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libfrog.so")
 
 FROG_OK = 0
 ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "EBADINDEX", -5: "ENOTUPLOADED",
-          -6: "EIO", -7: "EUNSUPPORTED"}
+          -6: "EIO", -7: "EUNSUPPORTED", -8: "ENOTPREPARED"}
 (STAT_EXPANSIONS, STAT_EN, STAT_DIST, STAT_SCANNED, STAT_ENTRY, STAT_LSTART, STAT_LEND, STAT_LOADED,
  STAT_SCANROWS) = range(9)
 STAT_N = 9
@@ -30,7 +30,7 @@ SYMBOLS = (
     "frog_index_from_arrays", "frog_index_export", "frog_index_info", "frog_index_save",
     "frog_index_load", "frog_index_upload", "frog_index_upload_ex", "frog_index_free",
     "frog_build_index_gpu", "frog_index_build_stats", "frog_rank_bounds", "frog_search",
-    "frog_search_ex", "frog_bruteforce_filtered", "frog_last_error",
+    "frog_search_ex", "frog_index_prepare_sample", "frog_bruteforce_filtered", "frog_last_error",
 )
 
 
@@ -101,6 +101,8 @@ def lib() -> C.CDLL:
     L.frog_search.argtypes = [P, P, i64, P, P, i32, i32, P, P, P]
     L.frog_search_ex.restype = i32
     L.frog_search_ex.argtypes = [P, P, i64, P, P, i32, i32, C.POINTER(SearchParams), P, P, P, P]
+    L.frog_index_prepare_sample.restype = i32
+    L.frog_index_prepare_sample.argtypes = [P, C.c_uint64]
     L.frog_bruteforce_filtered.restype = i32
     L.frog_bruteforce_filtered.argtypes = [P, P, i64, P, P, i32, P, P, P, P]
     _lib = L
@@ -219,6 +221,15 @@ class Index:
         else:
             _check(lib().frog_index_upload_ex(self._h, device, STORAGE[storage]))
         self.storage = storage
+        self._prepared = set()
+        return self
+
+    def prepare_sample(self, seed: int = 0) -> "Index":
+        """Build the shared entry sample of `seed` on the device (entry_mode 1;
+        synchronous, idempotent)."""
+        seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+        _check(lib().frog_index_prepare_sample(self._h, C.c_uint64(seed)))
+        self._prepared = getattr(self, "_prepared", set()) | {seed}
         return self
 
     def free(self):
@@ -278,6 +289,9 @@ def search(index: Index, Q, lo, hi, k: int, L: int, *, stats: bool = False, stre
     st = torch.empty((nq, STAT_N), dtype=torch.int32, device=Q.device) if stats else None
     events = params.pop("events", None)
     p = search_params(**params)
+    if p.entry_mode == 1 and p.seed not in getattr(index, "_prepared", ()):
+        # the sample's level lists are built once per seed, before the search
+        index.prepare_sample(p.seed)
     if events is not None:
         # three torch.cuda.Event(enable_timing=True): before the entry-point
         # kernel, between the kernels, after the traversal kernel

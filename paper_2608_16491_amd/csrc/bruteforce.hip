@@ -21,6 +21,11 @@
 //      or above some kept list's threshold; if the smallest such threshold
 //      minus the approximation bound exceeds the k-th exact distance, the
 //      result is certified exact (reported per query).
+//   4. Queries the margin test leaves uncertified (near-tied distances that
+//      the fp32 approximation cannot separate, e.g. vectors with large norms
+//      close to each other) are recomputed exhaustively: every rank of the
+//      interval with the exact canonical distance (launch_exact_ranges), so
+//      every returned row is the exact filtered k-NN.
 //
 // The approximation bound: with unit roundoff u = 2^-24, fp32 |q|^2 and |x|^2
 // (d terms each), the fp32 dot product (d products) and the final two
@@ -408,7 +413,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         }
         tiles[t].ie = (int32_t)items.size();
     }
-    const float maxnorm = index_maxnorm(const_cast<frog_index*>(ix));
+    const float maxnorm = ix->maxnorm;
     int kkeep = 2 * k < 64 ? 64 : (2 * k + 63) / 64 * 64;
     if (kkeep > 256) kkeep = 256;
     auto align = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -417,7 +422,8 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
     const size_t ebytes = align((size_t)nq);
     const size_t lbytes = align(items.size() * kQT * (size_t)kkeep * 4);
     const size_t sbytes = align(items.size() * kQT * 4);
-    const size_t ws_bytes = tbytes + ibytes + ebytes + 2 * lbytes + 2 * sbytes + 256;
+    const size_t cbytes = align((size_t)nq * 4);
+    const size_t ws_bytes = tbytes + ibytes + ebytes + 2 * lbytes + 2 * sbytes + cbytes + 256;
     void* ws = nullptr;
     e = hipMallocAsync(&ws, ws_bytes, stream);
     if (e != hipSuccess) return fail(FROG_ENOMEM, "bruteforce workspace: %s", hipGetErrorString(e));
@@ -426,6 +432,8 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
     Item* dI = reinterpret_cast<Item*>(base + tbytes);
     uint8_t* dE = reinterpret_cast<uint8_t*>(base + tbytes + ibytes);
     char* lists = base + tbytes + ibytes + ebytes;
+    // certification flags: the caller's array, else one in the workspace
+    int32_t* dcert = cert ? cert : reinterpret_cast<int32_t*>(lists + 2 * lbytes + 2 * sbytes);
     if (!tiles.empty()) e = hipMemcpyAsync(dT, tiles.data(), tiles.size() * sizeof(Tile), hipMemcpyHostToDevice, stream);
     if (e == hipSuccess && !items.empty())
         e = hipMemcpyAsync(dI, items.data(), items.size() * sizeof(Item), hipMemcpyHostToDevice, stream);
@@ -434,7 +442,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         (void)hipFreeAsync(ws, stream);
         return fail(FROG_EHIP, "bruteforce upload: %s", hipGetErrorString(e));
     }
-    hipLaunchKernelGGL(bf_pad_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, nq, k, dE, ids, dists, cert);
+    hipLaunchKernelGGL(bf_pad_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, nq, k, dE, ids, dists, dcert);
     if (!tiles.empty()) {
         BFParams P{};
         P.X = ix->dX;
@@ -456,7 +464,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         P.pfill = reinterpret_cast<int32_t*>(lists + 2 * lbytes + sbytes);
         P.ids = ids;
         P.dists = dists;
-        P.cert = cert;
+        P.cert = dcert;
         const int smem_scan = (int)(kWaves * scan_lds_per_wave(kkeep));
         void (*scan)(BFParams) = bf_scan_kernel<0>;
         switch (ix->dp) {
@@ -475,11 +483,27 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
                            smem_merge, stream, P);
     }
     e = hipGetLastError();
+    // which queries the margin test certified
+    std::vector<int32_t> hc((size_t)nq, 1);
+    if (e == hipSuccess && !tiles.empty())
+        e = hipMemcpyAsync(hc.data(), dcert, (size_t)nq * 4, hipMemcpyDeviceToHost, stream);
     (void)hipFreeAsync(ws, stream);
     // keep the host-side arrays alive until the copies have run
-    (void)hipStreamSynchronize(stream);
-    if (e != hipSuccess) return fail(FROG_EHIP, "bruteforce launch: %s", hipGetErrorString(e));
-    return FROG_OK;
+    const hipError_t es = hipStreamSynchronize(stream);
+    if (e != hipSuccess || es != hipSuccess)
+        return fail(FROG_EHIP, "bruteforce launch: %s", hipGetErrorString(e != hipSuccess ? e : es));
+    // the rest: every rank of the interval, exactly
+    std::vector<int32_t> fq, flr;
+    for (int64_t q = 0; q < nq; ++q)
+        if (!empty[(size_t)q] && hc[(size_t)q] == 0) {
+            fq.push_back((int32_t)q);
+            flr.push_back(L[(size_t)q]);
+            flr.push_back(R[(size_t)q]);
+        }
+    if (fq.empty()) return FROG_OK;
+    const DevIndex dix{ix->dX, ix->dXh, ix->dENC, ix->dattr, ix->dperm, ix->n, ix->d, ix->dp, ix->H, ix->m,
+                       ix->storage};
+    return launch_exact_ranges(dix, Q, fq.data(), flr.data(), (int64_t)fq.size(), k, ids, dists, cert, stream);
 }
 
 }  // namespace frog

@@ -732,6 +732,7 @@ int build_device(const float* X, const double* attr, int64_t n, int d, const fro
     out->dENC = dENC;
     out->dattr = dattr;
     out->dperm = dperm;
+    out->maxnorm = stored_maxnorm(out);
     (void)hipSetDevice(prev);
     return FROG_OK;
 }

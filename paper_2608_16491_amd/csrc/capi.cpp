@@ -53,17 +53,16 @@ void release_device(frog_index* ix) {
         hipFree(ix->dENC);
         hipFree(ix->dattr);
         hipFree(ix->dperm);
-        if (ix->dshared) hipFree(ix->dshared);
-        if (ix->dshared_x) hipFree(ix->dshared_x);
-        if (ix->dshared_p) hipFree(ix->dshared_p);
-        if (ix->dshared_nrm) hipFree(ix->dshared_nrm);
+        for (auto& kv : ix->samples) {
+            frog_index::Sample& s = *kv.second;
+            if (s.ranks) hipFree(s.ranks);
+            if (s.xrows) hipFree(s.xrows);
+            if (s.prio) hipFree(s.prio);
+            if (s.norm) hipFree(s.norm);
+        }
         hipSetDevice(prev);
     }
-    ix->dshared = nullptr;
-    ix->dshared_x = nullptr;
-    ix->dshared_p = nullptr;
-    ix->dshared_nrm = nullptr;
-    ix->shared_valid = false;
+    ix->samples.clear();
     ix->dX = nullptr;
     ix->dXh = nullptr;
     ix->maxnorm = -1.f;
@@ -403,6 +402,31 @@ float stored_value(const frog_index* ix, int64_t i, int c) {
     return v;
 }
 
+// the largest squared norm of the stored rows (in double, then widened by
+// a relative 1e-6 so that it bounds the fp32 value), on all host threads
+float stored_maxnorm(const frog_index* ix) {
+    const int T = host_threads(0);
+    std::vector<double> part((size_t)T, 0.0);
+    std::vector<std::thread> th;
+    for (int t = 0; t < T; ++t)
+        th.emplace_back([&, t]() {
+            double mx = 0.0;
+            for (int64_t i = ix->n * t / T; i < ix->n * (t + 1) / T; ++i) {
+                double s = 0.0;
+                for (int c = 0; c < ix->d; ++c) {
+                    const double v = stored_value(ix, i, c);
+                    s += v * v;
+                }
+                mx = std::max(mx, s);
+            }
+            part[(size_t)t] = mx;
+        });
+    for (auto& x : th) x.join();
+    double mx = 0.0;
+    for (double v : part) mx = std::max(mx, v);
+    return (float)(mx * (1.0 + 1e-6));
+}
+
 }  // namespace frog
 
 extern "C" {
@@ -462,6 +486,7 @@ int frog_index_upload_ex(frog_index_t* ix, int device, int storage) {
     if (e == hipSuccess) e = hipMemcpy(ix->dattr, ix->attr.data(), (size_t)ix->n * sizeof(double), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(ix->dperm, ix->perm.data(), (size_t)ix->n * sizeof(int32_t), hipMemcpyHostToDevice);
     if (e != hipSuccess) return bail(fail(FROG_EHIP, "upload: %s", hipGetErrorString(e)));
+    ix->maxnorm = frog::stored_maxnorm(ix);
     hipSetDevice(prev);
     return FROG_OK;
 }
@@ -543,10 +568,12 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
     a.entry_mode = q.entry_mode;
     a.hotspot_mode = q.hotspot_mode;
     a.eager = q.eager_check;
+    if (q.entry_mode == 1 && L > 248)
+        return fail(FROG_EUNSUPPORTED,
+                    "entry_mode 1 keeps at most 256 candidates per query and work item and needs L + 8 of them "
+                    "(L=%d > 248); entry_mode 0 takes L up to 256", L);
     if (q.entry_mode == 1) {
-        frog_index* mix = const_cast<frog_index*>(ix);
-        a.maxnorm = frog::index_maxnorm(mix);
-        rc = frog::shared_levels(mix, q.seed, &a.lv);
+        rc = frog::find_sample(ix, q.seed, &a.lv, &a.maxnorm);
         if (rc) return rc;
     }
     return frog::launch_search(view(ix), a, stream);
@@ -583,117 +610,131 @@ static uint64_t mix64(uint64_t x) {
     return z ^ (z >> 31);
 }
 
-float index_maxnorm(frog_index* ix) {
-    std::lock_guard<std::mutex> g(ix->shared_mu);
-    if (ix->maxnorm < 0.f) {
-        double mx = 0.0;
-        for (int64_t i = 0; i < ix->n; ++i) {
-            double s = 0.0;
-            for (int c = 0; c < ix->d; ++c) {
-                const double v = stored_value(ix, i, c);
-                s += v * v;
-            }
-            mx = std::max(mx, s);
-        }
-        ix->maxnorm = (float)(mx * (1.0 + 1e-6));
-    }
-    return ix->maxnorm;
-}
-
 // Level j (1 <= j <= nlev) holds the ranks whose priority p has at least j
 // leading zero bits (p < 2^(32-j)); nlev covers the smallest threshold any
-// query can ask for (one entry point out of n).
-int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out) {
-    std::lock_guard<std::mutex> g(ix->shared_mu);
+// query can ask for (one entry point out of n).  Builds one seed's lists, row
+// copies, priorities and norms on the index's device (synchronously).
+int build_sample(const frog_index* ix, uint64_t seed, frog_index::Sample* S) {
+    const int64_t n = ix->n;
     const uint64_t key = mix64(seed);
-    if (!ix->shared_valid || ix->shared_seed != seed) {
-        const int64_t n = ix->n;
-        const uint64_t tmin = ((uint64_t)1 << 32) / (uint64_t)n + 1;   // >= ceil(2^32 / n)
-        int cl = 0;
-        while (((uint64_t)1 << cl) < tmin) ++cl;
-        const int nlev = std::max(1, std::min(31, 32 - cl + 1));
-        std::vector<uint8_t> depth((size_t)n);
-        std::vector<int64_t> cnt((size_t)nlev + 2, 0);
-        std::vector<uint32_t> prio_rank((size_t)n);
-        for (int64_t i = 0; i < n; ++i) {
-            const uint32_t p = (uint32_t)(mix64(key ^ (uint64_t)i) >> 32);
-            prio_rank[(size_t)i] = p;
-            const int z = p == 0 ? 32 : __builtin_clz(p);
-            depth[(size_t)i] = (uint8_t)std::min(z, nlev);
-            for (int j = 1; j <= depth[(size_t)i]; ++j) ++cnt[(size_t)j];
-        }
-        int64_t off[34] = {};
-        off[1] = 0;
-        for (int j = 1; j <= nlev; ++j) off[j + 1] = off[j] + cnt[(size_t)j];
-        std::vector<int32_t> ranks((size_t)std::max<int64_t>(off[nlev + 1], 1));
-        std::vector<int64_t> fill(off, off + nlev + 2);
-        for (int64_t i = 0; i < n; ++i)
-            for (int j = 1; j <= depth[(size_t)i]; ++j) ranks[(size_t)fill[(size_t)j]++] = (int32_t)i;
-        // priorities and squared norms, by rank and then in list order
-        const int64_t total = off[nlev + 1];
-        std::vector<uint32_t> prio((size_t)(n + total));
-        std::vector<float> nrm((size_t)(n + total));
-        for (int64_t i = 0; i < n; ++i) {
-            float sq = 0.f;
-            for (int c = 0; c < ix->d; ++c) {
-                const float v = stored_value(ix, i, c);
-                sq += v * v;
-            }
-            prio[(size_t)i] = prio_rank[(size_t)i];
-            nrm[(size_t)i] = sq;
-        }
-        for (int64_t p = 0; p < total; ++p) {
-            prio[(size_t)(n + p)] = prio_rank[(size_t)ranks[(size_t)p]];
-            nrm[(size_t)(n + p)] = nrm[(size_t)ranks[(size_t)p]];
-        }
-        int prev = 0;
-        if (hipGetDevice(&prev) != hipSuccess) return fail(FROG_EHIP, "hipGetDevice failed");
-        if (hipSetDevice(ix->device) != hipSuccess) return fail(FROG_EHIP, "hipSetDevice failed");
-        if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
-        if (ix->dshared_x) { (void)hipFree(ix->dshared_x); ix->dshared_x = nullptr; }
-        if (ix->dshared_p) { (void)hipFree(ix->dshared_p); ix->dshared_p = nullptr; }
-        if (ix->dshared_nrm) { (void)hipFree(ix->dshared_nrm); ix->dshared_nrm = nullptr; }
-        ix->shared_valid = false;
-        hipError_t e = hipMalloc(&ix->dshared, ranks.size() * sizeof(int32_t));
-        if (e == hipSuccess)
-            e = hipMemcpy(ix->dshared, ranks.data(), ranks.size() * sizeof(int32_t), hipMemcpyHostToDevice);
-        if (e == hipSuccess) e = hipMalloc(&ix->dshared_p, prio.size() * sizeof(uint32_t));
-        if (e == hipSuccess) e = hipMemcpy(ix->dshared_p, prio.data(), prio.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
-        if (e == hipSuccess) e = hipMalloc(&ix->dshared_nrm, nrm.size() * sizeof(float));
-        if (e == hipSuccess) e = hipMemcpy(ix->dshared_nrm, nrm.data(), nrm.size() * sizeof(float), hipMemcpyHostToDevice);
-        // the listed stored rows, so that a scan over a list reads contiguous rows
-        const int row_bytes = ix->dp * (ix->storage == FROG_STORAGE_F32 ? 4 : 2);
-        if (e == hipSuccess) e = hipMalloc(&ix->dshared_x, (size_t)std::max<int64_t>(total, 1) * row_bytes);
-        int rc = FROG_OK;
-        if (e == hipSuccess && total > 0) {
-            const void* rows = ix->storage == FROG_STORAGE_F32 ? (const void*)ix->dX : (const void*)ix->dXh;
-            rc = launch_gather_rows(rows, row_bytes, ix->dshared, total, ix->dshared_x, nullptr);
-            if (rc == FROG_OK) e = hipDeviceSynchronize();
-        }
-        (void)hipSetDevice(prev);
-        if (e != hipSuccess || rc != FROG_OK) {
-            if (ix->dshared) { (void)hipFree(ix->dshared); ix->dshared = nullptr; }
-            if (ix->dshared_x) { (void)hipFree(ix->dshared_x); ix->dshared_x = nullptr; }
-            if (ix->dshared_p) { (void)hipFree(ix->dshared_p); ix->dshared_p = nullptr; }
-            if (ix->dshared_nrm) { (void)hipFree(ix->dshared_nrm); ix->dshared_nrm = nullptr; }
-            if (rc != FROG_OK) return rc;
-            return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "shared sample levels: %s",
-                        hipGetErrorString(e));
-        }
-        std::copy(off, off + 34, ix->shared_off);
-        ix->shared_nlev = nlev;
-        ix->shared_seed = seed;
-        ix->shared_valid = true;
+    const uint64_t tmin = ((uint64_t)1 << 32) / (uint64_t)n + 1;   // >= ceil(2^32 / n)
+    int cl = 0;
+    while (((uint64_t)1 << cl) < tmin) ++cl;
+    const int nlev = std::max(1, std::min(31, 32 - cl + 1));
+    std::vector<uint8_t> depth((size_t)n);
+    std::vector<int64_t> cnt((size_t)nlev + 2, 0);
+    std::vector<uint32_t> prio_rank((size_t)n);
+    for (int64_t i = 0; i < n; ++i) {
+        const uint32_t p = (uint32_t)(mix64(key ^ (uint64_t)i) >> 32);
+        prio_rank[(size_t)i] = p;
+        const int z = p == 0 ? 32 : __builtin_clz(p);
+        depth[(size_t)i] = (uint8_t)std::min(z, nlev);
+        for (int j = 1; j <= depth[(size_t)i]; ++j) ++cnt[(size_t)j];
     }
-    out->ranks = ix->dshared;
-    out->xrows = ix->storage == FROG_STORAGE_F32 ? static_cast<const float*>(ix->dshared_x) : nullptr;
-    out->xrowsh = ix->storage != FROG_STORAGE_F32 ? static_cast<const uint16_t*>(ix->dshared_x) : nullptr;
-    out->prio = ix->dshared_p;
-    out->norm = ix->dshared_nrm;
-    std::copy(ix->shared_off, ix->shared_off + 34, out->off);
-    out->nlev = ix->shared_nlev;
-    out->key = key;
+    int64_t off[34] = {};
+    for (int j = 1; j <= nlev; ++j) off[j + 1] = off[j] + cnt[(size_t)j];
+    std::vector<int32_t> ranks((size_t)std::max<int64_t>(off[nlev + 1], 1));
+    std::vector<int64_t> fill(off, off + nlev + 2);
+    for (int64_t i = 0; i < n; ++i)
+        for (int j = 1; j <= depth[(size_t)i]; ++j) ranks[(size_t)fill[(size_t)j]++] = (int32_t)i;
+    // priorities and squared norms, by rank and then in list order
+    const int64_t total = off[nlev + 1];
+    std::vector<uint32_t> prio((size_t)(n + total));
+    std::vector<float> nrm((size_t)(n + total));
+    for (int64_t i = 0; i < n; ++i) {
+        float sq = 0.f;
+        for (int c = 0; c < ix->d; ++c) {
+            const float v = stored_value(ix, i, c);
+            sq += v * v;
+        }
+        prio[(size_t)i] = prio_rank[(size_t)i];
+        nrm[(size_t)i] = sq;
+    }
+    for (int64_t p = 0; p < total; ++p) {
+        prio[(size_t)(n + p)] = prio_rank[(size_t)ranks[(size_t)p]];
+        nrm[(size_t)(n + p)] = nrm[(size_t)ranks[(size_t)p]];
+    }
+    auto drop = [&]() {
+        if (S->ranks) (void)hipFree(S->ranks);
+        if (S->xrows) (void)hipFree(S->xrows);
+        if (S->prio) (void)hipFree(S->prio);
+        if (S->norm) (void)hipFree(S->norm);
+        S->ranks = nullptr; S->xrows = nullptr; S->prio = nullptr; S->norm = nullptr;
+    };
+    hipError_t e = hipMalloc(&S->ranks, ranks.size() * sizeof(int32_t));
+    if (e == hipSuccess)
+        e = hipMemcpy(S->ranks, ranks.data(), ranks.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMalloc(&S->prio, prio.size() * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMemcpy(S->prio, prio.data(), prio.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMalloc(&S->norm, nrm.size() * sizeof(float));
+    if (e == hipSuccess) e = hipMemcpy(S->norm, nrm.data(), nrm.size() * sizeof(float), hipMemcpyHostToDevice);
+    // the listed stored rows, so that a scan over a list reads contiguous rows
+    const int row_bytes = ix->dp * (ix->storage == FROG_STORAGE_F32 ? 4 : 2);
+    if (e == hipSuccess) e = hipMalloc(&S->xrows, (size_t)std::max<int64_t>(total, 1) * row_bytes);
+    int rc = FROG_OK;
+    if (e == hipSuccess && total > 0) {
+        const void* rows = ix->storage == FROG_STORAGE_F32 ? (const void*)ix->dX : (const void*)ix->dXh;
+        rc = launch_gather_rows(rows, row_bytes, S->ranks, total, S->xrows, nullptr);
+        if (rc == FROG_OK) e = hipDeviceSynchronize();
+    }
+    if (e != hipSuccess || rc != FROG_OK) {
+        drop();
+        if (rc != FROG_OK) return rc;
+        return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "shared sample levels: %s",
+                    hipGetErrorString(e));
+    }
+    std::copy(off, off + 34, S->off);
+    S->nlev = nlev;
+    return FROG_OK;
+}
+
+int find_sample(const frog_index* ix, uint64_t seed, SharedLevels* out, float* maxnorm) {
+    std::lock_guard<std::mutex> g(ix->shared_mu);
+    auto it = ix->samples.find(seed);
+    if (it == ix->samples.end())
+        return fail(FROG_ENOTPREPARED, "entry_mode 1 with seed %llu: call frog_index_prepare_sample first",
+                    (unsigned long long)seed);
+    const frog_index::Sample& S = *it->second;
+    out->ranks = S.ranks;
+    out->xrows = ix->storage == FROG_STORAGE_F32 ? static_cast<const float*>(S.xrows) : nullptr;
+    out->xrowsh = ix->storage != FROG_STORAGE_F32 ? static_cast<const uint16_t*>(S.xrows) : nullptr;
+    out->prio = S.prio;
+    out->norm = S.norm;
+    std::copy(S.off, S.off + 34, out->off);
+    out->nlev = S.nlev;
+    out->key = mix64(seed);
+    *maxnorm = ix->maxnorm;
     return FROG_OK;
 }
 
 }  // namespace frog
+
+extern "C" {
+
+int frog_index_prepare_sample(frog_index_t* ix, uint64_t seed) {
+    frog::clear_error();
+    int rc = check_device_index(ix);
+    if (rc) return rc;
+    {
+        std::lock_guard<std::mutex> g(ix->shared_mu);
+        if (ix->samples.count(seed)) return FROG_OK;
+    }
+    // built outside the lock, so searches with other seeds are not held up
+    std::unique_ptr<frog_index::Sample> S(new (std::nothrow) frog_index::Sample);
+    if (!S) return fail(FROG_ENOMEM, "allocation failed");
+    rc = frog::build_sample(ix, seed, S.get());
+    if (rc) return rc;
+    std::lock_guard<std::mutex> g(ix->shared_mu);
+    if (ix->samples.count(seed)) {
+        // another thread prepared the same seed meanwhile: keep its copy
+        (void)hipFree(S->ranks);
+        (void)hipFree(S->xrows);
+        (void)hipFree(S->prio);
+        (void)hipFree(S->norm);
+        return FROG_OK;
+    }
+    ix->samples.emplace(seed, std::move(S));
+    return FROG_OK;
+}
+
+}  // extern "C"

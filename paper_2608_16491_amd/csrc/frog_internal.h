@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cstdint>
+#include <map>
 #include <memory>
 #include <mutex>
 #include <string>
@@ -52,22 +53,24 @@ struct frog_index {
     int32_t* dENC = nullptr;
     double* dattr = nullptr;
     int32_t* dperm = nullptr;
-    float maxnorm = -1.f;        // largest squared norm of the stored rows, computed on first use
+    float maxnorm = -1.f;        // largest squared norm of the stored rows, set at upload
     // work of the GPU construction: distances evaluated, sibling-search expansions
     int64_t build_distances = 0, build_expansions = 0;
     double build_kernel_ms = 0.0;   // from the first kernel's start to the last one's end
-    // shared entry sample (entry_mode 1): for one seed, the ascending rank
-    // lists of levels 1..nlev (level j: ranks whose priority is below
-    // 2^(32-j)), concatenated on the device; built on first use
-    std::mutex shared_mu;
-    bool shared_valid = false;
-    uint64_t shared_seed = 0;
-    int shared_nlev = 0;
-    int64_t shared_off[34] = {};
-    int32_t* dshared = nullptr;
-    void* dshared_x = nullptr;   // the levels' stored rows, in list order, dp values each
-    uint32_t* dshared_p = nullptr;  // priorities: rank order [0, n), then the levels' lists
-    float* dshared_nrm = nullptr;   // squared norms of the stored rows, same layout
+    // shared entry samples (entry_mode 1), one per prepared seed: built by
+    // frog_index_prepare_sample, immutable afterwards, freed only with the
+    // device copy (so a pointer taken under the mutex stays valid while the
+    // index stays uploaded)
+    struct Sample {
+        int nlev = 0;
+        int64_t off[34] = {};
+        int32_t* ranks = nullptr;   // ascending rank lists of levels 1..nlev, concatenated
+        void* xrows = nullptr;      // the levels' stored rows, in list order, dp values each
+        uint32_t* prio = nullptr;   // priorities: rank order [0, n), then the levels' lists
+        float* norm = nullptr;      // squared norms of the stored rows, same layout
+    };
+    mutable std::mutex shared_mu;
+    std::map<uint64_t, std::unique_ptr<Sample>> samples;
 };
 
 namespace frog {
@@ -143,10 +146,13 @@ struct SearchLaunch {
     float maxnorm;   // entry_mode 1: largest squared row norm of the index
 };
 
-// capi.cpp: the shared sample's levels for `seed` on the index's device
-// (built and uploaded on first use), and the largest squared row norm
-int shared_levels(frog_index* ix, uint64_t seed, SharedLevels* out);
-float index_maxnorm(frog_index* ix);
+// capi.cpp: the prepared shared sample of `seed` (FROG_ENOTPREPARED if
+// frog_index_prepare_sample has not built it) and the largest squared norm
+// of the stored rows
+int find_sample(const frog_index* ix, uint64_t seed, SharedLevels* out, float* maxnorm);
+int build_sample(const frog_index* ix, uint64_t seed, frog_index::Sample* S);
+// largest squared norm of the device copy's (stored) rows, taken at upload
+float stored_maxnorm(const frog_index* ix);
 
 // search.hip
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream);
@@ -156,6 +162,12 @@ bool search_shape_supported(int dp, int m, int L);
 // copy the rows of the listed ranks: out[i] = X[ranks[i]] (row_bytes each, a
 // multiple of 16)
 int launch_gather_rows(const void* X, int row_bytes, const int32_t* ranks, int64_t count, void* out, void* stream);
+// exhaustive filtered k-NN of nf selected queries (host arrays: query
+// indices hq, rank intervals hlr [nf][2], non-empty): ids/dists rows of those
+// queries are overwritten with the exact result, cert[q] set to 2 (if not
+// NULL); synchronises `stream`.  fp32 rows, 1 <= k <= 256.
+int launch_exact_ranges(const DevIndex& ix, const float* Q, const int32_t* hq, const int32_t* hlr, int64_t nf, int k,
+                        int32_t* ids, float* dists, int32_t* cert, void* stream);
 // bruteforce.hip
 int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const double* lo,
                       const double* hi, int k, int32_t* ids, float* dists, int32_t* cert,

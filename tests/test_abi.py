@@ -87,6 +87,8 @@ def test_device_calls_need_an_uploaded_index():
     assert rc == -5 and b"uploaded" in L.frog_last_error()
     rc = L.frog_bruteforce_filtered(ix.handle, None, 1, None, None, 10, None, None, None, None)
     assert rc == -5
+    rc = L.frog_index_prepare_sample(ix.handle, 0)
+    assert rc == -5 and b"uploaded" in L.frog_last_error()
     rc = L.frog_search(None, None, 1, None, None, 10, 64, None, None, None)
     assert rc == -1
 

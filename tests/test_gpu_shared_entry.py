@@ -32,7 +32,7 @@ def mix128():
     return Case(w.X, w.attr, w.Q, w.lo, w.hi)
 
 
-@pytest.mark.parametrize("L", [10, 16, 24, 25, 32, 56, 64, 128, 256])
+@pytest.mark.parametrize("L", [10, 16, 24, 25, 32, 56, 64, 120, 121, 128, 248])
 def test_shared_tiny_parity_pool_sizes(tiny, L):
     g_ids, g_d = tiny.gpu(10, L, **SH)
     o_ids, o_d, _ = tiny.cpu(10, L, **SH)
@@ -72,9 +72,9 @@ def test_shared_forgetful_table_does_not_change_results(tiny, hash_log2):
     assert (g_st[:, F.STAT_DIST] >= ref_st[:, F.STAT_DIST]).all()
 
 
-def test_shared_seed_change_rebuilds_levels(tiny):
-    # seed 0, then 99 (new levels), then 0 again (levels rebuilt): each run
-    # matches the oracle for its seed
+def test_shared_seeds_keep_their_levels(tiny):
+    # seed 0, then 99 (its own levels), then 0 again (the first levels, kept):
+    # each run matches the oracle for its seed
     a_ids, a_d = tiny.gpu(10, 64, **SH)
     tiny.gpu(10, 64, **dict(SH, seed=99))
     c_ids, c_d = tiny.gpu(10, 64, **SH)
@@ -95,11 +95,77 @@ def test_shared_mixture_d128_parity(mix128, L, emax, B):
     assert (g_st[ok, F.STAT_EXPANSIONS] == o_st[ok, oracle.STAT_EXPANSIONS]).all()
 
 
-def test_shared_k100_pool256(mix128):
+def test_shared_k100_pool248(mix128):
+    # the largest pool entry mode 1 takes
     p = dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=3000)
-    g_ids, g_d = mix128.gpu(100, 256, **p)
-    o_ids, o_d, _ = mix128.cpu(100, 256, **p)
+    g_ids, g_d = mix128.gpu(100, 248, **p)
+    o_ids, o_d, _ = mix128.cpu(100, 248, **p)
     assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+@pytest.mark.parametrize("L", [249, 256])
+def test_shared_refuses_pools_above_248(tiny, L):
+    # 256 kept candidates per list leave no margin above such pools: refused on
+    # the host before anything is enqueued
+    with pytest.raises(F.FrogError) as e:
+        tiny.gpu(10, L, **SH)
+    assert e.value.code == -7 and "L=%d" % L in str(e.value)
+
+
+def test_unprepared_seed_is_refused(tiny):
+    # the C ABI builds nothing inside a search: a seed whose sample was not
+    # prepared is an error, reported before anything is enqueued
+    import ctypes as C
+    L = F.lib()
+    p = F.search_params(entry_mode=1, seed=777, epn=16, epn_frac=1.0, epn_max=2000)
+    nq = tiny.dQ.shape[0]
+    ids = torch.full((nq, 10), -7, dtype=torch.int32, device="cuda")
+    ds = torch.empty((nq, 10), dtype=torch.float32, device="cuda")
+    rc = L.frog_search_ex(tiny.ix.handle, C.c_void_p(tiny.dQ.data_ptr()), nq, C.c_void_p(tiny.dlo.data_ptr()),
+                          C.c_void_p(tiny.dhi.data_ptr()), 10, 64, C.byref(p), C.c_void_p(ids.data_ptr()),
+                          C.c_void_p(ds.data_ptr()), None, None)
+    assert rc == -8 and b"prepare" in L.frog_last_error()
+    torch.cuda.synchronize()
+    assert (ids == -7).all()
+    assert L.frog_index_prepare_sample(tiny.ix.handle, C.c_uint64(777)) == 0
+    # idempotent
+    assert L.frog_index_prepare_sample(tiny.ix.handle, C.c_uint64(777)) == 0
+
+
+def test_concurrent_searches_with_different_seeds(tiny):
+    # two host threads, each on its own stream, search one index with
+    # different seeds (both prepared first); each result equals the oracle's
+    # for its seed on every repetition
+    import threading
+    seeds = [0, 4242]
+    for s in seeds:
+        tiny.ix.prepare_sample(s)
+    expect = {s: tiny.cpu(10, 64, **dict(SH, seed=s)) for s in seeds}
+    results, errors = {}, []
+
+    def work(seed):
+        try:
+            st = torch.cuda.Stream()
+            outs = []
+            with torch.cuda.stream(st):
+                for _ in range(6):
+                    outs.append(F.search(tiny.ix, tiny.dQ, tiny.dlo, tiny.dhi, 10, 64, stream=st,
+                                         **dict(SH, seed=seed)))
+            st.synchronize()
+            results[seed] = [(a.cpu().numpy(), b.cpu().numpy()) for a, b in outs]
+        except Exception as ex:   # reported by the main thread
+            errors.append(ex)
+
+    threads = [threading.Thread(target=work, args=(s,)) for s in seeds]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for s in seeds:
+        o_ids, o_d, _ = expect[s]
+        for g_ids, g_d in results[s]:
+            assert_parity(g_ids, g_d, o_ids, o_d)
 
 
 def test_shared_degenerate_ranges(tiny):
