@@ -2,21 +2,32 @@
 """Benchmark: filtered QPS at recall@10 >= 0.9 of range-filtered k-NN search
 (FROG, arxiv 2608.16491) on one MI355X.
 
-Workload (default): n = 1,000,000 base vectors, d = 128 fp32, a Gaussian
+Workload (default, c2): n = 1,000,000 base vectors, d = 128 fp32, a Gaussian
 mixture of 1,000 centres with per-point noise 0.3; the attribute is a random
 permutation of 0..n-1; 10,000 queries from the same mixture, each with a range
 of log-uniform selectivity on [2^-10, 1] at a random position; k = 10.
+`--workload c3|c4|c5` runs the other configurations (1M x 960 at L = 128;
+10M x 96 correlated attribute at L = 64; the fixed-selectivity sweep at
+k = 100, L = 256), each with its own sweep; their lines name their workload.
 
-Flow: build the index on the host, upload it, compute exact filtered k-NN on
-the GPU (matrix-core brute force) as ground truth, sweep the pool size L and
-the entry-point policy, pick the fastest setting whose recall@10 reaches 0.9,
-then time `--steps` searches of the whole query batch (inputs resident in HBM)
-with HIP events on the search stream.  A step is one call of frog_search over
-the batch: range -> ranks, hotspot, entry points, best-first traversal, top-k.
+Flow: build the index (host, and the same construction on the GPU), upload
+it, compute the exact filtered k-NN on the GPU (matrix-core brute force with
+an exact fallback, every row exact) as ground truth, sweep pool size, entry
+cap, budget, entry mode and index depth; the headline setting is the pinned
+one below when it reaches recall@10 0.9 on the batch and on a held-out batch
+from a separate seed stream, else the fastest setting that does.  Then time
+`--steps` steps after `--warmup` untimed ones.  A step is one repetition as
+the paper counts query time (Sec 8.1.3): the queries and ranges copied
+host-to-device from pinned memory, one frog_search call over the batch
+(range -> ranks, hotspot, entry points, best-first traversal, top-k), and the
+ids and distances copied back; HIP events on the stream the library enqueues
+on bracket the steps.  The kernels-only time with inputs already resident is
+reported beside it.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
 import argparse
+import atexit
 import hashlib
 import json
 import math
@@ -35,35 +46,57 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "search_c2_traffic.json")
-# the pool sizes the 1M x 128 workload is quoted on
-HEADLINE_L = (32, 64, 128)
+CSRC = os.path.join(ROOT, "paper_2608_16491_amd", "csrc")
+SEARCH_SOURCES = ("search_common.h", "search_shared.h", "search.hip", "search_shared.hip", "search_scan.hip",
+                  "search_pool.hip", "search_trav.hip", "wave_topk.h")
+SETTING_KEYS = ("L", "epn", "epn_frac", "epn_max", "budget", "entry_mode", "n_inv")
 
-# (L, epn, epn_frac, epn_max, budget[, entry_mode[, n_inv]]): the paper's fixed 16
-# entry points, then the per-query count min(cnt, epn_max) -- on the clustered
-# mixture a query must start inside its own cluster, which takes a few
-# thousand uniform samples.  entry_mode 0 draws them per query (stratified),
-# 1 from the rank priority shared by all queries (matrix-core entry scan).
-SWEEP = [
-    # entry mode 0 (per-query stratified sample)
-    (32, 16, 0.0, 0, 16), (64, 16, 0.0, 0, 16),
-    (32, 16, 1.0, 2560, 32), (64, 16, 1.0, 2560, 16), (32, 16, 1.0, 3072, 16), (64, 16, 1.0, 3072, 16),
-    (32, 16, 1.0, 2304, 32), (24, 16, 1.0, 2560, 32), (32, 16, 1.0, 2560, 24), (32, 16, 1.0, 2560, 28),
-    (40, 16, 1.0, 2560, 32), (48, 16, 1.0, 2560, 16), (64, 16, 1.0, 4096, 16),
-    # entry mode 1 (shared sample) on the paper's default index
-    (32, 16, 1.0, 2560, 24, 1), (24, 16, 1.0, 2560, 32, 1), (32, 16, 1.0, 2048, 32, 1),
-    (24, 16, 1.0, 2304, 32, 1), (32, 16, 1.0, 3072, 16, 1), (24, 16, 1.0, 3072, 24, 1),
-    (16, 16, 1.0, 3072, 32, 1), (32, 16, 1.0, 4096, 16, 1), (64, 16, 1.0, 2560, 16, 1),
-    (64, 16, 1.0, 3072, 16, 1), (128, 16, 1.0, 2048, 16, 1),
-    # entry mode 1 on indexes with one, two or three more layers (n_inv 6,
-    # 5 and 4, built on the GPU)
-    (32, 16, 1.0, 2048, 24, 1, 6), (32, 16, 1.0, 2304, 24, 1, 6), (32, 16, 1.0, 2560, 16, 1, 6),
-    (32, 16, 1.0, 2560, 24, 1, 6), (24, 16, 1.0, 2048, 32, 1, 6), (64, 16, 1.0, 2048, 16, 1, 6),
-    (32, 16, 1.0, 2304, 16, 1, 6), (32, 16, 1.0, 2304, 20, 1, 6), (32, 16, 1.0, 2432, 16, 1, 6),
-    (32, 16, 1.0, 2048, 24, 1, 5), (32, 16, 1.0, 2048, 16, 1, 5), (32, 16, 1.0, 2560, 16, 1, 5),
-    (32, 16, 1.0, 2304, 16, 1, 5), (32, 16, 1.0, 2432, 16, 1, 5), (24, 16, 1.0, 2304, 32, 1, 5),
-    (24, 16, 1.0, 2560, 24, 1, 5), (24, 16, 1.0, 2048, 32, 1, 5), (16, 16, 1.0, 3072, 32, 1, 5),
-    (32, 16, 1.0, 2304, 16, 1, 4), (32, 16, 1.0, 2560, 16, 1, 4), (24, 16, 1.0, 2304, 32, 1, 4),
-]
+# Settings are (L, epn, epn_frac, epn_max, budget, entry_mode, n_inv): the
+# paper's fixed 16 entry points, then the per-query count min(cnt, epn_max)
+# -- on the clustered mixtures a query must start inside its own cluster,
+# which takes a few thousand uniform samples.  entry_mode 0 draws them per
+# query (stratified), 1 from the rank priority shared by all queries (matrix-
+# core entry scan).  n_inv None is the paper's default for the dimension.
+SWEEPS = {
+    "c2": [
+        (32, 16, 0.0, 0, 16, 0, None), (64, 16, 0.0, 0, 16, 0, None),
+        (32, 16, 1.0, 2560, 24, 0, None), (32, 16, 1.0, 3072, 16, 0, None), (64, 16, 1.0, 2560, 16, 0, None),
+        (32, 16, 1.0, 2560, 24, 0, 6),
+        (32, 16, 1.0, 2560, 24, 1, None), (32, 16, 1.0, 3072, 16, 1, None), (64, 16, 1.0, 2560, 16, 1, None),
+        (128, 16, 1.0, 2048, 16, 1, None), (24, 16, 1.0, 2560, 32, 1, None), (16, 16, 1.0, 3072, 32, 1, None),
+        (32, 16, 1.0, 2048, 24, 1, 6), (32, 16, 1.0, 2304, 16, 1, 6), (32, 16, 1.0, 2560, 16, 1, 6),
+        (32, 16, 1.0, 2560, 24, 1, 6), (32, 16, 1.0, 2816, 16, 1, 6), (64, 16, 1.0, 2048, 16, 1, 6),
+        (32, 16, 1.0, 2304, 16, 1, 5), (32, 16, 1.0, 2560, 16, 1, 5), (32, 16, 1.0, 2048, 24, 1, 5),
+        (24, 16, 1.0, 2560, 24, 1, 5), (16, 16, 1.0, 3072, 32, 1, 5), (32, 16, 1.0, 2560, 16, 1, 4),
+    ],
+    "c3": [
+        (128, 16, 0.0, 0, 16, 0, None), (128, 16, 1.0, 256, 16, 0, None), (128, 16, 1.0, 512, 16, 0, None),
+        (128, 16, 1.0, 1024, 16, 0, None), (128, 16, 1.0, 512, 16, 1, None), (128, 16, 1.0, 1024, 16, 1, None),
+        (128, 16, 1.0, 2048, 16, 1, None), (128, 16, 1.0, 1024, 32, 1, None),
+    ],
+    "c4": [
+        (64, 16, 0.0, 0, 16, 0, None), (64, 16, 1.0, 2048, 16, 0, None), (64, 16, 1.0, 4096, 16, 0, None),
+        (64, 16, 1.0, 2048, 16, 1, None), (64, 16, 1.0, 4096, 16, 1, None), (64, 16, 1.0, 8192, 16, 1, None),
+        (64, 16, 1.0, 4096, 32, 1, None), (64, 16, 1.0, 8192, 32, 1, None), (64, 16, 1.0, 16384, 32, 1, None),
+        (64, 16, 1.0, 8192, 32, 1, 4), (64, 16, 1.0, 16384, 32, 1, 4), (64, 16, 1.0, 16384, 48, 1, 4),
+        (64, 16, 1.0, 32768, 48, 1, 4),
+    ],
+    # k = 100, L = 256: entry mode 1 keeps at most 256 candidates per list and
+    # takes L <= 248, so the named pool runs in entry mode 0
+    "c5": [
+        (256, 16, 0.0, 0, 16, 0, None), (256, 16, 1.0, 1024, 16, 0, None), (256, 16, 1.0, 2048, 16, 0, None),
+        (256, 16, 1.0, 3072, 16, 0, None), (256, 16, 1.0, 2048, 32, 0, None), (256, 16, 1.0, 3072, 32, 0, 6),
+        (248, 16, 1.0, 3072, 16, 1, None), (248, 16, 1.0, 3072, 32, 1, 6),
+    ],
+}
+# the pool sizes each workload is quoted on
+HEADLINE_L = {"c2": (32, 64, 128), "c3": (128,), "c4": (64,), "c5": (256,)}
+# the headline setting when it reaches the recall target on the batch and on
+# the held-out batch (pinned so that the committed kernel profiles are taken at
+# the setting the line reports)
+PINNED = {"c2": (32, 16, 1.0, 2560, 16, 1, 5)}
+# the paper's fixed selectivities (Sec 8.1.2): large, medium, small
+FIXED_SIGMAS = (2.0 ** -2, 2.0 ** -5, 2.0 ** -8)
 
 
 def _plain(o):
@@ -79,14 +112,19 @@ def log(*a):
 
 def source_sha():
     h = hashlib.sha256()
-    for name in ("search.hip", "wave_topk.h"):
-        with open(os.path.join(ROOT, "paper_2608_16491_amd", "csrc", name), "rb") as f:
+    for name in SEARCH_SOURCES:
+        with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def recall_at_k(ids, gt):
-    """|result ∩ exact| / |exact| per query (exact rows padded with -1)."""
+def recall_at_k(ids, gt, k=None):
+    """|result ∩ exact| / |exact| per query over the first k columns (exact
+    rows padded with -1)."""
+    ids = np.asarray(ids)
+    gt = np.asarray(gt)
+    if k is not None:
+        ids, gt = ids[:, :k], gt[:, :k]
     out = np.empty(len(ids))
     for i in range(len(ids)):
         g = gt[i][gt[i] >= 0]
@@ -97,31 +135,63 @@ def recall_at_k(ids, gt):
     return out
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def reap_children():
+    """End any process this run started that is still alive (none should be)."""
+    try:
+        import psutil
+        kids = psutil.Process().children(recursive=True)
+    except Exception:
+        return
+    for p in kids:
+        try:
+            log(f"ending leftover child process {p.pid} ({p.name()})")
+            p.terminate()
+        except Exception:
+            pass
+    try:
+        psutil.wait_procs(kids, timeout=5)
+    except Exception:
+        pass
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--workload", default="c2", choices=sorted(SWEEPS))
     ap.add_argument("--n", type=int, default=None, help="override n (smaller runs)")
     ap.add_argument("--nq", type=int, default=None, help="override the number of queries")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-oracle time")
     ap.add_argument("--setting", default=None,
-                    help="L,epn,epn_frac,epn_max,budget: skip the sweep (the profile pass takes several, "
-                         "separated by ';')")
+                    help="L,epn,epn_frac,epn_max,budget[,mode[,n_inv]]: skip the sweep (the profile pass takes "
+                         "several, separated by ';')")
     ap.add_argument("--hash-log2", type=int, default=10)
     ap.add_argument("--profile-pass", action="store_true",
                     help="run each given setting once, the brute force once and a 1 GiB copy, "
                          "for rocprofv3 counters")
     ap.add_argument("--details", default=None, help="write sweep details (JSON) here")
     ap.add_argument("--index-cache", default=None, help="load the index from / save it to this file")
+    ap.add_argument("--gpu-build", action="store_true",
+                    help="build the index on the GPU only (default for c3 and c4, whose host build takes minutes)")
     ap.add_argument("--ablation", action="store_true",
                     help="also measure the ablations of Sec 8.2.3 at the chosen setting: hotspot without its end "
                          "condition / without localisation, eager visited check, and (rebuilding the index) "
                          "beta = 0; reported under 'ablation' in --details")
     ap.add_argument("--sweep-params", action="store_true",
-                    help="also measure recall and QPS against beta, gamma, n_inv (GPU rebuilds), the budget and "
-                         "the entry-point cap; reported under 'sensitivity' in --details")
+                    help="also measure recall and QPS against beta, gamma (Sec 8.2.5), n_inv (GPU rebuilds), the "
+                         "budget and the entry-point cap; reported under 'sensitivity' in --details")
     ap.add_argument("--oracle-pg", action="store_true",
                     help="also compare FROG's recall with a per-query index over the in-range objects only "
                          "(a ceiling, on the first 200k objects); reported under 'oracle_pg' in --details")
@@ -129,6 +199,7 @@ def main():
                     help="skip timing the GPU construction against the host one")
     ap.add_argument("--no-16bit", "--no-fp16", dest="no_16bit", action="store_true",
                     help="skip the secondary measurements with the rows stored in fp16 and bf16")
+    ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-selectivity batches")
     ap.add_argument("--storage", default="fp32", choices=("fp32", "fp16", "bf16"),
                     help="row storage of the sweep and the timed steps (the ground truth always uses fp32 "
                          "rows); fp16 and bf16 are for profiling those paths, the metric is quoted on fp32")
@@ -139,30 +210,43 @@ def main():
               "(replicated index, no exchange) and multi-GPU runs are not part of it",
               file=sys.stderr)
         sys.exit(2)
+    atexit.register(reap_children)
 
     import torch
     import paper_2608_16491_amd as F
     import workloads
 
     dev = torch.device("cuda:0")
+    wl = args.workload
     t0 = time.time()
-    w = workloads.make(args.workload, n=args.n, nq=args.nq)
+    w = workloads.make(wl, n=args.n, nq=args.nq)
     log(f"workload {w.name}: n={w.n} d={w.d} nq={w.nq} k={w.k} ({time.time() - t0:.1f}s)")
+    k = w.k
+    gpu_only = args.gpu_build or wl in ("c3", "c4")
+    default_ninv = F.build_params(w.d).n_inv
+
+    # ------------------------------------------------------------------ index
     t0 = time.time()
+    t_build = None
     if args.index_cache and os.path.exists(args.index_cache):
         ix = F.Index.load(args.index_cache)
+        gpu_only = False
         log(f"index loaded from {args.index_cache}")
+    elif gpu_only:
+        ix = F.Index.build(w.X, w.attr, device=0)
+        log(f"GPU build: {time.time() - t0:.1f}s")
     else:
         ix = F.Index.build(w.X, w.attr)
-        if args.index_cache:
-            ix.save(args.index_cache)
-    t_build = time.time() - t0
+        t_build = time.time() - t0
+    if args.index_cache and not os.path.exists(args.index_cache):
+        ix.save(args.index_cache)
     n, d, H, m = ix.info()
-    log(f"host build: {t_build:.1f}s  H={H} m={m}")
+    if t_build is not None:
+        log(f"host build: {t_build:.1f}s  H={H} m={m}")
     # the same construction on the GPU (Sec 6): timed, and checked equal to
     # the host's entry for entry
     gpu_build = None
-    if not args.no_gpu_build and not args.profile_pass:
+    if not args.no_gpu_build and not args.profile_pass and not gpu_only:
         torch.cuda.synchronize()
         t0 = time.time()
         gix = F.Index.build(w.X, w.attr, device=0)
@@ -172,43 +256,37 @@ def main():
         gd, ge, gkms = gix.build_stats()
         gix.free()
         del g_enc
-        host_ref = None if (args.index_cache and os.path.exists(args.index_cache)) else t_build
         # the distances are fp64 arithmetic in dimension order: 3 flops (sub,
         # mul, add) per dimension, against the fp64 vector peak
         gflop = 3.0 * d * gd / 1e9
-        gpu_build = {"s": t_gb, "host_s": host_ref, "speedup": (host_ref / t_gb) if host_ref else None,
+        gpu_build = {"s": t_gb, "host_s": t_build, "speedup": (t_build / t_gb) if t_build else None,
                      "equal_to_host": same, "distances": gd, "expansions": ge, "kernel_s": gkms / 1e3,
                      "fp64_tflops": gflop / (gkms / 1e3) / 1e3 if gkms > 0 else None,
                      "fp64_frac": gflop / (gkms / 1e3) / 1e3 / FP64_VECTOR_PEAK_TFLOPS if gkms > 0 else None}
-        log(f"GPU build: {t_gb:.2f}s wall, kernels {gkms / 1e3:.2f}s (host build {t_build:.1f}s"
-            f"{', loaded from cache' if host_ref is None else ''}), ENC equal to the host build: {same}, "
-            f"{gd} distances, {ge} sibling-search expansions, "
+        log(f"GPU build: {t_gb:.2f}s wall, kernels {gkms / 1e3:.2f}s (host build {t_build}), ENC equal to the "
+            f"host build: {same}, {gd} distances, {ge} sibling-search expansions, "
             f"{gflop / max(gkms, 1e-9):.2f} TFLOP/s fp64 in the distance loops")
-    ix.upload(0)
+    if not gpu_only:
+        ix.upload(0)
     Q = torch.as_tensor(w.Q, device=dev)
     lo = torch.as_tensor(w.lo, device=dev)
     hi = torch.as_tensor(w.hi, device=dev)
-    k = w.k
     stream = torch.cuda.current_stream()
 
     # indexes by n_inv (the number of deepest segment-tree layers left out,
-    # Sec 6): the paper's default is the host build above; others are built
-    # on the GPU on first use (same construction, same result as the host's)
-    default_ninv = F.build_params(d).n_inv
+    # Sec 6): the paper's default is the one above; others are built on the
+    # GPU on first use (same construction, same result as the host's)
     indexes = {default_ninv: ix}
-    cur = {"ni": default_ninv}   # the index run() uses when no n_inv is given
 
     def index_for(ni):
+        ni = default_ninv if ni is None else ni
         if ni not in indexes:
             t0 = time.time()
             indexes[ni] = F.Index.build(w.X, w.attr, device=0, n_inv=ni)
+            if args.storage != "fp32":
+                indexes[ni].upload(0, storage=args.storage)
             log(f"index with n_inv={ni} built on the GPU in {time.time() - t0:.2f}s (H={indexes[ni].info()[2]})")
         return indexes[ni]
-
-    def run(L, epn, frac, emax, B=16, mode=0, ni=None, hl2=args.hash_log2, stats=False, events=None):
-        index = index_for(cur["ni"] if ni is None else ni)
-        return F.search(index, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                        entry_mode=mode, hash_log2=hl2, stats=stats, events=events)
 
     def norm_setting(v):
         v = list(v)
@@ -217,11 +295,22 @@ def main():
         if len(v) == 5:
             v.append(0)
         if len(v) == 6:
-            v.append(default_ninv)
-        return int(v[0]), int(v[1]), float(v[2]), int(v[3]), int(v[4]), int(v[5]), int(v[6])
+            v.append(None)
+        ni = default_ninv if v[6] is None else int(v[6])
+        return int(v[0]), int(v[1]), float(v[2]), int(v[3]), int(v[4]), int(v[5]), ni
 
     def parse_setting(text):
         return norm_setting([float(x) for x in text.split(",")])
+
+    def params(s):
+        L, epn, frac, emax, B, mode, ni = s
+        return dict(epn=epn, epn_frac=frac, epn_max=emax, budget=B, entry_mode=mode, hash_log2=args.hash_log2)
+
+    def run(s, Qx=None, lox=None, hix=None, **extra):
+        p = params(s)
+        p.update(extra)
+        return F.search(index_for(s[6]), Q if Qx is None else Qx, lo if lox is None else lox,
+                        hi if hix is None else hix, k, s[0], **p)
 
     def timed(fn, reps, warm=2):
         # untimed calls first: the first calls after an index upload or a
@@ -239,13 +328,13 @@ def main():
 
     if args.profile_pass:
         settings = [parse_setting(t) for t in args.setting.split(";")]
-        for (L, epn, frac, emax, B, mode, ni) in settings:
-            index_for(ni)
+        for s in settings:
+            index_for(s[6])
         if args.storage != "fp32":
             for index in indexes.values():
                 index.upload(0, storage=args.storage)
-        for (L, epn, frac, emax, B, mode, ni) in settings:
-            run(L, epn, frac, emax, B, mode, ni)
+        for s in settings:
+            run(s)
             torch.cuda.synchronize()
         if args.storage == "fp32":
             F.bruteforce(ix, Q, lo, hi, k)
@@ -258,7 +347,7 @@ def main():
             "one 1 GiB copy")
         return
 
-    # ground truth: exact filtered k-NN on the GPU
+    # ------------------------------------------------------------------ ground truth
     t0 = time.time()
     gt_ids, gt_d, cert = F.bruteforce(ix, Q, lo, hi, k)
     torch.cuda.synchronize()
@@ -266,207 +355,388 @@ def main():
     bf_time = timed(lambda: F.bruteforce(ix, Q, lo, hi, k), 1)
     gt_ids = gt_ids.cpu().numpy()
     cert = cert.cpu().numpy()
-    # bytes per stored value of the searched rows
-    eb = 4 if args.storage == "fp32" else 2
+    assert np.isin(cert, (1, 2)).all(), "brute force returned a row it did not make exact"
     if args.storage != "fp32":
         ix.upload(0, storage=args.storage)
     cnt = (w.hi - w.lo + 1).astype(np.int64)
     bf_flops = 2.0 * d * float(cnt.sum())
-    log(f"ground truth: {t_gt:.2f}s first call, {bf_time * 1e3:.1f} ms timed, certified "
-        f"{cert.mean() * 100:.2f}%, useful {bf_flops / bf_time / 1e12:.1f} TFLOP/s")
-    band = np.clip(np.floor(-np.log2(w.sigma)).astype(int), 0, 9)
+    log(f"ground truth: {t_gt:.2f}s first call, {bf_time * 1e3:.1f} ms timed, certified by the margin "
+        f"{(cert == 1).mean() * 100:.2f}% (rest exhaustive), useful {bf_flops / bf_time / 1e12:.1f} TFLOP/s")
+    nbands = 12 if wl == "c4" else 10
+    band = np.clip(np.floor(-np.log2(w.sigma)).astype(int), 0, nbands - 1)
+    rk = 10 if k > 10 else None     # c5 also reports recall@10
 
-    # sweep
+    # ------------------------------------------------------------------ sweep
     rows = []
-    settings = [norm_setting(x) for x in SWEEP] if args.setting is None else [parse_setting(args.setting)]
-    for (L, epn, frac, emax, B, mode, ni) in settings:
-        index_for(ni)
-    if args.storage != "fp32":
-        for index in indexes.values():
-            index.upload(0, storage=args.storage)
-    for (L, epn, frac, emax, B, mode, ni) in settings:
+    settings = [norm_setting(x) for x in SWEEPS[wl]] if args.setting is None else [parse_setting(args.setting)]
+    pinned = norm_setting(PINNED[wl]) if (wl in PINNED and args.setting is None and args.n is None
+                                          and args.nq is None) else None
+    if pinned is not None and pinned not in settings:
+        settings.append(pinned)
+    for s in settings:
+        index_for(s[6])
+    for s in settings:
+        L, epn, frac, emax, B, mode, ni = s
         if L < k:
             continue
-        ids, _ = run(L, epn, frac, emax, B, mode, ni)
+        ids, _ = run(s)
         torch.cuda.synchronize()
-        rec = recall_at_k(ids.cpu().numpy(), gt_ids)
-        run(L, epn, frac, emax, B, mode, ni)
-        t = timed(lambda: run(L, epn, frac, emax, B, mode, ni), 10)
-        rows.append(dict(L=L, epn=epn, epn_frac=frac, epn_max=emax, budget=B, entry_mode=mode, n_inv=ni,
-                         recall=float(rec.mean()), qps=w.nq / t, ms=t * 1e3,
-                         recall_band=[float(rec[band == b].mean()) if (band == b).any() else None
-                                      for b in range(10)]))
-        log(f"L={L:4d} epn={epn} frac={frac:<6} max={emax:5d} B={B:2d} mode={mode}  recall={rec.mean():.4f}  "
-            f"{t * 1e3:8.3f} ms  {w.nq / t:12.0f} QPS")
-    # the headline takes the pool sizes the workload names; the fastest
-    # setting of any pool size is reported beside it
-    ok_any = [r for r in rows if r["recall"] >= 0.9]
-    ok = [r for r in ok_any if r["L"] in HEADLINE_L] if args.setting is None else ok_any
-    chosen = max(ok, key=lambda r: r["qps"]) if ok else max(rows, key=lambda r: r["recall"])
-    fastest_any = max(ok_any, key=lambda r: r["qps"]) if ok_any else None
-    met = bool(ok)
-    L, epn, frac, emax, B, mode, ni = (chosen["L"], chosen["epn"], chosen["epn_frac"], chosen["epn_max"],
-                                       chosen["budget"], chosen["entry_mode"], chosen["n_inv"])
-    cur["ni"] = ni
-    ix = indexes[ni]
-    n, d, H, m = ix.info()
-    log(f"chosen: L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} entry_mode={mode} n_inv={ni} "
-        f"recall={chosen['recall']:.4f}" + ("" if met else "  (recall target NOT met)"))
-    if fastest_any is not None and fastest_any is not chosen:
-        log(f"fastest of any pool size: L={fastest_any['L']} max={fastest_any['epn_max']} B={fastest_any['budget']} "
-            f"mode={fastest_any['entry_mode']} n_inv={fastest_any['n_inv']} recall={fastest_any['recall']:.4f} "
-            f"{fastest_any['qps']:.0f} QPS")
+        idn = ids.cpu().numpy()
+        rec = recall_at_k(idn, gt_ids)
+        t = timed(lambda: run(s), 10)
+        row = dict(zip(SETTING_KEYS, s), recall=float(rec.mean()), qps=w.nq / t, ms=t * 1e3,
+                   recall_band=[float(rec[band == b].mean()) if (band == b).any() else None
+                                for b in range(nbands)])
+        if rk:
+            row["recall@10"] = float(recall_at_k(idn, gt_ids, rk).mean())
+        rows.append(row)
+        log(f"L={L:4d} epn={epn} frac={frac:<4} max={emax:5d} B={B:2d} mode={mode} n_inv={ni}  "
+            f"recall={rec.mean():.4f}  {t * 1e3:8.3f} ms  {w.nq / t:12.0f} QPS")
 
-    # timed steps; each step also records events around the library's kernels
-    # on the same stream (entry_mode 0: the search kernel; entry_mode 1: the
-    # matrix-core entry scan, then the search kernel)
+    def key(r):
+        return tuple(r[x] for x in SETTING_KEYS)
+
+    # held-out batch from the reserve stream: the chosen setting's recall is
+    # checked on queries the choice never saw
+    qn, lon, hin, _ = workloads.more_queries(w, "held_out", w.nq)
+    Qh, lo_h, hi_h = (torch.as_tensor(qn, device=dev), torch.as_tensor(lon, device=dev),
+                      torch.as_tensor(hin, device=dev))
+    if args.storage != "fp32":
+        ix.upload(0)
+    gt_h = F.bruteforce(ix, Qh, lo_h, hi_h, k)[0].cpu().numpy()
+    if args.storage != "fp32":
+        ix.upload(0, storage=args.storage)
+
+    def held_out_recall(s):
+        ids_h, _ = run(s, Qh, lo_h, hi_h)
+        torch.cuda.synchronize()
+        return float(recall_at_k(ids_h.cpu().numpy(), gt_h).mean())
+
+    ok_any = [r for r in rows if r["recall"] >= 0.9]
+    ok = [r for r in ok_any if r["L"] in HEADLINE_L[wl]] if args.setting is None else ok_any
+    chosen = None
+    how = None
+    if pinned is not None:
+        pr = next(r for r in rows if key(r) == pinned)
+        if pr["recall"] >= 0.9:
+            pr["recall_held_out"] = held_out_recall(pinned)
+            if pr["recall_held_out"] >= 0.9:
+                chosen, how = pr, "pinned setting; recall target met on the batch and on the held-out batch"
+    if chosen is None:
+        for r in sorted(ok, key=lambda r: -r["qps"]):
+            r["recall_held_out"] = held_out_recall(key(r))
+            if r["recall_held_out"] >= 0.9:
+                chosen, how = r, "fastest sweep setting meeting the recall target on the batch and held-out batch"
+                break
+    met = chosen is not None
+    if chosen is None:
+        chosen = max(rows, key=lambda r: r["recall"])
+        chosen["recall_held_out"] = held_out_recall(key(chosen))
+        how = "recall target not reached: the setting with the best recall"
+    fastest_any = max(ok_any, key=lambda r: r["qps"]) if ok_any else None
+    best_sweep = max(ok, key=lambda r: r["qps"]) if ok else None
+    sel = key(chosen)
+    L, epn, frac, emax, B, mode, ni = sel
+    ix = index_for(ni)
+    n, d, H, m = ix.info()
+    dp = (d + 31) // 32 * 32
+    log(f"chosen ({how}): L={L} epn={epn} epn_frac={frac} epn_max={emax} budget={B} entry_mode={mode} n_inv={ni} "
+        f"recall={chosen['recall']:.4f} held-out={chosen['recall_held_out']:.4f}")
+
+    # ------------------------------------------------------------------ timed steps
+    # (a) the paper's query time: the batch's queries and ranges from pinned
+    # host memory to the device (one copy: the three arrays are packed in one
+    # pinned buffer), the search, and its ids and distances back to pinned
+    # host memory (one copy), per step, in order on one stream
+    nq, qb, rb = w.nq, w.nq * d * 4, w.nq * 8
+    inb = (qb + 2 * rb + 255) // 256 * 256
+    host_in = torch.empty(inb, dtype=torch.uint8).pin_memory()
+    host_in[:qb].view(torch.float32).copy_(torch.from_numpy(np.ascontiguousarray(w.Q).reshape(-1)))
+    host_in[qb:qb + rb].view(torch.float64).copy_(torch.from_numpy(np.ascontiguousarray(w.lo)))
+    host_in[qb + rb:qb + 2 * rb].view(torch.float64).copy_(torch.from_numpy(np.ascontiguousarray(w.hi)))
+    outb = 2 * nq * k * 4
+    p_sel = params(sel)
+
+    def buffers():
+        dev_in = torch.empty(inb, dtype=torch.uint8, device=dev)
+        dev_out = torch.empty(outb, dtype=torch.uint8, device=dev)
+        host_out = torch.empty(outb, dtype=torch.uint8).pin_memory()
+        views = (dev_in[:qb].view(torch.float32).view(nq, d), dev_in[qb:qb + rb].view(torch.float64),
+                 dev_in[qb + rb:qb + 2 * rb].view(torch.float64),
+                 dev_out[:outb // 2].view(torch.int32).view(nq, k), dev_out[outb // 2:].view(torch.float32).view(nq, k))
+        return dev_in, dev_out, host_out, views
+
+    bufs = [buffers(), buffers()]
+
+    def step(b=0):
+        dev_in, dev_out, host_out, (Qd, lod, hid, ids_d, ds_d) = bufs[b]
+        dev_in.copy_(host_in, non_blocking=True)
+        F.search(ix, Qd, lod, hid, k, L, out=(ids_d, ds_d), **p_sel)
+        host_out.copy_(dev_out, non_blocking=True)
+
     for _ in range(args.warmup):
-        run(L, epn, frac, emax, B, mode)
+        step()
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    marks[0].record(stream)
+    for i in range(args.steps):
+        step()
+        marks[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
+    per_step = marks[0].elapsed_time(marks[-1]) / 1000.0 / args.steps
+    per_step_med = float(np.median(step_ms)) / 1000.0
+    qps = w.nq / per_step
+    # the transfers' result equals the resident search's
+    ref_ids, _ = run(sel)
+    torch.cuda.synchronize()
+    got = bufs[0][2][:outb // 2].view(torch.int32).view(nq, k)
+    assert (ref_ids.cpu() == got).all(), "transfer-inclusive step returned other ids"
+    log(f"timed {args.steps} steps with transfers: {per_step * 1e3:.3f} ms/step mean, {per_step_med * 1e3:.3f} median, "
+        f"min {min(step_ms):.3f} max {max(step_ms):.3f} (wall {wall / args.steps * 1e3:.3f}), {qps:.0f} QPS; steps "
+        + " ".join(f"{x:.3f}" for x in step_ms))
+
+    # (a') the same steps overlapped as a serving loop would run them: the
+    # next batch's copy in and the previous batch's copy out proceed on a
+    # second stream while the current batch is searched (two buffer sets)
+    cs = torch.cuda.Stream()
+    h2d = [torch.cuda.Event() for _ in range(2)]
+    done = [torch.cuda.Event() for _ in range(2)]
+    out = [torch.cuda.Event() for _ in range(2)]
+    for b in range(2):
+        done[b].record(stream)
+        out[b].record(stream)
+
+    def stage_in(i):
+        b = i % 2
+        with torch.cuda.stream(cs):
+            cs.wait_event(done[b])          # the search two steps back has read this buffer
+            cs.wait_event(out[b])           # and its results have left it
+            bufs[b][0].copy_(host_in, non_blocking=True)
+            h2d[b].record(cs)
+
+    def stage_run(i):
+        b = i % 2
+        _, dev_out, host_out, (Qd, lod, hid, ids_d, ds_d) = bufs[b]
+        stream.wait_event(h2d[b])
+        F.search(ix, Qd, lod, hid, k, L, out=(ids_d, ds_d), **p_sel)
+        done[b].record(stream)
+        with torch.cuda.stream(cs):
+            cs.wait_event(done[b])
+            host_out.copy_(dev_out, non_blocking=True)
+            out[b].record(cs)
+
+    def pipelined(nsteps):
+        stage_in(0)
+        for i in range(nsteps):
+            if i + 1 < nsteps:
+                stage_in(i + 1)
+            stage_run(i)
+        stream.wait_stream(cs)
+
+    pipelined(args.warmup)
+    torch.cuda.synchronize()
+    pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pe0.record(stream)
+    cs.wait_event(pe0)
+    pipelined(args.steps)
+    pe1.record(stream)
+    torch.cuda.synchronize()
+    per_step_pipe = pe0.elapsed_time(pe1) / 1000.0 / args.steps
+    log(f"overlapped steps with transfers: {per_step_pipe * 1e3:.3f} ms/step, {w.nq / per_step_pipe:.0f} QPS")
+
+    # (b) kernels only, inputs resident; events around the library's phases
+    # (entry_mode 0: the search kernel; entry_mode 1: the matrix-core entry
+    # scan, then the pool and traversal kernels)
+    for _ in range(args.warmup):
+        run(sel)
     phase = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     for trio in phase:
         for ev in trio:
             ev.record(stream)            # materialise the events
-    torch.cuda.synchronize()
     ev_s, ev_e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    wall0 = time.perf_counter()
     ev_s.record(stream)
     for i in range(args.steps):
-        run(L, epn, frac, emax, B, mode, events=phase[i])
+        run(sel, events=phase[i])
     ev_e.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    per_step = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
+    per_step_res = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
     t_a = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
     t_b = sum(t[1].elapsed_time(t[2]) for t in phase) / 1000.0 / args.steps
-    qps = w.nq / per_step
-    log(f"timed {args.steps} steps: {per_step * 1e3:.3f} ms/step (events), wall {wall / args.steps * 1e3:.3f} ms/step, "
-        f"{qps:.0f} QPS; " + (f"search kernel {t_a * 1e3:.3f} ms" if mode == 0 else
-                              f"entry scan {t_a * 1e3:.3f} ms, search kernel {t_b * 1e3:.3f} ms"))
+    log(f"resident: {per_step_res * 1e3:.3f} ms/step, {w.nq / per_step_res:.0f} QPS; " +
+        (f"search kernel {t_a * 1e3:.3f} ms" if mode == 0 else
+         f"entry scan {t_a * 1e3:.3f} ms, pool + traversal {t_b * 1e3:.3f} ms"))
 
-    # algorithmic bytes: distinct evaluations and ENC entries from the exact-visited pass
-    ids_e, _, st_e = run(L, epn, frac, emax, B, mode, hl2=0, stats=True)
-    _, _, st_f = run(L, epn, frac, emax, B, mode, stats=True)
+    # ------------------------------------------------------------------ roofline
+    # algorithmic work per query (distinct evaluations D_q, entry points E_q,
+    # ENC entries S_q) from a pass with the exact visited set, whose counts
+    # equal the oracle's
+    _, _, st_e = run(sel, hash_log2=0, stats=True)
+    _, _, st_f = run(sel, stats=True)
     torch.cuda.synchronize()
     st_e = st_e.cpu().numpy().astype(np.int64)
     st_f = st_f.cpu().numpy().astype(np.int64)
-    D = st_e[:, F.STAT_DIST].sum()
-    S = st_e[:, F.STAT_SCANNED].sum()
-    NE = st_e[:, F.STAT_ENTRY].sum()
+    eb = 4 if args.storage == "fp32" else 2
+    D = int(st_e[:, F.STAT_DIST].sum())
+    S = int(st_e[:, F.STAT_SCANNED].sum())
+    NE = int(st_e[:, F.STAT_ENTRY].sum())
     nonempty = int((cnt > 0).sum())
     overhead = st_f[:, F.STAT_DIST].sum() / max(D, 1)
     per_query = (4 * d + 16 + 16 * math.ceil(math.log2(n + 1)) + 12 * k) * nonempty
+    # the method's own bytes per step: every distinct evaluation's vector, the
+    # ENC entries Alg. 4 examines, the query, its rank search, the output
+    method_bytes = eb * d * D + 4.0 * S + per_query
     phases = None
     if mode == 0:
-        # one kernel reads every distinct evaluated vector (entry points and
-        # traversal), the ENC entries Alg. 4 examines, the query, its rank
-        # search, and writes the output through the id map
-        alg_bytes = eb * d * D + 4.0 * S + per_query
         dominant, t_kernel = "coop_kernel", t_a
-        achieved = alg_bytes / t_kernel / 1e9
-        log(f"algorithmic bytes/launch {alg_bytes / 1e6:.1f} MB (evaluations {D}, entry points {NE}, "
-            f"ENC entries {S}); search kernel {achieved:.0f} GB/s = {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s, "
-            f"whole step {alg_bytes / per_step / 1e9:.0f} GB/s; forgetful-table evaluations x{overhead:.3f}")
+        achieved = method_bytes / t_kernel / 1e9
+        roof = {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "alg_bytes_per_launch": method_bytes,
+                "kernel_ms": t_kernel * 1e3}
+        log(f"coop_kernel: {method_bytes / 1e6:.1f} MB algorithmic (evaluations {D}, entry points {NE}, ENC entries "
+            f"{S}) in {t_a * 1e3:.3f} ms = {achieved:.0f} GB/s ({achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s)")
     else:
-        # entry scan: the rows of every tile's run, once per tile (row data
-        # and, above level 0, its rank); pool and search kernels: the kept
-        # candidates re-ranked, the traversal's distinct evaluations, the ENC
-        # entries, the query, its rank search and the output
+        # entry scan: one distance per (query, sample point), 3d flops each
+        # (subtract, multiply, add), on the fp32 matrix cores; its tiles issue
+        # 2 dp flops per (tile row, tile query)
         scan_rows = int(st_f[:, F.STAT_SCANROWS].sum())
+        useful = 3.0 * d * NE
+        issued = 2.0 * dp * 16 * scan_rows
+        occupancy = NE / max(16.0 * scan_rows, 1.0)
+        scan_tf = useful / t_a / 1e12
+        # pool + traversal: the sample's re-ranked candidates, the traversal's
+        # distinct evaluations, the ENC entries and the per-query terms
         kkeep = 64 if L + 8 <= 64 else (128 if L + 8 <= 128 else 256)
         rerank = int(np.minimum(st_e[:, F.STAT_ENTRY], kkeep).sum())
-        scan_bytes = (eb * d + 4.0) * scan_rows
-        search_bytes = eb * d * (rerank + D - NE) + 4.0 * S + per_query
-        scan_flops = 2.0 * d * 16 * scan_rows
-        a_scan, a_search = scan_bytes / t_a / 1e9, search_bytes / t_b / 1e9
-        phases = {"entry_scan": {"kernel": "s_scan_kernel", "ms": t_a * 1e3, "rows": scan_rows,
-                                 "alg_bytes": scan_bytes, "GB_s": a_scan,
-                                 "matrix_TFLOP_s": scan_flops / t_a / 1e12},
-                  "search": {"kernel": "s_pool_kernel+s_search_kernel", "ms": t_b * 1e3,
-                             "alg_bytes": search_bytes, "GB_s": a_search}}
+        trav_bytes = eb * d * (D - NE) + 4.0 * S + per_query
+        search_bytes = eb * d * rerank + trav_bytes
+        a_search = search_bytes / t_b / 1e9
+        phases = {"entry_scan": {"kernel": "s_scan_kernel", "ms": t_a * 1e3, "bound": "mfma",
+                                 "useful_tflops": scan_tf, "useful_frac": scan_tf / FP32_MFMA_PEAK_TFLOPS,
+                                 "useful_tflops_2d": 2.0 * d * NE / t_a / 1e12,
+                                 "issued_tflops": issued / t_a / 1e12, "tile_occupancy": occupancy,
+                                 "tile_rows": scan_rows, "sample_points": NE,
+                                 "tile_row_bytes": (eb * d + 4.0) * scan_rows},
+                  "pool_and_traversal": {"kernel": "s_pool_kernel+s_search_kernel", "ms": t_b * 1e3, "bound": "hbm",
+                                         "alg_bytes": search_bytes, "GB_s": a_search,
+                                         "frac": a_search / HBM_PEAK_GBS,
+                                         "traversal_alg_bytes": trav_bytes,
+                                         "traversal_GB_s": trav_bytes / t_b / 1e9}}
         if t_a >= t_b:
-            dominant, t_kernel, alg_bytes, achieved = "s_scan_kernel", t_a, scan_bytes, a_scan
+            dominant = "s_scan_kernel"
+            roof = {"bound": "mfma", "kernel": dominant, "achieved": scan_tf, "peak": FP32_MFMA_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": scan_tf / FP32_MFMA_PEAK_TFLOPS, "flops_per_launch": useful,
+                    "tile_occupancy": occupancy, "kernel_ms": t_a * 1e3}
         else:
-            dominant, t_kernel, alg_bytes, achieved = ("s_pool_kernel+s_search_kernel", t_b, search_bytes,
-                                                       a_search)
-        log(f"entry scan: {scan_rows} tile rows, {scan_bytes / 1e6:.1f} MB, {a_scan:.0f} GB/s, "
-            f"{scan_flops / t_a / 1e12:.1f} TFLOP/s on the matrix cores; search kernel: "
-            f"{search_bytes / 1e6:.1f} MB (re-ranked {rerank}, traversal evaluations {D - NE}, ENC entries {S}), "
-            f"{a_search:.0f} GB/s; dominant {dominant} {achieved / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s; "
-            f"forgetful-table evaluations x{overhead:.3f}")
+            dominant = "s_pool_kernel+s_search_kernel"
+            roof = {"bound": "hbm", "kernel": dominant, "achieved": a_search, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": a_search / HBM_PEAK_GBS, "alg_bytes_per_launch": search_bytes,
+                    "kernel_ms": t_b * 1e3}
+        log(f"entry scan: {NE} sample points, {scan_rows} tile rows (occupancy {occupancy:.3f}), useful "
+            f"{scan_tf:.1f} TFLOP/s = {scan_tf / FP32_MFMA_PEAK_TFLOPS * 100:.1f}% of the fp32 matrix peak "
+            f"(issued {issued / t_a / 1e12:.1f}); pool + traversal {search_bytes / 1e6:.1f} MB algorithmic "
+            f"(re-ranked {rerank}, traversal evaluations {D - NE}, ENC entries {S}) = {a_search:.0f} GB/s "
+            f"({a_search / HBM_PEAK_GBS * 100:.1f}% of 8 TB/s); forgetful-table evaluations x{overhead:.3f}")
 
     # HBM traffic of the dominant kernel from the committed rocprofv3
     # counters, if they were taken on this source, workload and setting
-    traffic = None
+    roof["traffic"] = None
     sha = source_sha()
-    if os.path.exists(TRAFFIC_FILE):
+    if os.path.exists(TRAFFIC_FILE) and wl == "c2":
         tf = json.load(open(TRAFFIC_FILE))
         if (tf.get("source_sha") == sha and tf.get("n") == n and tf.get("nq") == w.nq
                 and tf.get("storage", "fp32") == args.storage):
             for ent in tf.get("settings", []):
                 names = dominant.split("+")
-                if norm_setting(ent["setting"]) == (L, epn, frac, emax, B, mode, ni) and all(
-                        x in ent["kernels"] for x in names):
-                    traffic = sum(1024.0 * (ent["kernels"][x]["fetch_kib"] * tf["fetch_factor"]
-                                            + ent["kernels"][x]["write_kib"] * tf["write_factor"]) for x in names)
+                if norm_setting(ent["setting"]) == sel and all(x in ent["kernels"] for x in names):
+                    roof["traffic"] = sum(1024.0 * (ent["kernels"][x]["fetch_kib"] * tf["fetch_factor"]
+                                                    + ent["kernels"][x]["write_kib"] * tf["write_factor"])
+                                          for x in names)
 
-    # per selectivity band: each octave of the mixed batch re-run as a batch of
-    # its own (smaller batches, so lower QPS than the mixed batch)
-    per_band = []
-    for b in range(10):
-        sel = np.nonzero(band == b)[0]
-        if len(sel) == 0:
-            continue
-        sel_t = torch.as_tensor(sel, device=dev)
-        Qb, lob, hib = Q[sel_t].contiguous(), lo[sel_t].contiguous(), hi[sel_t].contiguous()
-        fb = lambda: F.search(ix, Qb, lob, hib, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                              entry_mode=mode, hash_log2=args.hash_log2, query_base=0)
-        idb, _ = fb()
-        torch.cuda.synchronize()
-        tb = timed(fb, 5)
-        # the exhaustive filtered search of the same batch: the pre-filter
-        # baseline at recall 1
-        # (fp32 rows only: with a 16-bit --storage every index holds 16-bit rows)
-        tbf = None
-        if args.storage == "fp32":
-            fbf = lambda: F.bruteforce(ix, Qb, lob, hib, k)
-            fbf()
-            tbf = timed(fbf, 2)
-        per_band.append(dict(band=f"[2^-{b + 1}, 2^-{b}]", nq=int(len(sel)), qps=len(sel) / tb, ms=tb * 1e3,
-                             recall_in_mixed_batch=chosen["recall_band"][b],
-                             bruteforce_qps=len(sel) / tbf if tbf else None,
-                             bruteforce_ms=tbf * 1e3 if tbf else None))
-    log("per band (own batch), FROG / brute force: " +
-        ", ".join(f"{r['band']} {r['qps'] / 1e6:.2f}M/" +
-                  (f"{r['bruteforce_qps'] / 1e6:.3f}M" if r['bruteforce_qps'] else "-") for r in per_band))
+    # ------------------------------------------------------------------ fixed selectivities
+    # the paper's three fixed-selectivity settings on full batches of their
+    # own: the chosen setting, the fastest sweep setting on the chosen index
+    # reaching recall 0.9, and the brute force (the pre-filter baseline,
+    # recall 1)
+    fixed = None
+    if wl == "c2" and not args.no_fixed and args.n is None:
+        fixed = []
+        # the chosen index's sweep settings, plus larger entry caps (the widest
+        # ranges hold the most clusters, which a query must sample into)
+        same_index = [s for s in settings if s[6] == ni and s[0] >= k]
+        same_index += [x for x in (norm_setting((32, 16, 1.0, e, b, 1, ni)) for e, b in
+                                   ((4096, 16), (6144, 16), (8192, 16), (8192, 24)))
+                       if x not in same_index]
+        for sig in FIXED_SIGMAS:
+            qf, lof_np, hif_np, _ = workloads.more_queries(w, "fixed", w.nq, sigma=sig)
+            Qf, lof, hif = (torch.as_tensor(qf, device=dev), torch.as_tensor(lof_np, device=dev),
+                            torch.as_tensor(hif_np, device=dev))
+            if args.storage != "fp32":
+                ix.upload(0)
+            gtf = F.bruteforce(ix, Qf, lof, hif, k)[0].cpu().numpy()
+            tbf = timed(lambda: F.bruteforce(ix, Qf, lof, hif, k), 2, warm=1)
+            if args.storage != "fp32":
+                ix.upload(0, storage=args.storage)
+            per = []
+            for s in same_index:
+                ids_f, _ = run(s, Qf, lof, hif)
+                torch.cuda.synchronize()
+                rec_f = float(recall_at_k(ids_f.cpu().numpy(), gtf).mean())
+                tf_ = timed(lambda: run(s, Qf, lof, hif), 5)
+                per.append(dict(zip(SETTING_KEYS, s), recall=rec_f, qps=len(qf) / tf_))
+            at_sel = next(r for r in per if key(r) == sel)
+            okf = [r for r in per if r["recall"] >= 0.9]
+            bestf = max(okf, key=lambda r: r["qps"]) if okf else max(per, key=lambda r: r["recall"])
+            fixed.append(dict(sigma=sig, nq=len(qf), chosen_setting=at_sel,
+                              fastest_at_recall_0_9=bestf if okf else None,
+                              best_recall=None if okf else bestf, bruteforce_qps=len(qf) / tbf))
+            log(f"fixed sigma 2^{math.log2(sig):.0f}: chosen setting recall {at_sel['recall']:.4f} "
+                f"{at_sel['qps'] / 1e6:.2f}M QPS; fastest at recall >= 0.9: "
+                + (f"{bestf['qps'] / 1e6:.2f}M QPS (L={bestf['L']} max={bestf['epn_max']} B={bestf['budget']} "
+                   f"mode={bestf['entry_mode']})" if okf else "none")
+                + f"; brute force {len(qf) / tbf / 1e6:.3f}M QPS")
 
-    # 16-bit rows (the paper keeps the vectors in half precision, Sec 8.1):
-    # the same host index uploaded with its rows rounded to binary16, then to
-    # bfloat16, the sweep's shared-sample settings, recall against the fp32
-    # ground truth
+    # per band of a fixed-band workload (c5): each band's queries as a batch
+    per_band = None
+    if wl == "c5":
+        per_band = []
+        for sig in np.unique(w.sigma):
+            selq = np.nonzero(w.sigma == sig)[0]
+            sel_t = torch.as_tensor(selq, device=dev)
+            Qb, lob, hib = Q[sel_t].contiguous(), lo[sel_t].contiguous(), hi[sel_t].contiguous()
+            idb, _ = run(sel, Qb, lob, hib)
+            torch.cuda.synchronize()
+            idb = idb.cpu().numpy()
+            tb = timed(lambda: run(sel, Qb, lob, hib), 5)
+            per_band.append(dict(sigma=float(sig), nq=int(len(selq)), qps=len(selq) / tb,
+                                 recall=float(recall_at_k(idb, gt_ids[selq]).mean()),
+                                 recall_at_10=float(recall_at_k(idb, gt_ids[selq], 10).mean())))
+            log(f"band sigma={sig}: {len(selq)} queries, {len(selq) / tb / 1e6:.3f}M QPS, recall@{k} "
+                f"{per_band[-1]['recall']:.4f}, recall@10 {per_band[-1]['recall_at_10']:.4f}")
+
+    # ------------------------------------------------------------------ 16-bit rows
+    # the paper keeps the vectors in half precision (Sec 8.1.4): the same host
+    # index uploaded with its rows rounded to binary16, then to bfloat16, at
+    # the sweep's shared-sample settings on the chosen index
     half = {"fp16": None, "bf16": None}
     for sto, desc in (("fp16", "fp16 rows (binary16, nearest even)"), ("bf16", "bf16 rows (bfloat16, nearest even)")):
-        if args.no_16bit or args.storage != "fp32":
+        if args.no_16bit or args.storage != "fp32" or d > 128 or wl != "c2":
             break
         ix.upload(0, storage=sto)
         hrows = []
-        for (Lh, eh, fh, mh, Bh, modeh, nih) in [norm_setting(x) for x in SWEEP]:
-            if modeh != 1 or Lh < k or nih != ni:
-                continue
-            fh_run = lambda: F.search(ix, Q, lo, hi, k, Lh, epn=eh, epn_frac=fh, epn_max=mh, budget=Bh,
-                                      entry_mode=1, hash_log2=args.hash_log2)
-            ids_h, _ = fh_run()
+        for s in [x for x in settings if x[5] == 1 and x[0] >= k and x[6] == ni]:
+            ids_h, _ = run(s)
             torch.cuda.synchronize()
             rec_h = recall_at_k(ids_h.cpu().numpy(), gt_ids)
-            fh_run()
-            th = timed(fh_run, 5)
-            hrows.append(dict(L=Lh, epn=eh, epn_frac=fh, epn_max=mh, budget=Bh, entry_mode=1,
-                              recall=float(rec_h.mean()), qps=w.nq / th, ms=th * 1e3))
-            log(f"{sto} rows: L={Lh:4d} max={mh:5d} B={Bh:2d}  recall={rec_h.mean():.4f}  {th * 1e3:8.3f} ms  "
+            th = timed(lambda: run(s), 5)
+            hrows.append(dict(zip(SETTING_KEYS, s), recall=float(rec_h.mean()), qps=w.nq / th, ms=th * 1e3))
+            log(f"{sto} rows: L={s[0]:4d} max={s[3]:5d} B={s[4]:2d}  recall={rec_h.mean():.4f}  {th * 1e3:8.3f} ms  "
                 f"{w.nq / th:12.0f} QPS")
         okh = [r for r in hrows if r["recall"] >= 0.9]
         best = max(okh, key=lambda r: r["qps"]) if okh else max(hrows, key=lambda r: r["recall"])
-        # phase split of the best setting: entry scan, then pool + search
         reps = 10
         ph = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
         for trio in ph:
@@ -474,34 +744,31 @@ def main():
                 ev.record(stream)
         torch.cuda.synchronize()
         for i in range(reps):
-            F.search(ix, Q, lo, hi, k, best["L"], epn=best["epn"], epn_frac=best["epn_frac"],
-                     epn_max=best["epn_max"], budget=best["budget"], entry_mode=1, hash_log2=args.hash_log2,
-                     events=ph[i])
+            run(key(best), events=ph[i])
         torch.cuda.synchronize()
         ha = sum(t[0].elapsed_time(t[1]) for t in ph) / 1000.0 / reps
         hb = sum(t[1].elapsed_time(t[2]) for t in ph) / 1000.0 / reps
         half[sto] = {"storage": desc + ", fp32 queries, fp64-accumulated distances",
-                     "best": best, "recall_target_met": bool(okh), "vs_fp32_value": best["qps"] / qps,
+                     "best": best, "recall_target_met": bool(okh),
+                     "vs_fp32_resident": best["qps"] / (w.nq / per_step_res),
                      "entry_scan_ms": ha * 1e3, "search_ms": hb * 1e3, "sweep": hrows}
         log(f"{sto} rows: best L={best['L']} max={best['epn_max']} B={best['budget']} recall={best['recall']:.4f} "
-            f"{best['qps']:.0f} QPS (x{best['qps'] / qps:.2f} of fp32); entry scan {ha * 1e3:.3f} ms, "
-            f"search {hb * 1e3:.3f} ms")
+            f"{best['qps']:.0f} QPS; entry scan {ha * 1e3:.3f} ms, search {hb * 1e3:.3f} ms")
         ix.upload(0)
 
-    # ablations (Sec 8.2.3) at the chosen setting
+    # ------------------------------------------------------------------ ablations (Sec 8.2.3)
     ablation = None
     if args.ablation:
         ablation = []
 
         def abl(name, hm=0, eager=0, hl2=args.hash_log2, index=ix):
-            f = lambda: F.search(index, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                                 entry_mode=mode, hash_log2=hl2, hotspot_mode=hm, eager_check=eager)
+            pa = dict(params(sel), hash_log2=hl2, hotspot_mode=hm, eager_check=eager)
+            f = lambda: F.search(index, Q, lo, hi, k, L, **pa)
             ids_a, _ = f()
             torch.cuda.synchronize()
             rec_a = recall_at_k(ids_a.cpu().numpy(), gt_ids)
             ta = timed(f, 5)
-            _, _, st_a = F.search(index, Q, lo, hi, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                                  entry_mode=mode, hash_log2=0, hotspot_mode=hm, eager_check=eager, stats=True)
+            _, _, st_a = F.search(index, Q, lo, hi, k, L, stats=True, **dict(pa, hash_log2=0))
             st_a = st_a.cpu().numpy().astype(np.int64)
             row = dict(variant=name, hash_log2=hl2, recall=float(rec_a.mean()), qps=w.nq / ta, ms=ta * 1e3,
                        expansions=float(st_a[:, F.STAT_EXPANSIONS].mean()),
@@ -525,24 +792,24 @@ def main():
         abl("beta = 0 (no attribute fusion)", index=ix0)
         ix0.free()
 
-    # sensitivity (Sec 8.2.5 for beta and gamma; n_inv, B and the entry cap likewise): construction parameters through GPU rebuilds, the
-    # expansion budget and the entry-point cap at query time, each around the
-    # chosen setting with the others at their defaults
+    # ------------------------------------------------------------------ sensitivity
+    # construction parameters through GPU rebuilds (beta and gamma: Sec 8.2.5;
+    # n_inv likewise), the expansion budget and the entry-point cap at query
+    # time, each around the chosen setting with the others at their defaults
     sensitivity = None
     if args.sweep_params:
         sensitivity = []
-
         base_ix = indexes[default_ninv]
 
-        def measure(index, Lx=L, Bx=B, emx=emax):
-            f = lambda: F.search(index, Q, lo, hi, k, Lx, epn=epn, epn_frac=frac, epn_max=emx, budget=Bx,
-                                 entry_mode=mode, hash_log2=args.hash_log2)
+        def measure(index, Bx=B, emx=emax):
+            pm = dict(params(sel), budget=Bx, epn_max=emx)
+            f = lambda: F.search(index, Q, lo, hi, k, L, **pm)
             ids_s, _ = f()
             torch.cuda.synchronize()
             rec_s = float(recall_at_k(ids_s.cpu().numpy(), gt_ids).mean())
             return rec_s, w.nq / timed(f, 5)
 
-        defaults = dict(beta=0.2, gamma=0.5, n_inv=7)
+        defaults = dict(beta=0.2, gamma=0.5, n_inv=default_ninv)
         grid = [("default", None)] + [("beta", v) for v in (0.0, 0.1, 0.3, 0.5)] + \
                [("gamma", v) for v in (0.25, 1.0, 2.0)] + [("n_inv", v) for v in (5, 6, 8, 9)]
         for name, v in grid:
@@ -565,10 +832,10 @@ def main():
             sensitivity.append(dict(param="epn_max", value=emx, recall=rec_s, qps=qps_s))
             log(f"sensitivity epn_max={emx}: recall={rec_s:.4f}, {qps_s:.0f} QPS")
 
-    # the ceiling of Sec 8's comparison: per query, an index built over the
-    # in-range objects only (an "oracle" proximity graph for that range),
-    # searched over its whole domain with the same pool size and budget,
-    # against FROG's one index; a sample of queries per selectivity
+    # ------------------------------------------------------------------ oracle-PG ceiling
+    # per query, an index built over the in-range objects only (an "oracle"
+    # proximity graph for that range, Sec 8.2.6), searched over its whole
+    # domain with the same setting, against FROG's one index
     oracle_pg = None
     if args.oracle_pg:
         oracle_pg = []
@@ -581,18 +848,16 @@ def main():
         for sig in (0.001, 0.01, 0.1, 0.5):
             cnt_pg = max(int(round(sig * n_pg)), 1)
             rec_f, rec_o = [], []
-            for qn in rng_pg.choice(w.nq, 64, replace=False):
+            for qn1 in rng_pg.choice(w.nq, 64, replace=False):
                 st = int(rng_pg.integers(0, n_pg - cnt_pg + 1))
                 lo_v, hi_v = float(As[st]), float(As[st + cnt_pg - 1])
-                q1 = torch.as_tensor(w.Q[qn:qn + 1], device=dev)
+                q1 = torch.as_tensor(w.Q[qn1:qn1 + 1], device=dev)
                 lo1 = torch.tensor([lo_v], dtype=torch.float64, device=dev)
                 hi1 = torch.tensor([hi_v], dtype=torch.float64, device=dev)
                 gt1, _, _ = F.bruteforce(ixf, q1, lo1, hi1, k)
-                f1, _ = F.search(ixf, q1, lo1, hi1, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                                 entry_mode=1)
+                f1, _ = F.search(ixf, q1, lo1, hi1, k, L, **params(sel))
                 ixo = F.Index.build(Xs[st:st + cnt_pg], As[st:st + cnt_pg], device=0)
-                o1, _ = F.search(ixo, q1, lo1, hi1, k, L, epn=epn, epn_frac=frac, epn_max=emax, budget=B,
-                                 entry_mode=1)
+                o1, _ = F.search(ixo, q1, lo1, hi1, k, L, **params(sel))
                 torch.cuda.synchronize()
                 ixo.free()
                 gt_set = set(gt1.cpu().numpy()[0].tolist()) - {-1}
@@ -609,7 +874,9 @@ def main():
                 f"{np.mean(rec_o):.4f} (n={n_pg}, 64 queries, L={L})")
         ixf.free()
 
-    # CPU oracle on a bounded sample (same index arrays, same parameters)
+    # ------------------------------------------------------------------ CPU oracle
+    # the oracle's FROGSearch on a bounded sample (same index arrays, same
+    # parameters) on every host thread, and on one thread for 200 queries
     cpu = None
     try:
         import oracle
@@ -622,32 +889,32 @@ def main():
             Xr = np.ldexp(np.rint(mant * 256.0) / 256.0, ex).astype(np.float32)
         ox = oracle.OracleIndex(arrs["perm"], arrs["attr_sorted"], Xr, arrs["ENC"])
         threads = oracle.default_threads()
+
+        def ocall(a, b, th):
+            oracle.search(ox, w.Q[a:b], w.lo[a:b], w.hi[a:b], k, L, epn=epn, epn_frac=frac, epn_max=emax, B=B,
+                          entry_mode=mode, threads=th, qidx=np.arange(a, b))
+
         probe = min(200, w.nq)
         t0 = time.time()
-        oracle.search(ox, w.Q[:probe], w.lo[:probe], w.hi[:probe], k, L, epn=epn, epn_frac=frac,
-                      epn_max=emax, B=B, entry_mode=mode, threads=threads)
+        ocall(0, probe, 1)
+        t1 = max(time.time() - t0, 1e-3)
+        one = {"value": probe / t1, "queries": probe, "s": t1}
+        t0 = time.time()
+        ocall(0, probe, threads)
         tp = max(time.time() - t0, 1e-3)
         ns = int(min(w.nq, max(probe, probe * args.cpu_seconds / tp)))
-        reps = 1
         if ns > probe:
             t0 = time.time()
-            oracle.search(ox, w.Q[:ns], w.lo[:ns], w.hi[:ns], k, L, epn=epn, epn_frac=frac,
-                          epn_max=emax, B=B, entry_mode=mode, threads=threads)
+            ocall(0, ns, threads)
             tp = time.time() - t0
-            # the whole batch takes less than the target: repeat it
-            reps = max(1, min(100, int(args.cpu_seconds / max(tp, 1e-3))))
-            if ns == w.nq and reps > 1:
-                t0 = time.time()
-                for _ in range(reps):
-                    oracle.search(ox, w.Q, w.lo, w.hi, k, L, epn=epn, epn_frac=frac, epn_max=emax,
-                                  B=B, entry_mode=mode, threads=threads)
-                tp = (time.time() - t0) / reps
-            else:
-                reps = 1
+        else:
+            ns = probe
         what = f"first {ns} of the {w.nq} queries" if ns < w.nq else f"all {w.nq} queries"
         cpu = {"value": ns / tp, "unit": "queries/s", "cores": threads, "kind": "oracle",
-               "sample": f"{what}, same index and setting, {reps} pass(es), {tp * reps:.1f}s"}
-        log(f"cpu oracle: {ns} queries x {reps} in {tp * reps:.1f}s on {threads} threads = {ns / tp:.0f} QPS")
+               "sample": f"{what}, same index and setting, {tp:.1f}s", "cpu_model": cpu_model(),
+               "one_thread": one}
+        log(f"cpu oracle: {ns} queries in {tp:.1f}s on {threads} threads = {ns / tp:.0f} QPS; one thread, "
+            f"{probe} queries in {t1:.1f}s = {probe / t1:.0f} QPS ({cpu_model()})")
     except Exception as ex:  # the oracle is optional on the timing path
         log(f"cpu oracle skipped: {ex}")
     # the oracle's exhaustive filtered k-NN on a bounded sample of the same
@@ -674,62 +941,73 @@ def main():
     except Exception as ex:
         log(f"cpu exhaustive oracle skipped: {ex}")
 
+    # ------------------------------------------------------------------ the line
+    desc = {"c2": "Gaussian mixture (1000 centres, noise 0.3), random-permutation attribute, selectivity "
+                  "log-uniform [2^-10,1]",
+            "c3": "Gaussian mixture (500 centres, noise 0.5), random-permutation attribute, selectivity "
+                  "log-uniform [2^-10,1]",
+            "c4": "unit-normalised Gaussian mixture (2000 centres, noise 0.3), attribute = rank of a random "
+                  "projection, selectivity log-uniform [2^-12,1]",
+            "c5": "Gaussian mixture (1000 centres, noise 0.3), random-permutation attribute, fixed selectivities "
+                  "0.1%/1%/10%/50%/100%"}[wl]
+    metric = METRIC if wl == "c2" else f"filtered QPS at recall@{k}≥0.9, {wl}: n={n} d={d} fp32"
     result = {
-        "metric": METRIC,
+        "metric": metric,
         "value": qps if met else None,
         "unit": "queries/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": per_step * 1e3,
+        "ms_per_step_median": per_step_med * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32" if args.storage == "fp32" else f"{args.storage} rows, f32 queries, f64 accumulation",
         "data": "synthetic",
         "config": {
-            "workload": f"{w.name}: n={n} d={d} Gaussian mixture (1000 centres, noise 0.3), "
-                        f"random-permutation attribute, {w.nq} queries, selectivity log-uniform "
-                        f"[2^-10,1], k={k}",
+            "workload": f"{wl}: n={n} d={d} {desc}, {w.nq} queries, k={k}",
+            "step": "H2D of queries and ranges from pinned host memory, one search call, D2H of ids and "
+                    "distances, in order on one stream (Sec 8.1.3 query time); index resident",
             "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": B, "entry_mode": mode,
-            "hash_log2": args.hash_log2, "recall@10": chosen["recall"], "recall_target_met": met,
+            "hash_log2": args.hash_log2, f"recall@{k}": chosen["recall"],
+            "recall_held_out": chosen.get("recall_held_out"), "recall_target_met": met, "choice": how,
             "index": {"n_inv": ni, "H": H, "m": m, "paper_default_n_inv": default_ninv,
-                      "built": "host" if ni == default_ninv else "GPU (frog_build_index_gpu)",
-                      "host_build_s": round(t_build, 1)},
-            "pool_sizes_named": sorted(HEADLINE_L),
+                      "built": "host" if (ni == default_ninv and not gpu_only) else "GPU (frog_build_index_gpu)",
+                      "host_build_s": None if t_build is None else round(t_build, 1)},
+            "pool_sizes_named": sorted(HEADLINE_L[wl]),
+            # the sampled entry points' share of the method's bytes (the rest
+            # is the graph traversal)
+            "entry_points_share_of_method_bytes": eb * d * NE / max(method_bytes, 1.0),
+            "fastest_sweep_setting": best_sweep,
             "fastest_any_pool_size": fastest_any,
         },
-        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "alg_bytes_per_launch": alg_bytes, "kernel_ms": t_kernel * 1e3,
-                     "step_achieved": alg_bytes / per_step / 1e9},
+        "resident": {"qps": w.nq / per_step_res, "ms_per_step": per_step_res * 1e3,
+                     "what": "the same search with queries, ranges and results kept in HBM (kernels only)"},
+        "overlapped": {"qps": w.nq / per_step_pipe, "ms_per_step": per_step_pipe * 1e3,
+                       "what": "the same steps with transfers, the next batch's copy in and the previous batch's "
+                               "copy out on a second stream during the search"},
+        "roofline": roof,
         "phases": phases,
         "cpu_baseline": cpu,
         "cpu_exact": cpu_exact,
-        # the exhaustive filtered search as the pre-filter baseline: recall 1
-        # (certified), queries per second of the same batch
-        # the same search with the rows stored in fp16 and in bf16
-        # (secondary; the metric above is fp32)
+        "fixed_selectivity": fixed,
+        "per_band": per_band,
         "fp16_storage": half["fp16"],
         "bf16_storage": half["bf16"],
         # index construction (Sec 6) on the GPU, wall time including the host
         # sort and the copies, against the host construction
         "gpu_build": gpu_build,
+        # the exhaustive filtered search: ground truth and pre-filter baseline
         "bruteforce": {"ms": bf_time * 1e3, "qps": w.nq / bf_time, "recall@10": 1.0,
                        "useful_tflops": bf_flops / bf_time / 1e12,
                        "mfma_frac": bf_flops / bf_time / 1e12 / FP32_MFMA_PEAK_TFLOPS,
-                       "certified": float(cert.mean()),
-                       # each selectivity band as its own batch: FROG at the
-                       # chosen setting against the brute force (recall 1)
-                       "per_band": [{"band": r["band"], "frog_qps": r["qps"], "bruteforce_qps": r["bruteforce_qps"]}
-                                    for r in per_band]},
+                       "certified_by_margin": float((cert == 1).mean())},
     }
     if args.details:
         with open(args.details, "w") as f:
-            json.dump(dict(result=result, sweep=rows, per_band=per_band, ablation=ablation, sensitivity=sensitivity,
-                           oracle_pg=oracle_pg,
-                           alg_bytes=alg_bytes,
-                           source_sha=sha,
+            json.dump(dict(result=result, sweep=rows, ablation=ablation, sensitivity=sensitivity,
+                           oracle_pg=oracle_pg, method_bytes=method_bytes, source_sha=sha,
                            eval_overhead=float(overhead),
                            mean_stats_exact=st_e.mean(0).tolist(),
                            mean_stats_timed=st_f.mean(0).tolist()), f, indent=1, default=_plain)

@@ -23,7 +23,8 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["build_index.cpp"]
-HIP_SOURCES = ["capi.cpp", "search.hip", "bruteforce.hip", "build_gpu.hip"]
+HIP_SOURCES = ["capi.cpp", "search.hip", "search_shared.hip", "search_scan.hip", "search_pool.hip", "search_trav.hip",
+               "exact.hip", "bruteforce.hip", "build_gpu.hip"]
 
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
@@ -48,7 +49,7 @@ def _compile_one(src, obj, verbose):
     _run(cmd, verbose)
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
+def build(verbose: bool = False, jobs: int = 8) -> str:
     """Compile every source (always) and link libfrog.so; returns its path."""
     os.makedirs(OBJ, exist_ok=True)
     objs = []

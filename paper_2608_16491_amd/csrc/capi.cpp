@@ -533,10 +533,16 @@ int frog_rank_bounds(const frog_index_t* ix, const double* d_lo, const double* d
     return frog::launch_rank_bounds(view(ix), d_lo, d_hi, nq, d_lr, stream);
 }
 
-int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo,
-                   const double* d_hi, int k, int L, const frog_search_params_t* p, int32_t* d_ids,
-                   float* d_dists, int32_t* d_stats, void* stream) {
-    frog::clear_error();
+}  // extern "C"
+
+namespace {
+
+// Validation and argument marshalling shared by frog_search_ex and
+// the other search entry points; on FROG_OK with *empty == false, *a is ready to launch.
+int search_args(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo, const double* d_hi,
+                int k, int L, const frog_search_params_t* p, int32_t* d_ids, float* d_dists, int32_t* d_stats,
+                frog::SearchLaunch* out, bool* empty) {
+    *empty = true;
     int rc = check_device_index(ix);
     if (rc) return rc;
     frog_search_params_t q;
@@ -560,7 +566,8 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
         return fail(FROG_EUNSUPPORTED, "no search kernel for padded d=%d, m=%d, L=%d", ix->dp, ix->m, L);
     if (nq == 0) return FROG_OK;
     if (!d_queries || !d_lo || !d_hi || !d_ids || !d_dists) return fail(FROG_EINVAL, "NULL device pointer");
-    frog::SearchLaunch a{};
+    frog::SearchLaunch& a = *out;
+    a = frog::SearchLaunch{};
     a.Q = d_queries; a.nq = nq; a.lo = d_lo; a.hi = d_hi; a.k = k; a.L = L;
     a.epn = q.epn; a.epn_max = q.epn_frac > 0.0 ? q.epn_max : q.epn; a.epn_frac = q.epn_frac;
     a.B = q.budget; a.hash_log2 = q.hash_log2; a.seed = q.seed; a.qbase = q.query_base;
@@ -576,6 +583,22 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
         rc = frog::find_sample(ix, q.seed, &a.lv, &a.maxnorm);
         if (rc) return rc;
     }
+    *empty = false;
+    return FROG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo,
+                   const double* d_hi, int k, int L, const frog_search_params_t* p, int32_t* d_ids,
+                   float* d_dists, int32_t* d_stats, void* stream) {
+    frog::clear_error();
+    frog::SearchLaunch a;
+    bool empty = true;
+    const int rc = search_args(ix, d_queries, nq, d_lo, d_hi, k, L, p, d_ids, d_dists, d_stats, &a, &empty);
+    if (rc || empty) return rc;
     return frog::launch_search(view(ix), a, stream);
 }
 

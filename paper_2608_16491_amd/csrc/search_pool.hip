@@ -1,0 +1,187 @@
+// FROGSearch, entry mode 1: each query's pool from its tile's scan lists
+// (exact re-rank, margin test).
+
+#include "search_shared.h"
+
+namespace frog {
+namespace {
+
+// The pool of each query: one wavefront per query.
+template <int C, int LP, int KK, typename XT = float>
+__global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
+    using namespace topk;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const DevIndex& ix = P.ix;
+    const SearchLaunch& A = P.a;
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    WaveLds<LP> W(smem, P.lds_per_wave, 0);
+    char* lbase = smem + (size_t)wave * P.lds_per_wave + P.lds_list;
+    // KK: entries of each chunk list the scan left (their stride); the merged
+    // list keeps kkeep >= 64 of them (an offer of 64 fits after a cut)
+    constexpr int kkeep = KK > 64 ? KK : 64;
+    const BufList Lst{reinterpret_cast<uint64_t*>(lbase), reinterpret_cast<int32_t*>(lbase + (size_t)2 * kkeep * 8)};
+    const double u_round = 5.9604644775390625e-08;   // 2^-24
+
+    {
+        const int64_t qi = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+        if (qi >= A.nq) return;   // wave-uniform; no workgroup barrier follows
+        const SPlan p = P.plan[qi];
+        if (p.l > p.r) return;
+        QueryCtx<C, XT> Q;
+        Q.load(ix, A, P.lr, qi);
+        Q.load_vector(ix);
+        Q.shared = true;
+        Q.T = p.T;
+        Q.pkey = A.lv.key;
+
+        // the kkeep smallest approximate distances over the tile's lists
+        buf_init(Lst);
+        const int64_t t = p.tslot / kSQ;
+        const int slot = p.tslot % kSQ;
+        float texcl = __int_as_float(0x7f800000);   // every row left out is at or above this
+        // the chunks' fill, threshold and sample count in lanes 0..7, then
+        // all their entries at once (no round trip between chunks)
+        int mf = 0, mc = 0;
+        float mt = __int_as_float(0x7f800000);
+        if (lane < kSChunks) {
+            const int64_t base = (t * kSChunks + lane) * kSQ + slot;
+            mf = P.pfill[base];
+            mt = P.pthr[base];
+            mc = P.pcnt[base];
+        }
+        int64_t ne = 0;
+#pragma unroll
+        for (int o = 1; o < kSChunks; o <<= 1) {
+            mc += __shfl_xor(mc, o);
+            mt = fminf(mt, __shfl_xor(mt, o));
+        }
+        ne = uniform(mc);
+        texcl = __int_as_float(uniform(__float_as_int(mt)));
+        constexpr int kR = KK > 64 ? KK / 64 : 1;   // entries per lane and chunk
+        float av[kSChunks][kR];
+        int32_t rw[kSChunks][kR];
+#pragma unroll
+        for (int c = 0; c < kSChunks; ++c) {
+            const int fi = __builtin_amdgcn_readlane(mf, c);
+            const int64_t base = (t * kSChunks + c) * kSQ + slot;
+#pragma unroll
+            for (int r = 0; r < kR; ++r) {
+                const int j = r * 64 + lane;
+                av[c][r] = j < fi ? P.pv[base * KK + j] : __int_as_float(0x7f800000);
+                rw[c][r] = j < fi ? P.pr[base * KK + j] : -1;
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < kSChunks; ++c) {
+#pragma unroll
+            for (int r = 0; r < kR; ++r) {
+                const uint64_t gm = ballot(rw[c][r] >= 0 && av[c][r] < __int_as_float(Lst.st[1]));
+                if (gm) buf_offer<kkeep>(Lst, gm, av[c][r], rw[c][r]);
+            }
+        }
+        buf_cut<kkeep>(Lst);
+        texcl = fminf(texcl, __int_as_float(Lst.st[1]));
+        const int f = uniform(Lst.st[0]);
+
+        // exact distances of the kept rows: the pool of the L nearest
+        Pool<LP> pool;
+#pragma unroll
+        for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+        pool.np = 0;
+        if (f <= 64) {
+            // one key per lane: a bitonic sort over the wavefront, the first L are the pool
+            const int32_t id = lane < f ? (int32_t)(uint32_t)Lst.key[lane] : 0;
+            const float dd = Q.eval_batch(ix, f, id);
+            uint64_t key = lane < f ? make_key(dd, id) : kEmpty;
+#pragma unroll
+            for (int kb = 2; kb <= 64; kb <<= 1) {
+#pragma unroll
+                for (int jb = kb >> 1; jb > 0; jb >>= 1) {
+                    const uint64_t other = (uint64_t)__shfl_xor((long long)key, jb);
+                    const bool up = (lane & kb) == 0;
+                    const bool low = (lane & jb) == 0;
+                    key = (low == up) ? (other < key ? other : key) : (other > key ? other : key);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < LP; ++s) pool.key[s] = (s == 0 && lane < A.L) ? key : kEmpty;
+            pool.np = f < A.L ? f : A.L;
+        } else {
+            for (int j0 = 0; j0 < f; j0 += 64) {
+                const int nb = f - j0 < 64 ? f - j0 : 64;
+                const int32_t id = lane < nb ? (int32_t)(uint32_t)Lst.key[j0 + lane] : 0;
+                const float dd = Q.eval_batch(ix, nb, id);
+                merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
+            }
+        }
+        // margin test: a row left out has exact distance >= texcl - eps
+        bool certified = true;
+        if (!(texcl == __int_as_float(0x7f800000))) {
+            certified = false;
+            if (pool.np >= A.L) {
+                double qsq = 0.0;
+                for (int cc = lane; cc < ix.d; cc += 64) qsq += (double)Q.qrow[cc] * (double)Q.qrow[cc];
+#pragma unroll
+                for (int o = 32; o >= 1; o >>= 1) qsq += __shfl_xor(qsq, o);
+                const double eps = 2.0 * (2.0 * ix.d + 4.0) * u_round * (qsq + (double)A.maxnorm);
+                uint64_t lk = 0;
+#pragma unroll
+                for (int s = 0; s < LP; ++s)
+                    if (s == ((A.L - 1) >> 6)) lk = readlane64(pool.key[s], (A.L - 1) & 63);
+                const double dL = (double)__uint_as_float((uint32_t)(lk >> 32));
+                certified = (double)texcl - eps > dL;
+            }
+        }
+        certified = uniform(certified ? 1 : 0) != 0;
+        if (!certified) {
+            // every sample row, exactly
+#pragma unroll
+            for (int s = 0; s < LP; ++s) { pool.key[s] = kEmpty; pool.flag[s] = 0u; }
+            pool.np = 0;
+            ne = 0;
+            for (int64_t b0 = p.a; b0 < p.b; b0 += 64) {
+                const int64_t pos = b0 + lane;
+                const int32_t rk = pos < p.b ? level_rank(A.lv, p.lev, pos) : 0;
+                const bool in = pos < p.b && (p.all || s_priority(A.lv.key, rk) < p.T);
+                const uint64_t pm = ballot(in);
+                const int nb = __popcll(pm);
+                ne += nb;
+                if (nb == 0) continue;
+                if (in) W.enbuf[mbcnt(pm)] = rk;
+                wave_sync();
+                const int32_t id = lane < nb ? W.enbuf[lane] : 0;
+                wave_sync();
+                const float dd = Q.eval_batch(ix, nb, id);
+                merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < LP; ++s) P.pools[qi * 64 * LP + s * 64 + lane] = pool.key[s];
+        if (lane == 0) P.pne[qi] = (int32_t)ne;
+    }
+}
+
+template <int C, typename XT = float>
+void (*pick_s_pool_c(int L))(SParams) {
+    const int kk = shared_kkeep(L);
+    if (L <= 64) return kk == 64 ? s_pool_kernel<C, 1, 64, XT> : s_pool_kernel<C, 1, 128, XT>;
+    if (L <= 128) return kk == 128 ? s_pool_kernel<C, 2, 128, XT> : s_pool_kernel<C, 2, 256, XT>;
+    return s_pool_kernel<C, 4, 256, XT>;
+}
+
+}  // namespace
+
+void (*pick_s_pool(int dp, int L, int storage))(SParams) {
+    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_s_pool_c<2, __half>(L) : pick_s_pool_c<4, __half>(L);
+    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_s_pool_c<2, bf16x>(L) : pick_s_pool_c<4, bf16x>(L);
+    switch (dp) {
+        case 32: return pick_s_pool_c<1>(L);
+        case 64: return pick_s_pool_c<2>(L);
+        case 96: return pick_s_pool_c<3>(L);
+        case 128: return pick_s_pool_c<4>(L);
+        default: return pick_s_pool_c<0>(L);
+    }
+}
+
+}  // namespace frog

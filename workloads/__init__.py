@@ -31,6 +31,11 @@ available here; the synthetic mixtures stand in for them):
 
 ``n`` and ``nq`` may be overridden to make a smaller workload of the same
 structure (used for parity tests the oracle finishes in seconds).
+
+:func:`more_queries` draws further query batches over the same base set from
+the reserve stream: a held-out batch of the workload's own selectivity mix
+(to check a setting chosen on the main batch), and batches at one fixed
+selectivity.
 """
 from __future__ import annotations
 
@@ -38,7 +43,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["Workload", "make", "NAMES", "ranges_for_selectivity"]
+__all__ = ["Workload", "make", "NAMES", "ranges_for_selectivity", "more_queries"]
 
 NAMES = ("tiny", "c2", "c3", "c4", "c5")
 
@@ -164,3 +169,44 @@ def make(name: str, *, seed: int = 0, n: int | None = None, nq: int | None = Non
                         dict(kind="gaussian-mixture-unit", centres=2000, noise=0.3,
                              attribute="projection-rank", seed=seed))
     raise ValueError(f"unknown workload {name!r}; expected one of {NAMES}")
+
+
+# the reserve stream's children, by purpose
+_PURPOSE = {"held_out": 0, "fixed": 1}
+# mixture parameters of the workloads drawn from one (centres, noise, unit length)
+_MIXTURE = {"c2": (1000, 0.3, False), "c5": (1000, 0.3, False), "c3": (500, 0.5, False),
+            "c4": (2000, 0.3, True)}
+
+
+def more_queries(w: Workload, purpose: str, nq: int, *, sigma: float | None = None, seed: int = 0):
+    """Queries and ranges over the base set of ``w`` (made by :func:`make`
+    with the same seed), drawn from a child of the reserve stream that depends
+    on ``purpose`` ("held_out" or "fixed") and, for fixed batches, on sigma.
+    ``held_out``: the workload's own selectivity distribution; ``fixed``:
+    every range of selectivity ``sigma``.  Query vectors come from the same
+    mixture (the centres are the base stream's first draw).  Returns
+    (Q, lo, hi, sigma array)."""
+    if w.name not in _MIXTURE:
+        raise ValueError(f"more_queries: {w.name} is not a mixture workload")
+    centres, noise, unit = _MIXTURE[w.name]
+    ss = np.random.SeedSequence(seed).spawn(5)
+    base = np.random.Generator(np.random.PCG64(ss[0]))
+    C = base.standard_normal((centres, w.d), dtype=np.float32)
+    key = [_PURPOSE[purpose]] + ([] if sigma is None else [int(round(-np.log2(sigma) * 1000))])
+    child = np.random.SeedSequence(entropy=ss[4].entropy, spawn_key=tuple(ss[4].spawn_key) + tuple(key))
+    rq, rr = [np.random.Generator(np.random.PCG64(c)) for c in child.spawn(2)]
+    aq = rq.integers(0, centres, nq)
+    Q = rq.standard_normal((nq, w.d), dtype=np.float32)
+    Q *= np.float32(noise)
+    Q += C[aq]
+    if unit:
+        Q /= np.linalg.norm(Q, axis=1, keepdims=True).astype(np.float32)
+    if purpose == "fixed":
+        sig = np.full(nq, float(sigma))
+    elif w.name == "c5":
+        bands = np.array([0.001, 0.01, 0.10, 0.50, 1.00])
+        sig = bands[np.arange(nq) * len(bands) // nq]
+    else:
+        sig = _log_uniform(rr, nq, 12.0 if w.name == "c4" else 10.0)
+    lo, hi = ranges_for_selectivity(rr, sig, w.n)
+    return Q, lo, hi, sig
