@@ -237,6 +237,33 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
                    const frog_search_params_t* p, int32_t* d_ids, float* d_dists,
                    int32_t* d_stats, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): exactly
+ * frog_search_ex (same arguments, same results, same errors), except that the
+ * per-call workspace (work counters, rank intervals, chunk pools; in
+ * entry_mode 1 the plans, tiles, candidate lists and pools) lives in a fixed
+ * 64 MiB array of device memory inside the library instead of coming from
+ * hipMallocAsync.  Nothing is allocated or freed by this call.
+ *   - Each GPU the library runs on holds its own array until the process
+ *     ends; its address is looked up once per device, on the first call there.
+ *   - Every call on a GPU shares that GPU's array, and the array keeps the
+ *     last call's contents (the kernels clear what must start at zero):
+ *     calls that overlap on one GPU (other streams, other threads) race and
+ *     must be serialised by the caller.
+ *   - A call whose workspace exceeds 64 MiB is refused with FROG_EUNSUPPORTED
+ *     before anything is enqueued.  Roughly: entry_mode 0 needs 12 bytes per
+ *     query plus, when the entry count exceeds one 768-point chunk,
+ *     512 * ceil(L/64) bytes per chunk (about 2 KB per query at 2,560 entry
+ *     points and L <= 64); entry_mode 1 about 4.8 KB per query at L <= 56
+ *     (about 13,900 queries per call), 9.4 KB up to L = 120 and 18.6 KB up to
+ *     L = 248; the exact visited set (hash_log2 = 0) adds n/8 bytes per
+ *     resident wavefront and is refused at realistic n.
+ *   - entry_mode 1 needs the seed prepared (frog_index_prepare_sample). */
+int frog_search_noalloc(const frog_index_t* idx, const float* d_queries, int64_t nq,
+                        const double* d_lo, const double* d_hi, int k, int L,
+                        const frog_search_params_t* p, int32_t* d_ids, float* d_dists,
+                        int32_t* d_stats, void* stream);
+
 /* Exhaustive filtered k-NN (Def. 2, RFANNS): the exact k nearest objects whose
  * attribute lies in [lo, hi], by (distance, rank), padded with (-1, +inf).
  * The dot products q.x run on fp32 matrix cores; a per-query margin test

@@ -30,7 +30,8 @@ SYMBOLS = (
     "frog_index_from_arrays", "frog_index_export", "frog_index_info", "frog_index_save",
     "frog_index_load", "frog_index_upload", "frog_index_upload_ex", "frog_index_free",
     "frog_build_index_gpu", "frog_index_build_stats", "frog_rank_bounds", "frog_search",
-    "frog_search_ex", "frog_index_prepare_sample", "frog_bruteforce_filtered", "frog_last_error",
+    "frog_search_ex", "frog_search_noalloc", "frog_index_prepare_sample", "frog_bruteforce_filtered",
+    "frog_last_error",
 )
 
 
@@ -101,6 +102,8 @@ def lib() -> C.CDLL:
     L.frog_search.argtypes = [P, P, i64, P, P, i32, i32, P, P, P]
     L.frog_search_ex.restype = i32
     L.frog_search_ex.argtypes = [P, P, i64, P, P, i32, i32, C.POINTER(SearchParams), P, P, P, P]
+    L.frog_search_noalloc.restype = i32
+    L.frog_search_noalloc.argtypes = [P, P, i64, P, P, i32, i32, C.POINTER(SearchParams), P, P, P, P]
     L.frog_index_prepare_sample.restype = i32
     L.frog_index_prepare_sample.argtypes = [P, C.c_uint64]
     L.frog_bruteforce_filtered.restype = i32

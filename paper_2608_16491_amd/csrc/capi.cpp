@@ -602,6 +602,21 @@ int frog_search_ex(const frog_index_t* ix, const float* d_queries, int64_t nq, c
     return frog::launch_search(view(ix), a, stream);
 }
 
+int frog_search_noalloc(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo,
+                        const double* d_hi, int k, int L, const frog_search_params_t* p, int32_t* d_ids,
+                        float* d_dists, int32_t* d_stats, void* stream) {
+    frog::clear_error();
+    frog::SearchLaunch a;
+    bool empty = true;
+    int rc = search_args(ix, d_queries, nq, d_lo, d_hi, k, L, p, d_ids, d_dists, d_stats, &a, &empty);
+    if (rc || empty) return rc;
+    void* ws = nullptr;
+    size_t cap = 0;
+    rc = frog::scratch_area(&ws, &cap);
+    if (rc) return rc;
+    return frog::launch_search_ws(view(ix), a, stream, ws, cap);
+}
+
 int frog_search(const frog_index_t* ix, const float* d_queries, int64_t nq, const double* d_lo,
                 const double* d_hi, int k, int L, int32_t* d_ids, float* d_dists, void* stream) {
     return frog_search_ex(ix, d_queries, nq, d_lo, d_hi, k, L, nullptr, d_ids, d_dists, nullptr, stream);

@@ -156,6 +156,12 @@ float stored_maxnorm(const frog_index* ix);
 
 // search.hip
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream);
+// the same with the per-call workspace in caller-provided device memory of
+// ws_cap bytes (no allocation; FROG_EUNSUPPORTED if the call needs more)
+int launch_search_ws(const DevIndex& ix, const SearchLaunch& a, void* stream, void* ws, size_t ws_cap);
+// the library's fixed workspace array on the current device (its address,
+// taken once per device) and its size
+int scratch_area(void** ptr, size_t* bytes);
 int launch_rank_bounds(const DevIndex& ix, const double* lo, const double* hi, int64_t nq,
                        int32_t* lr, void* stream);
 bool search_shape_supported(int dp, int m, int L);

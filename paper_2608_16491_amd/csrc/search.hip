@@ -7,6 +7,14 @@
 #include "search_shared.h"
 
 namespace frog {
+
+// Workspace of frog_search_noalloc: a fixed array of device memory, one per
+// GPU the library runs on, held until the process ends.  In host code its
+// name is only a stand-in: the device address comes from
+// hipGetSymbolAddress, taken once per device (scratch_area).
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
 namespace {
 
 // The whole search in one persistent kernel.  The four wavefronts of a
@@ -233,8 +241,12 @@ bool search_shape_supported(int dp, int m, int L) {
 }
 
 int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
+    return launch_search_ws(ix, a, stream_v, nullptr, 0);
+}
+
+int launch_search_ws(const DevIndex& ix, const SearchLaunch& a, void* stream_v, void* wsv, size_t ws_cap) {
     hipStream_t stream = (hipStream_t)stream_v;
-    if (a.entry_mode == 1) return launch_shared(ix, a, stream);
+    if (a.entry_mode == 1) return launch_shared(ix, a, stream, wsv, ws_cap);
     const KernelFn fn = pick_kernel(ix.dp, a.L, ix.storage);
     const int lpw = lds_per_wave(a.L, a.hash_log2);
     const int smem = lpw * kWavesPerBlock + 16;
@@ -274,9 +286,19 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
         if (cap < blocks) blocks = (int)(cap > 0 ? cap : 1);
         ws += (size_t)blocks * kWavesPerBlock * P.gvis_words * 4;
     }
-    void* wsp = nullptr;
-    hipError_t e = hipMallocAsync(&wsp, ws, stream);
-    if (e != hipSuccess) return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
+    void* wsp = wsv;
+    hipError_t e = hipSuccess;
+    if (wsv) {
+        if (ws > ws_cap)
+            return fail(FROG_EUNSUPPORTED,
+                        "this call needs %zu bytes of workspace; the scratch array holds %zu (nq=%lld, L=%d, "
+                        "entry_mode 0%s)", ws, ws_cap, (long long)a.nq, a.L,
+                        a.hash_log2 == 0 ? ", exact visited set" : "");
+    } else {
+        e = hipMallocAsync(&wsp, ws, stream);
+        if (e != hipSuccess)
+            return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
+    }
     char* base = reinterpret_cast<char*>(wsp);
     P.counter = reinterpret_cast<unsigned int*>(base);
     int32_t* lr = reinterpret_cast<int32_t*>(base + off_lr);
@@ -295,8 +317,28 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
         (void)hipEventRecord(ev[2], stream);
     }
     e = hipGetLastError();
-    (void)hipFreeAsync(wsp, stream);
+    if (!wsv) (void)hipFreeAsync(wsp, stream);
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
+    return FROG_OK;
+}
+
+int scratch_area(void** ptr, size_t* bytes) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return fail(FROG_EHIP, "scratch: no usable current device (%d)", dev);
+    std::lock_guard<std::mutex> g(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(FROG_EHIP, "scratch: hipGetSymbolAddress: %s", hipGetErrorString(e));
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    *bytes = kScratchBytes;
     return FROG_OK;
 }
 

@@ -106,7 +106,9 @@ SKernel pick_s_scan(int dp, int kkeep, int storage);   // search_scan.hip
 SKernel pick_s_pool(int dp, int L, int storage);       // search_pool.hip
 SKernel pick_s_search(int dp, int L, int storage);     // search_trav.hip
 // entry_mode 1: plan, group, scan on the matrix cores, then search (search_shared.hip)
-int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream);
+// ws: NULL (stream-ordered allocation) or ws_cap bytes of caller-provided
+// device memory
+int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream, void* ws, size_t ws_cap);
 
 namespace {
 

@@ -244,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
 }  // namespace
 
 // entry_mode 1: plan, group, scan on the matrix cores, then search
-int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream) {
+int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream, void* ws, size_t ws_cap) {
     const int kkeep = shared_kkeep(a.L);
     auto sfn = pick_s_search(ix.dp, a.L, ix.storage);
     auto pfn = pick_s_pool(ix.dp, a.L, ix.storage);
@@ -314,9 +314,19 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
         if (cap < blocks) blocks = (int)(cap > 0 ? cap : 1);
         off += (size_t)blocks * kWavesPerBlock * P.gvis_words * 4;
     }
-    void* wsp = nullptr;
-    hipError_t e = hipMallocAsync(&wsp, off, stream);
-    if (e != hipSuccess) return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
+    void* wsp = ws;
+    hipError_t e = hipSuccess;
+    if (ws) {
+        if (off > ws_cap)
+            return fail(FROG_EUNSUPPORTED,
+                        "this call needs %zu bytes of workspace; the scratch array holds %zu (nq=%lld, L=%d, "
+                        "entry_mode 1%s)", off, ws_cap, (long long)a.nq, a.L,
+                        a.hash_log2 == 0 ? ", exact visited set" : "");
+    } else {
+        e = hipMallocAsync(&wsp, off, stream);
+        if (e != hipSuccess)
+            return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
+    }
     char* base = reinterpret_cast<char*>(wsp);
     P.meta = reinterpret_cast<uint32_t*>(base + o_meta);
     int32_t* lr = reinterpret_cast<int32_t*>(base + o_lr);
@@ -357,7 +367,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream)
     hipLaunchKernelGGL(sfn, dim3(blocks), dim3(kBlock), smem, stream, P);
     if (ev) (void)hipEventRecord(ev[2], stream);
     e = hipGetLastError();
-    (void)hipFreeAsync(wsp, stream);
+    if (!ws) (void)hipFreeAsync(wsp, stream);
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
     return FROG_OK;
 }
