@@ -230,8 +230,13 @@ int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
  * p->entry_mode == 1 the seed's sample must be prepared
  * (frog_index_prepare_sample), else FROG_ENOTPREPARED; nothing is built or
  * freed here, so searches on several streams or threads may share an index
- * whatever their seeds.  The per-call workspace comes from hipMallocAsync on
- * `stream` and is released on it (stream-ordered). */
+ * whatever their seeds.  The per-call workspace (counters, rank intervals,
+ * chunk pools; in entry_mode 1 plans, tiles, candidate lists and pools: about
+ * 5 KB per query at L <= 56 in entry_mode 1) is a device buffer the library
+ * keeps per (device, stream) for the life of the process, grown
+ * stream-ordered when a call needs more, so repeated calls allocate nothing;
+ * threads enqueueing on one stream take turns, other streams have their own
+ * buffer. */
 int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
                    const double* d_lo, const double* d_hi, int k, int L,
                    const frog_search_params_t* p, int32_t* d_ids, float* d_dists,

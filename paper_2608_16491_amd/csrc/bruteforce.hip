@@ -42,6 +42,7 @@
 #include <cstdint>
 #include <vector>
 
+#include "ws_pool.h"
 #include "frog_internal.h"
 #include "wave_topk.h"
 
@@ -425,7 +426,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
     const size_t cbytes = align((size_t)nq * 4);
     const size_t ws_bytes = tbytes + ibytes + ebytes + 2 * lbytes + 2 * sbytes + cbytes + 256;
     void* ws = nullptr;
-    e = hipMallocAsync(&ws, ws_bytes, stream);
+    e = ws_alloc(&ws, ws_bytes, stream);
     if (e != hipSuccess) return fail(FROG_ENOMEM, "bruteforce workspace: %s", hipGetErrorString(e));
     char* base = reinterpret_cast<char*>(ws);
     Tile* dT = reinterpret_cast<Tile*>(base);
@@ -439,7 +440,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
         e = hipMemcpyAsync(dI, items.data(), items.size() * sizeof(Item), hipMemcpyHostToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(dE, empty.data(), (size_t)nq, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) {
-        (void)hipFreeAsync(ws, stream);
+        (void)ws_free(ws, stream);
         return fail(FROG_EHIP, "bruteforce upload: %s", hipGetErrorString(e));
     }
     hipLaunchKernelGGL(bf_pad_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, nq, k, dE, ids, dists, dcert);
@@ -487,7 +488,7 @@ int launch_bruteforce(const frog_index* ix, const float* Q, int64_t nq, const do
     std::vector<int32_t> hc((size_t)nq, 1);
     if (e == hipSuccess && !tiles.empty())
         e = hipMemcpyAsync(hc.data(), dcert, (size_t)nq * 4, hipMemcpyDeviceToHost, stream);
-    (void)hipFreeAsync(ws, stream);
+    (void)ws_free(ws, stream);
     // keep the host-side arrays alive until the copies have run
     const hipError_t es = hipStreamSynchronize(stream);
     if (e != hipSuccess || es != hipSuccess)

@@ -12,6 +12,7 @@
 #include <thread>
 
 #include "frog_internal.h"
+#include "ws_pool.h"
 
 namespace frog {
 
@@ -776,3 +777,114 @@ int frog_index_prepare_sample(frog_index_t* ix, uint64_t seed) {
 }
 
 }  // extern "C"
+
+namespace frog {
+
+namespace {
+
+hipMemPool_t device_pool(hipError_t* err) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static hipMemPool_t pools[kMaxDevices] = {};
+    int dev = -1;
+    *err = hipGetDevice(&dev);
+    if (*err != hipSuccess) return nullptr;
+    if (dev < 0 || dev >= kMaxDevices) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> g(mu);
+    if (!pools[dev]) {
+        hipMemPoolProps props{};
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t pool = nullptr;
+        *err = hipMemPoolCreate(&pool, &props);
+        if (*err != hipSuccess) return nullptr;
+        uint64_t keep = ~0ull;
+        *err = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+        if (*err != hipSuccess) {
+            (void)hipMemPoolDestroy(pool);
+            return nullptr;
+        }
+        pools[dev] = pool;
+    }
+    return pools[dev];
+}
+
+}  // namespace
+
+hipError_t ws_alloc(void** ptr, size_t bytes, hipStream_t stream) {
+    hipError_t e = hipSuccess;
+    hipMemPool_t pool = device_pool(&e);
+    if (!pool) return e;
+    return hipMallocFromPoolAsync(ptr, bytes, pool, stream);
+}
+
+hipError_t ws_free(void* ptr, hipStream_t stream) { return hipFreeAsync(ptr, stream); }
+
+struct Slot {
+    std::mutex mu;          // held by the lease while a call enqueues
+    void* ptr = nullptr;
+    size_t cap = 0;
+};
+
+namespace {
+
+Slot* slot_for(hipStream_t stream, hipError_t* err) {
+    static std::mutex mu;
+    static std::map<std::pair<int, hipStream_t>, std::unique_ptr<Slot>> slots;
+    int dev = -1;
+    *err = hipGetDevice(&dev);
+    if (*err != hipSuccess) return nullptr;
+    std::lock_guard<std::mutex> g(mu);
+    std::unique_ptr<Slot>& sl = slots[std::make_pair(dev, stream)];
+    if (!sl) {
+        sl.reset(new (std::nothrow) Slot);
+        if (!sl) {
+            *err = hipErrorOutOfMemory;
+            return nullptr;
+        }
+    }
+    return sl.get();
+}
+
+}  // namespace
+
+hipError_t WsLease::acquire(hipStream_t stream, size_t bytes, void** ptr) {
+    release();
+    hipError_t e = hipSuccess;
+    Slot* sl = slot_for(stream, &e);
+    if (!sl) return e;
+    sl->mu.lock();
+    slot_ = sl;
+    // The buffer's earlier uses were enqueued on this stream handle, so they
+    // run before this call's work.  (A handle is only recycled once the
+    // destroyed stream's work has completed and its object is released.)
+    if (sl->cap < bytes) {
+        if (sl->ptr) (void)ws_free(sl->ptr, stream);
+        sl->ptr = nullptr;
+        sl->cap = 0;
+        // a little headroom, so that batches of slowly growing size do not
+        // reallocate every time
+        const size_t want = bytes + bytes / 8;
+        e = ws_alloc(&sl->ptr, want, stream);
+        if (e != hipSuccess) {
+            sl->ptr = nullptr;
+            return e;
+        }
+        sl->cap = want;
+    }
+    *ptr = sl->ptr;
+    return hipSuccess;
+}
+
+void WsLease::release() {
+    if (!slot_) return;
+    slot_->mu.unlock();
+    slot_ = nullptr;
+}
+
+}  // namespace frog

@@ -2,6 +2,7 @@
 // distance (the brute force's fallback for queries its margin test cannot
 // certify).
 
+#include "ws_pool.h"
 #include "search_common.h"
 
 namespace frog {
@@ -148,7 +149,7 @@ int launch_exact_ranges(const DevIndex& ix, const float* Q, const int32_t* hq, c
     const size_t o_part = o_fo + align((size_t)(nf + 1) * 8);
     const size_t bytes = o_part + (size_t)nitems * 64 * lp * 8;
     void* ws = nullptr;
-    hipError_t e = hipMallocAsync(&ws, bytes, stream);
+    hipError_t e = ws_alloc(&ws, bytes, stream);
     if (e != hipSuccess) return fail(FROG_ENOMEM, "exact ranges workspace: %s", hipGetErrorString(e));
     char* base = reinterpret_cast<char*>(ws);
     XParams P{};
@@ -176,7 +177,7 @@ int launch_exact_ranges(const DevIndex& ix, const float* Q, const int32_t* hq, c
                            stream, P);
         e = hipGetLastError();
     }
-    (void)hipFreeAsync(ws, stream);
+    (void)ws_free(ws, stream);
     // the host arrays must outlive the copies
     const hipError_t e2 = hipStreamSynchronize(stream);
     if (e != hipSuccess || e2 != hipSuccess)

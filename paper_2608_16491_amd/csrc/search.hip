@@ -3,6 +3,7 @@
 // row gather the shared sample's preparation uses.  The search's design is
 // described in search_common.h.
 
+#include "ws_pool.h"
 #include "search_common.h"
 #include "search_shared.h"
 
@@ -37,7 +38,7 @@ __device__ __forceinline__ uint64_t ctl_word(uint32_t q, uint32_t next, uint32_t
     return ((uint64_t)q << 32) | ((uint64_t)next << 16) | nch;
 }
 
-template <int C, int LP, typename XT = float>
+template <int C, int LP, typename XT = float, bool LEAN = false>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_WAVES_PER_EU)))
 void coop_kernel(KParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -166,7 +167,7 @@ void coop_kernel(KParams P) {
                 }
             }
         }
-        traverse<C, LP, XT>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
+        traverse<C, LP, XT, LEAN>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
         if (A.stats && lane == 0) A.stats[qi * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
     }
 }
@@ -190,23 +191,28 @@ __global__ void init_kernel(unsigned int* counter, unsigned int* done, int64_t n
 
 using KernelFn = void (*)(KParams);
 
+template <int C, typename XT, bool LEAN>
+KernelFn pick_lp_l(int L) {
+    if (L <= 64) return coop_kernel<C, 1, XT, LEAN>;
+    if (L <= 128) return coop_kernel<C, 2, XT, LEAN>;
+    return coop_kernel<C, 4, XT, LEAN>;
+}
+
 template <int C, typename XT = float>
-KernelFn pick_lp(int L) {
-    if (L <= 64) return coop_kernel<C, 1, XT>;
-    if (L <= 128) return coop_kernel<C, 2, XT>;
-    return coop_kernel<C, 4, XT>;
+KernelFn pick_lp(int L, bool lean) {
+    return lean ? pick_lp_l<C, XT, true>(L) : pick_lp_l<C, XT, false>(L);
 }
 
 // fp16 rows come with dp = 64 or 128 (the upload checks it)
-KernelFn pick_kernel(int dp, int L, int storage) {
-    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_lp<2, __half>(L) : pick_lp<4, __half>(L);
-    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_lp<2, bf16x>(L) : pick_lp<4, bf16x>(L);
+KernelFn pick_kernel(int dp, int L, int storage, bool lean) {
+    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_lp<2, __half>(L, lean) : pick_lp<4, __half>(L, lean);
+    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_lp<2, bf16x>(L, lean) : pick_lp<4, bf16x>(L, lean);
     switch (dp) {
-        case 32: return pick_lp<1>(L);
-        case 64: return pick_lp<2>(L);
-        case 96: return pick_lp<3>(L);
-        case 128: return pick_lp<4>(L);
-        default: return pick_lp<0>(L);
+        case 32: return pick_lp<1>(L, lean);
+        case 64: return pick_lp<2>(L, lean);
+        case 96: return pick_lp<3>(L, lean);
+        case 128: return pick_lp<4>(L, lean);
+        default: return pick_lp<0>(L, lean);
     }
 }
 
@@ -247,7 +253,7 @@ int launch_search(const DevIndex& ix, const SearchLaunch& a, void* stream_v) {
 int launch_search_ws(const DevIndex& ix, const SearchLaunch& a, void* stream_v, void* wsv, size_t ws_cap) {
     hipStream_t stream = (hipStream_t)stream_v;
     if (a.entry_mode == 1) return launch_shared(ix, a, stream, wsv, ws_cap);
-    const KernelFn fn = pick_kernel(ix.dp, a.L, ix.storage);
+    const KernelFn fn = pick_kernel(ix.dp, a.L, ix.storage, lean_launch(a));
     const int lpw = lds_per_wave(a.L, a.hash_log2);
     const int smem = lpw * kWavesPerBlock + 16;
     if (smem > 160 * 1024) return fail(FROG_EUNSUPPORTED, "LDS per block %d too large", smem);
@@ -288,6 +294,7 @@ int launch_search_ws(const DevIndex& ix, const SearchLaunch& a, void* stream_v, 
     }
     void* wsp = wsv;
     hipError_t e = hipSuccess;
+    WsLease lease;
     if (wsv) {
         if (ws > ws_cap)
             return fail(FROG_EUNSUPPORTED,
@@ -295,7 +302,7 @@ int launch_search_ws(const DevIndex& ix, const SearchLaunch& a, void* stream_v, 
                         "entry_mode 0%s)", ws, ws_cap, (long long)a.nq, a.L,
                         a.hash_log2 == 0 ? ", exact visited set" : "");
     } else {
-        e = hipMallocAsync(&wsp, ws, stream);
+        e = lease.acquire(stream, ws, &wsp);
         if (e != hipSuccess)
             return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
     }
@@ -317,7 +324,7 @@ int launch_search_ws(const DevIndex& ix, const SearchLaunch& a, void* stream_v, 
         (void)hipEventRecord(ev[2], stream);
     }
     e = hipGetLastError();
-    if (!wsv) (void)hipFreeAsync(wsp, stream);
+    lease.release();
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
     return FROG_OK;
 }

@@ -100,6 +100,16 @@ __device__ __forceinline__ int mbcnt(uint64_t m) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
+// The values of the lanes in `mask`, moved to lanes 0 .. popc(mask) - 1 in
+// lane order (a forward permute: every lane sends its value to a distinct
+// lane, the others after the selected ones).
+__device__ __forceinline__ int32_t compact_lanes(int32_t v, uint64_t mask) {
+    const int lane = __lane_id();
+    const int below = mbcnt(mask);
+    const int dst = ((mask >> lane) & 1ull) ? below : __popcll(mask) + (lane - below);
+    return __builtin_amdgcn_ds_permute(dst << 2, v);
+}
+
 __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
     uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, l);
     uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
@@ -650,13 +660,18 @@ __device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const Que
 
 // a2, a4-a11 for one query whose pool holds the L nearest entry points:
 // HotspotLocalization, the best-first loop of Alg. 2, output and statistics.
-template <int C, int LP, typename XT>
+// LEAN: the timed configuration (no statistics, lazy check, LDS visited
+// table), with the statistics and the ablation branches compiled out and the
+// EN list of a single-load hotspot slice compacted by lane permutes; the
+// trajectory is the same.
+template <int C, int LP, typename XT, bool LEAN = false>
 __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis_words, const QueryCtx<C, XT>& Q,
                          Pool<LP>& pool, const WaveLds<LP>& W, const Visited& vis) {
     const int lane = lane_id();
     const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
     const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
     const int64_t qi = Q.qi, l = Q.l, r = Q.r;
+    const bool eager = !LEAN && A.eager;
     int32_t st[FROG_STAT_N];
 #pragma unroll
     for (int i = 0; i < FROG_STAT_N; ++i) st[i] = 0;
@@ -702,15 +717,21 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
     int32_t pre_u = -1;
     int32_t pre_v = -1;
     for (;;) {
-        // a4: first unexpanded entry
-        int sel = -1;
+        // a4: first unexpanded entry, and the one after it (the prefetch's
+        // guess at the next selection), from one ballot per register
+        int sel = -1, nsel = -1;
 #pragma unroll
         for (int s = 0; s < LP; ++s) {
-            const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
-            if (sel < 0 && mk != 0) sel = s * 64 + __builtin_ctzll(mk);
+            uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
+            if (sel < 0 && mk != 0) {
+                sel = s * 64 + __builtin_ctzll(mk);
+                mk &= mk - 1;
+            }
+            if (nsel < 0 && sel >= 0 && mk != 0) nsel = s * 64 + __builtin_ctzll(mk);
         }
         sel = uniform(sel);
         if (sel < 0) break;
+        nsel = uniform(nsel);
         const int ss = sel >> 6, sl = sel & 63;
         int32_t u = 0;
 #pragma unroll
@@ -726,14 +747,6 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         // a5 + a6: ENC slice of the hotspot, compaction under budget B
         const int32_t* row = ix.ENC + ((int64_t)u * H + Ls) * m;
         const bool hit = u == pre_u;
-        // next prefetch: the first unexpanded entry after u
-        int nsel = -1;
-#pragma unroll
-        for (int s = 0; s < LP; ++s) {
-            const uint64_t mk = ballot(pool.flag[s] == 0u && pool.key[s] != kEmpty);
-            if (nsel < 0 && mk != 0) nsel = s * 64 + __builtin_ctzll(mk);
-        }
-        nsel = uniform(nsel);
         int32_t nu = -1;
 #pragma unroll
         for (int s = 0; s < LP; ++s)
@@ -746,13 +759,32 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
             pre_v = lane < nent ? nrow[lane] : -1;
             st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
         }
+        if (LEAN && nent <= 64) {
+            // one load holds the hotspot slice: admit the first B in-range
+            // entries (Alg. 4), move them to lanes 0.., check them against
+            // the visited table (lazy check) and move the fresh ones down
+            const int32_t v0 = hit ? cur_pre : (lane < nent ? row[lane] : -1);
+            const uint64_t pm = ballot(v0 >= l && v0 <= r);
+            const int tot = __popcll(pm);
+            const int nen = tot < B ? tot : B;
+            const uint64_t am = ballot(((pm >> lane) & 1ull) && mbcnt(pm) < nen);
+            const int32_t v = compact_lanes(v0, am);
+            const bool fresh = lane < nen && !Q.is_entry(v) && vis.check_insert(v);
+            const uint64_t fm = ballot(fresh);
+            const int ns = __popcll(fm);
+            if (ns == 0) continue;
+            const int32_t myid = compact_lanes(v, fm);
+            const float dd = Q.eval(ix, ns, lane < ns ? myid : 0);
+            merge<LP>(pool, lane < ns ? make_key(dd, myid) : kEmpty, ns, L, W.st_key, W.st_flag);
+            continue;
+        }
         int nen = 0;
         int64_t scanned = nent;
         for (int64_t off = 0; off < nent && nen < B; off += 64) {
             const int64_t e = off + lane;
             const int32_t v = (off == 0 && hit) ? cur_pre : (e < nent ? row[e] : -1);
             bool pred = v >= l && v <= r;
-            if (A.eager) {
+            if (eager) {
                 // ablation: visited candidates are skipped here and do not
                 // count against the budget; a repeat of an earlier lane's
                 // candidate in this load is visited by then (exact set only)
@@ -768,7 +800,7 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
             const int admit = tot < B - nen ? tot : B - nen;
             if (pred && rk < admit) {
                 enbuf[nen + rk] = v;
-                if (A.eager) vis.insert(v);
+                if (eager) vis.insert(v);
             }
             if (!(off == 0 && hit)) st[FROG_STAT_LOADED] += (int32_t)(nent - off < 64 ? nent - off : 64);
             if (admit == B - nen && admit > 0) {
@@ -787,7 +819,7 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         // a7: lazy visited check on the compacted list
         int32_t v = lane < nen ? enbuf[lane] : -1;
         bool fresh = false;
-        if (lane < nen) fresh = A.eager || (!Q.is_entry(v) && vis.check_insert(v));
+        if (lane < nen) fresh = eager || (!Q.is_entry(v) && vis.check_insert(v));
         const uint64_t fm = ballot(fresh);
         const int ns = __popcll(fm);
         wave_sync();
@@ -822,7 +854,7 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         }
     }
     // the traversal's columns; the shared scan's row count is written by the scan
-    if (A.stats && lane < FROG_STAT_SCANROWS) {
+    if (!LEAN && A.stats && lane < FROG_STAT_SCANROWS) {
         int32_t val = 0;
 #pragma unroll
         for (int i = 0; i < FROG_STAT_SCANROWS; ++i)

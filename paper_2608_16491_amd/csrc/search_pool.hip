@@ -165,7 +165,8 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
 template <int C, typename XT = float>
 void (*pick_s_pool_c(int L))(SParams) {
     const int kk = shared_kkeep(L);
-    if (L <= 64) return kk == 64 ? s_pool_kernel<C, 1, 64, XT> : s_pool_kernel<C, 1, 128, XT>;
+    if (L <= 64)
+        return kk == 48 ? s_pool_kernel<C, 1, 48, XT> : (kk == 64 ? s_pool_kernel<C, 1, 64, XT> : s_pool_kernel<C, 1, 128, XT>);
     if (L <= 128) return kk == 128 ? s_pool_kernel<C, 2, 128, XT> : s_pool_kernel<C, 2, 256, XT>;
     return s_pool_kernel<C, 4, 256, XT>;
 }

@@ -9,8 +9,10 @@ namespace {
 // KT = dp / 16 float4 chunks of the query operand in registers (d <= 128);
 // KT = 0 reloads it for every block (fp32 rows only).  XT is the rows'
 // storage type: 16-bit rows are widened exactly to fp32 on load.
+// Three wavefronts per SIMD: about 160 VGPRs (one row buffer) and, with
+// 48-entry lists (L <= 40), 12.5 KB of LDS per wavefront.
 template <int KT, int KK, typename XT = float>
-__global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) void s_scan_kernel(SParams P) {
     static_assert(sizeof(XT) == 4 || (KT > 0 && KT % 2 == 0), "16-bit rows need dp a multiple of 32 held in registers");
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -156,9 +158,7 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
     };
     // one 16-row block: q.x on the matrix cores (four independent
     // accumulation chains), then the candidates
-    auto process = [&](const float4 (&x)[KT > 0 ? KT : 1], int32_t rk, uint32_t pri, float xn, int64_t blk) {
-        const bool inrun = c0 + blk * 16 + ii < c1;
-        make_room();
+    auto products = [&](const float4 (&x)[KT > 0 ? KT : 1], int64_t blk) -> floatx4_t {
         floatx4_t acc;
         if constexpr (KT > 0) {
             floatx4_t a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0, a2 = a0, a3 = a0;
@@ -181,6 +181,10 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, xv.w, acc, 0, 0, 0);
             }
         }
+        return acc;
+    };
+    auto candidates = [&](const floatx4_t& acc, int32_t rk, uint32_t pri, float xn, int64_t blk) {
+        const bool inrun = c0 + blk * 16 + ii < c1;
         const uint64_t below = (1ull << lane) - 1;
         // lane holds D[4kk + e][ii]: query slot 4kk + e, the block's row ii
 #pragma unroll
@@ -203,32 +207,29 @@ __global__ __launch_bounds__(kBlock) void s_scan_kernel(SParams P) {
             for (int g = 0; g < 4; ++g) fill[4 * g + e] += __popcll(m & (0xFFFFull << (16 * g)));
         }
     };
-    // two row buffers in turn: the loads of block b + 2 are issued as soon
-    // as block b is multiplied, ranks two blocks ahead of their rows
-    // (positions past the end are clamped to the last one, so the loads are
-    // in bounds and unconditional: a load under a branch would make the
-    // compiler wait for it, and for every load issued before it, at once)
+    // one row buffer: the loads of block b + 1 are issued as soon as block
+    // b's products are issued, and run during b's candidate logic and the
+    // other wavefronts' work (positions past the end are clamped to the last
+    // one, so the loads are in bounds and unconditional: a load under a branch
+    // would make the compiler wait for it, and for every load issued before
+    // it, at once)
     if (nblk > 0) {
-        float4 xa[KT > 0 ? KT : 1], xb[KT > 0 ? KT : 1];
-        load_rows(0, xa);
-        int32_t ra = rank_at(0);
-        uint32_t pa = lprio[pos_at(0)];
-        float na = lnorm[pos_at(0)];
-        load_rows(1, xb);
-        int32_t rb = rank_at(1);
-        uint32_t pb = lprio[pos_at(1)];
-        float nb = lnorm[pos_at(1)];
-        for (int64_t blk = 0; blk < nblk; blk += 2) {
-            process(xa, ra, pa, na, blk);
-            load_rows(blk + 2, xa);
-            ra = rank_at(blk + 2);
-            pa = lprio[pos_at(blk + 2)];
-            na = lnorm[pos_at(blk + 2)];
-            if (blk + 1 < nblk) process(xb, rb, pb, nb, blk + 1);
-            load_rows(blk + 3, xb);
-            rb = rank_at(blk + 3);
-            pb = lprio[pos_at(blk + 3)];
-            nb = lnorm[pos_at(blk + 3)];
+        float4 x[KT > 0 ? KT : 1];
+        load_rows(0, x);
+        int32_t rk = rank_at(0);
+        uint32_t pr = lprio[pos_at(0)];
+        float xn = lnorm[pos_at(0)];
+        for (int64_t blk = 0; blk < nblk; ++blk) {
+            make_room();
+            const floatx4_t acc = products(x, blk);
+            load_rows(blk + 1, x);
+            const int32_t rk1 = rank_at(blk + 1);
+            const uint32_t pr1 = lprio[pos_at(blk + 1)];
+            const float xn1 = lnorm[pos_at(blk + 1)];
+            candidates(acc, rk, pr, xn, blk);
+            rk = rk1;
+            pr = pr1;
+            xn = xn1;
         }
     }
     // the item's lists: entries kept, threshold, sample rows seen
@@ -290,6 +291,7 @@ void (*pick_s_scan_k(int dp, int storage))(SParams) {
 }  // namespace
 
 void (*pick_s_scan(int dp, int kkeep, int storage))(SParams) {
+    if (kkeep == 48) return pick_s_scan_k<48>(dp, storage);
     if (kkeep == 64) return pick_s_scan_k<64>(dp, storage);
     if (kkeep == 128) return pick_s_scan_k<128>(dp, storage);
     return pick_s_scan_k<256>(dp, storage);

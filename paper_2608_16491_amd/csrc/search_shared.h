@@ -104,13 +104,17 @@ using SKernel = void (*)(SParams);
 // kernels of the other units, picked by shape
 SKernel pick_s_scan(int dp, int kkeep, int storage);   // search_scan.hip
 SKernel pick_s_pool(int dp, int L, int storage);       // search_pool.hip
-SKernel pick_s_search(int dp, int L, int storage);     // search_trav.hip
+// lean: no statistics, lazy check, LDS visited table (the timed configuration)
+SKernel pick_s_search(int dp, int L, int storage, bool lean);   // search_trav.hip
 // entry_mode 1: plan, group, scan on the matrix cores, then search (search_shared.hip)
 // ws: NULL (stream-ordered allocation) or ws_cap bytes of caller-provided
 // device memory
 int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream, void* ws, size_t ws_cap);
 
 namespace {
+
+// the timed configuration, which the lean traversal serves
+inline bool lean_launch(const SearchLaunch& a) { return !a.stats && !a.eager && a.hash_log2 > 0; }
 
 __device__ __forceinline__ int32_t level_rank(const SharedLevels& lv, int j, int64_t pos) {
     return j == 0 ? (int32_t)pos : lv.ranks[lv.off[j] + pos];
@@ -154,7 +158,7 @@ __host__ __device__ constexpr size_t s_scan_lds_per_wave(int kkeep) {
 
 // candidates kept per query and work item: K >= L + 8, room for the margin
 // (the C ABI refuses L > 248 in entry mode 1)
-inline int shared_kkeep(int L) { return L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256); }
+inline int shared_kkeep(int L) { return L + 8 <= 48 ? 48 : (L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256)); }
 // the pool kernel's merged list: at least 64
 inline int pool_kkeep(int kkeep) { return kkeep > 64 ? kkeep : 64; }
 

@@ -2,6 +2,7 @@
 // kernels (rank interval, threshold, level, run, bucket; bucket offsets;
 // order; tiles) and the launch of the whole mode-1 pipeline.
 
+#include "ws_pool.h"
 #include "search_shared.h"
 
 namespace frog {
@@ -246,7 +247,7 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
 // entry_mode 1: plan, group, scan on the matrix cores, then search
 int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream, void* ws, size_t ws_cap) {
     const int kkeep = shared_kkeep(a.L);
-    auto sfn = pick_s_search(ix.dp, a.L, ix.storage);
+    auto sfn = pick_s_search(ix.dp, a.L, ix.storage, lean_launch(a));
     auto pfn = pick_s_pool(ix.dp, a.L, ix.storage);
     // search kernel: pool staging, EN list and visited table per wave
     const int lps = lds_per_wave(a.L, a.hash_log2);
@@ -316,6 +317,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     }
     void* wsp = ws;
     hipError_t e = hipSuccess;
+    WsLease lease;
     if (ws) {
         if (off > ws_cap)
             return fail(FROG_EUNSUPPORTED,
@@ -323,7 +325,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
                         "entry_mode 1%s)", off, ws_cap, (long long)a.nq, a.L,
                         a.hash_log2 == 0 ? ", exact visited set" : "");
     } else {
-        e = hipMallocAsync(&wsp, off, stream);
+        e = lease.acquire(stream, off, &wsp);
         if (e != hipSuccess)
             return fail(e == hipErrorOutOfMemory ? FROG_ENOMEM : FROG_EHIP, "workspace: %s", hipGetErrorString(e));
     }
@@ -367,7 +369,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     hipLaunchKernelGGL(sfn, dim3(blocks), dim3(kBlock), smem, stream, P);
     if (ev) (void)hipEventRecord(ev[2], stream);
     e = hipGetLastError();
-    if (!ws) (void)hipFreeAsync(wsp, stream);
+    lease.release();
     if (e != hipSuccess) return fail(FROG_EHIP, "search launch: %s", hipGetErrorString(e));
     return FROG_OK;
 }

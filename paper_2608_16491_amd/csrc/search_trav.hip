@@ -6,7 +6,7 @@ namespace frog {
 namespace {
 
 // Traversal: persistent, one wavefront per query, from the pool s_pool_kernel wrote.
-template <int C, int LP, typename XT = float>
+template <int C, int LP, typename XT = float, bool LEAN = false>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_SEARCH_WAVES_PER_EU)))
 void s_search_kernel(SParams P) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -50,28 +50,35 @@ void s_search_kernel(SParams P) {
             np += __popcll(ballot(pool.key[s] != kEmpty));
         }
         pool.np = np;
-        traverse<C, LP, XT>(ix, A, P.gvis_words, Q, pool, W, vis);
+        traverse<C, LP, XT, LEAN>(ix, A, P.gvis_words, Q, pool, W, vis);
     }
 }
 
+template <int C, typename XT, bool LEAN>
+void (*pick_s_search_l(int L))(SParams) {
+    if (L <= 64) return s_search_kernel<C, 1, XT, LEAN>;
+    if (L <= 128) return s_search_kernel<C, 2, XT, LEAN>;
+    return s_search_kernel<C, 4, XT, LEAN>;
+}
+
 template <int C, typename XT = float>
-void (*pick_s_search_c(int L))(SParams) {
-    if (L <= 64) return s_search_kernel<C, 1, XT>;
-    if (L <= 128) return s_search_kernel<C, 2, XT>;
-    return s_search_kernel<C, 4, XT>;
+void (*pick_s_search_c(int L, bool lean))(SParams) {
+    return lean ? pick_s_search_l<C, XT, true>(L) : pick_s_search_l<C, XT, false>(L);
 }
 
 }  // namespace
 
-void (*pick_s_search(int dp, int L, int storage))(SParams) {
-    if (storage == FROG_STORAGE_F16) return dp == 64 ? pick_s_search_c<2, __half>(L) : pick_s_search_c<4, __half>(L);
-    if (storage == FROG_STORAGE_BF16) return dp == 64 ? pick_s_search_c<2, bf16x>(L) : pick_s_search_c<4, bf16x>(L);
+void (*pick_s_search(int dp, int L, int storage, bool lean))(SParams) {
+    if (storage == FROG_STORAGE_F16)
+        return dp == 64 ? pick_s_search_c<2, __half>(L, lean) : pick_s_search_c<4, __half>(L, lean);
+    if (storage == FROG_STORAGE_BF16)
+        return dp == 64 ? pick_s_search_c<2, bf16x>(L, lean) : pick_s_search_c<4, bf16x>(L, lean);
     switch (dp) {
-        case 32: return pick_s_search_c<1>(L);
-        case 64: return pick_s_search_c<2>(L);
-        case 96: return pick_s_search_c<3>(L);
-        case 128: return pick_s_search_c<4>(L);
-        default: return pick_s_search_c<0>(L);
+        case 32: return pick_s_search_c<1>(L, lean);
+        case 64: return pick_s_search_c<2>(L, lean);
+        case 96: return pick_s_search_c<3>(L, lean);
+        case 128: return pick_s_search_c<4>(L, lean);
+        default: return pick_s_search_c<0>(L, lean);
     }
 }
 

@@ -137,10 +137,10 @@ __device__ __forceinline__ void buf_init(const BufList& B) {
 // leave no such x).  The bisection over the value bits stops at the first x
 // that qualifies (for the exact cut: exactly K entries at or below x), so it
 // rarely runs to a single value.  The new threshold is at or below the value
-// of every dropped entry.  K is 32, 64, 128 or 256.
+// of every dropped entry.  K is 32, 48, 64, 128 or 256.
 template <int K>
 __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
-    constexpr int R = 2 * K / 64;   // entries per lane
+    constexpr int R = (2 * K + 63) / 64;   // entries per lane (the last register partly)
     const int lane = __lane_id();
     const int f = __builtin_amdgcn_readfirstlane(B.st[0]);
     if (f <= K) return;

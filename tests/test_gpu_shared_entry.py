@@ -32,7 +32,7 @@ def mix128():
     return Case(w.X, w.attr, w.Q, w.lo, w.hi)
 
 
-@pytest.mark.parametrize("L", [10, 16, 24, 25, 32, 56, 64, 120, 121, 128, 248])
+@pytest.mark.parametrize("L", [10, 16, 24, 25, 32, 40, 41, 56, 64, 120, 121, 128, 248])
 def test_shared_tiny_parity_pool_sizes(tiny, L):
     g_ids, g_d = tiny.gpu(10, L, **SH)
     o_ids, o_d, _ = tiny.cpu(10, L, **SH)
