@@ -110,7 +110,10 @@ enum {
     FROG_STAT_SCANROWS = 8,   /* entry_mode 1: rows the shared entry scan read for the
                                  query's tile of 16, credited to the tile's first query
                                  (0 for the others and in entry_mode 0) */
-    FROG_STAT_N = 9
+    FROG_STAT_FALLBACK = 9,   /* entry_mode 1: 1 if the margin test could not prove the
+                                 scan's candidates hold the L nearest sample points, so
+                                 the whole sample was evaluated exactly (0 otherwise) */
+    FROG_STAT_N = 10
 };
 
 /* Fill *p with the paper's defaults for dimension d. */
@@ -218,9 +221,8 @@ int frog_rank_bounds(const frog_index_t* idx, const double* d_lo, const double* 
 
 /* FROGSearch (Alg. 2 with HotspotLocalization, Alg. 3, and ENIdentification,
  * Alg. 4) for nq queries with default parameters.  d_queries: nq x d floats
- * row-major; d_lo/d_hi: nq doubles; k >= 1, L in [k, 256] (pool size ef_s;
- * at most 248 with entry_mode 1, else FROG_EUNSUPPORTED); outputs d_ids
- * (int32) and d_dists (float), nq x k each. */
+ * row-major; d_lo/d_hi: nq doubles; k >= 1, L in [k, 256] (pool size ef_s);
+ * outputs d_ids (int32) and d_dists (float), nq x k each. */
 int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
                 const double* d_lo, const double* d_hi, int k, int L,
                 int32_t* d_ids, float* d_dists, void* stream);
@@ -261,7 +263,7 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
  *     512 * ceil(L/64) bytes per chunk (about 2 KB per query at 2,560 entry
  *     points and L <= 64); entry_mode 1 about 4.8 KB per query at L <= 56
  *     (about 13,900 queries per call), 9.4 KB up to L = 120 and 18.6 KB up to
- *     L = 248; the exact visited set (hash_log2 = 0) adds n/8 bytes per
+ *     L = 256; the exact visited set (hash_log2 = 0) adds n/8 bytes per
  *     resident wavefront and is refused at realistic n.
  *   - entry_mode 1 needs the seed prepared (frog_index_prepare_sample). */
 int frog_search_noalloc(const frog_index_t* idx, const float* d_queries, int64_t nq,

@@ -20,8 +20,8 @@ FROG_OK = 0
 ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "EBADINDEX", -5: "ENOTUPLOADED",
           -6: "EIO", -7: "EUNSUPPORTED", -8: "ENOTPREPARED"}
 (STAT_EXPANSIONS, STAT_EN, STAT_DIST, STAT_SCANNED, STAT_ENTRY, STAT_LSTART, STAT_LEND, STAT_LOADED,
- STAT_SCANROWS) = range(9)
-STAT_N = 9
+ STAT_SCANROWS, STAT_FALLBACK) = range(10)
+STAT_N = 10
 STORAGE_F32, STORAGE_F16, STORAGE_BF16 = 0, 1, 2
 STORAGE = {"fp32": STORAGE_F32, "fp16": STORAGE_F16, "bf16": STORAGE_BF16}
 

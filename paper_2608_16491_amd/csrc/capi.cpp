@@ -576,10 +576,6 @@ int search_args(const frog_index_t* ix, const float* d_queries, int64_t nq, cons
     a.entry_mode = q.entry_mode;
     a.hotspot_mode = q.hotspot_mode;
     a.eager = q.eager_check;
-    if (q.entry_mode == 1 && L > 248)
-        return fail(FROG_EUNSUPPORTED,
-                    "entry_mode 1 keeps at most 256 candidates per query and work item and needs L + 8 of them "
-                    "(L=%d > 248); entry_mode 0 takes L up to 256", L);
     if (q.entry_mode == 1) {
         rc = frog::find_sample(ix, q.seed, &a.lv, &a.maxnorm);
         if (rc) return rc;

@@ -168,7 +168,10 @@ void coop_kernel(KParams P) {
             }
         }
         traverse<C, LP, XT, LEAN>(P.ix, P.a, P.gvis_words, Q, pool, W, vis);
-        if (A.stats && lane == 0) A.stats[qi * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
+        if (A.stats && lane == 0) {
+            A.stats[qi * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
+            A.stats[qi * FROG_STAT_N + FROG_STAT_FALLBACK] = 0;
+        }
     }
 }
 

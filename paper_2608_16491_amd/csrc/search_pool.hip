@@ -7,7 +7,7 @@ namespace frog {
 namespace {
 
 // The pool of each query: one wavefront per query.
-template <int C, int LP, int KK, typename XT = float>
+template <int C, int LP, int KK, typename XT = float, int MK = (KK > 64 ? KK : 64)>
 __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -18,8 +18,10 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
     WaveLds<LP> W(smem, P.lds_per_wave, 0);
     char* lbase = smem + (size_t)wave * P.lds_per_wave + P.lds_list;
     // KK: entries of each chunk list the scan left (their stride); the merged
-    // list keeps kkeep >= 64 of them (an offer of 64 fits after a cut)
-    constexpr int kkeep = KK > 64 ? KK : 64;
+    // list keeps MK >= 64 of them (an offer of 64 fits after a cut), twice
+    // the chunk lists' 256 for pools above 248 so that the margin test spans
+    // many ranks past the pool's last
+    constexpr int kkeep = MK;
     const BufList Lst{reinterpret_cast<uint64_t*>(lbase), reinterpret_cast<int32_t*>(lbase + (size_t)2 * kkeep * 8)};
     const double u_round = 5.9604644775390625e-08;   // 2^-24
 
@@ -158,7 +160,10 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
         }
 #pragma unroll
         for (int s = 0; s < LP; ++s) P.pools[qi * 64 * LP + s * 64 + lane] = pool.key[s];
-        if (lane == 0) P.pne[qi] = (int32_t)ne;
+        if (lane == 0) {
+            P.pne[qi] = (int32_t)ne;
+            if (A.stats) A.stats[qi * FROG_STAT_N + FROG_STAT_FALLBACK] = certified ? 0 : 1;
+        }
     }
 }
 
@@ -168,6 +173,7 @@ void (*pick_s_pool_c(int L))(SParams) {
     if (L <= 64)
         return kk == 48 ? s_pool_kernel<C, 1, 48, XT> : (kk == 64 ? s_pool_kernel<C, 1, 64, XT> : s_pool_kernel<C, 1, 128, XT>);
     if (L <= 128) return kk == 128 ? s_pool_kernel<C, 2, 128, XT> : s_pool_kernel<C, 2, 256, XT>;
+    if (L > 248) return s_pool_kernel<C, 4, 256, XT, 512>;
     return s_pool_kernel<C, 4, 256, XT>;
 }
 

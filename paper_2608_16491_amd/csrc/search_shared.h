@@ -157,10 +157,10 @@ __host__ __device__ constexpr size_t s_scan_lds_per_wave(int kkeep) {
 }
 
 // candidates kept per query and work item: K >= L + 8, room for the margin
-// (the C ABI refuses L > 248 in entry mode 1)
+// (pools above 248 keep 256 per work item and 512 when merged)
 inline int shared_kkeep(int L) { return L + 8 <= 48 ? 48 : (L + 8 <= 64 ? 64 : (L + 8 <= 128 ? 128 : 256)); }
 // the pool kernel's merged list: at least 64
-inline int pool_kkeep(int kkeep) { return kkeep > 64 ? kkeep : 64; }
+inline int pool_kkeep(int kkeep, int L) { return L > 248 ? 512 : (kkeep > 64 ? kkeep : 64); }
 
 }  // namespace
 }  // namespace frog

@@ -107,7 +107,10 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
         P.plan[q] = p;
         P.lr[2 * q] = p.l;
         P.lr[2 * q + 1] = p.r;
-        if (P.a.stats) P.a.stats[q * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
+        if (P.a.stats) {
+            P.a.stats[q * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
+            P.a.stats[q * FROG_STAT_N + FROG_STAT_FALLBACK] = 0;
+        }
     }
 }
 
@@ -254,7 +257,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     const int smem = lps * kWavesPerBlock;
     // pool kernel: pool staging and EN list, then the re-rank list
     const int base_lds = lds_per_wave(a.L, 0);
-    const int lpw = base_lds + 2 * pool_kkeep(kkeep) * 8 + 16;
+    const int lpw = base_lds + 2 * pool_kkeep(kkeep, a.L) * 8 + 16;
     const int smem_pool = lpw * kWavesPerBlock;
     if (smem > 160 * 1024 || smem_pool > 160 * 1024)
         return fail(FROG_EUNSUPPORTED, "LDS per block %d / %d too large", smem, smem_pool);

@@ -52,8 +52,6 @@ def mix128():
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("L", [16, 24, 32, 64, 128, 256])
 def test_fp16_tiny_parity(tiny, mode, L):
-    if mode == 1:
-        L = min(L, 248)   # entry mode 1 takes L <= 248
     p = dict(SH, entry_mode=mode)
     g_ids, g_d = tiny.gpu(10, L, **p)
     o_ids, o_d, _ = tiny.cpu(10, L, **p)

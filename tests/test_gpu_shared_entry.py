@@ -93,6 +93,7 @@ def test_shared_mixture_d128_parity(mix128, L, emax, B):
     ok = np.setdiff1d(np.arange(len(g_ids)), res)
     assert (g_st[ok, F.STAT_ENTRY] == o_st[ok, oracle.STAT_ENTRY]).all()
     assert (g_st[ok, F.STAT_EXPANSIONS] == o_st[ok, oracle.STAT_EXPANSIONS]).all()
+    assert g_st[:, F.STAT_FALLBACK].mean() < 0.01
 
 
 def test_shared_k100_pool248(mix128):
@@ -104,12 +105,21 @@ def test_shared_k100_pool248(mix128):
 
 
 @pytest.mark.parametrize("L", [249, 256])
-def test_shared_refuses_pools_above_248(tiny, L):
-    # 256 kept candidates per list leave no margin above such pools: refused on
-    # the host before anything is enqueued
-    with pytest.raises(F.FrogError) as e:
-        tiny.gpu(10, L, **SH)
-    assert e.value.code == -7 and "L=%d" % L in str(e.value)
+def test_shared_pools_above_248(tiny, L):
+    # pools above 248: 256 candidates per work item, 512 merged
+    g_ids, g_d = tiny.gpu(10, L, **SH)
+    o_ids, o_d, _ = tiny.cpu(10, L, **SH)
+    assert_parity(g_ids, g_d, o_ids, o_d)
+
+
+def test_shared_k100_pool256(mix128):
+    # the 512-entry merged list leaves the margin test room: few queries fall
+    # back to evaluating their whole sample
+    p = dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=3000)
+    g_ids, g_d, g_st = mix128.gpu(100, 256, stats=True, **p)
+    o_ids, o_d, _ = mix128.cpu(100, 256, **p)
+    assert_parity(g_ids, g_d, o_ids, o_d)
+    assert g_st[:, F.STAT_FALLBACK].mean() < 0.05
 
 
 def test_unprepared_seed_is_refused(tiny):

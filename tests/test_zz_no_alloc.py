@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 
 # statistics columns that depend on the tiles the planning forms (bucket
 # order follows atomic arrival): the scan's row counts
-TILE_COLUMNS = (F.STAT_SCANROWS,)
+TILE_COLUMNS = (F.STAT_SCANROWS, F.STAT_FALLBACK)
 
 
 def _ptr(t):
