@@ -28,7 +28,8 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
     {
         const int64_t qi = (int64_t)blockIdx.x * kWavesPerBlock + wave;
         if (qi >= A.nq) return;   // wave-uniform; no workgroup barrier follows
-        const SPlan p = P.plan[qi];
+        const SPlan* pp = P.plan + qi;
+        const SPlan p = *pp;
         if (p.l > p.r) return;
         QueryCtx<C, XT> Q;
         Q.load(ix, A, P.lr, qi);
@@ -37,49 +38,75 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
         Q.T = p.T;
         Q.pkey = A.lv.key;
 
-        // the kkeep smallest approximate distances over the tile's lists
+        // the kkeep smallest approximate distances over the query's lists:
+        // window wi's tile and slot in lane wi, its chunks numbered after
+        // those of windows 0..wi-1, list i's fill, threshold and sample count
+        // in lane i
         buf_init(Lst);
-        const int64_t t = p.tslot / kSQ;
-        const int slot = p.tslot % kSQ;
-        float texcl = __int_as_float(0x7f800000);   // every row left out is at or above this
-        // the chunks' fill, threshold and sample count in lanes 0..7, then
-        // all their entries at once (no round trip between chunks)
+        const bool tiled = p.nw <= kSMaxWin;   // else no lists: the exact pass below
+        const int nwq = tiled ? p.nw : 0;
+        int wt = 0, wslot = 0, wn = 0;
+        if (lane < nwq) {
+            const int32_t ts = pp->tslot[lane];
+            wt = (ts >> 3) / kSQ;
+            wslot = (ts >> 3) % kSQ;
+            wn = (ts & 7) + 1;
+        }
+        int wbase = wn;   // inclusive prefix over lanes 0..kSMaxWin-1
+#pragma unroll
+        for (int o = 1; o < kSMaxWin; o <<= 1) {
+            const int v = __shfl_up(wbase, o);
+            if (lane >= o) wbase += v;
+        }
+        const int nl = __builtin_amdgcn_readlane(wbase, kSMaxWin - 1);   // lists, at most kSMaxWin kSMaxChunks
+        wbase -= wn;
+        int wi = 0;
+#pragma unroll
+        for (int x = 1; x < kSMaxWin; ++x)
+            if (x < nwq && __builtin_amdgcn_readlane(wbase, x) <= lane) wi = x;
+        const int lt = __shfl(wt, wi), ls = __shfl(wslot, wi), lc = lane - __shfl(wbase, wi);
+        const int64_t lid = ((int64_t)lt * P.nchunk + lc) * kSQ + ls;   // (item, slot) of list `lane`
         int mf = 0, mc = 0;
         float mt = __int_as_float(0x7f800000);
-        if (lane < kSChunks) {
-            const int64_t base = (t * kSChunks + lane) * kSQ + slot;
-            mf = P.pfill[base];
-            mt = P.pthr[base];
-            mc = P.pcnt[base];
+        if (lane < nl) {
+            mf = P.pfill[lid];
+            mt = P.pthr[lid];
+            mc = P.pcnt[lid];
         }
         int64_t ne = 0;
 #pragma unroll
-        for (int o = 1; o < kSChunks; o <<= 1) {
+        for (int o = 1; o < 64; o <<= 1) {
             mc += __shfl_xor(mc, o);
             mt = fminf(mt, __shfl_xor(mt, o));
         }
         ne = uniform(mc);
-        texcl = __int_as_float(uniform(__float_as_int(mt)));
-        constexpr int kR = KK > 64 ? KK / 64 : 1;   // entries per lane and chunk
-        float av[kSChunks][kR];
-        int32_t rw[kSChunks][kR];
+        float texcl = __int_as_float(uniform(__float_as_int(mt)));   // every row left out is at or above this
+        // several lists' entries at a time (no round trip between them)
+        constexpr int kR = KK > 64 ? KK / 64 : 1;   // entries per lane and list
+        constexpr int kG = kR == 1 ? 16 : 4;
+        for (int i0 = 0; i0 < nl; i0 += kG) {
+            float av[kG][kR];
+            int32_t rw[kG][kR];
 #pragma unroll
-        for (int c = 0; c < kSChunks; ++c) {
-            const int fi = __builtin_amdgcn_readlane(mf, c);
-            const int64_t base = (t * kSChunks + c) * kSQ + slot;
+            for (int g = 0; g < kG; ++g) {
+                const int i = (i0 + g) & 63;
+                const int fi = i0 + g < nl ? __builtin_amdgcn_readlane(mf, i) : 0;
+                const int64_t li = ((int64_t)__builtin_amdgcn_readlane((int32_t)(lid >> 32), i) << 32) |
+                                   (uint32_t)__builtin_amdgcn_readlane((int32_t)lid, i);
 #pragma unroll
-            for (int r = 0; r < kR; ++r) {
-                const int j = r * 64 + lane;
-                av[c][r] = j < fi ? P.pv[base * KK + j] : __int_as_float(0x7f800000);
-                rw[c][r] = j < fi ? P.pr[base * KK + j] : -1;
+                for (int r = 0; r < kR; ++r) {
+                    const int j = r * 64 + lane;
+                    av[g][r] = j < fi ? P.pv[li * KK + j] : __int_as_float(0x7f800000);
+                    rw[g][r] = j < fi ? P.pr[li * KK + j] : -1;
+                }
             }
-        }
 #pragma unroll
-        for (int c = 0; c < kSChunks; ++c) {
+            for (int g = 0; g < kG; ++g) {
 #pragma unroll
-            for (int r = 0; r < kR; ++r) {
-                const uint64_t gm = ballot(rw[c][r] >= 0 && av[c][r] < __int_as_float(Lst.st[1]));
-                if (gm) buf_offer<kkeep>(Lst, gm, av[c][r], rw[c][r]);
+                for (int r = 0; r < kR; ++r) {
+                    const uint64_t gm = ballot(rw[g][r] >= 0 && av[g][r] < __int_as_float(Lst.st[1]));
+                    if (gm) buf_offer<kkeep>(Lst, gm, av[g][r], rw[g][r]);
+                }
             }
         }
         buf_cut<kkeep>(Lst);
@@ -118,8 +145,8 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
             }
         }
         // margin test: a row left out has exact distance >= texcl - eps
-        bool certified = true;
-        if (!(texcl == __int_as_float(0x7f800000))) {
+        bool certified = tiled;
+        if (tiled && !(texcl == __int_as_float(0x7f800000))) {
             certified = false;
             if (pool.np >= A.L) {
                 double qsq = 0.0;

@@ -19,16 +19,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     const int lane = lane_id();
     const int wave = threadIdx.x >> 6;
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x >> 6) + wave;
-    const int64_t t = item / kSChunks;
-    const int c = (int)(item % kSChunks);
+    const int64_t t = item / P.nchunk;
+    const int c = (int)(item % P.nchunk);
     if (t >= P.tmax) return;        // wave-uniform; no workgroup barrier follows
     const STile& T = P.tiles[t];
     if (T.nq == 0) return;
     const SharedLevels& lv = P.a.lv;
     const int lev = T.lev;
     const int64_t len = (int64_t)T.ub - T.ua;
-    const int64_t c0 = T.ua + len * c / kSChunks;
-    const int64_t c1 = T.ua + len * (c + 1) / kSChunks;
+    const int nch = tile_chunks(len, P.nchunk, P.chunk_log2);
+    if (c >= nch) return;
+    const int64_t c0 = T.ua + len * c / nch;
+    const int64_t c1 = T.ua + len * (c + 1) / nch;
     const int dp = P.ix.dp, dp4 = dp >> 2, d = P.ix.d;
     constexpr int kkeep = KK;
     char* wb = smem + (size_t)wave * s_scan_lds_per_wave(kkeep);

@@ -20,23 +20,32 @@ namespace frog {
 // The sample depends on (seed, rank) only, so queries over overlapping ranges
 // at the same level draw from the same rows, and their entry distances form
 // a dense product (16 queries x a run of rows) for the fp32 matrix cores in
-// place of per-query gathers:
+// place of per-query gathers.  Each level's list is cut into windows of W
+// positions (a power of two); a query's run meets a few consecutive windows,
+// and each (query, window) pair is one slot of a tile, so that a tile covers
+// at most one window and reads only the rows of that window that its 16
+// queries' runs span:
 //   s_plan_kernel     per query (one wavefront): rank interval, threshold,
-//                     level, run in the level's list, and a bucket (level,
-//                     range midpoint) for grouping
-//   s_offsets_kernel  bucket offsets (one workgroup)
-//   s_order_kernel    the queries in bucket order
-//   s_tile_kernel     tiles of 16 consecutive queries: the union of their
-//                     runs in the finest level among them
-//   s_scan_kernel     one wavefront per (tile, eighth of the union): 16 x 16
+//                     level, run in the level's list, its windows, and per
+//                     window a bucket (window, kind and place of the pair's
+//                     piece of the run inside it)
+//   s_wprefix_kernel, s_wscan_kernel
+//                     bucket offsets, each window's places padded to a
+//                     multiple of 16
+//   s_order_kernel    the pairs in bucket order
+//   s_tile_kernel     tiles of 16 consecutive places: the span of their
+//                     pieces of the window
+//   s_scan_kernel     one wavefront per (tile, chunk of its span): 16 x 16
 //                     blocks of q.x on the matrix cores, the approximate
 //                     squared distance |q|^2 + |x|^2 - 2 q.x of each query's
 //                     sample rows, the kkeep smallest per query kept in LDS
-//   s_pool_kernel     one wavefront per query: the kkeep smallest of its
-//                     tile's lists, re-ranked with the exact canonical
-//                     distance into the pool (the L nearest entry points); a
-//                     margin test proves that no row left out could enter the
-//                     pool, else the whole sample is evaluated exactly
+//   s_pool_kernel     one wavefront per query: the kkeep smallest of all its
+//                     lists (every chunk of every window), re-ranked with the
+//                     exact canonical distance into the pool (the L nearest
+//                     entry points); a margin test proves that no row left out
+//                     could enter the pool, else the whole sample is
+//                     evaluated exactly (so is the sample of a query whose run
+//                     meets more than kSMaxWin windows)
 //   s_search_kernel   one wavefront per query (persistent grid, ~100 VGPRs,
 //                     5 wavefronts per SIMD): the traversal from that pool,
 //                     where the sample's ranks count as visited by their
@@ -45,9 +54,16 @@ namespace frog {
 // run to run; results do not, since every pool is the exact L nearest of the
 // sample.
 
-constexpr int kSQ = 16;        // queries per tile
-constexpr int kSChunks = 8;    // work items per tile
-constexpr int kSBins = 2048;   // buckets of the range midpoint per level
+constexpr int kSQ = 16;          // queries per tile
+constexpr int kSMaxChunks = 4;   // work items per tile at most
+constexpr int kSChunkRows = 512; // rows per work item at least
+constexpr int kSMaxWin = 8;      // windows per query at most (more: no tiles, an exact pass)
+static_assert(kSMaxWin * kSMaxChunks <= 64, "a query's lists fit one wavefront");
+constexpr int kSSub = 16;        // buckets per window for pieces that start at its start / inside it
+constexpr int kSFull = 32;       // buckets per window for pieces that cover it (equivalent; spread
+                                 // so that their atomic counters do not contend)
+constexpr int kSPer = 2 * kSSub + kSFull;   // buckets per window
+constexpr int kOffPer = 3;       // windows per thread of s_wscan_kernel (nwin <= 3072)
 
 struct SPlan {
     int32_t l, r;
@@ -55,10 +71,12 @@ struct SPlan {
     int32_t all;     // every rank of the range is an entry point
     int32_t lev;     // level whose list holds the sample
     int32_t a, b;    // run [a, b) of [l, r] in that list
-    int32_t bin, pos;
-    int32_t tslot;   // tile * 16 + slot (-1: empty range)
-    int32_t pad[2];
+    int32_t w0, nw;  // first window the run meets (in its level) and how many
+    int32_t pad[7];
+    int32_t pos[kSMaxWin];    // per window: place within its bucket
+    int32_t tslot[kSMaxWin];  // per window: (tile * 16 + slot) * 8 + the tile's work items - 1
 };
+static_assert(sizeof(SPlan) == 128, "plan layout");
 
 struct STile {
     int32_t q[kSQ];
@@ -66,8 +84,8 @@ struct STile {
     int32_t r[kSQ];
     uint32_t T[kSQ];
     uint32_t allmask;
-    int32_t lev;      // finest level among the tile's queries
-    int32_t ua, ub;   // run of the union of their intervals in that level's list
+    int32_t lev;      // level of the tile's window (all its pairs lie in that window)
+    int32_t ua, ub;   // span of the slots' pieces of the window, positions in the level's list
     int32_t nq;       // 0: unused tile
     int32_t pad[3];
 };
@@ -77,20 +95,26 @@ struct SParams {
     SearchLaunch a;
     int32_t* lr;        // [nq][2] rank intervals (written by s_plan_kernel)
     SPlan* plan;
-    uint32_t* hist;     // [nbins] queries per bucket
-    uint32_t* bstart;   // [nbins] first place of each bucket
+    uint32_t* hist;     // [nbins] pairs per bucket
+    uint32_t* bstart;   // [nbins] first place of each bucket within its window
+    uint32_t* wstart;   // [nwin] first place of each window
     uint32_t* meta;     // [0] places used in `order`, [1] tiles, [2] query counter
-    int32_t* order;     // [nq + 16 (nlev + 1)] queries by bucket, each level's run
-                        // padded to a multiple of 16 with -1 (no tile spans two levels)
+    int32_t* order;     // [norder] pairs (query * kSMaxWin + window index) by bucket,
+                        // each window's places padded to a multiple of 16 with -1
     STile* tiles;       // [tmax]
     int64_t tmax;
-    int nbins;
+    int nbins;          // nwin * kSPer
+    int nwin;           // windows of all levels
+    int win_log2;       // W = 2^win_log2 positions per window
+    int nchunk;         // work items per tile at most (<= kSMaxChunks)
+    int chunk_log2;     // a tile's span is split into chunks of at least 2^chunk_log2 = W / nchunk rows
+    int32_t winbase[34];  // first window of level j; winbase[nlev + 1] = nwin
     int kkeep;
-    float* pv;          // [tmax * kSChunks][16][kkeep] approximate distances
-    int32_t* pr;        // [tmax * kSChunks][16][kkeep] ranks
-    float* pthr;        // [tmax * kSChunks][16] threshold of a full list, else +inf
-    int32_t* pfill;     // [tmax * kSChunks][16] entries kept
-    int32_t* pcnt;      // [tmax * kSChunks][16] sample rows seen
+    float* pv;          // [tmax * nchunk][16][kkeep] approximate distances
+    int32_t* pr;        // [tmax * nchunk][16][kkeep] ranks
+    float* pthr;        // [tmax * nchunk][16] threshold of a full list, else +inf
+    int32_t* pfill;     // [tmax * nchunk][16] entries kept
+    int32_t* pcnt;      // [tmax * nchunk][16] sample rows seen
     uint64_t* pools;    // [nq][64 LP] the L nearest sample points per query (sorted keys)
     int32_t* pne;       // [nq] sample size
     uint32_t* gvis;
@@ -120,31 +144,28 @@ __device__ __forceinline__ int32_t level_rank(const SharedLevels& lv, int j, int
     return j == 0 ? (int32_t)pos : lv.ranks[lv.off[j] + pos];
 }
 
-// first position of level j's list whose rank is >= x.  One thread: a
-// 16-ary search whose 15 probes per round are independent loads (about 5
-// dependent rounds at n = 1M instead of 20 binary steps), then a binary
-// search over the last 16 positions.
-__device__ int64_t level_lower(const SharedLevels& lv, int64_t n, int j, int64_t x) {
-    if (j == 0) return x < 0 ? 0 : (x > n ? n : x);
-    const int32_t* a = lv.ranks + lv.off[j];
-    // the answer lies in [lo, hi]: a[i] < x for i < lo, a[hi] >= x or hi = end
-    int64_t lo = 0, hi = lv.off[j + 1] - lv.off[j];
-    while (hi - lo > 16) {
-        const int64_t step = (hi - lo) / 16;   // probes lo + t step, t = 1..15, all < hi
-        int c = 0;
-#pragma unroll
-        for (int t = 1; t < 16; ++t) c += a[lo + t * step] < x ? 1 : 0;
-        // the ranks ascend: probes 1..c are below x, c + 1 .. 15 are not
-        const int64_t nlo = c > 0 ? lo + c * step + 1 : lo;
-        if (c < 15) hi = lo + (c + 1) * step;
-        lo = nlo;
-    }
-    while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (a[mid] < x) lo = mid + 1;
-        else hi = mid;
-    }
-    return lo;
+// work items of a tile whose span is `span` rows: chunks of at least
+// 2^chunk_log2 rows, at most nchunk
+__host__ __device__ __forceinline__ int tile_chunks(int64_t span, int nchunk, int chunk_log2) {
+    const int64_t c = (span + ((int64_t)1 << chunk_log2) - 1) >> chunk_log2;
+    return c < 1 ? 1 : (c < nchunk ? (int)c : nchunk);
+}
+
+// bucket of window wi of query q's run: its window, then the kind of piece
+// (pieces that start at the window's start and end inside it, by where they
+// end; pieces that cover the window; pieces that start inside it, by where
+// they start), so that the pieces of a tile's 16 places lie close
+__device__ __forceinline__ int pair_bin(const SParams& P, int64_t q, int lev, int32_t a, int32_t b, int32_t w0,
+                                        int wi) {
+    const int64_t ws = (int64_t)(w0 + wi) << P.win_log2;
+    const int64_t we = ws + ((int64_t)1 << P.win_log2);
+    const int64_t sa = a > ws ? a : ws;
+    const int64_t sb = b < we ? b : we;
+    int sub;
+    if (sa > ws) sub = kSSub + kSFull + (int)(((sa - ws) * kSSub) >> P.win_log2);
+    else if (sb < we) sub = (int)(((sb - ws - 1) * kSSub) >> P.win_log2);
+    else sub = kSSub + (int)(q % kSFull);
+    return (P.winbase[lev] + w0 + wi) * kSPer + sub;
 }
 
 __device__ __forceinline__ uint32_t s_priority(uint64_t key, int32_t i) {

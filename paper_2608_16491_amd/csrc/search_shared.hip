@@ -47,15 +47,16 @@ __device__ int64_t half_count(const TA* __restrict__ a, int64_t n, F below) {
 
 // One wavefront per query: the rank interval of its range (the two bounds
 // searched side by side, one per half-wave), the threshold, the level, the
-// run of the level's list (again one bound per half-wave) and a bucket.
+// run of the level's list (again one bound per half-wave), its windows, and
+// a bucket and place per window (lane wi takes window wi).
 __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
     const int64_t q = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (q >= P.a.nq) return;   // wave-uniform
     const SharedLevels& lv = P.a.lv;
     const int64_t n = P.ix.n;
+    const int lane = lane_id();
     const double lo_v = P.a.lo[q], hi_v = P.a.hi[q];
     SPlan p{};
-    p.tslot = -1;
     if (isnan(lo_v) || isnan(hi_v)) {
         p.l = 0;
         p.r = -1;
@@ -65,9 +66,7 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
         p.l = __builtin_amdgcn_readlane((int32_t)c, 0);
         p.r = __builtin_amdgcn_readlane((int32_t)c, 32) - 1;
     }
-    if (p.l > p.r) {
-        p.bin = P.nbins - 1;
-    } else {
+    if (p.l <= p.r) {
         const int64_t cnt = (int64_t)p.r - p.l + 1;
         int64_t E = P.a.epn;
         if (P.a.epn_frac > 0.0) {
@@ -98,13 +97,28 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
             p.a = __builtin_amdgcn_readlane((int32_t)c, 0);
             p.b = __builtin_amdgcn_readlane((int32_t)c, 32);
         }
-        // queries sorted by the midpoint of their range share most of their
-        // runs, so a tile's union stays close to one run
-        p.bin = p.lev * kSBins + (int)((((int64_t)p.l + p.r) * kSBins) / (2 * n));
+        if (p.b > p.a) {
+            p.w0 = p.a >> P.win_log2;
+            p.nw = ((p.b - 1) >> P.win_log2) - p.w0 + 1;
+        }
     }
-    if (lane_id() == 0) {
-        p.pos = (int32_t)atomicAdd(P.hist + p.bin, 1u);
-        P.plan[q] = p;
+    // a place in the bucket of each window (none when the run meets more
+    // than kSMaxWin windows: the pool kernel then evaluates the sample exactly)
+    if (p.nw <= kSMaxWin && lane < p.nw) {
+        const int bin = pair_bin(P, q, p.lev, p.a, p.b, p.w0, lane);
+        P.plan[q].pos[lane] = (int32_t)atomicAdd(P.hist + bin, 1u);
+    }
+    if (lane == 0) {
+        SPlan* dst = P.plan + q;
+        dst->l = p.l;
+        dst->r = p.r;
+        dst->T = p.T;
+        dst->all = p.all;
+        dst->lev = p.lev;
+        dst->a = p.a;
+        dst->b = p.b;
+        dst->w0 = p.w0;
+        dst->nw = p.nw;
         P.lr[2 * q] = p.l;
         P.lr[2 * q + 1] = p.r;
         if (P.a.stats) {
@@ -114,84 +128,97 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
     }
 }
 
-// Bucket offsets: level by level, each level's run of places padded to a
-// multiple of 16; inside a level, buckets in order of the range midpoint.
-// The empty ranges' bucket comes last.  Wavefront w owns levels w and w + 16
-// (nlev <= 31); lane i owns buckets [32 i, 32 i + 32) of a level, read and
-// written as 16-byte vectors.
-__global__ __launch_bounds__(1024) void s_offsets_kernel(SParams P) {
-    static_assert(kSBins == 64 * 32, "32 buckets per lane");
-    constexpr int kWaves = 1024 / 64;
-    __shared__ uint32_t start[34];
+// Bucket offsets in two steps.  s_wprefix_kernel, one thread per window:
+// the exclusive prefix of the window's kSPer counts (its buckets in order)
+// and the window's total padded to a multiple of 16, so that no tile spans
+// two windows.  s_wscan_kernel, one workgroup: the windows' starts (levels in
+// order, windows in list order), an exclusive scan of the padded totals in
+// place; thread t owns windows [kOffPer t, kOffPer t + kOffPer) (the launch
+// keeps nwin within 1024 kOffPer).  A pair's place is then its window's
+// start + its bucket's prefix + its place in the bucket.
+__global__ __launch_bounds__(256) void s_wprefix_kernel(SParams P) {
+    constexpr int kV = kSPer / 4;   // 16-byte vectors per window
+    static_assert(kSPer % 4 == 0, "16-byte vectors");
+    const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (x >= P.nwin) return;
+    const uint4* src = reinterpret_cast<const uint4*>(P.hist + x * kSPer);
+    uint4* dst = reinterpret_cast<uint4*>(P.bstart + x * kSPer);
+    uint4 h[kV];
+#pragma unroll
+    for (int i = 0; i < kV; ++i) h[i] = src[i];
+    uint32_t run = 0;
+#pragma unroll
+    for (int i = 0; i < kV; ++i) {
+        uint4 o;
+        o.x = run;
+        run += h[i].x;
+        o.y = run;
+        run += h[i].y;
+        o.z = run;
+        run += h[i].z;
+        o.w = run;
+        run += h[i].w;
+        dst[i] = o;
+    }
+    P.wstart[x] = (run + kSQ - 1) / kSQ * kSQ;
+}
+
+__global__ __launch_bounds__(1024) void s_wscan_kernel(SParams P) {
+    __shared__ uint32_t wsum[16];
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
-    const int nlev = P.a.lv.nlev;
-    uint4 h[2][8];
-    uint32_t excl[2] = {0u, 0u};
+    uint32_t v[kOffPer];
+    uint32_t tot = 0;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const int j = w + kWaves * s;   // wave-uniform
-        uint32_t sum = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) h[s][i] = make_uint4(0u, 0u, 0u, 0u);
-        if (j <= nlev) {
-            const uint4* src = reinterpret_cast<const uint4*>(P.hist + (size_t)j * kSBins + lane * 32);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                h[s][i] = src[i];
-                sum += h[s][i].x + h[s][i].y + h[s][i].z + h[s][i].w;
-            }
-        }
-        // exclusive scan of the lanes' sums
-        uint32_t inc = sum;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t v = __shfl_up(inc, o);
-            if (lane >= o) inc += v;
-        }
-        excl[s] = inc - sum;
-        if (lane == 63 && j <= nlev) start[j + 1] = (inc + kSQ - 1) / kSQ * kSQ;
+    for (int u = 0; u < kOffPer; ++u) {
+        const int x = t * kOffPer + u;
+        v[u] = x < P.nwin ? P.wstart[x] : 0u;
+        tot += v[u];
     }
+    // exclusive scan of the threads' totals: within the wavefront, then over
+    // the 16 wavefronts
+    uint32_t inc = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t s = __shfl_up(inc, o);
+        if (lane >= o) inc += s;
+    }
+    if (lane == 63) wsum[w] = inc;
     __syncthreads();
+    uint32_t run = inc - tot, all = 0;
+    for (int i = 0; i < 16; ++i) {
+        run += i < w ? wsum[i] : 0u;
+        all += wsum[i];
+    }
+#pragma unroll
+    for (int u = 0; u < kOffPer; ++u) {
+        const int x = t * kOffPer + u;
+        if (x < P.nwin) P.wstart[x] = run;
+        run += v[u];
+    }
     if (t == 0) {
-        start[0] = 0;
-        for (int i = 1; i <= nlev + 1; ++i) start[i] += start[i - 1];
-        P.bstart[P.nbins - 1] = start[nlev + 1];
-        P.meta[0] = start[nlev + 1];
-        P.meta[1] = start[nlev + 1] / kSQ;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        const int j = w + kWaves * s;
-        if (j > nlev) continue;
-        uint32_t run = start[j] + excl[s];
-        uint4* dst = reinterpret_cast<uint4*>(P.bstart + (size_t)j * kSBins + lane * 32);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            uint4 o;
-            o.x = run;
-            run += h[s][i].x;
-            o.y = run;
-            run += h[s][i].y;
-            o.z = run;
-            run += h[s][i].z;
-            o.w = run;
-            run += h[s][i].w;
-            dst[i] = o;
-        }
+        P.meta[0] = all;
+        P.meta[1] = all / kSQ;
     }
 }
 
+// thread per query: each (query, window) pair to its place
 __global__ void s_order_kernel(SParams P) {
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= P.a.nq) return;
-    const SPlan& p = P.plan[q];
-    P.order[P.bstart[p.bin] + p.pos] = (int32_t)q;
+    const SPlan* p = P.plan + q;
+    const int nw = p->nw;
+    if (nw > kSMaxWin || p->l > p->r) return;
+    const int lev = p->lev;
+    const int32_t a = p->a, b = p->b, w0 = p->w0;
+    for (int wi = 0; wi < nw; ++wi)
+        P.order[P.wstart[P.winbase[lev] + w0 + wi] + P.bstart[pair_bin(P, q, lev, a, b, w0, wi)] + p->pos[wi]] =
+            (int32_t)(q * kSMaxWin + wi);
 }
 
-// one wavefront per tile: lanes 0..15 take its slots
+// one wavefront per tile: lanes 0..15 take its slots, each slot the piece of
+// its query's run inside the tile's window
 __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
     const int lane = lane_id();
     const int64_t t = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
@@ -199,18 +226,24 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
     const int64_t places = P.meta[0];
     STile* T = P.tiles + t;
     const int64_t i = t * kSQ + lane;
-    int32_t q = -1;
-    if (lane < kSQ && i < places) q = P.order[i];
+    int32_t e = -1;
+    if (lane < kSQ && i < places) e = P.order[i];
+    const int32_t q = e >= 0 ? e / kSMaxWin : -1;
+    const int wi = e >= 0 ? e % kSMaxWin : 0;
+    SPlan* p = P.plan + (q >= 0 ? q : 0);
     int32_t l = 0, r = -1, lev = 64, all = 0;
+    int32_t sa = 0x7FFFFFFF, sb = -1;
     uint32_t thr = 0u;
     if (q >= 0) {
-        SPlan& p = P.plan[q];
-        l = p.l;
-        r = p.r;
-        thr = p.T;
-        lev = p.lev;
-        all = p.all;
-        p.tslot = (int32_t)(t * kSQ + lane);
+        l = p->l;
+        r = p->r;
+        thr = p->T;
+        lev = p->lev;
+        all = p->all;
+        const int64_t ws = (int64_t)(p->w0 + wi) << P.win_log2;
+        const int64_t we = ws + ((int64_t)1 << P.win_log2);
+        sa = (int32_t)(p->a > ws ? p->a : ws);
+        sb = (int32_t)(p->b < we ? p->b : we);
     }
     if (lane < kSQ) {
         T->q[lane] = q;
@@ -220,22 +253,19 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
     }
     const uint64_t valid = __ballot(q >= 0);
     const uint64_t allm = __ballot(q >= 0 && all);
-    int32_t ul = q >= 0 ? l : 0x7FFFFFFF, ur = q >= 0 ? r : -1, lv = lev;
+    int32_t ua = sa, ub = sb, lv = lev;
 #pragma unroll
     for (int o = 1; o < kSQ; o <<= 1) {
-        ul = min(ul, __shfl_xor(ul, o));
-        ur = max(ur, __shfl_xor(ur, o));
+        ua = min(ua, __shfl_xor(ua, o));
+        ub = max(ub, __shfl_xor(ub, o));
         lv = min(lv, __shfl_xor(lv, o));
     }
-    ul = uniform(ul);
-    ur = uniform(ur);
+    ua = uniform(ua);
+    ub = uniform(ub);
     lv = uniform(lv);
     const int nq = __popcll(valid);
-    // lane 0: the union's first position, lane 1: its end
-    int64_t pos = 0;
-    if (nq > 0 && lane < 2) pos = level_lower(P.a.lv, P.ix.n, lv, lane == 0 ? (int64_t)ul : (int64_t)ur + 1);
-    const int32_t ua = __builtin_amdgcn_readlane((int32_t)pos, 0);
-    const int32_t ub = __builtin_amdgcn_readlane((int32_t)pos, 1);
+    static_assert(kSMaxChunks <= 8, "chunk count in 3 bits");
+    if (q >= 0) p->tslot[wi] = (int32_t)((t * kSQ + lane) * 8 + tile_chunks((int64_t)ub - ua, P.nchunk, P.chunk_log2) - 1);
     if (lane == 0) {
         T->allmask = (uint32_t)allm;
         T->lev = nq > 0 ? lv : 0;
@@ -282,9 +312,40 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     SParams P{};
     P.ix = ix;
     P.a = a;
-    const int64_t norder = a.nq + (int64_t)kSQ * (a.lv.nlev + 1);
+    // (the plan packs a pair's tile, slot and chunk count in one int32)
+    if (a.nq > ((int64_t)1 << 24))
+        return fail(FROG_EUNSUPPORTED, "entry_mode 1 takes at most 2^24 queries per call (nq=%lld)", (long long)a.nq);
+    // windows: W >= 1024 positions, at least 2/5 of the largest sample (a
+    // run, about E to 2E positions, then meets at most about 6 windows) and
+    // at least n / 1024 (about 2048 windows over all levels); wider while the
+    // levels hold more windows than the offsets kernel takes
+    {
+        const int64_t emax = a.epn_frac > 0.0 && a.epn_max > a.epn ? a.epn_max : a.epn;
+        int lg = 10;
+        while (((int64_t)1 << lg) < (2 * emax + 4) / 5 || ((int64_t)1 << lg) * 1024 < ix.n) ++lg;
+        for (;; ++lg) {
+            const int64_t W = (int64_t)1 << lg;
+            int64_t nw = 0;
+            for (int j = 0; j <= a.lv.nlev; ++j) {
+                P.winbase[j] = (int32_t)nw;
+                const int64_t len = j == 0 ? ix.n : a.lv.off[j + 1] - a.lv.off[j];
+                nw += (len + W - 1) / W;
+            }
+            P.winbase[a.lv.nlev + 1] = (int32_t)nw;
+            P.nwin = (int)nw;
+            if (nw <= 1024 * kOffPer) break;   // what s_wscan_kernel takes
+        }
+        P.win_log2 = lg;
+        const int64_t W = (int64_t)1 << lg;
+        // chunks of W / nchunk rows, at least kSChunkRows: 2 of 512 at
+        // W = 1024, 4 of W / 4 from W = 2048 on
+        P.nchunk = W / kSChunkRows < kSMaxChunks ? (int)(W / kSChunkRows) : kSMaxChunks;
+        P.chunk_log2 = lg - (P.nchunk == 4 ? 2 : (P.nchunk == 2 ? 1 : 0));
+    }
+    // places: at most kSMaxWin pairs per query, plus up to 15 of padding per window
+    const int64_t norder = (int64_t)kSMaxWin * a.nq + (int64_t)kSQ * P.nwin;
     P.tmax = (norder + kSQ - 1) / kSQ;
-    P.nbins = (a.lv.nlev + 1) * kSBins + 1;
+    P.nbins = P.nwin * kSPer;
     P.kkeep = kkeep;
     P.lds_per_wave = lpw;
     P.lds_list = base_lds;
@@ -292,7 +353,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     int blocks = max_blocks((const void*)sfn, smem);
     const int64_t need = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     if (need < blocks) blocks = (int)need;
-    const int64_t items = P.tmax * kSChunks;
+    const int64_t items = P.tmax * P.nchunk;
     auto align = [](size_t x) { return (x + 255) / 256 * 256; };
     size_t off = 0;
     auto take = [&](size_t bytes) { const size_t o = off; off += align(bytes); return o; };
@@ -301,6 +362,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     const size_t o_plan = take((size_t)a.nq * sizeof(SPlan));
     const size_t o_hist = take((size_t)P.nbins * 4);
     const size_t o_bstart = take((size_t)P.nbins * 4);
+    const size_t o_wstart = take((size_t)P.nwin * 4);
     const size_t o_order = take((size_t)norder * 4);
     const size_t o_tiles = take((size_t)P.tmax * sizeof(STile));
     const size_t o_pv = take((size_t)items * kSQ * kkeep * 4);
@@ -339,6 +401,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     P.plan = reinterpret_cast<SPlan*>(base + o_plan);
     P.hist = reinterpret_cast<uint32_t*>(base + o_hist);
     P.bstart = reinterpret_cast<uint32_t*>(base + o_bstart);
+    P.wstart = reinterpret_cast<uint32_t*>(base + o_wstart);
     P.order = reinterpret_cast<int32_t*>(base + o_order);
     P.tiles = reinterpret_cast<STile*>(base + o_tiles);
     P.pv = reinterpret_cast<float*>(base + o_pv);
@@ -359,7 +422,8 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
                        P.nbins, P.order, norder);
     const int64_t plan_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL(s_plan_kernel, dim3((unsigned)plan_blocks), dim3(kBlock), 0, stream, P);
-    hipLaunchKernelGGL(s_offsets_kernel, dim3(1), dim3(1024), 0, stream, P);
+    hipLaunchKernelGGL(s_wprefix_kernel, dim3((unsigned)((P.nwin + 255) / 256)), dim3(256), 0, stream, P);
+    hipLaunchKernelGGL(s_wscan_kernel, dim3(1), dim3(1024), 0, stream, P);
     hipLaunchKernelGGL(s_order_kernel, dim3(qb), dim3(256), 0, stream, P);
     hipLaunchKernelGGL(s_tile_kernel, dim3((unsigned)((P.tmax + kWavesPerBlock - 1) / kWavesPerBlock)), dim3(kBlock),
                        0, stream, P);
