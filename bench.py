@@ -27,6 +27,7 @@ reported beside it.
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
 import argparse
+import gc
 import atexit
 import hashlib
 import json
@@ -479,25 +480,37 @@ def main():
         F.search(ix, Qd, lod, hid, k, L, out=(ids_d, ds_d), **p_sel)
         host_out.copy_(dev_out, non_blocking=True)
 
-    # warm-up: the first steps that mix copies and kernels after a
-    # synchronisation pay a one-time cost of a few milliseconds (seen with
-    # any search entry point and without allocation), so the untimed steps run
-    # in two rounds with a synchronisation between them
-    for rnd in range(2):
-        for _ in range(max(1, args.warmup)):
-            step()
+    def event_loop(nsteps):
+        # a marker event between steps; torch creates an event at its first
+        # record, so every marker is recorded once before the loop (creating
+        # timing events inside the loop cost one step a few milliseconds now
+        # and then)
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps + 1)]
+        for ev in marks:
+            ev.record(stream)
         torch.cuda.synchronize()
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    marks[0].record(stream)
-    for i in range(args.steps):
-        step()
-        marks[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
-    per_step = marks[0].elapsed_time(marks[-1]) / 1000.0 / args.steps
+        t0 = time.perf_counter()
+        marks[0].record(stream)
+        for i in range(nsteps):
+            step()
+            marks[i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return [marks[i].elapsed_time(marks[i + 1]) for i in range(nsteps)], \
+            marks[0].elapsed_time(marks[-1]) / 1000.0 / nsteps, wall
+
+    # warm-up: the same loop, untimed, for at least two rounds and a quarter
+    # of a second (a process's first fraction of a second of such steps has
+    # shown a one-time stall of a few milliseconds); the collector of Python
+    # objects is paused while steps are enqueued
+    gc.disable()
+    t_warm = time.perf_counter()
+    rounds = 0
+    while rounds < 2 or time.perf_counter() - t_warm < 0.25:
+        event_loop(max(1, args.warmup))
+        rounds += 1
+    step_ms, per_step, wall = event_loop(args.steps)
+    gc.enable()
     per_step_med = float(np.median(step_ms)) / 1000.0
     qps = w.nq / per_step
     # the transfers' result equals the resident search's
@@ -548,8 +561,10 @@ def main():
         stream.wait_stream(cs)
 
     pipelined(args.warmup)
-    torch.cuda.synchronize()
     pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pe0.record(stream)                      # created at their first record, before the timed region
+    pe1.record(stream)
+    torch.cuda.synchronize()
     pe0.record(stream)
     cs.wait_event(pe0)
     pipelined(args.steps)
@@ -568,12 +583,16 @@ def main():
         for ev in trio:
             ev.record(stream)            # materialise the events
     ev_s, ev_e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev_s.record(stream)
+    ev_e.record(stream)
+    gc.disable()
     torch.cuda.synchronize()
     ev_s.record(stream)
     for i in range(args.steps):
         run(sel, events=phase[i])
     ev_e.record(stream)
     torch.cuda.synchronize()
+    gc.enable()
     per_step_res = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
     t_a = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
     t_b = sum(t[1].elapsed_time(t[2]) for t in phase) / 1000.0 / args.steps
@@ -620,7 +639,8 @@ def main():
         scan_tf = useful / t_a / 1e12
         # pool + traversal: the sample's re-ranked candidates, the traversal's
         # distinct evaluations, the ENC entries and the per-query terms
-        kkeep = 64 if L + 8 <= 64 else (128 if L + 8 <= 128 else 256)
+        # (the pool kernel's merged list: 64, 128 or 256 entries, 512 above L = 248)
+        kkeep = 64 if L + 8 <= 64 else (128 if L + 8 <= 128 else (256 if L <= 248 else 512))
         rerank = int(np.minimum(st_e[:, F.STAT_ENTRY], kkeep).sum())
         trav_bytes = eb * d * (D - NE) + 4.0 * S + per_query
         search_bytes = eb * d * rerank + trav_bytes
@@ -637,7 +657,8 @@ def main():
                                          "alg_bytes": search_bytes, "GB_s": a_search,
                                          "frac": a_search / HBM_PEAK_GBS,
                                          "traversal_alg_bytes": trav_bytes,
-                                         "traversal_GB_s": trav_bytes / t_b / 1e9}}
+                                         "traversal_GB_s": trav_bytes / t_b / 1e9,
+                                         "expansions": int(st_e[:, F.STAT_EXPANSIONS].sum())}}
         if t_a >= t_b:
             dominant = "s_scan_kernel"
             roof = {"bound": "mfma", "kernel": dominant, "achieved": scan_tf, "peak": FP32_MFMA_PEAK_TFLOPS,

@@ -234,7 +234,7 @@ int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
  * freed here, so searches on several streams or threads may share an index
  * whatever their seeds.  The per-call workspace (counters, rank intervals,
  * chunk pools; in entry_mode 1 plans, tiles, candidate lists and pools: about
- * 5 KB per query at L <= 56 in entry_mode 1) is a device buffer the library
+ * 7 KB per query at L <= 40) is a device buffer the library
  * keeps per (device, stream) for the life of the process, grown
  * stream-ordered when a call needs more, so repeated calls allocate nothing;
  * threads enqueueing on one stream take turns, other streams have their own
@@ -249,7 +249,7 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
  * frog_search_ex (same arguments, same results, same errors), except that the
  * per-call workspace (work counters, rank intervals, chunk pools; in
  * entry_mode 1 the plans, tiles, candidate lists and pools) lives in a fixed
- * 64 MiB array of device memory inside the library instead of coming from
+ * 128 MiB array of device memory inside the library instead of coming from
  * hipMallocAsync.  Nothing is allocated or freed by this call.
  *   - Each GPU the library runs on holds its own array until the process
  *     ends; its address is looked up once per device, on the first call there.
@@ -257,14 +257,15 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
  *     last call's contents (the kernels clear what must start at zero):
  *     calls that overlap on one GPU (other streams, other threads) race and
  *     must be serialised by the caller.
- *   - A call whose workspace exceeds 64 MiB is refused with FROG_EUNSUPPORTED
+ *   - A call whose workspace exceeds 128 MiB is refused with FROG_EUNSUPPORTED
  *     before anything is enqueued.  Roughly: entry_mode 0 needs 12 bytes per
  *     query plus, when the entry count exceeds one 768-point chunk,
  *     512 * ceil(L/64) bytes per chunk (about 2 KB per query at 2,560 entry
- *     points and L <= 64); entry_mode 1 about 4.8 KB per query at L <= 56
- *     (about 13,900 queries per call), 9.4 KB up to L = 120 and 18.6 KB up to
- *     L = 256; the exact visited set (hash_log2 = 0) adds n/8 bytes per
- *     resident wavefront and is refused at realistic n.
+ *     points and L <= 64); entry_mode 1 at n = 1M about 7.2 KB per query at
+ *     L <= 40 (about 18,400 queries per call), 9.2 KB up to L = 56, 17.9 KB
+ *     up to L = 120 and 35 KB up to L = 256, plus about 2 MB; the exact
+ *     visited set (hash_log2 = 0) adds n/8 bytes per resident wavefront and
+ *     is refused at realistic n.
  *   - entry_mode 1 needs the seed prepared (frog_index_prepare_sample). */
 int frog_search_noalloc(const frog_index_t* idx, const float* d_queries, int64_t nq,
                         const double* d_lo, const double* d_hi, int k, int L,

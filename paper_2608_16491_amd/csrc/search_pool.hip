@@ -39,19 +39,13 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
         Q.pkey = A.lv.key;
 
         // the kkeep smallest approximate distances over the query's lists:
-        // window wi's tile and slot in lane wi, its chunks numbered after
-        // those of windows 0..wi-1, list i's fill, threshold and sample count
-        // in lane i
+        // window wi's chunk count in lane wi, its chunks numbered after those
+        // of windows 0..wi-1, list i's fill, threshold and sample count in
+        // lane i
         buf_init(Lst);
         const bool tiled = p.nw <= kSMaxWin;   // else no lists: the exact pass below
         const int nwq = tiled ? p.nw : 0;
-        int wt = 0, wslot = 0, wn = 0;
-        if (lane < nwq) {
-            const int32_t ts = pp->tslot[lane];
-            wt = (ts >> 3) / kSQ;
-            wslot = (ts >> 3) % kSQ;
-            wn = (ts & 7) + 1;
-        }
+        const int wn = lane < nwq ? pp->wchunks[lane] : 0;
         int wbase = wn;   // inclusive prefix over lanes 0..kSMaxWin-1
 #pragma unroll
         for (int o = 1; o < kSMaxWin; o <<= 1) {
@@ -64,8 +58,8 @@ __global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
 #pragma unroll
         for (int x = 1; x < kSMaxWin; ++x)
             if (x < nwq && __builtin_amdgcn_readlane(wbase, x) <= lane) wi = x;
-        const int lt = __shfl(wt, wi), ls = __shfl(wslot, wi), lc = lane - __shfl(wbase, wi);
-        const int64_t lid = ((int64_t)lt * P.nchunk + lc) * kSQ + ls;   // (item, slot) of list `lane`
+        const int lc = lane - __shfl(wbase, wi);
+        const int64_t lid = (qi * kSMaxWin + wi) * P.nchunk + lc;   // list `lane`: (pair, chunk)
         int mf = 0, mc = 0;
         float mt = __int_as_float(0x7f800000);
         if (lane < nl) {

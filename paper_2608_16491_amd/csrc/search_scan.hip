@@ -46,7 +46,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     // feeds two K steps).
     const int ii = lane & 15;
     const int kk = lane >> 4;
-    const int qrow = T.q[ii];
+    const int qrow = T.pair[ii] >= 0 ? T.pair[ii] / kSMaxWin : -1;
     const float* Qr = P.a.Q + (int64_t)(qrow >= 0 ? qrow : 0) * d;
     auto qchunk = [&](int u) -> float4 {
         const int b = sizeof(XT) == 4 ? 16 * u + 4 * kk : 32 * (u >> 1) + 8 * kk + 4 * (u & 1);
@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         ql[e] = T.l[sl];
         qr[e] = T.r[sl];
         qT[e] = T.T[sl];
-        qv[e] = T.q[sl] >= 0;
+        qv[e] = T.pair[sl] >= 0;
         qall[e] = (T.allmask >> sl) & 1u;
     }
     uint32_t scnt[4] = {0u, 0u, 0u, 0u};   // sample rows of slot 4kk + e seen by this lane
@@ -237,8 +237,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     // the item's lists: entries kept, threshold, sample rows seen
     if (P.a.stats && lane == 0) {
         int first = 0;
-        while (first < kSQ - 1 && T.q[first] < 0) ++first;
-        atomicAdd(P.a.stats + (int64_t)T.q[first] * FROG_STAT_N + FROG_STAT_SCANROWS, (int32_t)(nblk * 16));
+        while (first < kSQ - 1 && T.pair[first] < 0) ++first;
+        atomicAdd(P.a.stats + (int64_t)(T.pair[first] / kSMaxWin) * FROG_STAT_N + FROG_STAT_SCANROWS,
+                  (int32_t)(nblk * 16));
     }
     // the lists' states to LDS for the last cuts and the write-out
     {
@@ -258,21 +259,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     for (int g = 0; g < 4; ++g)
 #pragma unroll
         for (int e = 0; e < 4; ++e) scount[4 * g + e] = (uint32_t)__shfl((int)scnt[e], 16 * g);
-    const int64_t base = item * kSQ;
+    // slot i's list: (its pair, this chunk)
 #pragma unroll
     for (int i = 0; i < kSQ; ++i) {
+        const int32_t pid = T.pair[i];
+        if (pid < 0) continue;   // uniform: an empty slot has no list
+        const int64_t lid = (int64_t)pid * P.nchunk + c;
         buf_cut<kkeep>(list_of(i));
         const int fi = __builtin_amdgcn_readfirstlane(lst[2 * i]);
         const uint64_t* kb = lkey + (size_t)i * 2 * kkeep;
         for (int j = lane; j < fi; j += 64) {
             const uint64_t key = kb[j];
-            P.pv[(base + i) * kkeep + j] = ord_value((uint32_t)(key >> 32));
-            P.pr[(base + i) * kkeep + j] = (int32_t)(uint32_t)key;
+            P.pv[lid * kkeep + j] = ord_value((uint32_t)(key >> 32));
+            P.pr[lid * kkeep + j] = (int32_t)(uint32_t)key;
         }
         if (lane == 0) {
-            P.pthr[base + i] = __int_as_float(lst[2 * i + 1]);   // +inf unless a cut dropped rows
-            P.pfill[base + i] = fi;
-            P.pcnt[base + i] = (int32_t)scount[i];
+            P.pthr[lid] = __int_as_float(lst[2 * i + 1]);   // +inf unless a cut dropped rows
+            P.pfill[lid] = fi;
+            P.pcnt[lid] = (int32_t)scount[i];
         }
     }
 }

@@ -74,12 +74,12 @@ struct SPlan {
     int32_t w0, nw;  // first window the run meets (in its level) and how many
     int32_t pad[7];
     int32_t pos[kSMaxWin];    // per window: place within its bucket
-    int32_t tslot[kSMaxWin];  // per window: (tile * 16 + slot) * 8 + the tile's work items - 1
+    int32_t wchunks[kSMaxWin];  // per window: work items of the pair's tile (its chunk lists)
 };
 static_assert(sizeof(SPlan) == 128, "plan layout");
 
 struct STile {
-    int32_t q[kSQ];
+    int32_t pair[kSQ];   // query * kSMaxWin + window index (-1: empty slot)
     int32_t l[kSQ];
     int32_t r[kSQ];
     uint32_t T[kSQ];
@@ -110,11 +110,13 @@ struct SParams {
     int chunk_log2;     // a tile's span is split into chunks of at least 2^chunk_log2 = W / nchunk rows
     int32_t winbase[34];  // first window of level j; winbase[nlev + 1] = nwin
     int kkeep;
-    float* pv;          // [tmax * nchunk][16][kkeep] approximate distances
-    int32_t* pr;        // [tmax * nchunk][16][kkeep] ranks
-    float* pthr;        // [tmax * nchunk][16] threshold of a full list, else +inf
-    int32_t* pfill;     // [tmax * nchunk][16] entries kept
-    int32_t* pcnt;      // [tmax * nchunk][16] sample rows seen
+    // candidate lists, one per (pair, chunk of the pair's tile): list
+    // (query * kSMaxWin + window index) * nchunk + chunk
+    float* pv;          // [nq * kSMaxWin * nchunk][kkeep] approximate distances
+    int32_t* pr;        // [nq * kSMaxWin * nchunk][kkeep] ranks
+    float* pthr;        // [nq * kSMaxWin * nchunk] threshold of a full list, else +inf
+    int32_t* pfill;     // [nq * kSMaxWin * nchunk] entries kept
+    int32_t* pcnt;      // [nq * kSMaxWin * nchunk] sample rows seen
     uint64_t* pools;    // [nq][64 LP] the L nearest sample points per query (sorted keys)
     int32_t* pne;       // [nq] sample size
     uint32_t* gvis;

@@ -246,7 +246,7 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
         sb = (int32_t)(p->b < we ? p->b : we);
     }
     if (lane < kSQ) {
-        T->q[lane] = q;
+        T->pair[lane] = e;
         T->l[lane] = l;
         T->r[lane] = r;
         T->T[lane] = thr;
@@ -264,8 +264,7 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
     ub = uniform(ub);
     lv = uniform(lv);
     const int nq = __popcll(valid);
-    static_assert(kSMaxChunks <= 8, "chunk count in 3 bits");
-    if (q >= 0) p->tslot[wi] = (int32_t)((t * kSQ + lane) * 8 + tile_chunks((int64_t)ub - ua, P.nchunk, P.chunk_log2) - 1);
+    if (q >= 0) p->wchunks[wi] = tile_chunks((int64_t)ub - ua, P.nchunk, P.chunk_log2);
     if (lane == 0) {
         T->allmask = (uint32_t)allm;
         T->lev = nq > 0 ? lv : 0;
@@ -312,9 +311,9 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     SParams P{};
     P.ix = ix;
     P.a = a;
-    // (the plan packs a pair's tile, slot and chunk count in one int32)
-    if (a.nq > ((int64_t)1 << 24))
-        return fail(FROG_EUNSUPPORTED, "entry_mode 1 takes at most 2^24 queries per call (nq=%lld)", (long long)a.nq);
+    // (a pair id, query * kSMaxWin + window index, is an int32)
+    if (a.nq > ((int64_t)1 << 28))
+        return fail(FROG_EUNSUPPORTED, "entry_mode 1 takes at most 2^28 queries per call (nq=%lld)", (long long)a.nq);
     // windows: W >= 1024 positions, at least 2/5 of the largest sample (a
     // run, about E to 2E positions, then meets at most about 6 windows) and
     // at least n / 1024 (about 2048 windows over all levels); wider while the
@@ -338,8 +337,10 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
         P.win_log2 = lg;
         const int64_t W = (int64_t)1 << lg;
         // chunks of W / nchunk rows, at least kSChunkRows: 2 of 512 at
-        // W = 1024, 4 of W / 4 from W = 2048 on
-        P.nchunk = W / kSChunkRows < kSMaxChunks ? (int)(W / kSChunkRows) : kSMaxChunks;
+        // W = 1024, 4 of W / 4 from W = 2048 on (2 for 256-entry lists,
+        // whose cuts and merges cost more per list)
+        const int cmax = kkeep >= 256 ? 2 : kSMaxChunks;
+        P.nchunk = W / kSChunkRows < cmax ? (int)(W / kSChunkRows) : cmax;
         P.chunk_log2 = lg - (P.nchunk == 4 ? 2 : (P.nchunk == 2 ? 1 : 0));
     }
     // places: at most kSMaxWin pairs per query, plus up to 15 of padding per window
@@ -365,11 +366,12 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     const size_t o_wstart = take((size_t)P.nwin * 4);
     const size_t o_order = take((size_t)norder * 4);
     const size_t o_tiles = take((size_t)P.tmax * sizeof(STile));
-    const size_t o_pv = take((size_t)items * kSQ * kkeep * 4);
-    const size_t o_pr = take((size_t)items * kSQ * kkeep * 4);
-    const size_t o_pthr = take((size_t)items * kSQ * 4);
-    const size_t o_pfill = take((size_t)items * kSQ * 4);
-    const size_t o_pcnt = take((size_t)items * kSQ * 4);
+    const int64_t nlists = a.nq * kSMaxWin * P.nchunk;   // (pair, chunk)
+    const size_t o_pv = take((size_t)nlists * kkeep * 4);
+    const size_t o_pr = take((size_t)nlists * kkeep * 4);
+    const size_t o_pthr = take((size_t)nlists * 4);
+    const size_t o_pfill = take((size_t)nlists * 4);
+    const size_t o_pcnt = take((size_t)nlists * 4);
     const int lp = lp_of(a.L);
     const size_t o_pools = take((size_t)a.nq * 64 * lp * 8);
     const size_t o_pne = take((size_t)a.nq * 4);
