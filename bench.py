@@ -482,20 +482,23 @@ def main():
 
     def event_loop(nsteps):
         # a marker event between steps; torch creates an event at its first
-        # record, so every marker is recorded once before the loop (creating
-        # timing events inside the loop cost one step a few milliseconds now
-        # and then)
+        # record, so every marker is recorded once before the loop.  One
+        # untimed step is enqueued before the first marker, so that the timed
+        # steps start behind work already queued, as in the steady state
+        # (started from an idle device, the first step also timed the host
+        # enqueueing its copy: 2-3 ms at 50 MB)
         marks = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps + 1)]
         for ev in marks:
             ev.record(stream)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        step()
         marks[0].record(stream)
         for i in range(nsteps):
             step()
             marks[i + 1].record(stream)
         torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
+        wall = (time.perf_counter() - t0) * nsteps / (nsteps + 1)   # host clock, per timed step's share
         return [marks[i].elapsed_time(marks[i + 1]) for i in range(nsteps)], \
             marks[0].elapsed_time(marks[-1]) / 1000.0 / nsteps, wall
 

@@ -234,7 +234,7 @@ int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
  * freed here, so searches on several streams or threads may share an index
  * whatever their seeds.  The per-call workspace (counters, rank intervals,
  * chunk pools; in entry_mode 1 plans, tiles, candidate lists and pools: about
- * 7 KB per query at L <= 40) is a device buffer the library
+ * 4 KB per query at L <= 40) is a device buffer the library
  * keeps per (device, stream) for the life of the process, grown
  * stream-ordered when a call needs more, so repeated calls allocate nothing;
  * threads enqueueing on one stream take turns, other streams have their own
@@ -261,8 +261,8 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
  *     before anything is enqueued.  Roughly: entry_mode 0 needs 12 bytes per
  *     query plus, when the entry count exceeds one 768-point chunk,
  *     512 * ceil(L/64) bytes per chunk (about 2 KB per query at 2,560 entry
- *     points and L <= 64); entry_mode 1 at n = 1M about 7.2 KB per query at
- *     L <= 40 (about 18,400 queries per call), 9.2 KB up to L = 56, 17.9 KB
+ *     points and L <= 64); entry_mode 1 at n = 1M about 4.0 KB per query at
+ *     L <= 40 (about 33,000 queries per call), 5.0 KB up to L = 56, 9.6 KB
  *     up to L = 120 and 35 KB up to L = 256, plus about 2 MB; the exact
  *     visited set (hash_log2 = 0) adds n/8 bytes per resident wavefront and
  *     is refused at realistic n.

@@ -56,7 +56,7 @@ namespace frog {
 
 constexpr int kSQ = 16;          // queries per tile
 constexpr int kSMaxChunks = 4;   // work items per tile at most
-constexpr int kSChunkRows = 512; // rows per work item at least
+constexpr int kSChunkRows = 1024;  // rows per work item at least
 constexpr int kSMaxWin = 8;      // windows per query at most (more: no tiles, an exact pass)
 static_assert(kSMaxWin * kSMaxChunks <= 64, "a query's lists fit one wavefront");
 constexpr int kSSub = 16;        // buckets per window for pieces that start at its start / inside it

@@ -336,9 +336,13 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
         }
         P.win_log2 = lg;
         const int64_t W = (int64_t)1 << lg;
-        // chunks of W / nchunk rows, at least kSChunkRows: 2 of 512 at
-        // W = 1024, 4 of W / 4 from W = 2048 on (2 for 256-entry lists,
-        // whose cuts and merges cost more per list)
+        // chunks of W / nchunk rows, at least kSChunkRows: one per tile at
+        // W = 1024, up to 4 of W / 4 above (2 for 256-entry lists, whose
+        // cuts and merges cost more per list).  A work item's fixed cost
+        // (the 16 queries' operands, the final cuts and write-out of 16
+        // lists) outweighs the tail of fewer, longer items: at C2 512-row
+        // chunks ran the scan 4 % and the pool 9 % slower, 256-row ones
+        // 8 % and 30 %.
         const int cmax = kkeep >= 256 ? 2 : kSMaxChunks;
         P.nchunk = W / kSChunkRows < cmax ? (int)(W / kSChunkRows) : cmax;
         P.chunk_log2 = lg - (P.nchunk == 4 ? 2 : (P.nchunk == 2 ? 1 : 0));
