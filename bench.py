@@ -655,7 +655,12 @@ def main():
                                  "issued_tflops": issued / t_a / 1e12, "tile_occupancy": occupancy,
                                  "tile_rows": scan_rows, "sample_points": NE,
                                  "margin_fallbacks": fallbacks,
-                                 "tile_row_bytes": (eb * d + 4.0) * scan_rows},
+                                 "tile_row_bytes": (eb * d + 4.0) * scan_rows,
+                                 # the useful rate if the tiles' rows streamed at
+                                 # the HBM peak: the ceiling this tiling's
+                                 # arithmetic intensity allows
+                                 "useful_tflops_at_hbm_peak": useful / ((eb * d + 4.0) * scan_rows
+                                                                        / (HBM_PEAK_GBS * 1e9)) / 1e12},
                   "pool_and_traversal": {"kernel": "s_pool_kernel+s_search_kernel", "ms": t_b * 1e3, "bound": "hbm",
                                          "alg_bytes": search_bytes, "GB_s": a_search,
                                          "frac": a_search / HBM_PEAK_GBS,
@@ -665,6 +670,7 @@ def main():
         if t_a >= t_b:
             dominant = "s_scan_kernel"
             roof = {"bound": "mfma", "kernel": dominant, "achieved": scan_tf, "peak": FP32_MFMA_PEAK_TFLOPS,
+                    "attainable_at_hbm_peak": phases["entry_scan"]["useful_tflops_at_hbm_peak"],
                     "unit": "TFLOP/s", "frac": scan_tf / FP32_MFMA_PEAK_TFLOPS, "flops_per_launch": useful,
                     "tile_occupancy": occupancy, "kernel_ms": t_a * 1e3}
         else:

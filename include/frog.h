@@ -234,7 +234,7 @@ int frog_search(const frog_index_t* idx, const float* d_queries, int64_t nq,
  * freed here, so searches on several streams or threads may share an index
  * whatever their seeds.  The per-call workspace (counters, rank intervals,
  * chunk pools; in entry_mode 1 plans, tiles, candidate lists and pools: about
- * 4 KB per query at L <= 40) is a device buffer the library
+ * 13.5 KB per query at L <= 40, sized for the worst case) is a device buffer the library
  * keeps per (device, stream) for the life of the process, grown
  * stream-ordered when a call needs more, so repeated calls allocate nothing;
  * threads enqueueing on one stream take turns, other streams have their own
@@ -249,7 +249,7 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
  * frog_search_ex (same arguments, same results, same errors), except that the
  * per-call workspace (work counters, rank intervals, chunk pools; in
  * entry_mode 1 the plans, tiles, candidate lists and pools) lives in a fixed
- * 128 MiB array of device memory inside the library instead of coming from
+ * 256 MiB array of device memory inside the library instead of coming from
  * hipMallocAsync.  Nothing is allocated or freed by this call.
  *   - Each GPU the library runs on holds its own array until the process
  *     ends; its address is looked up once per device, on the first call there.
@@ -257,12 +257,12 @@ int frog_search_ex(const frog_index_t* idx, const float* d_queries, int64_t nq,
  *     last call's contents (the kernels clear what must start at zero):
  *     calls that overlap on one GPU (other streams, other threads) race and
  *     must be serialised by the caller.
- *   - A call whose workspace exceeds 128 MiB is refused with FROG_EUNSUPPORTED
+ *   - A call whose workspace exceeds 256 MiB is refused with FROG_EUNSUPPORTED
  *     before anything is enqueued.  Roughly: entry_mode 0 needs 12 bytes per
  *     query plus, when the entry count exceeds one 768-point chunk,
  *     512 * ceil(L/64) bytes per chunk (about 2 KB per query at 2,560 entry
- *     points and L <= 64); entry_mode 1 at n = 1M about 4.0 KB per query at
- *     L <= 40 (about 33,000 queries per call), 5.0 KB up to L = 56, 9.6 KB
+ *     points and L <= 64); entry_mode 1 at n = 1M about 13.5 KB per query at
+ *     L <= 40 (about 19,700 queries per call), 17.6 KB up to L = 56, 34.5 KB
  *     up to L = 120 and 35 KB up to L = 256, plus about 2 MB; the exact
  *     visited set (hash_log2 = 0) adds n/8 bytes per resident wavefront and
  *     is refused at realistic n.

@@ -13,7 +13,7 @@ namespace frog {
 // GPU the library runs on, held until the process ends.  In host code its
 // name is only a stand-in: the device address comes from
 // hipGetSymbolAddress, taken once per device (scratch_area).
-constexpr size_t kScratchBytes = (size_t)128 << 20;
+constexpr size_t kScratchBytes = (size_t)256 << 20;
 static __device__ __align__(256) char scratch[kScratchBytes];
 
 namespace {

@@ -47,6 +47,7 @@
 
 #include <cstdint>
 #include <map>
+#include <tuple>
 #include <mutex>
 #include <type_traits>
 #include <vector>
@@ -662,8 +663,9 @@ __device__ void entry_chunk(const DevIndex& ix, const SearchLaunch& A, const Que
 // HotspotLocalization, the best-first loop of Alg. 2, output and statistics.
 // LEAN: the timed configuration (no statistics, lazy check, LDS visited
 // table), with the statistics and the ablation branches compiled out and the
-// EN list of a single-load hotspot slice compacted by lane permutes; the
-// trajectory is the same.
+// EN list compacted by lane permutes whenever the slice's first 64 entries
+// hold it (almost always: the budget fills within about 40 entries at the
+// bench settings); the trajectory is the same.
 template <int C, int LP, typename XT, bool LEAN = false>
 __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis_words, const QueryCtx<C, XT>& Q,
                          Pool<LP>& pool, const WaveLds<LP>& W, const Visited& vis) {
@@ -671,6 +673,7 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
     const int T = A.hash_log2 > 0 ? (1 << A.hash_log2) : 0;
     const int H = ix.H, m = ix.m, B = A.B, L = A.L, k = A.k;
     const int64_t qi = Q.qi, l = Q.l, r = Q.r;
+    const int32_t l32 = (int32_t)l, r32 = (int32_t)r;   // ranks fit int32
     const bool eager = !LEAN && A.eager;
     int32_t st[FROG_STAT_N];
 #pragma unroll
@@ -759,24 +762,31 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
             pre_v = lane < nent ? nrow[lane] : -1;
             st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
         }
-        if (LEAN && nent <= 64) {
-            // one load holds the hotspot slice: admit the first B in-range
-            // entries (Alg. 4), move them to lanes 0.., check them against
-            // the visited table (lazy check) and move the fresh ones down
+        if (LEAN) {
+            // the first 64 entries of the hotspot slice (the prefetched ones
+            // on a hit); when they hold the whole slice or at least B
+            // in-range entries, the EN list of Alg. 4 (the first B in-range
+            // entries in stored order) lies in them: admit those, move them
+            // to lanes 0.., check them against the visited table (lazy
+            // check) and move the fresh ones down.  Otherwise the general
+            // path below scans on.
             const int32_t v0 = hit ? cur_pre : (lane < nent ? row[lane] : -1);
-            const uint64_t pm = ballot(v0 >= l && v0 <= r);
+            const bool inr = v0 >= l32 && v0 <= r32;
+            const uint64_t pm = ballot(inr);
             const int tot = __popcll(pm);
-            const int nen = tot < B ? tot : B;
-            const uint64_t am = ballot(((pm >> lane) & 1ull) && mbcnt(pm) < nen);
-            const int32_t v = compact_lanes(v0, am);
-            const bool fresh = lane < nen && !Q.is_entry(v) && vis.check_insert(v);
-            const uint64_t fm = ballot(fresh);
-            const int ns = __popcll(fm);
-            if (ns == 0) continue;
-            const int32_t myid = compact_lanes(v, fm);
-            const float dd = Q.eval(ix, ns, lane < ns ? myid : 0);
-            merge<LP>(pool, lane < ns ? make_key(dd, myid) : kEmpty, ns, L, W.st_key, W.st_flag);
-            continue;
+            if (nent <= 64 || tot >= B) {
+                const int nen = tot < B ? tot : B;
+                const uint64_t am = ballot(inr && mbcnt(pm) < nen);
+                const int32_t v = compact_lanes(v0, am);
+                const bool fresh = lane < nen && !Q.is_entry(v) && vis.check_insert(v);
+                const uint64_t fm = ballot(fresh);
+                const int ns = __popcll(fm);
+                if (ns == 0) continue;
+                const int32_t myid = compact_lanes(v, fm);
+                const float dd = Q.eval(ix, ns, lane < ns ? myid : 0);
+                merge<LP>(pool, lane < ns ? make_key(dd, myid) : kEmpty, ns, L, W.st_key, W.st_flag);
+                continue;
+            }
         }
         int nen = 0;
         int64_t scanned = nent;
@@ -870,19 +880,19 @@ inline int lds_per_wave(int L, int hash_log2) {
     return 64 * lp * 8 + 64 * lp * 4 + 64 * 4 + (hash_log2 > 0 ? (4 << hash_log2) : 0);
 }
 
-// workgroups of kernel `fn` (kBlock threads, `smem` bytes of LDS) the whole
-// device holds at once
-inline int max_blocks(const void* fn, int smem) {
+// workgroups of kernel `fn` (`threads` threads, `smem` bytes of LDS) the
+// whole device holds at once
+inline int max_blocks(const void* fn, int smem, int threads = kBlock) {
     static std::mutex mu;
-    static std::map<std::pair<const void*, int>, int> cache;
+    static std::map<std::tuple<const void*, int, int>, int> cache;
     std::lock_guard<std::mutex> g(mu);
-    auto key = std::make_pair(fn, smem);
+    auto key = std::make_tuple(fn, smem, threads);
     auto it = cache.find(key);
     if (it != cache.end()) return it->second;
     int dev = 0, per_cu = 0, cus = 0;
     (void)hipGetDevice(&dev);
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, smem) != hipSuccess || per_cu < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, smem) != hipSuccess || per_cu < 1)
         per_cu = 1;
     const int v = per_cu * (cus > 0 ? cus : 1);
     cache[key] = v;

@@ -19,15 +19,21 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     const int lane = lane_id();
     const int wave = threadIdx.x >> 6;
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x >> 6) + wave;
-    const int64_t t = item / P.nchunk;
-    const int c = (int)(item % P.nchunk);
+    // when second-round tiles take more chunks than the others, items are
+    // chunk-major (every tile's first chunk, then the second chunks, ...):
+    // items past a tile's chunk count exit, and they fill whole workgroups
+    // (whose LDS is then free again) instead of sitting beside live ones;
+    // otherwise tile-major, a tile's chunks side by side in a workgroup
+    const bool cmaj = P.nchunk > P.nbase;
+    const int c = (int)(cmaj ? item / P.tmax : item % P.nchunk);
+    const int64_t t = cmaj ? item % P.tmax : item / P.nchunk;
     if (t >= P.tmax) return;        // wave-uniform; no workgroup barrier follows
     const STile& T = P.tiles[t];
     if (T.nq == 0) return;
     const SharedLevels& lv = P.a.lv;
     const int lev = T.lev;
     const int64_t len = (int64_t)T.ub - T.ua;
-    const int nch = tile_chunks(len, P.nchunk, P.chunk_log2);
+    const int nch = T.nch;
     if (c >= nch) return;
     const int64_t c0 = T.ua + len * c / nch;
     const int64_t c1 = T.ua + len * (c + 1) / nch;

@@ -87,7 +87,8 @@ struct STile {
     int32_t lev;      // level of the tile's window (all its pairs lie in that window)
     int32_t ua, ub;   // span of the slots' pieces of the window, positions in the level's list
     int32_t nq;       // 0: unused tile
-    int32_t pad[3];
+    int32_t nch;      // its work items (chunks of its span)
+    int32_t pad[2];
 };
 
 struct SParams {
@@ -106,8 +107,10 @@ struct SParams {
     int nbins;          // nwin * kSPer
     int nwin;           // windows of all levels
     int win_log2;       // W = 2^win_log2 positions per window
-    int nchunk;         // work items per tile at most (<= kSMaxChunks)
-    int chunk_log2;     // a tile's span is split into chunks of at least 2^chunk_log2 = W / nchunk rows
+    int nchunk;         // work items per tile at most (<= kSMaxChunks): the lists' stride per pair
+    int nbase;          // work items of a tile of the scan's first round at most
+    int chunk_log2;     // such a tile's span is split into chunks of at least 2^chunk_log2 = W / nbase rows
+    int scan_slots;     // scan wavefronts the device holds at once
     int32_t winbase[34];  // first window of level j; winbase[nlev + 1] = nwin
     int kkeep;
     // candidate lists, one per (pair, chunk of the pair's tile): list

@@ -264,8 +264,20 @@ __global__ __launch_bounds__(kBlock) void s_tile_kernel(SParams P) {
     ub = uniform(ub);
     lv = uniform(lv);
     const int nq = __popcll(valid);
-    if (q >= 0) p->wchunks[wi] = tile_chunks((int64_t)ub - ua, P.nchunk, P.chunk_log2);
+    // work items: the scan's wavefronts take the tiles' first chunks in tile
+    // order; tiles beyond the first scan_slots (a second round) are cut in up
+    // to 4 times as many chunks, so that the round that ends the scan is
+    // short (with fewer tiles than slots, as many tiles are cut as still fit
+    // in one round)
+    const int64_t ntiles = P.meta[1];
+    const int64_t nfit = (P.scan_slots - ntiles) / 3;   // a tile cut in 4 adds 3 items
+    const int64_t nsplit = ntiles > P.scan_slots ? ntiles - P.scan_slots : (nfit < ntiles ? nfit : ntiles);
+    const int64_t span = (int64_t)ub - ua;
+    int nch = tile_chunks(span, P.nbase, P.chunk_log2);
+    if (t >= ntiles - nsplit && span >= 256) nch = 4 * nch < P.nchunk ? 4 * nch : P.nchunk;
+    if (q >= 0) p->wchunks[wi] = nch;
     if (lane == 0) {
+        T->nch = nch;
         T->allmask = (uint32_t)allm;
         T->lev = nq > 0 ? lv : 0;
         T->ua = nq > 0 ? ua : 0;
@@ -308,6 +320,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
         hipError_t e = hipFuncSetAttribute((const void*)scan, hipFuncAttributeMaxDynamicSharedMemorySize, smem_scan);
         if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
+    const int scan_slots = max_blocks((const void*)scan, smem_scan, 64 * scan_waves) * scan_waves;
     SParams P{};
     P.ix = ix;
     P.a = a;
@@ -336,20 +349,26 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
         }
         P.win_log2 = lg;
         const int64_t W = (int64_t)1 << lg;
-        // chunks of W / nchunk rows, at least kSChunkRows: one per tile at
-        // W = 1024, up to 4 of W / 4 above (2 for 256-entry lists, whose
-        // cuts and merges cost more per list).  A work item's fixed cost
-        // (the 16 queries' operands, the final cuts and write-out of 16
-        // lists) outweighs the tail of fewer, longer items: at C2 512-row
-        // chunks ran the scan 4 % and the pool 9 % slower, 256-row ones
-        // 8 % and 30 %.
+        // work items: a tile of the scan's first round (the first
+        // scan_slots tiles) is cut into chunks of W / nbase rows, at least
+        // kSChunkRows: one per tile at W = 1024, up to 4 of W / 4 above (2
+        // for 256-entry lists, whose cuts and merges cost more per list); a
+        // tile of the second round into up to 4 times as many, so that the
+        // round that ends the scan is short.  Uniform items fit worse: at C2
+        // (3,600 tiles on 3,072 slots) one 1024-row item per tile took
+        // 475 us, two 512-row items 492 us, four 256-row items 512 us (each
+        // item carries its 16 queries' operands and 16 lists' final cuts and
+        // write-out), and cutting only the second round's tiles in four,
+        // 426 us.
         const int cmax = kkeep >= 256 ? 2 : kSMaxChunks;
-        P.nchunk = W / kSChunkRows < cmax ? (int)(W / kSChunkRows) : cmax;
-        P.chunk_log2 = lg - (P.nchunk == 4 ? 2 : (P.nchunk == 2 ? 1 : 0));
+        P.nbase = W / kSChunkRows < cmax ? (int)(W / kSChunkRows) : cmax;
+        P.chunk_log2 = lg - (P.nbase == 4 ? 2 : (P.nbase == 2 ? 1 : 0));
+        P.nchunk = 4 * P.nbase < cmax ? 4 * P.nbase : cmax;
     }
     // places: at most kSMaxWin pairs per query, plus up to 15 of padding per window
     const int64_t norder = (int64_t)kSMaxWin * a.nq + (int64_t)kSQ * P.nwin;
     P.tmax = (norder + kSQ - 1) / kSQ;
+    P.scan_slots = scan_slots;
     P.nbins = P.nwin * kSPer;
     P.kkeep = kkeep;
     P.lds_per_wave = lpw;

@@ -65,8 +65,8 @@ def test_noalloc_equals_search_ex_two_calls(case, mode, L, emax):
 def test_noalloc_refuses_oversized_calls(case):
     ix, Q, lo, hi = case
     lib = F.lib()
-    # entry mode 1 at L <= 40 takes about 4 KB per query: 40,000 queries
-    # need about 160 MB, more than the 128 MiB array
+    # entry mode 1 at L <= 40 takes about 13.5 KB per query: 40,000 queries
+    # need about 540 MB, more than the 256 MiB array
     nq = 40000
     rep = (nq + Q.shape[0] - 1) // Q.shape[0]
     Qb = Q.repeat(rep, 1)[:nq].contiguous()
