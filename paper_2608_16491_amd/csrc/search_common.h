@@ -437,39 +437,42 @@ __device__ int merge(Pool<LP>& P, uint64_t nkey, int ns, int L, uint64_t* st_key
             if (s == (t >> 6)) thr = readlane64(P.key[s], t & 63);
         cand = cand && nkey < thr;
     }
-    uint64_t cmask = ballot(cand);
+    const uint64_t cmask = ballot(cand);
     if (cmask == 0) return 0;
-    // drop duplicates: of a pool key, or of an earlier new key
-    bool keep = cand;
-    for (uint64_t m = cmask; m; m &= m - 1) {
-        const int j = __builtin_ctzll(m);
-        const uint64_t kj = readlane64(nkey, j);
-        bool eq = false;
-#pragma unroll
-        for (int s = 0; s < LP; ++s) eq |= P.key[s] == kj;
-        if (ballot(eq) != 0 && lane == j) keep = false;
-        if (lane > j && nkey == kj) keep = false;
-    }
-    const uint64_t kmask = ballot(keep);
-    const int nk = __popcll(kmask);
-    if (nk == 0) return 0;
-    // positions
+    // one pass over the candidates in lane order: a candidate equal to a
+    // pool key or to an earlier candidate is dropped (so the first of equal
+    // candidates is kept unless the pool holds it); a kept one counts the
+    // pool keys below it (its place among the pool), and every lane counts
+    // the kept candidates below its pool keys (their shift) and below its
+    // own candidate (its place among the new keys)
+    uint64_t kmask = cmask;
     int ltN = 0, cntP = 0;
     int ltP[LP];
 #pragma unroll
     for (int s = 0; s < LP; ++s) ltP[s] = 0;
-    for (uint64_t m = kmask; m; m &= m - 1) {
+    for (uint64_t m = cmask; m; m &= m - 1) {
         const int j = __builtin_ctzll(m);
         const uint64_t kj = readlane64(nkey, j);
+        bool inpool = false;
         int c = 0;
 #pragma unroll
         for (int s = 0; s < LP; ++s) {
+            inpool |= ballot(P.key[s] == kj) != 0;
             c += __popcll(ballot(P.key[s] < kj));
-            ltP[s] += kj < P.key[s] ? 1 : 0;
         }
+        const bool earlier = (ballot(cand && nkey == kj) & ((1ull << j) - 1)) != 0;
+        if (inpool || earlier) {
+            kmask &= ~(1ull << j);
+            continue;
+        }
+#pragma unroll
+        for (int s = 0; s < LP; ++s) ltP[s] += kj < P.key[s] ? 1 : 0;
         if (lane == j) cntP = c;
         ltN += kj < nkey ? 1 : 0;
     }
+    const int nk = __popcll(kmask);
+    if (nk == 0) return 0;
+    const bool keep = (kmask >> lane) & 1ull;
     // scatter
 #pragma unroll
     for (int s = 0; s < LP; ++s) {

@@ -6,9 +6,11 @@
 namespace frog {
 namespace {
 
-// The pool of each query: one wavefront per query.
+// The pool of each query: one wavefront per query.  Four wavefronts per
+// SIMD for pools of at most 64 (128 VGPRs: a few values spill, and the
+// kernel still ran 89 -> 81 us at C2), three above (no spill).
 template <int C, int LP, int KK, typename XT = float, int MK = (KK > 64 ? KK : 64)>
-__global__ __launch_bounds__(kBlock) void s_pool_kernel(SParams P) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 ? 4 : 3))) void s_pool_kernel(SParams P) {
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const DevIndex& ix = P.ix;
