@@ -107,9 +107,10 @@ enum {
     FROG_STAT_LSTART = 5,     /* hotspot first layer (Alg. 3) */
     FROG_STAT_LEND = 6,       /* hotspot last layer */
     FROG_STAT_LOADED = 7,     /* ENC entries actually loaded by the kernel */
-    FROG_STAT_SCANROWS = 8,   /* entry_mode 1: rows the shared entry scan read for the
-                                 query's tile of 16, credited to the tile's first query
-                                 (0 for the others and in entry_mode 0) */
+    FROG_STAT_SCANROWS = 8,   /* entry_mode 1: rows the shared entry scan read, each
+                                 tile's rows credited to the query of its first slot
+                                 (a query has a tile per window its run meets), so the
+                                 column sums to the scan's rows; 0 in entry_mode 0 */
     FROG_STAT_FALLBACK = 9,   /* entry_mode 1: 1 if the margin test could not prove the
                                  scan's candidates hold the L nearest sample points, so
                                  the whole sample was evaluated exactly (0 otherwise) */
