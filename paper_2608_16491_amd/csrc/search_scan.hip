@@ -112,9 +112,15 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         const int64_t pos = c0 + blk * 16 + ii;
         return pos < c1 ? pos : c1 - 1;   // in bounds past the end
     };
+    // the rank load is unconditional (level 0 reads a priority word in its
+    // place and discards it): a load under a branch would make the compiler
+    // wait, at the first use of any older load, for the loads of the next
+    // block issued before it
+    const int32_t* rsrc = lranks ? lranks : reinterpret_cast<const int32_t*>(lv.prio);
     auto rank_at = [&](int64_t blk) -> int32_t {
         const int64_t pos = pos_at(blk);
-        return lranks ? lranks[pos] : (int32_t)pos;
+        const int32_t v = rsrc[pos];
+        return lranks ? v : (int32_t)pos;
     };
     auto load_rows = [&](int64_t blk, float4 (&x)[KT > 0 ? KT : 1]) {
         if constexpr (KT > 0) {
