@@ -150,6 +150,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     for (int e = 0; e < 4; ++e) thr_l[e] = __int_as_float(0x7f800000);
     // cut every list that the next block (at most 16 entries each) could overflow
     auto make_room = [&]() {
+        // fast path: the fullest list has room (a max over the 16 fills)
+        int fmax = fill[0];
+#pragma unroll
+        for (int i = 1; i < kSQ; ++i) fmax = fill[i] > fmax ? fill[i] : fmax;
+        if (fmax <= 2 * kkeep - 16) return;
         uint32_t over = 0u;
 #pragma unroll
         for (int i = 0; i < kSQ; ++i) over |= (fill[i] > 2 * kkeep - 16 ? 1u : 0u) << i;
@@ -203,7 +208,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
         // lane holds D[4kk + e][ii]: query slot 4kk + e, the block's row ii
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const bool insample = inrun && qv[e] && rk >= ql[e] && rk <= qr[e] && (qall[e] || pri < qT[e]);
+            // bitwise: every test evaluated, no branch per term
+            const bool insample = inrun & qv[e] & (rk >= ql[e]) & (rk <= qr[e]) & (qall[e] | (pri < qT[e]));
             scnt[e] += insample ? 1u : 0u;
             const float ap = qn[e] + xn - 2.f * acc[e];
             const bool cand = insample && ap < thr_l[e];
