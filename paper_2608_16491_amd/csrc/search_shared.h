@@ -64,6 +64,8 @@ constexpr int kSFull = 32;       // buckets per window for pieces that cover it 
                                  // so that their atomic counters do not contend)
 constexpr int kSPer = 2 * kSSub + kSFull;   // buckets per window
 constexpr int kOffPer = 3;       // windows per thread of s_wscan_kernel (nwin <= 3072)
+constexpr int kQSub = 64;        // counters per class of the traversal's query order
+constexpr int kQLine = 32;       // their stride (one 128-byte line each: atomics on one line serialise)
 
 struct SPlan {
     int32_t l, r;
@@ -72,7 +74,8 @@ struct SPlan {
     int32_t lev;     // level whose list holds the sample
     int32_t a, b;    // run [a, b) of [l, r] in that list
     int32_t w0, nw;  // first window the run meets (in its level) and how many
-    int32_t pad[7];
+    int32_t qpos;    // place among the queries of its class and counter (traversal order)
+    int32_t pad[6];
     int32_t pos[kSMaxWin];    // per window: place within its bucket
     int32_t wchunks[kSMaxWin];  // per window: work items of the pair's tile (its chunk lists)
 };
@@ -100,6 +103,10 @@ struct SParams {
     uint32_t* bstart;   // [nbins] first place of each bucket within its window
     uint32_t* wstart;   // [nwin] first place of each window
     uint32_t* meta;     // [0] places used in `order`, [1] tiles, [2] query counter
+    uint32_t* qhist;    // [2 kQSub] queries per (class, counter) at stride kQLine, then [2 kQSub]
+                        // their first places
+    int32_t* qorder;    // [nq] the traversal's query order: queries whose sample is a strict
+                        // subset of their range, then the others (covered or empty ranges)
     int32_t* order;     // [norder] pairs (query * kSMaxWin + window index) by bucket,
                         // each window's places padded to a multiple of 16 with -1
     STile* tiles;       // [tmax]

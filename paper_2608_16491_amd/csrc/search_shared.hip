@@ -8,9 +8,11 @@
 namespace frog {
 namespace {
 
-__global__ void s_init_kernel(uint32_t* meta, uint32_t* hist, int nbins, int32_t* order, int64_t norder) {
+__global__ void s_init_kernel(uint32_t* meta, uint32_t* qhist, uint32_t* hist, int nbins, int32_t* order,
+                              int64_t norder) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < 4) meta[i] = 0u;
+    if (i < 2 * kQSub) qhist[i * kQLine] = 0u;
     if (i < nbins) hist[i] = 0u;
     if (i < norder) order[i] = -1;
 }
@@ -110,6 +112,11 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
     }
     if (lane == 0) {
         SPlan* dst = P.plan + q;
+        // the traversal's order: class 0 (the sample is a strict subset of
+        // the range: long traversals) before class 1 (covered or empty
+        // ranges: short ones), each class spread over kQSub counters
+        const int cls = p.l > p.r || p.all ? 1 : 0;
+        dst->qpos = (int32_t)atomicAdd(P.qhist + (cls * kQSub + (q & (kQSub - 1))) * kQLine, 1u);
         dst->l = p.l;
         dst->r = p.r;
         dst->T = p.T;
@@ -185,7 +192,23 @@ __global__ __launch_bounds__(1024) void s_wscan_kernel(SParams P) {
         if (lane >= o) inc += s;
     }
     if (lane == 63) wsum[w] = inc;
+    // the first place of each (class, counter) of the traversal's query
+    // order: an exclusive scan of 2 kQSub counts over the first two wavefronts
+    static_assert(kQSub == 64, "one wavefront per class");
+    __shared__ uint32_t qsum[2];
+    uint32_t qc = 0u, qinc = 0u;
+    if (t < 2 * kQSub) {
+        qc = P.qhist[t * kQLine];
+        qinc = qc;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t s = __shfl_up(qinc, o);
+            if (lane >= o) qinc += s;
+        }
+        if (lane == 63) qsum[w] = qinc;
+    }
     __syncthreads();
+    if (t < 2 * kQSub) P.qhist[2 * kQSub * kQLine + t] = qinc - qc + (w == 1 ? qsum[0] : 0u);
     uint32_t run = inc - tot, all = 0;
     for (int i = 0; i < 16; ++i) {
         run += i < w ? wsum[i] : 0u;
@@ -203,11 +226,14 @@ __global__ __launch_bounds__(1024) void s_wscan_kernel(SParams P) {
     }
 }
 
-// thread per query: each (query, window) pair to its place
+// thread per query: the query to its place in the traversal's order, and
+// each (query, window) pair to its place
 __global__ void s_order_kernel(SParams P) {
     const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= P.a.nq) return;
     const SPlan* p = P.plan + q;
+    const int cls = p->l > p->r || p->all ? 1 : 0;
+    P.qorder[P.qhist[2 * kQSub * kQLine + cls * kQSub + (q & (kQSub - 1))] + p->qpos] = (int32_t)q;
     const int nw = p->nw;
     if (nw > kSMaxWin || p->l > p->r) return;
     const int lev = p->lev;
@@ -382,6 +408,8 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     size_t off = 0;
     auto take = [&](size_t bytes) { const size_t o = off; off += align(bytes); return o; };
     const size_t o_meta = take(16);
+    const size_t o_qhist = take((2 * kQSub * kQLine + 2 * kQSub) * 4);
+    const size_t o_qorder = take((size_t)a.nq * 4);
     const size_t o_lr = take((size_t)a.nq * 8);
     const size_t o_plan = take((size_t)a.nq * sizeof(SPlan));
     const size_t o_hist = take((size_t)P.nbins * 4);
@@ -421,6 +449,8 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     }
     char* base = reinterpret_cast<char*>(wsp);
     P.meta = reinterpret_cast<uint32_t*>(base + o_meta);
+    P.qhist = reinterpret_cast<uint32_t*>(base + o_qhist);
+    P.qorder = reinterpret_cast<int32_t*>(base + o_qorder);
     int32_t* lr = reinterpret_cast<int32_t*>(base + o_lr);
     P.lr = lr;
     P.plan = reinterpret_cast<SPlan*>(base + o_plan);
@@ -443,8 +473,8 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     // (the planning kernels come before the first, the pool kernel after the
     // second)
     const int64_t ninit = norder > P.nbins ? norder : P.nbins;
-    hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.hist,
-                       P.nbins, P.order, norder);
+    hipLaunchKernelGGL(s_init_kernel, dim3((unsigned)((ninit + 255) / 256)), dim3(256), 0, stream, P.meta, P.qhist,
+                       P.hist, P.nbins, P.order, norder);
     const int64_t plan_blocks = (a.nq + kWavesPerBlock - 1) / kWavesPerBlock;
     hipLaunchKernelGGL(s_plan_kernel, dim3((unsigned)plan_blocks), dim3(kBlock), 0, stream, P);
     hipLaunchKernelGGL(s_wprefix_kernel, dim3((unsigned)((P.nwin + 255) / 256)), dim3(256), 0, stream, P);

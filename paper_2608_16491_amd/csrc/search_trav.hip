@@ -5,7 +5,11 @@
 namespace frog {
 namespace {
 
-// Traversal: persistent, one wavefront per query, from the pool s_pool_kernel wrote.
+// Traversal: persistent, one wavefront per query, from the pool s_pool_kernel
+// wrote.  Queries are taken in the planned order: those whose sample is a
+// strict subset of their range first, then those whose range the sample
+// covers (no candidate is new, the traversal is short) and the empty ones,
+// which then fill the kernel's tail (the results do not depend on the order).
 template <int C, int LP, typename XT = float, bool LEAN = false>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(FROG_SEARCH_WAVES_PER_EU)))
 void s_search_kernel(SParams P) {
@@ -23,8 +27,9 @@ void s_search_kernel(SParams P) {
     for (;;) {
         uint32_t qq = 0;
         if (lane == 0) qq = atomicAdd(P.meta + 2, 1u);
-        const int64_t qi = (int64_t)(uint32_t)uniform((int)__shfl((int)qq, 0));
-        if (qi >= A.nq) break;
+        const int64_t idx = (int64_t)(uint32_t)uniform((int)__shfl((int)qq, 0));
+        if (idx >= A.nq) break;
+        const int64_t qi = uniform(P.qorder[idx]);
         const SPlan p = P.plan[qi];
         if (p.l > p.r) {
             for (int j = lane; j < A.k; j += 64) {
