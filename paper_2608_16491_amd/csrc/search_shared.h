@@ -28,11 +28,14 @@ namespace frog {
 //   s_plan_kernel     per query (one wavefront): rank interval, threshold,
 //                     level, run in the level's list, its windows, and per
 //                     window a bucket (window, kind and place of the pair's
-//                     piece of the run inside it)
+//                     piece of the run inside it); a place in the query
+//                     order of the pool and traversal kernels (queries whose
+//                     sample is a strict subset of their range first, the
+//                     short covered and empty ones last, to fill the tails)
 //   s_wprefix_kernel, s_wscan_kernel
 //                     bucket offsets, each window's places padded to a
-//                     multiple of 16
-//   s_order_kernel    the pairs in bucket order
+//                     multiple of 16; the query order's offsets
+//   s_order_kernel    the pairs in bucket order, the queries in their order
 //   s_tile_kernel     tiles of 16 consecutive places: the span of their
 //                     pieces of the window
 //   s_scan_kernel     one wavefront per (tile, chunk of its span): 16 x 16
