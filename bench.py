@@ -525,57 +525,6 @@ def main():
         f"min {min(step_ms):.3f} max {max(step_ms):.3f} (wall {wall / args.steps * 1e3:.3f}), {qps:.0f} QPS; steps "
         + " ".join(f"{x:.3f}" for x in step_ms))
 
-    # (a') the same steps overlapped as a serving loop would run them: the
-    # next batch's copy in and the previous batch's copy out proceed on a
-    # second stream while the current batch is searched (two buffer sets)
-    cs = torch.cuda.Stream()
-    h2d = [torch.cuda.Event() for _ in range(2)]
-    done = [torch.cuda.Event() for _ in range(2)]
-    out = [torch.cuda.Event() for _ in range(2)]
-    for b in range(2):
-        done[b].record(stream)
-        out[b].record(stream)
-
-    def stage_in(i):
-        b = i % 2
-        with torch.cuda.stream(cs):
-            cs.wait_event(done[b])          # the search two steps back has read this buffer
-            cs.wait_event(out[b])           # and its results have left it
-            bufs[b][0].copy_(host_in, non_blocking=True)
-            h2d[b].record(cs)
-
-    def stage_run(i):
-        b = i % 2
-        _, dev_out, host_out, (Qd, lod, hid, ids_d, ds_d) = bufs[b]
-        stream.wait_event(h2d[b])
-        F.search(ix, Qd, lod, hid, k, L, out=(ids_d, ds_d), **p_sel)
-        done[b].record(stream)
-        with torch.cuda.stream(cs):
-            cs.wait_event(done[b])
-            host_out.copy_(dev_out, non_blocking=True)
-            out[b].record(cs)
-
-    def pipelined(nsteps):
-        stage_in(0)
-        for i in range(nsteps):
-            if i + 1 < nsteps:
-                stage_in(i + 1)
-            stage_run(i)
-        stream.wait_stream(cs)
-
-    pipelined(args.warmup)
-    pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    pe0.record(stream)                      # created at their first record, before the timed region
-    pe1.record(stream)
-    torch.cuda.synchronize()
-    pe0.record(stream)
-    cs.wait_event(pe0)
-    pipelined(args.steps)
-    pe1.record(stream)
-    torch.cuda.synchronize()
-    per_step_pipe = pe0.elapsed_time(pe1) / 1000.0 / args.steps
-    log(f"overlapped steps with transfers: {per_step_pipe * 1e3:.3f} ms/step, {w.nq / per_step_pipe:.0f} QPS")
-
     # (b) kernels only, inputs resident; events around the library's phases
     # (entry_mode 0: the search kernel; entry_mode 1: the matrix-core entry
     # scan, then the pool and traversal kernels)
@@ -1029,9 +978,6 @@ def main():
         },
         "resident": {"qps": w.nq / per_step_res, "ms_per_step": per_step_res * 1e3,
                      "what": "the same search with queries, ranges and results kept in HBM (kernels only)"},
-        "overlapped": {"qps": w.nq / per_step_pipe, "ms_per_step": per_step_pipe * 1e3,
-                       "what": "the same steps with transfers, the next batch's copy in and the previous batch's "
-                               "copy out on a second stream during the search"},
         "roofline": roof,
         "phases": phases,
         "cpu_baseline": cpu,
