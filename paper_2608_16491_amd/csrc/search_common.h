@@ -589,9 +589,13 @@ struct QueryCtx {
     uint64_t pkey = 0;
 
     __device__ void load(const DevIndex& ix, const SearchLaunch& A, const int32_t* lr, int64_t q) {
+        set(ix, A, q, uniform(lr[2 * q]), uniform(lr[2 * q + 1]));
+    }
+    // the same from a rank interval already at hand
+    __device__ void set(const DevIndex& ix, const SearchLaunch& A, int64_t q, int64_t l_, int64_t r_) {
         qi = q;
-        l = uniform(lr[2 * q]);
-        r = uniform(lr[2 * q + 1]);
+        l = l_;
+        r = r_;
         cnt = r - l + 1;
         E = A.epn;
         if (A.epn_frac > 0.0) {

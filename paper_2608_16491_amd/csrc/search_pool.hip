@@ -32,11 +32,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
         if (idx >= A.nq) return;   // wave-uniform; no workgroup barrier follows
         const int64_t qi = uniform(P.qorder[idx]);   // the planned order (short queries last)
         const SPlan* pp = P.plan + qi;
+        QueryCtx<C, XT> Q;
+        Q.qrow = A.Q + qi * ix.d;
+        Q.load_vector(ix);   // issued beside the plan's load
         const SPlan p = *pp;
         if (p.l > p.r) return;
-        QueryCtx<C, XT> Q;
-        Q.load(ix, A, P.lr, qi);
-        Q.load_vector(ix);
+        Q.set(ix, A, qi, p.l, p.r);
         Q.shared = true;
         Q.T = p.T;
         Q.pkey = A.lv.key;
@@ -48,7 +49,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
         buf_init(Lst);
         const bool tiled = p.nw <= kSMaxWin;   // else no lists: the exact pass below
         const int nwq = tiled ? p.nw : 0;
-        const int wn = lane < nwq ? pp->wchunks[lane] : 0;
+        int wn = 0;   // from the plan already loaded, not a second read
+#pragma unroll
+        for (int x = 0; x < kSMaxWin; ++x) wn = lane == x && x < nwq ? p.wchunks[x] : wn;
         int wbase = wn;   // inclusive prefix over lanes 0..kSMaxWin-1
 #pragma unroll
         for (int o = 1; o < kSMaxWin; o <<= 1) {
@@ -147,9 +150,19 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
             certified = false;
             if (pool.np >= A.L) {
                 double qsq = 0.0;
-                for (int cc = lane; cc < ix.d; cc += 64) qsq += (double)Q.qrow[cc] * (double)Q.qrow[cc];
+                if constexpr (C > 0) {
+                    // from the query chunks in registers: each aligned group of
+                    // 8 lanes holds the whole query
 #pragma unroll
-                for (int o = 32; o >= 1; o >>= 1) qsq += __shfl_xor(qsq, o);
+                    for (int c = 0; c < C; ++c)
+                        qsq += (double)Q.qv[c].x * Q.qv[c].x + (double)Q.qv[c].y * Q.qv[c].y +
+                               (double)Q.qv[c].z * Q.qv[c].z + (double)Q.qv[c].w * Q.qv[c].w;
+                    qsq = sum8(qsq);
+                } else {
+                    for (int cc = lane; cc < ix.d; cc += 64) qsq += (double)Q.qrow[cc] * (double)Q.qrow[cc];
+#pragma unroll
+                    for (int o = 32; o >= 1; o >>= 1) qsq += __shfl_xor(qsq, o);
+                }
                 const double eps = 2.0 * (2.0 * ix.d + 4.0) * u_round * (qsq + (double)A.maxnorm);
                 uint64_t lk = 0;
 #pragma unroll

@@ -100,7 +100,6 @@ struct STile {
 struct SParams {
     DevIndex ix;
     SearchLaunch a;
-    int32_t* lr;        // [nq][2] rank intervals (written by s_plan_kernel)
     SPlan* plan;
     uint32_t* hist;     // [nbins] pairs per bucket
     uint32_t* bstart;   // [nbins] first place of each bucket within its window

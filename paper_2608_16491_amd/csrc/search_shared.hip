@@ -126,8 +126,6 @@ __global__ __launch_bounds__(kBlock) void s_plan_kernel(SParams P) {
         dst->b = p.b;
         dst->w0 = p.w0;
         dst->nw = p.nw;
-        P.lr[2 * q] = p.l;
-        P.lr[2 * q + 1] = p.r;
         if (P.a.stats) {
             P.a.stats[q * FROG_STAT_N + FROG_STAT_SCANROWS] = 0;
             P.a.stats[q * FROG_STAT_N + FROG_STAT_FALLBACK] = 0;
@@ -410,7 +408,6 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     const size_t o_meta = take(16);
     const size_t o_qhist = take((2 * kQSub * kQLine + 2 * kQSub) * 4);
     const size_t o_qorder = take((size_t)a.nq * 4);
-    const size_t o_lr = take((size_t)a.nq * 8);
     const size_t o_plan = take((size_t)a.nq * sizeof(SPlan));
     const size_t o_hist = take((size_t)P.nbins * 4);
     const size_t o_bstart = take((size_t)P.nbins * 4);
@@ -451,8 +448,6 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     P.meta = reinterpret_cast<uint32_t*>(base + o_meta);
     P.qhist = reinterpret_cast<uint32_t*>(base + o_qhist);
     P.qorder = reinterpret_cast<int32_t*>(base + o_qorder);
-    int32_t* lr = reinterpret_cast<int32_t*>(base + o_lr);
-    P.lr = lr;
     P.plan = reinterpret_cast<SPlan*>(base + o_plan);
     P.hist = reinterpret_cast<uint32_t*>(base + o_hist);
     P.bstart = reinterpret_cast<uint32_t*>(base + o_bstart);

@@ -40,7 +40,7 @@ void s_search_kernel(SParams P) {
             continue;
         }
         QueryCtx<C, XT> Q;
-        Q.load(ix, A, P.lr, qi);
+        Q.set(ix, A, qi, p.l, p.r);   // the plan's rank interval
         Q.load_vector(ix);
         Q.shared = true;
         Q.T = p.T;
