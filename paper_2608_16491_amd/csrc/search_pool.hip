@@ -6,6 +6,30 @@
 namespace frog {
 namespace {
 
+// The sum of s and the minimum of m over the wavefront, uniform (every lane
+// active): data-parallel-primitive moves within each row of 16 lanes, then
+// the four rows' results.
+__device__ __forceinline__ void wave_sum_min(int& s, float& m) {
+    auto step = [&](auto ctrl) {
+        constexpr int c = decltype(ctrl)::value;
+        s += __builtin_amdgcn_mov_dpp(s, c, 0xF, 0xF, false);
+        m = fminf(m, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(m), c, 0xF, 0xF, false)));
+    };
+    step(std::integral_constant<int, 0xB1>{});
+    step(std::integral_constant<int, 0x4E>{});
+    step(std::integral_constant<int, 0x141>{});
+    step(std::integral_constant<int, 0x140>{});
+    int rs = __builtin_amdgcn_readlane(s, 0);
+    float rm = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), 0));
+#pragma unroll
+    for (int r = 16; r < 64; r += 16) {
+        rs += __builtin_amdgcn_readlane(s, r);
+        rm = fminf(rm, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), r)));
+    }
+    s = rs;
+    m = rm;
+}
+
 // The pool of each query: one wavefront per query.  Four wavefronts per
 // SIMD for pools of at most 64 (128 VGPRs: a few values spill, and the
 // kernel still ran 89 -> 81 us at C2), three above (no spill).
@@ -73,14 +97,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
             mt = P.pthr[lid];
             mc = P.pcnt[lid];
         }
-        int64_t ne = 0;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            mc += __shfl_xor(mc, o);
-            mt = fminf(mt, __shfl_xor(mt, o));
-        }
-        ne = uniform(mc);
-        float texcl = __int_as_float(uniform(__float_as_int(mt)));   // every row left out is at or above this
+        wave_sum_min(mc, mt);
+        int64_t ne = mc;
+        float texcl = mt;   // every row left out is at or above this
         // several lists' entries at a time (no round trip between them)
         constexpr int kR = KK > 64 ? KK / 64 : 1;   // entries per lane and list
         constexpr int kG = kR == 1 ? 16 : 4;

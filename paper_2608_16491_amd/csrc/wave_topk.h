@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 namespace frog {
 namespace topk {
@@ -16,6 +17,33 @@ __device__ __forceinline__ void list_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The minimum of mn and the maximum of mx over the wavefront, uniform (every
+// lane active): data-parallel-primitive moves within each row of 16 lanes
+// (quad swaps, half-row and row mirrors), then the four rows' results.
+__device__ __forceinline__ void wave_minmax_u32(uint32_t& mn, uint32_t& mx) {
+    auto step = [&](auto ctrl) {
+        constexpr int c = decltype(ctrl)::value;
+        const uint32_t a = (uint32_t)__builtin_amdgcn_mov_dpp((int)mn, c, 0xF, 0xF, false);
+        const uint32_t b = (uint32_t)__builtin_amdgcn_mov_dpp((int)mx, c, 0xF, 0xF, false);
+        mn = a < mn ? a : mn;
+        mx = b > mx ? b : mx;
+    };
+    step(std::integral_constant<int, 0xB1>{});
+    step(std::integral_constant<int, 0x4E>{});
+    step(std::integral_constant<int, 0x141>{});
+    step(std::integral_constant<int, 0x140>{});
+    uint32_t rmn = (uint32_t)__builtin_amdgcn_readlane((int)mn, 0), rmx = (uint32_t)__builtin_amdgcn_readlane((int)mx, 0);
+#pragma unroll
+    for (int r = 16; r < 64; r += 16) {
+        const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)mn, r);
+        const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)mx, r);
+        rmn = a < rmn ? a : rmn;
+        rmx = b > rmx ? b : rmx;
+    }
+    mn = rmn;
+    mx = rmx;
 }
 
 __device__ __forceinline__ float wave_max_pos(float v, int& pos) {
@@ -155,12 +183,7 @@ __device__ __forceinline__ void buf_cut(const BufList& B, bool exact = true) {
             vmax = v > vmax ? v : vmax;
         }
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        const uint32_t a = __shfl_xor(vmin, o), b = __shfl_xor(vmax, o);
-        vmin = a < vmin ? a : vmin;
-        vmax = b > vmax ? b : vmax;
-    }
+    wave_minmax_u32(vmin, vmax);
     // an x in [vmin, vmax] with #(entries <= x) equal to K (exact) or in
     // [K, 5K/4] (loose); failing that, the smallest x with #(entries <= x) >= K
     uint32_t lo = __builtin_amdgcn_readfirstlane(vmin), hi = __builtin_amdgcn_readfirstlane(vmax);
