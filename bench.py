@@ -208,8 +208,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; the search shards by query "
-              "(replicated index, no exchange) and multi-GPU runs are not part of it",
+        print("bench.py measures one GPU only (--gpus 1); the search would shard by query "
+              "(replicated index, no exchange) and is not run across GPUs here",
               file=sys.stderr)
         sys.exit(2)
     atexit.register(reap_children)
