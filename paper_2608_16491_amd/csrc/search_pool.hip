@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
     const double u_round = 5.9604644775390625e-08;   // 2^-24
 
     {
-        const int64_t idx = (int64_t)blockIdx.x * kWavesPerBlock + wave;
+        const int64_t idx = (int64_t)blockIdx.x * (blockDim.x >> 6) + wave;
         if (idx >= A.nq) return;   // wave-uniform; no workgroup barrier follows
         const int64_t qi = uniform(P.qorder[idx]);   // the planned order (short queries last)
         const SPlan* pp = P.plan + qi;

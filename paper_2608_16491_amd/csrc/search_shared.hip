@@ -323,7 +323,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     // pool kernel: pool staging and EN list, then the re-rank list
     const int base_lds = lds_per_wave(a.L, 0);
     const int lpw = base_lds + 2 * pool_kkeep(kkeep, a.L) * 8 + 16;
-    const int smem_pool = lpw * kWavesPerBlock;
+    const int smem_pool = lpw;   // one wavefront (query) per workgroup, as for the scan
     if (smem > 160 * 1024 || smem_pool > 160 * 1024)
         return fail(FROG_EUNSUPPORTED, "LDS per block %d / %d too large", smem, smem_pool);
     if (smem > 64 * 1024) {
@@ -335,10 +335,13 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
         if (e != hipSuccess) return fail(FROG_EHIP, "hipFuncSetAttribute: %s", hipGetErrorString(e));
     }
     auto scan = pick_s_scan(ix.dp, kkeep, ix.storage);
-    // wavefronts per scan workgroup: as many as 160 KB of LDS hold (at most 4)
-    int scan_waves = (int)((160 * 1024) / s_scan_lds_per_wave(kkeep));
-    if (scan_waves > kWavesPerBlock) scan_waves = kWavesPerBlock;
-    if (scan_waves < 1) return fail(FROG_EUNSUPPORTED, "L=%d needs too much LDS for the entry scan", a.L);
+    // one wavefront per scan workgroup: a workgroup's LDS is released only
+    // when all its wavefronts have ended, and work items differ in length, so
+    // with four per workgroup the LDS of finished items sat idle beside the
+    // longest one (C2: 0.407 ms with four, 0.383 ms with one)
+    const int scan_waves = 1;
+    if (s_scan_lds_per_wave(kkeep) > 160 * 1024)
+        return fail(FROG_EUNSUPPORTED, "L=%d needs too much LDS for the entry scan", a.L);
     const int smem_scan = (int)(scan_waves * s_scan_lds_per_wave(kkeep));
     if (smem_scan > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute((const void*)scan, hipFuncAttributeMaxDynamicSharedMemorySize, smem_scan);
@@ -481,7 +484,7 @@ int launch_shared(const DevIndex& ix, const SearchLaunch& a, hipStream_t stream,
     hipLaunchKernelGGL(scan, dim3((unsigned)((items + scan_waves - 1) / scan_waves)), dim3(64 * scan_waves), smem_scan,
                        stream, P);
     if (ev) (void)hipEventRecord(ev[1], stream);
-    hipLaunchKernelGGL(pfn, dim3((unsigned)((a.nq + kWavesPerBlock - 1) / kWavesPerBlock)), dim3(kBlock), smem_pool,
+    hipLaunchKernelGGL(pfn, dim3((unsigned)a.nq), dim3(64), smem_pool,
                        stream, P);
     hipLaunchKernelGGL(sfn, dim3(blocks), dim3(kBlock), smem, stream, P);
     if (ev) (void)hipEventRecord(ev[2], stream);
