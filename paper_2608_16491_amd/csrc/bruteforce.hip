@@ -52,7 +52,7 @@ namespace {
 using namespace topk;
 
 constexpr int kQT = 16;       // queries per tile (one MFMA row block)
-constexpr int kWaves = 4;     // independent wavefronts per workgroup
+constexpr int kWaves = 1;     // wavefronts per workgroup: one, so that a finished work item releases its LDS at once
 constexpr int kThreads = 64 * kWaves;
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
