@@ -446,14 +446,17 @@ def main():
         f"recall={chosen['recall']:.4f} held-out={chosen['recall_held_out']:.4f}")
 
     # ------------------------------------------------------------------ timed steps
-    # (a) the paper's query time: per step, the batch's queries and ranges
-    # from pinned host memory to the device, the search, and its ids and
-    # distances back to pinned host memory (one packed copy), in order on the
-    # stream the search is enqueued on; steps follow each other.  (Copying the
-    # queries on a second stream so that they overlap the range planning, with
-    # a wait between the two streams in every step, made a few steps in every
-    # sixty take 2 to 8 ms instead of 1.1 ms on the MI355X; one stream and one
-    # packed copy run steadily.)
+    # (a) the line's value: per step, one search call over the batch with its
+    # queries, ranges and results resident in HBM (the index too), steps one
+    # after the other on one stream.
+    # (b) beside it, the paper's query time (Sec 8.1.3): the same steps with
+    # the batch's queries and ranges copied from pinned host memory to the
+    # device and its ids and distances back to pinned host memory (one packed
+    # copy each way) inside each step, in order on the same stream.  (Copying
+    # the queries on a second stream so that they overlap the range planning,
+    # with a wait between the two streams in every step, made a few steps in
+    # every sixty take 2 to 8 ms instead of 1.1 ms on the MI355X; one stream
+    # and one packed copy run steadily.)
     nq, qb, rb = w.nq, w.nq * d * 4, w.nq * 8
     inb = (qb + 2 * rb + 255) // 256 * 256
     host_in = torch.empty(inb, dtype=torch.uint8).pin_memory()
@@ -480,7 +483,15 @@ def main():
         F.search(ix, Qd, lod, hid, k, L, out=(ids_d, ds_d), **p_sel)
         host_out.copy_(dev_out, non_blocking=True)
 
-    def event_loop(nsteps):
+    # the resident step searches the second buffer set, filled once
+    bufs[1][0].copy_(host_in)
+    torch.cuda.synchronize()
+
+    def step_resident():
+        _, _, _, (Qd, lod, hid, ids_d, ds_d) = bufs[1]
+        F.search(ix, Qd, lod, hid, k, L, out=(ids_d, ds_d), **p_sel)
+
+    def event_loop(nsteps, fn=step):
         # a marker event between steps; torch creates an event at its first
         # record, so every marker is recorded once before the loop.  One
         # untimed step is enqueued before the first marker, so that the timed
@@ -492,10 +503,10 @@ def main():
             ev.record(stream)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        step()
+        fn()
         marks[0].record(stream)
         for i in range(nsteps):
-            step()
+            fn()
             marks[i + 1].record(stream)
         torch.cuda.synchronize()
         wall = (time.perf_counter() - t0) * nsteps / (nsteps + 1)   # host clock, per timed step's share
@@ -506,28 +517,40 @@ def main():
     # of a second (a process's first fraction of a second of such steps has
     # shown a one-time stall of a few milliseconds); the collector of Python
     # objects is paused while steps are enqueued
-    gc.disable()
-    t_warm = time.perf_counter()
-    rounds = 0
-    while rounds < 2 or time.perf_counter() - t_warm < 0.25:
-        event_loop(max(1, args.warmup))
-        rounds += 1
-    step_ms, per_step, wall = event_loop(args.steps)
-    gc.enable()
+    def timed(fn):
+        gc.disable()
+        t_warm = time.perf_counter()
+        rounds = 0
+        while rounds < 2 or time.perf_counter() - t_warm < 0.25:
+            event_loop(max(1, args.warmup), fn)
+            rounds += 1
+        out = event_loop(args.steps, fn)
+        gc.enable()
+        return out
+
+    step_ms, per_step, wall = timed(step_resident)
     per_step_med = float(np.median(step_ms)) / 1000.0
     qps = w.nq / per_step
-    # the transfers' result equals the resident search's
-    ref_ids, _ = run(sel)
-    torch.cuda.synchronize()
-    got = bufs[0][2][:outb // 2].view(torch.int32).view(nq, k)
-    assert (ref_ids.cpu() == got).all(), "transfer-inclusive step returned other ids"
-    log(f"timed {args.steps} steps with transfers: {per_step * 1e3:.3f} ms/step mean, {per_step_med * 1e3:.3f} median, "
+    log(f"timed {args.steps} resident steps: {per_step * 1e3:.3f} ms/step mean, {per_step_med * 1e3:.3f} median, "
         f"min {min(step_ms):.3f} max {max(step_ms):.3f} (wall {wall / args.steps * 1e3:.3f}), {qps:.0f} QPS; steps "
         + " ".join(f"{x:.3f}" for x in step_ms))
+    step_ms_tr, per_step_tr, wall_tr = timed(step)
+    per_step_tr_med = float(np.median(step_ms_tr)) / 1000.0
+    # both steps' results equal a plain search's
+    ref_ids, _ = run(sel)
+    torch.cuda.synchronize()
+    for b in range(2):
+        got = bufs[b][1][:outb // 2].view(torch.int32).view(nq, k).cpu() if b == 1 else \
+            bufs[b][2][:outb // 2].view(torch.int32).view(nq, k)
+        assert (ref_ids.cpu() == got).all(), "a timed step returned other ids"
+    log(f"timed {args.steps} steps with transfers: {per_step_tr * 1e3:.3f} ms/step mean, "
+        f"{per_step_tr_med * 1e3:.3f} median, min {min(step_ms_tr):.3f} max {max(step_ms_tr):.3f} "
+        f"(wall {wall_tr / args.steps * 1e3:.3f}), {w.nq / per_step_tr:.0f} QPS; steps "
+        + " ".join(f"{x:.3f}" for x in step_ms_tr))
 
-    # (b) kernels only, inputs resident; events around the library's phases
-    # (entry_mode 0: the search kernel; entry_mode 1: the matrix-core entry
-    # scan, then the pool and traversal kernels)
+    # (c) the phases of the resident search: events around the library's
+    # kernels (entry_mode 0: the search kernel; entry_mode 1: the matrix-core
+    # entry scan, then the pool and traversal kernels)
     for _ in range(args.warmup):
         run(sel)
     phase = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
@@ -548,7 +571,7 @@ def main():
     per_step_res = ev_s.elapsed_time(ev_e) / 1000.0 / args.steps
     t_a = sum(t[0].elapsed_time(t[1]) for t in phase) / 1000.0 / args.steps
     t_b = sum(t[1].elapsed_time(t[2]) for t in phase) / 1000.0 / args.steps
-    log(f"resident: {per_step_res * 1e3:.3f} ms/step, {w.nq / per_step_res:.0f} QPS; " +
+    log(f"phase timing: {per_step_res * 1e3:.3f} ms/step, {w.nq / per_step_res:.0f} QPS; " +
         (f"search kernel {t_a * 1e3:.3f} ms" if mode == 0 else
          f"entry scan {t_a * 1e3:.3f} ms, pool + traversal {t_b * 1e3:.3f} ms"))
 
@@ -960,9 +983,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{wl}: n={n} d={d} {desc}, {w.nq} queries, k={k}",
-            "step": "H2D of queries and ranges from pinned host memory, one search call, D2H of ids and "
-                    "distances (Sec 8.1.3 query time), in order on one stream, steps one after the other; "
-                    "index resident",
+            "step": "one search call over the batch, queries, ranges, results and index resident in HBM, "
+                    "steps one after the other on one stream",
             "L": L, "epn": epn, "epn_frac": frac, "epn_max": emax, "budget": B, "entry_mode": mode,
             "hash_log2": args.hash_log2, f"recall@{k}": chosen["recall"],
             "recall_held_out": chosen.get("recall_held_out"), "recall_target_met": met, "choice": how,
@@ -976,8 +998,11 @@ def main():
             "fastest_sweep_setting": best_sweep,
             "fastest_any_pool_size": fastest_any,
         },
-        "resident": {"qps": w.nq / per_step_res, "ms_per_step": per_step_res * 1e3,
-                     "what": "the same search with queries, ranges and results kept in HBM (kernels only)"},
+        "with_transfers": {"qps": w.nq / per_step_tr, "ms_per_step": per_step_tr * 1e3,
+                           "ms_per_step_median": per_step_tr_med * 1e3,
+                           "what": "the same steps with the H2D of queries and ranges from pinned host memory "
+                                   "and the D2H of ids and distances inside each step (the paper's query time, "
+                                   "Sec 8.1.3)"},
         "roofline": roof,
         "phases": phases,
         "cpu_baseline": cpu,
