@@ -517,7 +517,7 @@ def main():
     # of a second (a process's first fraction of a second of such steps has
     # shown a one-time stall of a few milliseconds); the collector of Python
     # objects is paused while steps are enqueued
-    def timed(fn):
+    def timed_loop(fn):
         gc.disable()
         t_warm = time.perf_counter()
         rounds = 0
@@ -528,13 +528,13 @@ def main():
         gc.enable()
         return out
 
-    step_ms, per_step, wall = timed(step_resident)
+    step_ms, per_step, wall = timed_loop(step_resident)
     per_step_med = float(np.median(step_ms)) / 1000.0
     qps = w.nq / per_step
     log(f"timed {args.steps} resident steps: {per_step * 1e3:.3f} ms/step mean, {per_step_med * 1e3:.3f} median, "
         f"min {min(step_ms):.3f} max {max(step_ms):.3f} (wall {wall / args.steps * 1e3:.3f}), {qps:.0f} QPS; steps "
         + " ".join(f"{x:.3f}" for x in step_ms))
-    step_ms_tr, per_step_tr, wall_tr = timed(step)
+    step_ms_tr, per_step_tr, wall_tr = timed_loop(step)
     per_step_tr_med = float(np.median(step_ms_tr)) / 1000.0
     # both steps' results equal a plain search's
     ref_ids, _ = run(sel)
