@@ -237,3 +237,35 @@ def test_duplicate_attribute_values(mode):
     valid = g_ids >= 0
     av = attr[np.where(valid, g_ids, 0)]
     assert ((av >= lo[:, None]) & (av <= hi[:, None]) | ~valid).all()
+
+
+@pytest.mark.parametrize("kind", ["one", "all_empty", "all_covered", "none_covered"])
+def test_shared_query_order_classes(tiny, kind):
+    # the pool and traversal take the queries in a planned order (ranges the
+    # sample does not cover first, then covered and empty ones): batches made
+    # of one class only, and a single query, give the oracle's rows
+    n = tiny.ox.n
+    rng = np.random.default_rng(11)
+    nq = 1 if kind == "one" else 70
+    if kind == "all_empty":
+        lo = rng.integers(10, n, nq).astype(np.float64)
+        hi = lo - 1.0
+    elif kind == "all_covered":
+        lo = rng.integers(0, n - 500, nq).astype(np.float64)
+        hi = lo + rng.integers(0, 400, nq)
+    else:
+        lo = rng.integers(0, n // 4, nq).astype(np.float64)
+        hi = lo + rng.integers(n // 2, 3 * n // 4, nq)
+    Q = tiny.Q[np.arange(nq) % tiny.Q.shape[0]]
+    c = Case.__new__(Case)
+    c.ox, c.ix = tiny.ox, tiny.ix
+    c.Q, c.lo, c.hi = Q, lo, hi
+    c.dQ = torch.as_tensor(Q).cuda()
+    c.dlo = torch.as_tensor(lo).cuda()
+    c.dhi = torch.as_tensor(hi).cuda()
+    p = dict(entry_mode=1, epn=16, epn_frac=1.0, epn_max=500)
+    g_ids, g_d = c.gpu(10, 32, **p)
+    o_ids, o_d, _ = c.cpu(10, 32, **p)
+    assert_parity(g_ids, g_d, o_ids, o_d, max_residual=0 if kind == "all_empty" else 1)
+    if kind == "all_empty":
+        assert (g_ids == -1).all()
