@@ -277,10 +277,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) voi
     for (int g = 0; g < 4; ++g)
 #pragma unroll
         for (int e = 0; e < 4; ++e) scount[4 * g + e] = (uint32_t)__shfl((int)scnt[e], 16 * g);
-    // slot i's list: (its pair, this chunk)
+    // slot i's list: (its pair, this chunk).  The slots' pairs are read
+    // once, one per lane, before the loop: a load inside it would make each
+    // slot wait for the stores of the lists before it (the wait counter
+    // counts stores too)
+    const int32_t pid_l = lane < kSQ ? T.pair[lane] : -1;
 #pragma unroll
     for (int i = 0; i < kSQ; ++i) {
-        const int32_t pid = T.pair[i];
+        const int32_t pid = __builtin_amdgcn_readlane(pid_l, i);
         if (pid < 0) continue;   // uniform: an empty slot has no list
         const int64_t lid = (int64_t)pid * P.nchunk + c;
         buf_cut<kkeep>(list_of(i));
