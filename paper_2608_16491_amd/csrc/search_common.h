@@ -289,9 +289,12 @@ __device__ __forceinline__ int chunk_dim(int sub, int c) {
     else return 8 * (sub + 8 * (c >> 1)) + 4 * (c & 1);
 }
 
-// Squared L2 of up to `cnt` (<= 64) candidates; lane j holds candidate j's
-// rank in `myid` and receives its distance in the return value.  The query's
-// float4 chunks this lane needs are in qv.
+// Squared L2 of up to `cnt` (1..64) candidates; lane j holds candidate j's
+// rank in `myid` and receives its distance in the return value (lanes from
+// cnt on receive an unspecified value).  The query's float4 chunks this lane
+// needs are in qv.  Lanes of a group past cnt read candidate cnt - 1 again,
+// so that every load is issued by every lane: a load under a lane predicate
+// is split off into a branch of its own, with a wait of its own.
 template <int C, typename XT = float>
 __device__ float eval_small(const XT* __restrict__ X, int dp, const float4 (&qv)[C], int cnt, int32_t myid) {
     // G = 8 lanes per vector: lane reads float4 chunks (lane % 8) + 8c; one
@@ -302,10 +305,9 @@ __device__ float eval_small(const XT* __restrict__ X, int dp, const float4 (&qv)
     float mine = 0.f;
     for (int sb0 = 0; sb0 < cnt; sb0 += 8) {
         const int j = sb0 + (lane >> 3);
-        const int id = __shfl(myid, j & 63);
-        const bool v = j < cnt;
+        const int id = __shfl(myid, (j < cnt ? j : cnt - 1) & 63);
         float4 x[C];
-        load_row<C, XT>(X, dp, id, sub, v, x);
+        load_row<C, XT>(X, dp, id, sub, true, x);
         double s = 0.0;
 #pragma unroll
         for (int c = 0; c < C; ++c) {
@@ -327,7 +329,7 @@ __device__ float eval_small(const XT* __restrict__ X, int dp, const float4 (&qv)
     return mine;
 }
 
-// Same result as eval_small for the entry-point batches (up to 64 candidates),
+// Same result as eval_small for the entry-point batches (1..64 candidates),
 // with two steps of 16 vectors in flight: the loads of step i+1 are issued
 // before step i is reduced, so the arithmetic overlaps the memory latency.
 template <int C, typename XT = float>
@@ -339,9 +341,8 @@ struct Gather16 {
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
             const int j = sb0 + 8 * g + (lane >> 3);
-            const int id = __shfl(myid, j & 63);
-            const bool v = j < cnt;
-            load_row<C, XT>(X, dp, id, sub, v, x[g]);
+            const int id = __shfl(myid, (j < cnt ? j : cnt - 1) & 63);
+            load_row<C, XT>(X, dp, id, sub, true, x[g]);
         }
     }
     __device__ __forceinline__ void consume(const float4 (&qv)[C], int sb0, float& mine) const {
@@ -762,13 +763,21 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         for (int s = 0; s < LP; ++s)
             if (s == (nsel >> 6) && nsel >= 0) nu = (int32_t)(uint32_t)readlane64(pool.key[s], nsel & 63);
         nu = uniform(nu);
-        const int32_t cur_pre = pre_v;
+        // The slice's first 64 entries (loaded on a miss) are issued before
+        // the prefetch, and the prefetch is issued on every hop (a valid row
+        // when there is no guess) with every lane active, its lanes past the
+        // slice masked where it is used: the loads in flight are then the same
+        // on every path, and waiting for the slice leaves the prefetch in
+        // flight (the wait counter retires loads in order; an optional load
+        // makes the wait drain them all).  The previous prefetch is not read
+        // after the next one is issued, so the two share a register.
+        const int lidx = lane < nent ? lane : 0;
+        int32_t x = pre_v;
+        if (!hit) x = row[lidx];
         pre_u = nu;
-        if (nu >= 0) {
-            const int32_t* nrow = ix.ENC + ((int64_t)nu * H + Ls) * m;
-            pre_v = lane < nent ? nrow[lane] : -1;
-            st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
-        }
+        pre_v = ix.ENC[((int64_t)(nu >= 0 ? nu : u) * H + Ls) * m + lidx];
+        if (nu >= 0) st[FROG_STAT_LOADED] += (int32_t)(nent < 64 ? nent : 64);
+        const int32_t v0 = lane < nent ? x : -1;
         if (LEAN) {
             // the first 64 entries of the hotspot slice (the prefetched ones
             // on a hit); when they hold the whole slice or at least B
@@ -777,7 +786,6 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
             // to lanes 0.., check them against the visited table (lazy
             // check) and move the fresh ones down.  Otherwise the general
             // path below scans on.
-            const int32_t v0 = hit ? cur_pre : (lane < nent ? row[lane] : -1);
             const bool inr = v0 >= l32 && v0 <= r32;
             const uint64_t pm = ballot(inr);
             const int tot = __popcll(pm);
@@ -799,7 +807,7 @@ __device__ void traverse(const DevIndex& ix, const SearchLaunch& A, int64_t gvis
         int64_t scanned = nent;
         for (int64_t off = 0; off < nent && nen < B; off += 64) {
             const int64_t e = off + lane;
-            const int32_t v = (off == 0 && hit) ? cur_pre : (e < nent ? row[e] : -1);
+            const int32_t v = off == 0 ? v0 : (e < nent ? row[e] : -1);
             bool pred = v >= l && v <= r;
             if (eager) {
                 // ablation: visited candidates are skipped here and do not
