@@ -30,7 +30,8 @@
 //     contiguous bytes per load instruction and vector), differences and
 //     squares in double, an 8-lane butterfly sum, one rounding to float --
 //     the library's canonical squared L2.  d > 128 uses all 64 lanes per
-//     vector.  No matrix cores: every gathered vector is used once;
+//     vector, a per-lane sum over its chunks and a 64-lane sum.  No matrix
+//     cores: every gathered vector is used once;
 //   - MergeTopEfS: a new key's position is (# pool keys below it) + (# new
 //     keys below it), counted with ballots; a pool key's position is its slot
 //     plus (# new keys below it); entries scatter through LDS.  Keys are
@@ -386,13 +387,86 @@ __device__ float eval_pipelined(const XT* __restrict__ X, int dp, const float4 (
     return mine;
 }
 
-// d > 128: all 64 lanes read one vector, float4 chunk lane + 64c.
+// The sum over all 64 lanes, the same value in every lane: each row of 16
+// by quad swaps [1,0,3,2], [2,3,0,1] and the half-row and row mirrors, then
+// the four rows' sums in a fixed order.
+__device__ __forceinline__ double sum64(double s) {
+    s = sum8(s);
+    s += dpp_f64<0x140>(s);
+    const double r0 = __longlong_as_double(((long long)(uint32_t)__builtin_amdgcn_readlane((int)(__double_as_longlong(s) >> 32), 0) << 32) |
+                                           (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(s), 0));
+    const double r1 = __longlong_as_double(((long long)(uint32_t)__builtin_amdgcn_readlane((int)(__double_as_longlong(s) >> 32), 16) << 32) |
+                                           (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(s), 16));
+    const double r2 = __longlong_as_double(((long long)(uint32_t)__builtin_amdgcn_readlane((int)(__double_as_longlong(s) >> 32), 32) << 32) |
+                                           (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(s), 32));
+    const double r3 = __longlong_as_double(((long long)(uint32_t)__builtin_amdgcn_readlane((int)(__double_as_longlong(s) >> 32), 48) << 32) |
+                                           (uint32_t)__builtin_amdgcn_readlane((int)__double_as_longlong(s), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+// d > 128: all 64 lanes read one vector, float4 chunk lane + 64c, the
+// differences and squares in double, summed over the lane's chunks in order
+// and then over the wavefront by sum64.  Rows of up to 1024 padded
+// dimensions (4 chunks per lane) keep the query's chunks in registers for
+// the call and issue a candidate's four loads before the first is used (a
+// chunk past the row reads the row's last chunk, its terms zeroed): one
+// memory wait per candidate.
+// Wider rows loop over their chunks.  Lane j < cnt receives candidate j's
+// distance; lanes from cnt on receive an unspecified value.
 __device__ float eval_large(const float* __restrict__ X, int dp, const float* __restrict__ q, int d, int cnt,
                             int32_t myid) {
     const int lane = lane_id();
     const float4* __restrict__ X4 = reinterpret_cast<const float4*>(X);
     const int dp4 = dp >> 2;
     float mine = 0.f;
+    if (dp4 <= 4 * 64) {
+        // the query's chunks are read per call: hoisted out of a caller's
+        // loop they would hold 16 registers across it
+        const float* qq = q;
+        asm volatile("" : "+v"(qq));
+        float4 qc[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int b = 4 * (lane + 64 * i);
+            float e[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float v = qq[b + t < d ? b + t : d - 1];
+                e[t] = b + t < d ? v : 0.f;
+            }
+            qc[i] = make_float4(e[0], e[1], e[2], e[3]);
+        }
+        auto part = [&](const float4 (&x)[4]) {
+            double s = 0.0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const bool in = lane + 64 * i < dp4;
+                // keep the query in fp32 registers: convert per use, not once
+                float4 qf = qc[i];
+                asm volatile("" : "+v"(qf.x), "+v"(qf.y), "+v"(qf.z), "+v"(qf.w));
+                const double q0 = qf.x, q1 = qf.y, q2 = qf.z, q3 = qf.w;
+                double t, u = 0.0;
+                t = q0 - (double)x[i].x; u += t * t;
+                t = q1 - (double)x[i].y; u += t * t;
+                t = q2 - (double)x[i].z; u += t * t;
+                t = q3 - (double)x[i].w; u += t * t;
+                s += in ? u : 0.0;
+            }
+            return s;
+        };
+        for (int j = 0; j < cnt; ++j) {
+            const int64_t id = __builtin_amdgcn_readlane(myid, j);
+            float4 x[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int c = lane + 64 * i < dp4 ? lane + 64 * i : dp4 - 1;
+                x[i] = X4[id * dp4 + c];
+            }
+            const double sj = sum64(part(x));
+            if (lane == j) mine = (float)sj;
+        }
+        return mine;
+    }
     for (int j = 0; j < cnt; ++j) {
         const int id = __builtin_amdgcn_readlane(myid, j);
         double s = 0.0;
@@ -401,14 +475,14 @@ __device__ float eval_large(const float* __restrict__ X, int dp, const float* __
             const int b = 4 * c;
             const double q0 = b < d ? q[b] : 0.f, q1 = b + 1 < d ? q[b + 1] : 0.f;
             const double q2 = b + 2 < d ? q[b + 2] : 0.f, q3 = b + 3 < d ? q[b + 3] : 0.f;
-            double t;
-            t = q0 - (double)x.x; s += t * t;
-            t = q1 - (double)x.y; s += t * t;
-            t = q2 - (double)x.z; s += t * t;
-            t = q3 - (double)x.w; s += t * t;
+            double t, u = 0.0;
+            t = q0 - (double)x.x; u += t * t;
+            t = q1 - (double)x.y; u += t * t;
+            t = q2 - (double)x.z; u += t * t;
+            t = q3 - (double)x.w; u += t * t;
+            s += u;
         }
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o);
+        s = sum64(s);
         if (lane == j) mine = (float)s;
     }
     return mine;

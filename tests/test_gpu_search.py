@@ -162,9 +162,11 @@ def test_mixture_d128_parity(mix128, L):
     assert (g_st[ok, F.STAT_EXPANSIONS] == o_st[ok, oracle.STAT_EXPANSIONS]).all()
 
 
-@pytest.mark.parametrize("d", [7, 96, 200])
+@pytest.mark.parametrize("d", [7, 96, 200, 1021, 1030])
 def test_other_dimensions(d):
-    # d=7 pads rows to 32 floats; d=96 uses 3 chunks per lane; d=200 the 64-lane path
+    # d=7 pads rows to 32 floats; d=96 uses 3 chunks per lane; d=200 the 64-lane
+    # path; d=1021 its widest rows with the query in registers (a query length
+    # not a multiple of 4); d=1030 its chunk loop (rows past 1024 floats)
     rng = np.random.default_rng(d)
     n, nq = 3000, 64
     X = rng.standard_normal((n, d)).astype(np.float32)
