@@ -408,9 +408,9 @@ __device__ __forceinline__ double sum64(double s) {
 // differences and squares in double, summed over the lane's chunks in order
 // and then over the wavefront by sum64.  Rows of up to 1024 padded
 // dimensions (4 chunks per lane) keep the query's chunks in registers for
-// the call and issue a candidate's four loads before the first is used (a
-// chunk past the row reads the row's last chunk, its terms zeroed): one
-// memory wait per candidate.
+// the call and issue a candidate's four loads together (a chunk past the
+// row reads the row's last chunk, its terms zeroed), two candidates in
+// flight.
 // Wider rows loop over their chunks.  Lane j < cnt receives candidate j's
 // distance; lanes from cnt on receive an unspecified value.
 __device__ float eval_large(const float* __restrict__ X, int dp, const float* __restrict__ q, int d, int cnt,
@@ -454,16 +454,26 @@ __device__ float eval_large(const float* __restrict__ X, int dp, const float* __
             }
             return s;
         };
-        for (int j = 0; j < cnt; ++j) {
-            const int64_t id = __builtin_amdgcn_readlane(myid, j);
-            float4 x[4];
+        // two candidates in flight: the next one's loads are issued before
+        // the current one's are used (a round past cnt reads candidate
+        // cnt - 1 again), so consecutive waits overlap
+        auto load = [&](int j, float4 (&x)[4]) {
+            const int64_t id = __builtin_amdgcn_readlane(myid, j < cnt ? j : cnt - 1);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int c = lane + 64 * i < dp4 ? lane + 64 * i : dp4 - 1;
                 x[i] = X4[id * dp4 + c];
             }
-            const double sj = sum64(part(x));
-            if (lane == j) mine = (float)sj;
+        };
+        float4 xa[4], xb[4];
+        load(0, xa);
+        for (int j = 0; j < cnt; j += 2) {
+            load(j + 1, xb);
+            const double sa = sum64(part(xa));
+            if (lane == j) mine = (float)sa;
+            load(j + 2, xa);
+            const double sb = sum64(part(xb));
+            if (lane == j + 1) mine = (float)sb;
         }
         return mine;
     }
