@@ -30,11 +30,32 @@ __device__ __forceinline__ void wave_sum_min(int& s, float& m) {
     m = rm;
 }
 
-// The pool of each query: one wavefront per query.  Four wavefronts per
-// SIMD for pools of at most 64 (128 VGPRs: a few values spill, and the
-// kernel still ran 89 -> 81 us at C2), three above (no spill).
+// Exact distances of up to 64 candidates for the pool kernel.  Pools of at
+// most 64 gather 16 rows per step, one step at a time: the kernel then fits
+// 80 VGPRs and 6 wavefronts per SIMD, so that a 10k-query batch runs in two
+// rounds of wavefronts (with two steps in flight it needed 128 VGPRs and
+// ran at 4 per SIMD: 67 against 62 us at C2).  Larger pools keep two steps
+// in flight at 3 per SIMD.  Both give the same distances (the same
+// per-candidate arithmetic).
+template <int C, int LP, typename XT, typename QC>
+__device__ __forceinline__ float pool_eval(const DevIndex& ix, const QC& Q, int cnt, int32_t myid) {
+    if constexpr (C > 0 && LP == 1) {
+        float mine = 0.f;
+        Gather16<C, XT> g;
+        for (int sb0 = 0; sb0 < cnt; sb0 += 16) {
+            g.issue(rows_of<XT>(ix), ix.dp, cnt, myid, sb0);
+            g.consume(Q.qv, sb0, mine);
+        }
+        return mine;
+    } else {
+        return Q.eval_batch(ix, cnt, myid);
+    }
+}
+
+// The pool of each query: one wavefront per query.  Six wavefronts per
+// SIMD for pools of at most 64, three above (no spill either way).
 template <int C, int LP, int KK, typename XT = float, int MK = (KK > 64 ? KK : 64)>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 ? 4 : 3))) void s_pool_kernel(SParams P) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 ? 6 : 3))) void s_pool_kernel(SParams P) {
     using namespace topk;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const DevIndex& ix = P.ix;
@@ -140,7 +161,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
         if (f <= 64) {
             // one key per lane: a bitonic sort over the wavefront, the first L are the pool
             const int32_t id = lane < f ? (int32_t)(uint32_t)Lst.key[lane] : 0;
-            const float dd = Q.eval_batch(ix, f, id);
+            const float dd = pool_eval<C, LP, XT>(ix, Q, f, id);
             uint64_t key = lane < f ? make_key(dd, id) : kEmpty;
 #pragma unroll
             for (int kb = 2; kb <= 64; kb <<= 1) {
@@ -159,7 +180,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
             for (int j0 = 0; j0 < f; j0 += 64) {
                 const int nb = f - j0 < 64 ? f - j0 : 64;
                 const int32_t id = lane < nb ? (int32_t)(uint32_t)Lst.key[j0 + lane] : 0;
-                const float dd = Q.eval_batch(ix, nb, id);
+                const float dd = pool_eval<C, LP, XT>(ix, Q, nb, id);
                 merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
             }
         }
@@ -210,7 +231,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(LP == 1 
                 wave_sync();
                 const int32_t id = lane < nb ? W.enbuf[lane] : 0;
                 wave_sync();
-                const float dd = Q.eval_batch(ix, nb, id);
+                const float dd = pool_eval<C, LP, XT>(ix, Q, nb, id);
                 merge<LP>(pool, lane < nb ? make_key(dd, id) : kEmpty, nb, A.L, W.st_key, W.st_flag);
             }
         }
