@@ -180,33 +180,30 @@ __global__ __launch_bounds__(kThreads) void bf_scan_kernel(BFParams P) {
             for (int t = 0; t < KT; ++t) x[t] = X4[(int64_t)rowc * dp4 + 4 * t + kk];
         }
     };
-    load_block(0, xa);
-    for (int blk = 0; blk < nblk; ++blk) {
+    // one block's products and candidates; x holds its rows (d <= 128)
+    auto process = [&](int blk, const float4 (&x)[KT > 0 ? KT : 1]) {
         const int row = it.rb + blk * 16 + ii;
         const int rowc = row <= it.re ? row : it.re;
-        if (blk + 1 < nblk) load_block(blk + 1, xb);
         floatx4 acc = {0.f, 0.f, 0.f, 0.f};
         float xn = 0.f;
         if constexpr (KT > 0) {
 #pragma unroll
             for (int t = 0; t < KT; ++t) {
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].x, xa[t].x, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].y, xa[t].y, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].z, xa[t].z, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].w, xa[t].w, acc, 0, 0, 0);
-                xn += xa[t].x * xa[t].x + xa[t].y * xa[t].y + xa[t].z * xa[t].z + xa[t].w * xa[t].w;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].x, x[t].x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].y, x[t].y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].z, x[t].z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[t].w, x[t].w, acc, 0, 0, 0);
+                xn += x[t].x * x[t].x + x[t].y * x[t].y + x[t].z * x[t].z + x[t].w * x[t].w;
             }
-#pragma unroll
-            for (int t = 0; t < KT; ++t) xa[t] = xb[t];
         } else {
             for (int t = 0; t < dp / 16; ++t) {
-                const float4 x = X4[(int64_t)rowc * dp4 + 4 * t + kk];
+                const float4 xv = X4[(int64_t)rowc * dp4 + 4 * t + kk];
                 const float4 q = qchunk(t);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.x, x.x, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, x.y, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.z, x.z, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, x.w, acc, 0, 0, 0);
-                xn += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.x, xv.x, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.y, xv.y, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.z, xv.z, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(q.w, xv.w, acc, 0, 0, 0);
+                xn += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
             }
         }
         xn += __shfl_xor(xn, 16);
@@ -226,6 +223,18 @@ __global__ __launch_bounds__(kThreads) void bf_scan_kernel(BFParams P) {
                 offer(TopList{lv + qi * kkeep, lr + qi * kkeep, lst + 4 * qi}, kkeep, gm, ap, rowc);
             }
         }
+    };
+    // two row buffers in turn: the next block's loads are issued on every
+    // step (past the last block they read it again) before the current
+    // block is used, so its wait leaves them in flight; a conditional load,
+    // or a copy between the buffers, would make the wait drain them
+    load_block(0, xa);
+    for (int blk = 0; blk < nblk; blk += 2) {
+        load_block(blk + 1 < nblk ? blk + 1 : nblk - 1, xb);
+        process(blk, xa);
+        if (blk + 1 >= nblk) break;
+        load_block(blk + 2 < nblk ? blk + 2 : nblk - 1, xa);
+        process(blk + 1, xb);
     }
     // write the chunk's lists
     const int64_t base = item * kQT;

@@ -47,6 +47,23 @@ def test_bruteforce_mixture(k):
     assert_parity(ids, ds, o_ids, o_d, max_residual=0)
 
 
+@pytest.mark.parametrize("d", [200, 1030])
+def test_bruteforce_wide_rows(d):
+    # rows wider than 128 floats take the chunk loop with the query read per
+    # chunk (d = 200: 14 steps of 16 dimensions; d = 1030: 66 steps)
+    print(f"[gpu] bruteforce wide rows d={d}", flush=True)
+    rng = np.random.default_rng(d)
+    n, nq = 3000, 48
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    attr = rng.permutation(n).astype(np.float64)
+    Q = rng.standard_normal((nq, d)).astype(np.float32)
+    sig = np.array([0.01, 0.1, 0.5, 1.0])[np.arange(nq) % 4]
+    lo, hi = workloads.ranges_for_selectivity(rng, sig, n)
+    ids, ds, cert, o_ids, o_d = _run(X, attr, Q, lo, hi, 10)
+    assert np.isin(cert, (1, 2)).all()
+    assert_parity(ids, ds, o_ids, o_d, max_residual=0)
+
+
 def test_bruteforce_edges():
     rng = np.random.default_rng(1)
     n, d = 2000, 40
