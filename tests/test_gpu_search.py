@@ -162,8 +162,9 @@ def test_mixture_d128_parity(mix128, L):
     assert (g_st[ok, F.STAT_EXPANSIONS] == o_st[ok, oracle.STAT_EXPANSIONS]).all()
 
 
+@pytest.mark.parametrize("entry_mode", [0, 1])
 @pytest.mark.parametrize("d", [7, 96, 200, 1021, 1030])
-def test_other_dimensions(d):
+def test_other_dimensions(d, entry_mode):
     # d=7 pads rows to 32 floats; d=96 uses 3 chunks per lane; d=200 the 64-lane
     # path; d=1021 its widest rows with the query in registers (a query length
     # not a multiple of 4); d=1030 its chunk loop (rows past 1024 floats)
@@ -175,8 +176,12 @@ def test_other_dimensions(d):
     sig = np.array([0.01, 0.1, 0.5, 1.0])[np.arange(nq) % 4]
     lo, hi = workloads.ranges_for_selectivity(rng, sig, n)
     c = Case(X, attr, Q, lo, hi)
-    g_ids, g_d = c.gpu(10, 64)
-    o_ids, o_d, _ = c.cpu(10, 64)
+    p = {}
+    if entry_mode == 1:   # the shared entry sample: matrix-core scan, pool, traversal
+        p = dict(entry_mode=1, epn=16, epn_frac=0.2, epn_max=600)
+        c.ix.prepare_sample(0)
+    g_ids, g_d = c.gpu(10, 64, **p)
+    o_ids, o_d, _ = c.cpu(10, 64, **p)
     assert_parity(g_ids, g_d, o_ids, o_d)
 
 
